@@ -1,0 +1,24 @@
+"""CPU oracle for the multi-bitwidth additive-codebook linear layer (Drop-by-Drop).
+
+TEST INFRASTRUCTURE ONLY. This package is imported by ``tests/``, by the smoke
+check in ``__graft_entry__.smoke()`` and by the ``cpu_baseline`` leg of
+``bench.py``; nothing on the product path imports, calls or links it, and it
+imports nothing from the product package. It is plain, slow and written to be
+checked against the paper by eye:
+
+* ``formats``   - exact decoding of fp16/bf16 bit patterns and round-to-nearest-
+                  even encodings (own bit manipulation for bf16, numpy for fp16,
+                  plus a format-generic rounding used to pin both);
+* ``aq``        - the partial reconstruction, the linear layer, the canonical
+                  rounded dequantization, the GEMM reference, the weighted MSE
+                  and the average-bits formula;
+* ``search``    - residual k-means encoding and exhaustive / beam code search on
+                  tiny groups (fixture generators and pins, not on the hot path).
+
+Every function cites the passage of the paper it follows. Pins live in
+``tests/test_oracle_*.py``; functions without a pin say "parity unpinned".
+"""
+from . import formats, aq, search  # noqa: F401
+from .aq import (reconstruct, linear, dequant_canonical, gemm_reference, wmse_frobenius,
+                 wmse_trace, bits_per_weight, code_bits_per_weight)  # noqa: F401
+from .search import encode_residual_kmeans, brute_force_codes, beam_search_codes  # noqa: F401

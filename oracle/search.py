@@ -1,0 +1,138 @@
+"""Encoders that produce codes: residual k-means initialisation and code search.
+
+Neither is on the inference hot path. They produce fixtures (codes for Gaussian
+weights, on which distortion must fall with k) and pin the meaning of "codes
+that minimise the quantization error" on tiny groups.
+
+App. C ("AQLM's Optimization Process") describes the initialisation: k-means
+on the weight groups gives the first codebook and its assignments; the
+differences between the weights and their centroids are clustered again to
+give the next codebook, and so on. The code-optimisation phase searches
+combinations of codewords that minimise the quantization error (beam search).
+"""
+from __future__ import annotations
+
+import itertools
+
+import numpy as np
+
+
+def _lloyd(points: np.ndarray, n_centroids: int, iters: int, rng: np.random.Generator):
+    """Lloyd's k-means on the rows of ``points``.
+
+    Initial centroids are distinct rows drawn without replacement (all rows,
+    repeated cyclically, if there are fewer rows than centroids). Each
+    iteration assigns every point to its nearest centroid (squared Euclidean
+    distance, ties to the lowest index) and moves every non-empty cluster's
+    centroid to its mean; empty clusters keep their centroid. The run ends
+    with one more assignment, so the returned assignment is nearest-centroid
+    for the returned centroids, which come from a mean update.
+    """
+    n = points.shape[0]
+    if n >= n_centroids:
+        idx = rng.choice(n, size=n_centroids, replace=False)
+    else:
+        idx = np.arange(n_centroids) % n
+    C = points[idx].copy()
+
+    def assign(C):
+        d = ((points[:, None, :] - C[None, :, :]) ** 2).sum(axis=2)   # [n][n_centroids]
+        return np.argmin(d, axis=1)
+
+    for _ in range(max(1, iters)):
+        a = assign(C)
+        for c in range(n_centroids):
+            members = points[a == c]
+            if len(members):
+                C[c] = members.mean(axis=0)
+    return C, assign(C)
+
+
+def encode_residual_kmeans(W, M: int, B: int, g: int, seed: int = 0, iters: int = 8):
+    """Residual k-means encoding of W into M codebooks of 2^B codewords (App. C, initialisation).
+
+    Returns (codes [M][d_out][d_in/g] int64, codebooks [M][2^B][g] fp64,
+    scales [d_out] fp64). Scales are 1: the paper's initialisation produces s
+    but does not say how; unit scales keep W^(k) = sum of codewords.
+    """
+    W = np.asarray(W, dtype=np.float64)
+    d_out, d_in = W.shape
+    if d_in % g:
+        raise ValueError("d_in must be a multiple of g")
+    rng = np.random.Generator(np.random.PCG64(seed))
+    residual = W.reshape(-1, g).copy()          # groups of g consecutive weights, row by row
+    codes = np.zeros((M, d_out, d_in // g), dtype=np.int64)
+    codebooks = np.zeros((M, 2 ** B, g), dtype=np.float64)
+    for m in range(M):
+        C, a = _lloyd(residual, 2 ** B, iters, rng)
+        codebooks[m] = C
+        codes[m] = a.reshape(d_out, d_in // g)
+        residual = residual - C[a]
+    return codes, codebooks, np.ones(d_out)
+
+
+def _group_errors(w_group: np.ndarray, codebooks: np.ndarray, scale: float, tuples: np.ndarray) -> np.ndarray:
+    """Squared error ||w - s * sum_m C_m[c_m]||^2 for every code tuple (rows of ``tuples``)."""
+    recon = np.zeros((tuples.shape[0], codebooks.shape[2]))
+    for m in range(tuples.shape[1]):
+        recon += codebooks[m][tuples[:, m]]
+    diff = w_group[None, :] - scale * recon
+    return (diff * diff).sum(axis=1)
+
+
+def brute_force_codes(W, codebooks, scales, k: int):
+    """Exhaustive code search with the first k codebooks, group by group.
+
+    For every (row i, group j) it tries all (2^B)^k code tuples and keeps one
+    with the smallest squared error ||W_ij - s_i sum_{m<k} C_m[c_m]||^2 (the
+    plain MSE, X = I, of §2.2); ties go to the lexicographically smallest tuple.
+    Returns (codes [k][d_out][d_in/g], total squared error).
+    Only for tiny g and 2^B: the cost is (2^B)^k per group.
+    """
+    W = np.asarray(W, dtype=np.float64)
+    codebooks = np.asarray(codebooks, dtype=np.float64)
+    scales = np.asarray(scales, dtype=np.float64)
+    n_cw, g = codebooks.shape[1], codebooks.shape[2]
+    d_out, d_in = W.shape
+    tuples = np.array(list(itertools.product(range(n_cw), repeat=k)), dtype=np.int64)  # lexicographic
+    codes = np.zeros((k, d_out, d_in // g), dtype=np.int64)
+    total = 0.0
+    for i in range(d_out):
+        for j in range(d_in // g):
+            err = _group_errors(W[i, j * g:(j + 1) * g], codebooks, scales[i], tuples)
+            best = int(np.argmin(err))          # argmin returns the first (smallest) tuple on ties
+            codes[:, i, j] = tuples[best]
+            total += float(err[best])
+    return codes, total
+
+
+def beam_search_codes(W, codebooks, scales, k: int, beam: int):
+    """Beam search over codebooks 0..k-1 in order, group by group (App. C, code optimisation).
+
+    Stage m extends every kept partial tuple (c_0..c_{m-1}) by every codeword
+    of codebook m and keeps the ``beam`` extensions with the smallest error of
+    the partial reconstruction; the last stage returns the best full tuple.
+    With beam >= (2^B)^(k-1) nothing is ever dropped before the last stage, so
+    the result equals exhaustive search; beam = 1 is greedy residual coding.
+    Returns (codes [k][d_out][d_in/g], total squared error).
+    """
+    W = np.asarray(W, dtype=np.float64)
+    codebooks = np.asarray(codebooks, dtype=np.float64)
+    scales = np.asarray(scales, dtype=np.float64)
+    n_cw, g = codebooks.shape[1], codebooks.shape[2]
+    d_out, d_in = W.shape
+    codes = np.zeros((k, d_out, d_in // g), dtype=np.int64)
+    total = 0.0
+    for i in range(d_out):
+        for j in range(d_in // g):
+            w = W[i, j * g:(j + 1) * g]
+            kept = np.zeros((1, 0), dtype=np.int64)
+            for m in range(k):
+                ext = np.concatenate([np.repeat(kept, n_cw, axis=0),
+                                      np.tile(np.arange(n_cw), len(kept))[:, None]], axis=1)
+                err = _group_errors(w, codebooks, scales[i], ext)
+                order = np.lexsort(tuple(ext[:, c] for c in range(ext.shape[1] - 1, -1, -1)) + (err,))
+                kept = ext[order[:beam]] if m < k - 1 else ext[order[:1]]
+            codes[:, i, j] = kept[0]
+            total += float(_group_errors(w, codebooks, scales[i], kept)[0])
+    return codes, total

@@ -1,0 +1,137 @@
+"""Seeded synthetic inputs for the multi-bitwidth additive-codebook linear layer.
+
+This module only draws random inputs and encodes them into the storage formats
+(fp16 / bf16 bit patterns, uint8 / uint16 code planes). It holds none of the
+method's arithmetic: no reconstruction, no product, no rounding of results.
+Both the CPU oracle and the GPU path take their inputs from here, so the two
+sides see the same bytes; neither side imports the other.
+
+Recipe (one ``numpy.random.Generator(PCG64(seed))`` per layer, draws in this
+order):
+
+1. codebooks ``normal(0, 0.02/sqrt(M), (M, 2**B, g))`` -> fp16, the standard
+   deviation is ``0.02/sqrt(M)`` so that a full sum of M codewords has a
+   standard deviation near 0.02, a typical LLM weight scale;
+2. codes ``integers(0, 2**B, (M, d_out, d_in/g))`` -> uint8 (B=8) or uint16
+   (B=16), plane-major: plane m holds codebook m's index for every
+   (output row, input group);
+3. scales ``uniform(0.5, 1.5, d_out)`` -> fp16, one per output row;
+4. activations ``normal(0, 1, (batch, d_in))`` -> fp16 or bf16 (round to
+   nearest even); the heavy-tailed variant multiplies
+   ``round(0.001*batch*d_in)`` positions, chosen without replacement, by 20
+   before the cast.
+
+The shapes stand in for the projections of Llama-7B-class models (4096x4096,
+11008x4096, 4096x11008, 14336x4096) quantized with M codebooks of 2**B
+codewords of g=8 weights each, the setting of the paper's experiments (§6).
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional
+
+import numpy as np
+
+__all__ = ["Layer", "LayerSpec", "make_layer", "make_activations", "float_to_bf16_bits",
+           "float_to_f16_bits", "CONFIGS", "config"]
+
+
+def float_to_f16_bits(a: np.ndarray) -> np.ndarray:
+    """fp64/fp32 values -> IEEE binary16 bit patterns (numpy's round-to-nearest-even)."""
+    return np.asarray(a, dtype=np.float64).astype(np.float16).view(np.uint16)
+
+
+def float_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """fp64 values -> bfloat16 bit patterns, rounding to nearest even.
+
+    The value is first rounded to binary32 (exact for the draws used here up to
+    one rounding; draws are then rounded once more), then the low 16 bits are
+    rounded away with ties to even. NaN stays NaN.
+    """
+    f = np.asarray(a, dtype=np.float64).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+    nan = np.isnan(f)
+    if nan.any():
+        r = r.copy()
+        r[nan] = 0x7FC0
+    return r
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerSpec:
+    name: str
+    d_out: int
+    d_in: int
+    g: int = 8
+    M: int = 4
+    B: int = 8
+    seed: int = 0
+    act_dtype: str = "f16"          # "f16" | "bf16"
+    batches: tuple = (1,)
+    ks: tuple = (1, 2, 3, 4)
+    heavy_tail: bool = False
+    n_tokens: int = 0               # >0: prefill GEMM workload
+
+
+@dataclasses.dataclass
+class Layer:
+    spec: LayerSpec
+    codes: np.ndarray      # [M][d_out][d_in/g] uint8 | uint16
+    codebooks: np.ndarray  # [M][2**B][g] uint16 (fp16 bits)
+    scales: np.ndarray     # [d_out] uint16 (fp16 bits)
+    rng: np.random.Generator  # continues after the layer draws (activations come next)
+
+
+def make_layer(spec: LayerSpec, seed: Optional[int] = None) -> Layer:
+    """Draw codebooks, codes and scales for ``spec`` (steps 1-3 of the recipe)."""
+    rng = np.random.Generator(np.random.PCG64(spec.seed if seed is None else seed))
+    M, B, g = spec.M, spec.B, spec.g
+    if spec.d_in % g:
+        raise ValueError("d_in must be a multiple of g")
+    cb = rng.normal(0.0, 0.02 / np.sqrt(M), size=(M, 1 << B, g))
+    codebooks = float_to_f16_bits(cb)
+    code_dt = np.uint8 if B <= 8 else np.uint16
+    codes = rng.integers(0, 1 << B, size=(M, spec.d_out, spec.d_in // g), dtype=np.int64).astype(code_dt)
+    scales = float_to_f16_bits(rng.uniform(0.5, 1.5, size=spec.d_out))
+    return Layer(spec, codes, codebooks, scales, rng)
+
+
+def make_activations(layer: Layer, rows: int, dtype: Optional[str] = None,
+                     heavy_tail: Optional[bool] = None) -> np.ndarray:
+    """Draw ``rows`` activation vectors of length d_in (step 4 of the recipe).
+
+    Returns the bit patterns as uint16 in the requested storage dtype.
+    """
+    spec = layer.spec
+    dtype = dtype or spec.act_dtype
+    heavy = spec.heavy_tail if heavy_tail is None else heavy_tail
+    x = layer.rng.normal(0.0, 1.0, size=(rows, spec.d_in))
+    if heavy:
+        n_out = int(round(0.001 * rows * spec.d_in))
+        pos = layer.rng.choice(rows * spec.d_in, size=n_out, replace=False)
+        x.reshape(-1)[pos] *= 20.0
+    if dtype == "f16":
+        return float_to_f16_bits(x)
+    if dtype == "bf16":
+        return float_to_bf16_bits(x)
+    raise ValueError(dtype)
+
+
+# The five workloads. Config 3 is a pair of layers (up and down projection).
+CONFIGS: List[LayerSpec] = [
+    LayerSpec("c1_1024x1024", 1024, 1024, seed=1, act_dtype="f16", batches=(1,)),
+    LayerSpec("c2_4096x4096", 4096, 4096, seed=2, act_dtype="f16", batches=(1, 4)),
+    LayerSpec("c3_up_11008x4096", 11008, 4096, seed=31, act_dtype="bf16", batches=(1, 8, 16), heavy_tail=True),
+    LayerSpec("c3_down_4096x11008", 4096, 11008, seed=32, act_dtype="bf16", batches=(1, 8, 16), heavy_tail=True),
+    LayerSpec("c4_14336x4096_B16", 14336, 4096, M=2, B=16, seed=4, act_dtype="f16", batches=(1,), ks=(1, 2)),
+    LayerSpec("c5_gemm_2048x4096x4096", 4096, 4096, seed=5, act_dtype="bf16", n_tokens=2048),
+]
+
+
+def config(name: str) -> LayerSpec:
+    for c in CONFIGS:
+        if c.name == name or c.name.startswith(name + "_"):
+            return c
+    raise KeyError(name)
