@@ -1,0 +1,288 @@
+"""Benchmark of the multi-bitwidth additive-codebook linear layer on one MI355X.
+
+One step is one pass of the whole hot path over a stack of R resident copies of the
+workload layer (R distinct weight sets, like R layers of a model, so that the working set
+exceeds the 256 MB Infinity Cache and every launch streams its codes from HBM):
+
+  for k in 1..4:   decode GEMV at batch 1 and batch 4   (4096 x 4096, M = 4, uint8 codes, fp16 x/y)
+                   dequantization to bf16                 (same layers)
+                   prefill GEMM, 2048 bf16 tokens          (4096 x 4096 layer, bf16 out)
+
+Each (operation, k, batch) runs as a burst of R launches captured in a HIP graph and timed
+with HIP events on the launch stream; the per-launch time is burst time / R.
+
+`value` is the decode GEMV throughput in algorithmic GB/s (code planes 0..k-1, their
+codebooks, scales, x and y) over all GEMV launches of the timed steps. `roofline` describes the
+GEMV kernel at batch 1, k = 4 (HBM-bound); `roofline_gemm` the prefill GEMM at k = 4
+(MFMA-bound). The CPU baseline is the fp64 oracle timed on a bounded sample.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--copies", type=int, default=64, help="resident layer copies per GEMV step")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no multi-GPU "
+              f"path; see DESIGN.md for how the layer would shard", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_12876_amd as A
+    from workloads import config, make_layer, make_activations
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    def to_dev(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+
+    # ---------------------------------------------------------------- decode workload
+    spec = config("c2")
+    R = args.copies
+    d_out, d_in, M = spec.d_out, spec.d_in, spec.M
+    log(f"creating {R} copies of the {d_out}x{d_in} M={M} layer")
+    base = make_layer(spec)
+    layers, xs1, xs4, ys1, ys4 = [], [], [], [], []
+    rng = np.random.default_rng(1234)
+    desc = A.make_desc(d_out, d_in, M, 8)
+    for r in range(R):
+        # copy r: the seeded layer with its code planes permuted along rows (distinct bytes, same statistics)
+        codes = base.codes if r == 0 else np.ascontiguousarray(np.roll(base.codes, r * 61, axis=1))
+        layers.append(A.create(desc, to_dev(codes), to_dev(base.codebooks), to_dev(base.scales)))
+    x1 = make_activations(base, 1, "f16")
+    x4 = make_activations(base, 4, "f16")
+    for r in range(R):
+        xs1.append(to_dev(x1).view(torch.float16))
+        xs4.append(to_dev(x4).view(torch.float16))
+        ys1.append(torch.empty((1, d_out), dtype=torch.float16, device=dev))
+        ys4.append(torch.empty((4, d_out), dtype=torch.float16, device=dev))
+    n_w = 16
+    Ws = [torch.empty((d_out, d_in), dtype=torch.bfloat16, device=dev) for _ in range(n_w)]
+
+    # ---------------------------------------------------------------- prefill workload
+    gspec = config("c5")
+    n_tok = gspec.n_tokens
+    G_COPIES = 4
+    if not args.no_gemm:
+        gl = make_layer(gspec)
+        gdesc = A.make_desc(gspec.d_out, gspec.d_in, gspec.M, 8)
+        glayers = [A.create(gdesc, to_dev(gl.codes if r == 0 else np.roll(gl.codes, r * 61, axis=1)),
+                            to_dev(gl.codebooks), to_dev(gl.scales)) for r in range(G_COPIES)]
+        Xg = to_dev(make_activations(gl, n_tok, "bf16")).view(torch.bfloat16)
+        Yg = [torch.empty((n_tok, gspec.d_out), dtype=torch.bfloat16, device=dev) for _ in range(G_COPIES)]
+    torch.cuda.synchronize()
+
+    ks = list(spec.ks)
+
+    def gemv_burst(k, b):
+        for r in range(R):
+            x, y = (xs1[r], ys1[r]) if b == 1 else (xs4[r], ys4[r])
+            A.gemv(layers[r], k, x, A.DType.F16, b, y, A.DType.F16)
+
+    def dequant_burst(k):
+        for r in range(n_w):
+            A.dequant(layers[r], k, Ws[r], A.DType.BF16)
+
+    def gemm_burst(k):
+        for r in range(G_COPIES):
+            A.gemm(glayers[r], k, Xg, n_tok, Yg[r], A.DType.BF16)
+
+    ops = []  # (name, k, b, fn, launches)
+    for k in ks:
+        ops.append(("gemv", k, 1, lambda k=k: gemv_burst(k, 1), R))
+        ops.append(("gemv", k, 4, lambda k=k: gemv_burst(k, 4), R))
+        ops.append(("dequant", k, 0, lambda k=k: dequant_burst(k), n_w))
+        if not args.no_gemm:
+            ops.append(("gemm", k, n_tok, lambda k=k: gemm_burst(k), G_COPIES))
+
+    # Eager reference outputs for the graph check below.
+    gemv_burst(4, 1)
+    torch.cuda.synchronize()
+    eager_y = ys1[0].clone()
+
+    # Capture each burst in a HIP graph (the library only launches kernels on the given stream).
+    graphs = []
+    for (name, k, b, fn, n) in ops:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        graphs.append(g)
+    torch.cuda.synchronize()
+
+    def gemv_bytes(k, b):
+        return k * (d_out * d_in // 8) + k * 256 * 8 * 2 + 2 * d_out + 2 * b * (d_in + d_out)
+
+    def run_step(record):
+        for i, g in enumerate(graphs):
+            if record is not None:
+                e0, e1 = record[i]
+                e0.record(stream)
+                g.replay()
+                e1.record(stream)
+            else:
+                g.replay()
+
+    for w in range(args.warmup):
+        run_step(None)
+    torch.cuda.synchronize()
+    # every replay recomputes the same outputs: check the graph against the eager result
+    ys1[0].zero_()
+    graphs[[i for i, o in enumerate(ops) if o[0] == "gemv" and o[1] == 4 and o[2] == 1][0]].replay()
+    torch.cuda.synchronize()
+    assert torch.equal(ys1[0], eager_y), "graph replay differs from the eager GEMV"
+
+    events = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        run_step(events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_op_ms = np.zeros(len(ops))
+    for s in range(args.steps):
+        for i, (e0, e1) in enumerate(events[s]):
+            per_op_ms[i] += e0.elapsed_time(e1)
+    per_launch_us = {}
+    for i, (name, k, b, fn, n) in enumerate(ops):
+        per_launch_us[(name, k, b)] = per_op_ms[i] * 1e3 / (args.steps * n)
+
+    gemv_total_bytes = sum(gemv_bytes(k, b) * R for (name, k, b, fn, n) in ops if name == "gemv")
+    gemv_total_us = sum(per_launch_us[(name, k, b)] * R for (name, k, b, fn, n) in ops if name == "gemv")
+    value = gemv_total_bytes / (gemv_total_us * 1e-6) / 1e9
+    per_k = {}
+    for k in ks:
+        e = {}
+        for b in (1, 4):
+            t = per_launch_us[("gemv", k, b)]
+            e[f"gemv_b{b}_us"] = round(t, 3)
+            e[f"gemv_b{b}_GBps"] = round(gemv_bytes(k, b) / (t * 1e-6) / 1e9, 1)
+            e[f"gemv_b{b}_frac_hbm"] = round(gemv_bytes(k, b) / (t * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+        t = per_launch_us[("dequant", k, 0)]
+        dq_bytes = k * d_out * d_in // 8 + k * 4096 + 2 * d_out + 2 * d_out * d_in
+        e["dequant_us"] = round(t, 3)
+        e["dequant_GBps"] = round(dq_bytes / (t * 1e-6) / 1e9, 1)
+        if not args.no_gemm:
+            t = per_launch_us[("gemm", k, n_tok)]
+            fl = 2.0 * n_tok * gspec.d_out * gspec.d_in
+            e["gemm_us"] = round(t, 2)
+            e["gemm_TFLOPs"] = round(fl / (t * 1e-6) / 1e12, 1)
+            e["gemm_frac_bf16_peak"] = round(fl / (t * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)
+        per_k[str(k)] = e
+
+    t_dom = per_launch_us[("gemv", 4, 1)]
+    ach = gemv_bytes(4, 1) / (t_dom * 1e-6) / 1e9
+    roofline = {"bound": "hbm", "kernel": "gemv_lut_kernel<K=4,BT=1> (k=4, batch 1)", "achieved": round(ach, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
+                "traffic": None, "bytes_per_launch": gemv_bytes(4, 1), "us_per_launch": round(t_dom, 3)}
+    out = {
+        "metric": "code-plane GEMV HBM GB/s (% peak) per bitwidth k; prefill GEMM TFLOP/s",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"decode GEMV {d_out}x{d_in}, M={M} codebooks of 256x8 fp16, uint8 codes, "
+                               f"fp16 x/y, batch 1 and 4, k=1..4; per k also dequant to bf16 and a "
+                               f"{n_tok}-token bf16 prefill GEMM on a {gspec.d_out}x{gspec.d_in} layer",
+                   "layer_copies": R, "launch": "HIP graph per burst of copies", "codes": "uint8",
+                   "accumulate": "fp32"},
+        "per_k": per_k,
+        "roofline": roofline,
+    }
+    if not args.no_gemm:
+        tg = per_launch_us[("gemm", 4, n_tok)]
+        fl = 2.0 * n_tok * gspec.d_out * gspec.d_in
+        achg = fl / (tg * 1e-6) / 1e12
+        out["roofline_gemm"] = {"bound": "mfma", "kernel": "gemm_kernel (k=4)", "achieved": round(achg, 1),
+                                "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achg / BF16_PEAK_TFLOPS, 4),
+                                "traffic": None, "us_per_launch": round(tg, 2)}
+        gemm_total_us = sum(per_launch_us[("gemm", k, n_tok)] for k in ks)
+        out["gemm_TFLOPs"] = round(len(ks) * fl / (gemm_total_us * 1e-6) / 1e12, 1)
+    step_us = {n: 0.0 for n in ("gemv", "dequant", "gemm")}
+    for i, (name, k, b, fn, n) in enumerate(ops):
+        step_us[name] += per_op_ms[i] * 1e3 / args.steps
+    tot = sum(step_us.values())
+    out["time_share"] = {n: round(v / tot, 4) for n, v in step_us.items() if v > 0}
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(base, x1, x4, ks, gemv_bytes)
+
+    for h in layers:
+        A.destroy(h)
+    if not args.no_gemm:
+        for h in glayers:
+            A.destroy(h)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(layer, x1bits, x4bits, ks, gemv_bytes):
+    """The fp64 oracle on the host cores: reconstruct W_k and multiply, for batch 1 and 4 at every k,
+    repeated until about 10 s have passed; reported in the GEMV's algorithmic GB/s."""
+    import oracle
+    from oracle import formats
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    C = formats.f16_bits_to_f64(layer.codebooks)
+    s = formats.f16_bits_to_f64(layer.scales)
+    x1 = formats.f16_bits_to_f64(x1bits)
+    x4 = formats.f16_bits_to_f64(x4bits)
+    total_bytes, t_total, passes = 0, 0.0, 0
+    t_start = time.perf_counter()
+    while True:
+        for k in ks:
+            t0 = time.perf_counter()
+            oracle.linear(x1, layer.codes, C, s, k)
+            oracle.linear(x4, layer.codes, C, s, k)
+            t_total += time.perf_counter() - t0
+            total_bytes += gemv_bytes(k, 1) + gemv_bytes(k, 4)
+        passes += 1
+        if time.perf_counter() - t_start > 10.0:
+            break
+    return {"value": round(total_bytes / t_total / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
+            "kind": "oracle",
+            "sample": f"{passes} pass(es) of: reconstruct W_k in fp64 and multiply, batch 1 and 4, k=1..4, "
+                      f"one {layer.spec.d_out}x{layer.spec.d_in} layer (gather single-threaded, product on BLAS)",
+            "seconds": round(t_total, 2), "host_cpus": len(os.sched_getaffinity(0))}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,149 @@
+/*
+ * aqmb - multi-bitwidth additive-codebook linear layers on AMD Instinct MI355X (gfx950).
+ *
+ * A quantized linear layer stores a weight matrix W (d_out rows, d_in columns) as
+ *   - M code planes: plane m holds, for every output row i and input group j
+ *     (g consecutive weights of row i), the index b_{ijm} of a codeword of codebook m;
+ *   - M codebooks C_0..C_{M-1}, each 2^B codewords of g fp16 values;
+ *   - one fp16 scale s_i per output row.
+ * At precision level k (1 <= k <= M) the layer uses only the first k codebooks:
+ *   W_k[i, j*g + t] = s_i * sum_{m<k} C_m[b_{ijm}][t]
+ * (Drop-by-Drop, section 5: partial reconstruction from the first k codebooks;
+ * section 3.2: groups are consecutive along d_in and concatenated; the per-row
+ * scale is the "Scales: d_out*16" term of the size estimate in appendix C).
+ * One stored set of codes serves every k; planes m >= k are never read.
+ *
+ * Conventions for every entry point:
+ *   - Data pointers passed to aqmb_create/gemv/gemm/dequant are DEVICE pointers on
+ *     the current HIP device. Row-major, densely packed, 16-byte aligned
+ *     (x, y, X, Y, W, codes, codebooks and scales).
+ *   - `stream` is a hipStream_t (0 = the null stream). gemv/gemm/dequant only
+ *     enqueue work on it and return; results are valid once the stream is synced.
+ *   - Arguments are validated on the host before anything is enqueued. On any
+ *     error nothing is launched and no output byte is written; the status says
+ *     why and aqmb_last_error() gives a message for the calling thread.
+ *   - No exception or abort crosses this interface.
+ *   - A layer is read-only for gemm and dequant, which may run concurrently on
+ *     different streams. aqmb_gemv uses a per-layer workspace: gemv calls on one
+ *     layer must be ordered (one stream, or synchronised by the caller).
+ */
+#ifndef AQMB_H
+#define AQMB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct aqmb_layer_s* aqmb_layer_t;
+typedef void* aqmb_stream_t; /* a hipStream_t */
+
+typedef enum {
+  AQMB_OK = 0,
+  AQMB_EINVAL = 1,        /* bad argument: null pointer, k outside [1, M], sizes that do not fit */
+  AQMB_EUNSUPPORTED = 2,  /* valid in the method but not implemented: g != 8, B not 8 or 16, batch > 16, dtype */
+  AQMB_ENOMEM = 3,        /* device allocation failed */
+  AQMB_EHIP = 4           /* a HIP runtime call or kernel launch failed; see aqmb_last_error() */
+} aqmb_status;
+
+typedef enum { AQMB_F16 = 0, AQMB_BF16 = 1, AQMB_F32 = 2 } aqmb_dtype;
+
+typedef struct {
+  int32_t d_out;          /* output rows of W, >= 1 */
+  int32_t d_in;           /* input columns of W, >= g, a multiple of g */
+  int32_t group_size;     /* g: weights per group; 8 is supported */
+  int32_t num_codebooks;  /* M: 1..8 */
+  int32_t code_bits;      /* B: 8 (uint8 codes, 256 codewords) or 16 (uint16 codes, 65536 codewords) */
+} aqmb_desc;
+
+/* Largest batch accepted by aqmb_gemv. */
+#define AQMB_MAX_BATCH 16
+
+/*
+ * Create a layer from device buffers (Alg. 1 stores a layer as AQLMFormat(C, b, s)).
+ *   codes     [M][d_out][d_in/g] uint8 (B = 8) or uint16 (B = 16): plane-major.
+ *   codebooks [M][2^B][g] fp16 bit patterns; codeword c of codebook m is g contiguous values.
+ *   scales    [d_out] fp16 bit patterns.
+ * The library copies everything into device memory it owns, re-tiling the codes
+ * inside each plane for coalesced reads while keeping planes outermost, so that
+ * level k reads only the first k planes. Synchronous: returns after the copy on
+ * `stream` has finished; the caller may free its buffers afterwards.
+ * Code values >= 2^B cannot occur for B = 8 or 16 (they fill their type).
+ * Errors: EINVAL (null pointer, bad sizes), EUNSUPPORTED (g, B or M not supported),
+ * ENOMEM, EHIP. On error *out is set to NULL.
+ */
+aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* codes,
+                        const uint16_t* codebooks, const uint16_t* scales, aqmb_stream_t stream);
+
+/* Free a layer and its device memory (waits for the device first). NULL is a no-op.
+ * EINVAL for a handle that is not a live layer. */
+aqmb_status aqmb_destroy(aqmb_layer_t layer);
+
+/* Copy the layer's descriptor into *out. EINVAL for a bad handle or a null out. */
+aqmb_status aqmb_get_desc(aqmb_layer_t layer, aqmb_desc* out);
+
+/*
+ * Decode GEMV: y[b][i] = sum_t x[b][t] * W_k[i][t] for b < batch (section 5 reconstruction,
+ * applied as a product without forming W_k).
+ *   x  [batch][d_in],  dtype x_dtype in {F16, BF16}
+ *   y  [batch][d_out], dtype y_dtype in {F16, BF16, F32}
+ * Products and sums are carried in fp32; the result is rounded once to y_dtype
+ * (round to nearest even). 1 <= batch <= AQMB_MAX_BATCH.
+ * Errors: EINVAL (bad handle, null pointer, k outside [1, M], batch < 1),
+ * EUNSUPPORTED (batch > AQMB_MAX_BATCH, dtype), EHIP.
+ */
+aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch,
+                      void* y, aqmb_dtype y_dtype, aqmb_stream_t stream);
+
+/*
+ * Prefill GEMM: Y[n][i] = s_i * sum_t X[n][t] * Wb_k[i][t] for n < n_tokens, where Wb_k is the
+ * unscaled reconstruction sum_{m<k} C_m[b_{ijm}] formed as a binary32 left fold over m and
+ * rounded to nearest-even bf16 (the operand fed to bf16 matrix cores); accumulation is fp32.
+ *   X  [n_tokens][d_in]  bf16
+ *   Y  [n_tokens][d_out] dtype y_dtype in {BF16, F32}
+ * Requires B = 8. Errors: EINVAL (bad handle, null pointer, k outside [1, M], n_tokens < 1),
+ * EUNSUPPORTED (B = 16, dtype), EHIP.
+ */
+aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y,
+                      aqmb_dtype y_dtype, aqmb_stream_t stream);
+
+/*
+ * Dequantize: W[i][t] = W_k[i][t] in w_dtype in {F16, BF16, F32}, bit-exact to this evaluation
+ * order: each fp16 codebook entry is taken exactly to binary32; the entries of planes
+ * 0..k-1 are summed as a binary32 left fold (C_0 + C_1, then + C_2, ...), each sum rounded
+ * to nearest even; the fold is multiplied by s_i in binary32 (one rounding, no fused
+ * multiply-add); the product is rounded to nearest even into w_dtype. Subnormals are kept.
+ *   W  [d_out][d_in]
+ * Errors: EINVAL (bad handle, null pointer, k outside [1, M]), EUNSUPPORTED (dtype), EHIP.
+ */
+aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype, aqmb_stream_t stream);
+
+/*
+ * Average storage bits per weight at level k (appendix C, Eq. avg_bits): codebooks
+ * 16*g*k*2^B bits, codes d_out*(d_in/g)*B bits per used plane, scales 16*d_out bits,
+ * over d_out*d_in weights. The printed codes term lacks the per-plane factor; the
+ * worked example there (about 2.002 bits for d_in=8192, d_out=28672, g=8, M=2, B=8)
+ * needs it. Returns a negative value for a null or invalid descriptor or k outside [1, M].
+ */
+double aqmb_bits_per_weight(const aqmb_desc* desc, int k);
+
+/* Static description of a status code. Never NULL. */
+const char* aqmb_strerror(aqmb_status status);
+
+/* Message describing the last error on the calling thread ("" if none). Never NULL. */
+const char* aqmb_last_error(void);
+
+/* Validate arguments exactly as the entry points do, without touching the GPU.
+ * op: 0 = gemv, 1 = gemm, 2 = dequant. For gemv `n` is the batch, for gemm the
+ * token count, ignored for dequant; `in_dtype` is x's dtype (gemv only) and
+ * `out_dtype` the output dtype. Returns the status the entry point would return
+ * before launching anything. */
+aqmb_status aqmb_validate(const aqmb_desc* desc, int op, int k, int n, aqmb_dtype in_dtype,
+                          aqmb_dtype out_dtype, const void* in, const void* out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AQMB_H */

@@ -1,0 +1,249 @@
+"""aqmb: multi-bitwidth additive-codebook linear layers on MI355X (gfx950).
+
+Thin ctypes binding over ``libaqmb.so`` (``include/aqmb.h``). The functions here have the
+C names without the ``aqmb_`` prefix and only marshal arguments: every step of the
+computation runs in the library's HIP kernels. PyTorch tensors are accepted for device
+buffers and the current PyTorch stream is used when no stream is given; PyTorch is plumbing
+(allocation and streams), not part of the computation.
+
+If the library has not been built, importing this package fails loudly: there is no
+fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import enum
+import os
+from typing import Optional
+
+__all__ = ["Status", "DType", "Desc", "AqmbError", "lib", "create", "destroy", "get_desc", "gemv", "gemm",
+           "dequant", "bits_per_weight", "strerror", "last_error", "validate", "QuantLinear", "LIB_PATH"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libaqmb.so")
+
+
+class Status(enum.IntEnum):
+    OK = 0
+    EINVAL = 1
+    EUNSUPPORTED = 2
+    ENOMEM = 3
+    EHIP = 4
+
+
+class DType(enum.IntEnum):
+    F16 = 0
+    BF16 = 1
+    F32 = 2
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("d_out", ctypes.c_int32), ("d_in", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("num_codebooks", ctypes.c_int32), ("code_bits", ctypes.c_int32)]
+
+
+class AqmbError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        self.status = Status(status)
+        super().__init__(f"{where}: {self.status.name}: {message}")
+
+
+def _load() -> ctypes.CDLL:
+    # One HIP runtime per process: PyTorch ships its own libamdhip64 (same SONAME). Importing
+    # torch first makes the library bind to that runtime, so device pointers, streams and
+    # devices are shared; loading the library first would start a second runtime.
+    import torch  # noqa: F401
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2606_12876_amd.build "
+                          f"or __graft_entry__.build()); there is no fallback implementation")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, st = ctypes.c_void_p, ctypes.c_int, ctypes.c_int
+    L.aqmb_create.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(Desc), vp, vp, vp, vp]
+    L.aqmb_destroy.argtypes = [vp]
+    L.aqmb_get_desc.argtypes = [vp, ctypes.POINTER(Desc)]
+    L.aqmb_gemv.argtypes = [vp, i32, vp, i32, i32, vp, i32, vp]
+    L.aqmb_gemm.argtypes = [vp, i32, vp, i32, vp, i32, vp]
+    L.aqmb_dequant.argtypes = [vp, i32, vp, i32, vp]
+    L.aqmb_validate.argtypes = [ctypes.POINTER(Desc), i32, i32, i32, i32, i32, vp, vp]
+    L.aqmb_bits_per_weight.argtypes = [ctypes.POINTER(Desc), i32]
+    L.aqmb_bits_per_weight.restype = ctypes.c_double
+    L.aqmb_strerror.argtypes = [i32]
+    L.aqmb_strerror.restype = ctypes.c_char_p
+    L.aqmb_last_error.argtypes = []
+    L.aqmb_last_error.restype = ctypes.c_char_p
+    for f in ("aqmb_create", "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemm", "aqmb_dequant",
+              "aqmb_validate"):
+        getattr(L, f).restype = st
+    return L
+
+
+lib = _load()
+
+
+def strerror(status: int) -> str:
+    return lib.aqmb_strerror(int(status)).decode()
+
+
+def last_error() -> str:
+    return lib.aqmb_last_error().decode()
+
+
+def _check(status: int, where: str):
+    if status != Status.OK:
+        raise AqmbError(status, where, last_error() or strerror(status))
+
+
+def _ptr(t) -> Optional[int]:
+    """Device address of a tensor (or an int address, or None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dtype(t, default=None) -> DType:
+    if isinstance(t, (DType, int)):
+        return DType(t)
+    import torch
+    m = {torch.float16: DType.F16, torch.bfloat16: DType.BF16, torch.float32: DType.F32}
+    if t.dtype not in m:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return m[t.dtype]
+
+
+def make_desc(d_out: int, d_in: int, num_codebooks: int, code_bits: int = 8, group_size: int = 8) -> Desc:
+    return Desc(d_out, d_in, group_size, num_codebooks, code_bits)
+
+
+def _nbytes(t) -> Optional[int]:
+    if hasattr(t, "numel") and hasattr(t, "element_size"):
+        return t.numel() * t.element_size()
+    return None
+
+
+def create(desc: Desc, codes, codebooks, scales, stream=None) -> int:
+    """aqmb_create: codes [M][d_out][d_in/g] uint8|uint16, codebooks [M][2^B][g] fp16 bits,
+    scales [d_out] fp16 bits, all device buffers. Returns the layer handle.
+
+    The C library sees raw pointers; when tensors are passed their sizes are checked here so
+    that a short buffer is rejected instead of read past its end."""
+    g = desc.group_size if desc.group_size > 0 else 1
+    need = {"codes": desc.num_codebooks * desc.d_out * (desc.d_in // g) * (1 if desc.code_bits <= 8 else 2),
+            "codebooks": desc.num_codebooks * (1 << max(0, min(desc.code_bits, 16))) * desc.group_size * 2,
+            "scales": desc.d_out * 2}
+    for name, t in (("codes", codes), ("codebooks", codebooks), ("scales", scales)):
+        n = _nbytes(t)
+        if n is not None and n < need[name]:
+            raise AqmbError(Status.EINVAL, "aqmb_create", f"{name} holds {n} bytes, the descriptor needs {need[name]}")
+    h = ctypes.c_void_p()
+    _check(lib.aqmb_create(ctypes.byref(h), ctypes.byref(desc), _ptr(codes), _ptr(codebooks), _ptr(scales),
+                           _stream(stream)), "aqmb_create")
+    return h.value
+
+
+def destroy(layer: int) -> None:
+    _check(lib.aqmb_destroy(layer), "aqmb_destroy")
+
+
+def get_desc(layer: int) -> Desc:
+    d = Desc()
+    _check(lib.aqmb_get_desc(layer, ctypes.byref(d)), "aqmb_get_desc")
+    return d
+
+
+_ELEM = {0: 2, 1: 2, 2: 4}
+
+
+def _need(t, n_elems: int, dtype, what: str, where: str):
+    n = _nbytes(t)
+    if n is not None and int(dtype) in _ELEM and n < n_elems * _ELEM[int(dtype)]:
+        raise AqmbError(Status.EINVAL, where, f"{what} holds {n} bytes, needs {n_elems * _ELEM[int(dtype)]}")
+
+
+def gemv(layer: int, k: int, x, x_dtype, batch: int, y, y_dtype, stream=None) -> None:
+    d = get_desc(layer)
+    if 1 <= batch <= 16:
+        _need(x, batch * d.d_in, x_dtype, "x", "aqmb_gemv")
+        _need(y, batch * d.d_out, y_dtype, "y", "aqmb_gemv")
+    _check(lib.aqmb_gemv(layer, k, _ptr(x), int(x_dtype), batch, _ptr(y), int(y_dtype), _stream(stream)),
+           "aqmb_gemv")
+
+
+def gemm(layer: int, k: int, X, n_tokens: int, Y, y_dtype, stream=None) -> None:
+    d = get_desc(layer)
+    if n_tokens >= 1:
+        _need(X, n_tokens * d.d_in, DType.BF16, "X", "aqmb_gemm")
+        _need(Y, n_tokens * d.d_out, y_dtype, "Y", "aqmb_gemm")
+    _check(lib.aqmb_gemm(layer, k, _ptr(X), n_tokens, _ptr(Y), int(y_dtype), _stream(stream)), "aqmb_gemm")
+
+
+def dequant(layer: int, k: int, W, w_dtype, stream=None) -> None:
+    d = get_desc(layer)
+    _need(W, d.d_out * d.d_in, w_dtype, "W", "aqmb_dequant")
+    _check(lib.aqmb_dequant(layer, k, _ptr(W), int(w_dtype), _stream(stream)), "aqmb_dequant")
+
+
+def bits_per_weight(desc: Desc, k: int) -> float:
+    return float(lib.aqmb_bits_per_weight(ctypes.byref(desc), k))
+
+
+def validate(desc: Desc, op: int, k: int, n: int, in_dtype, out_dtype, inp, out) -> Status:
+    return Status(lib.aqmb_validate(ctypes.byref(desc), op, k, n, int(in_dtype), int(out_dtype), _ptr(inp), _ptr(out)))
+
+
+class QuantLinear:
+    """A quantized linear layer y = x . W_k^T served at any precision level k <= M.
+
+    Holds the library's layer handle; ``forward`` allocates the output with PyTorch and calls
+    the library on the current stream.
+    """
+
+    def __init__(self, codes, codebooks, scales, group_size: int = 8):
+        import torch
+        M, d_out, n_groups = codes.shape
+        code_bits = 8 if codes.dtype == torch.uint8 else 16
+        self.desc = make_desc(d_out, n_groups * group_size, M, code_bits, group_size)
+        self.handle = create(self.desc, codes.contiguous(), codebooks.contiguous().view(torch.int16),
+                             scales.contiguous().view(torch.int16))
+        self.M, self.d_out, self.d_in = M, d_out, n_groups * group_size
+
+    def forward(self, x, k: int, out_dtype=None):
+        import torch
+        out_dtype = out_dtype or x.dtype
+        lead = x.shape[:-1]
+        x2 = x.reshape(-1, self.d_in).contiguous()
+        n = x2.shape[0]
+        y = torch.empty((n, self.d_out), dtype=out_dtype, device=x.device)
+        if n <= 16:
+            gemv(self.handle, k, x2, _dtype(x2), n, y, _dtype(y))
+        else:
+            gemm(self.handle, k, x2, n, y, _dtype(y))
+        return y.reshape(*lead, self.d_out)
+
+    __call__ = forward
+
+    def dequant(self, k: int, dtype=None):
+        import torch
+        W = torch.empty((self.d_out, self.d_in), dtype=dtype or torch.float16, device="cuda")
+        dequant(self.handle, k, W, _dtype(W))
+        return W
+
+    def close(self):
+        if self.handle:
+            destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

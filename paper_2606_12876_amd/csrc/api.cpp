@@ -1,0 +1,173 @@
+// The C-ABI entry points: layer registry, creation (copy + re-tile), dispatch.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <new>
+#include <unordered_set>
+
+#include "launch.h"
+#include "layer.h"
+
+namespace aqmb {
+aqmb_status fail(aqmb_status s, const char* fmt, ...);
+void clear_error();
+aqmb_status validate_desc(const aqmb_desc* d);
+aqmb_status validate_call(const aqmb_desc* d, int op, int k, int n, aqmb_dtype in_dt, aqmb_dtype out_dt,
+                          const void* in, const void* out);
+
+static std::mutex g_mu;
+static std::unordered_set<Layer*> g_live;
+
+static bool is_live(Layer* L) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  return L && g_live.count(L) && L->magic == kMagic;
+}
+
+static aqmb_status hip_fail(hipError_t e, const char* what) {
+  return fail(AQMB_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+static void free_layer(Layer* L) {
+  if (L->codes) (void)hipFree(L->codes);
+  if (L->codebooks) (void)hipFree(L->codebooks);
+  if (L->scales) (void)hipFree(L->scales);
+  if (L->ws) (void)hipFree(L->ws);
+  L->magic = 0;
+  delete L;
+}
+
+// The layer's memory lives on one device; launching on another would address foreign memory.
+static aqmb_status check_device(const Layer* L) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != L->device) return fail(AQMB_EINVAL, "layer lives on device %d but device %d is current", L->device, dev);
+  return AQMB_OK;
+}
+
+}  // namespace aqmb
+
+using namespace aqmb;
+
+extern "C" {
+
+aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* codes, const uint16_t* codebooks,
+                        const uint16_t* scales, aqmb_stream_t stream) {
+  clear_error();
+  if (!out) return fail(AQMB_EINVAL, "create: out is NULL");
+  *out = nullptr;
+  aqmb_status s = validate_desc(desc);
+  if (s != AQMB_OK) return s;
+  if (!codes || !codebooks || !scales) return fail(AQMB_EINVAL, "create: codes, codebooks or scales is NULL");
+  hipStream_t st = (hipStream_t)stream;
+
+  Layer* L = new (std::nothrow) Layer();
+  if (!L) return fail(AQMB_ENOMEM, "create: host allocation failed");
+  L->magic = kMagic;
+  L->d = *desc;
+  hipError_t e = hipGetDevice(&L->device);
+  if (e != hipSuccess) { free_layer(L); return hip_fail(e, "create: hipGetDevice"); }
+  const int code_size = desc->code_bits == 8 ? 1 : 2;
+  L->G = desc->d_in / desc->group_size;
+  L->J = kSliceBytes / code_size;
+  L->S = (L->G + L->J - 1) / L->J;
+  L->plane_bytes = (size_t)L->S * desc->d_out * kSliceBytes;
+  const size_t n_codewords = (size_t)1 << desc->code_bits;
+  const size_t cb_bytes = (size_t)desc->num_codebooks * n_codewords * desc->group_size * 2;
+  L->ws_floats = gemv_workspace_floats(*desc, L->G, L->S);
+
+  struct { void** p; size_t n; const char* what; } allocs[] = {
+      {(void**)&L->codes, (size_t)desc->num_codebooks * L->plane_bytes, "codes"},
+      {(void**)&L->codebooks, cb_bytes, "codebooks"},
+      {(void**)&L->scales, (size_t)desc->d_out * 2, "scales"},
+      {(void**)&L->ws, L->ws_floats * sizeof(float), "workspace"},
+  };
+  for (auto& a : allocs) {
+    e = hipMalloc(a.p, a.n);
+    if (e != hipSuccess) {
+      *a.p = nullptr;
+      (void)hipGetLastError();
+      free_layer(L);
+      return fail(AQMB_ENOMEM, "create: hipMalloc(%zu) for %s failed: %s", a.n, a.what, hipGetErrorString(e));
+    }
+  }
+  // The workspace holds per-call partial sums and arrival counters that every gemv
+  // call leaves at zero; they start at zero here.
+  if ((e = hipMemsetAsync(L->ws, 0, L->ws_floats * sizeof(float), st)) != hipSuccess ||
+      (e = hipMemcpyAsync(L->codebooks, codebooks, cb_bytes, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
+      (e = hipMemcpyAsync(L->scales, scales, (size_t)desc->d_out * 2, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
+      (e = launch_retile(*L, codes, st)) != hipSuccess || (e = hipStreamSynchronize(st)) != hipSuccess) {
+    free_layer(L);
+    return hip_fail(e, "create: upload");
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_live.insert(L);
+  }
+  *out = (aqmb_layer_t)L;
+  return AQMB_OK;
+}
+
+aqmb_status aqmb_destroy(aqmb_layer_t layer) {
+  clear_error();
+  if (!layer) return AQMB_OK;
+  Layer* L = (Layer*)layer;
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_live.count(L) || L->magic != kMagic) return fail(AQMB_EINVAL, "destroy: not a live layer");
+    g_live.erase(L);
+  }
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(L->device);
+  hipError_t e = hipDeviceSynchronize();
+  free_layer(L);
+  if (prev >= 0) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_fail(e, "destroy: hipDeviceSynchronize");
+  return AQMB_OK;
+}
+
+aqmb_status aqmb_get_desc(aqmb_layer_t layer, aqmb_desc* out) {
+  clear_error();
+  if (!is_live((Layer*)layer)) return fail(AQMB_EINVAL, "get_desc: not a live layer");
+  if (!out) return fail(AQMB_EINVAL, "get_desc: out is NULL");
+  *out = ((Layer*)layer)->d;
+  return AQMB_OK;
+}
+
+aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                      aqmb_dtype y_dtype, aqmb_stream_t stream) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "gemv: not a live layer");
+  aqmb_status s = validate_call(&L->d, 0, k, batch, x_dtype, y_dtype, x, y);
+  if (s != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  hipError_t e = launch_gemv(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv: launch");
+}
+
+aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
+                      aqmb_stream_t stream) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "gemm: not a live layer");
+  aqmb_status s = validate_call(&L->d, 1, k, n_tokens, AQMB_BF16, y_dtype, X, Y);
+  if (s != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  hipError_t e = launch_gemm(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemm: launch");
+}
+
+aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype, aqmb_stream_t stream) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "dequant: not a live layer");
+  aqmb_status s = validate_call(&L->d, 2, k, 0, AQMB_F16, w_dtype, nullptr, W);
+  if (s != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  hipError_t e = launch_dequant(*L, k, W, w_dtype, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "dequant: launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,66 @@
+// Device-side helpers shared by the kernels: 16-bit float conversions, vector types,
+// wave-size constants. Everything here is written for gfx950 (wave64, CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "../../include/aqmb.h"
+
+namespace aqmb {
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (read once: non-temporal hint).
+__device__ __forceinline__ uint4 load_stream16(const void* p) {
+  const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// fp16 bits -> fp32 (exact; fp16 subnormals become fp32 normals).
+__device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+__device__ __forceinline__ float f16lo(uint32_t w) { return f16_to_f32(w & 0xFFFFu); }
+__device__ __forceinline__ float f16hi(uint32_t w) { return f16_to_f32(w >> 16); }
+
+// bf16 bits -> fp32 (exact).
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xFFFF0000u); }
+
+// fp32 -> fp16 / bf16 bits, round to nearest even (the default rounding mode).
+__device__ __forceinline__ uint16_t f32_to_f16_bits(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16_bits(lo) | ((uint32_t)f32_to_bf16_bits(hi) << 16);
+}
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  return (uint32_t)f32_to_f16_bits(lo) | ((uint32_t)f32_to_f16_bits(hi) << 16);
+}
+
+// fp32 dot of two fp16 pairs plus an fp32 addend (products exact in fp32).
+__device__ __forceinline__ float dot2_f16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, a), __builtin_bit_cast(half2_t, b), c, false);
+}
+
+// Output element store for the three output dtypes.
+template <int DT> struct OutT;
+template <> struct OutT<AQMB_F16> {
+  static __device__ __forceinline__ void store(void* p, size_t i, float v) { ((uint16_t*)p)[i] = f32_to_f16_bits(v); }
+};
+template <> struct OutT<AQMB_BF16> {
+  static __device__ __forceinline__ void store(void* p, size_t i, float v) { ((uint16_t*)p)[i] = f32_to_bf16_bits(v); }
+};
+template <> struct OutT<AQMB_F32> {
+  static __device__ __forceinline__ void store(void* p, size_t i, float v) { ((float*)p)[i] = v; }
+};
+
+}  // namespace aqmb

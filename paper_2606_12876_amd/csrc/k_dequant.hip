@@ -1,0 +1,136 @@
+// Code re-tiling (layer creation) and the bit-exact dequantization kernel.
+#include "device.h"
+#include "launch.h"
+
+namespace aqmb {
+
+// [M][d_out][G] plane-major codes (1 or 2 bytes each) -> [M][S][d_out][16 bytes].
+template <int CS>
+__global__ __launch_bounds__(256) void retile_kernel(const unsigned char* __restrict__ in, unsigned char* __restrict__ out,
+                                                     int M, int d_out, int G, int S) {
+  constexpr int J = 16 / CS;
+  const size_t total = (size_t)M * S * d_out;
+  for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
+    const int i = (int)(q % d_out);
+    const size_t ms = q / d_out;
+    const int s = (int)(ms % S), m = (int)(ms / S);
+    unsigned char chunk[16];
+#pragma unroll
+    for (int jj = 0; jj < J; ++jj) {
+      const int j = s * J + jj;
+#pragma unroll
+      for (int b = 0; b < CS; ++b)
+        chunk[jj * CS + b] = j < G ? in[(((size_t)m * d_out + i) * G + j) * CS + b] : (unsigned char)0;
+    }
+    uint4 v;
+    __builtin_memcpy(&v, chunk, 16);
+    *(uint4*)(out + q * 16) = v;
+  }
+}
+
+hipError_t launch_retile(const Layer& L, const void* codes, hipStream_t st) {
+  const size_t total = (size_t)L.d.num_codebooks * L.S * L.d.d_out;
+  const unsigned grid = (unsigned)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
+  if (L.d.code_bits == 8)
+    retile_kernel<1><<<grid, 256, 0, st>>>((const unsigned char*)codes, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S);
+  else
+    retile_kernel<2><<<grid, 256, 0, st>>>((const unsigned char*)codes, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S);
+  return hipGetLastError();
+}
+
+// The stated evaluation order for W_k: binary32 left fold over planes, one binary32
+// multiply by the row scale, one rounding to the output format. Contraction into a
+// fused multiply-add is off so every step rounds on its own.
+#pragma clang fp contract(off)
+
+template <int OUT>
+__device__ __forceinline__ void store_group(void* W, size_t elem, const float (&w)[8]) {
+  if constexpr (OUT == AQMB_F32) {
+    float4* p = (float4*)((float*)W + elem);
+    p[0] = make_float4(w[0], w[1], w[2], w[3]);
+    p[1] = make_float4(w[4], w[5], w[6], w[7]);
+  } else if constexpr (OUT == AQMB_F16) {
+    *(uint4*)((uint16_t*)W + elem) = make_uint4(pack_f16x2(w[0], w[1]), pack_f16x2(w[2], w[3]),
+                                                pack_f16x2(w[4], w[5]), pack_f16x2(w[6], w[7]));
+  } else {
+    *(uint4*)((uint16_t*)W + elem) = make_uint4(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]),
+                                                pack_bf16x2(w[4], w[5]), pack_bf16x2(w[6], w[7]));
+  }
+}
+
+__device__ __forceinline__ void fold_codeword(float (&acc)[8], uint4 cw, bool first) {
+  const float v[8] = {f16lo(cw.x), f16hi(cw.x), f16lo(cw.y), f16hi(cw.y),
+                      f16lo(cw.z), f16hi(cw.z), f16lo(cw.w), f16hi(cw.w)};
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = first ? v[t] : acc[t] + v[t];
+}
+
+// One thread per group: the J lanes of a (row, slice) pair take its J groups, so a wave writes
+// whole row segments (J groups x 8 values) and the lanes of one row share one 16-byte code
+// chunk per plane (a single cache line). 256-entry codebooks are staged in LDS; 65536-entry
+// codebooks are read through the caches.
+template <int OUT, int CS>
+__global__ __launch_bounds__(256) void dequant_kernel(const unsigned char* __restrict__ codes,
+                                                      const uint16_t* __restrict__ codebooks,
+                                                      const uint16_t* __restrict__ scales, void* __restrict__ W,
+                                                      int d_out, int d_in, int G, int S, int k, size_t plane_bytes) {
+  constexpr int J = 16 / CS;
+  extern __shared__ uint4 cb_lds[];  // [k][256] codewords (B = 8 only)
+  if constexpr (CS == 1) {
+    for (int q = threadIdx.x; q < k * 256; q += blockDim.x) cb_lds[q] = ((const uint4*)codebooks)[q];
+    __syncthreads();
+  }
+  const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int jj = (int)(t % J);
+  const size_t pair = t / J;             // (slice, row) pair, rows fastest
+  if (pair >= (size_t)S * d_out) return;
+  const int i = (int)(pair % d_out), s = (int)(pair / d_out);
+  const int j = s * J + jj;
+  if (j >= G) return;
+  const size_t chunk = pair * 16 + (size_t)(jj * CS / 4) * 4;  // the code word holding this group
+  const float scale = f16_to_f32(scales[i]);
+  float acc[8];
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    if (m < k) {
+      const uint32_t word = *(const uint32_t*)(codes + m * plane_bytes + chunk);
+      uint4 cw;
+      if constexpr (CS == 1) {
+        cw = cb_lds[m * 256 + ((word >> (8 * (jj & 3))) & 0xFFu)];
+      } else {
+        cw = ((const uint4*)codebooks)[((size_t)m << 16) + ((word >> (16 * (jj & 1))) & 0xFFFFu)];
+      }
+      fold_codeword(acc, cw, m == 0);
+    }
+  }
+  float w[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    w[e] = acc[e] * scale;
+    // Keep the binary32 product: without this the backend may fuse the multiply and the
+    // fp16 conversion into one mixed-precision instruction that rounds only once.
+    asm volatile("" : "+v"(w[e]));
+  }
+  store_group<OUT>(W, (size_t)i * d_in + (size_t)j * 8, w);
+}
+
+hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hipStream_t st) {
+  const size_t n = (size_t)L.S * L.d.d_out * L.J;  // one thread per (slice, row, group in slice)
+  const unsigned grid = (unsigned)((n + 255) / 256);
+  const size_t lds = L.d.code_bits == 8 ? (size_t)k * 256 * 16 : 0;
+  auto go = [&](auto kern) {
+    kern<<<grid, 256, lds, st>>>(L.codes, L.codebooks, L.scales, W, L.d.d_out, L.d.d_in, L.G, L.S, k, L.plane_bytes);
+  };
+  if (L.d.code_bits == 8) {
+    if (w_dtype == AQMB_F32) go(dequant_kernel<AQMB_F32, 1>);
+    else if (w_dtype == AQMB_F16) go(dequant_kernel<AQMB_F16, 1>);
+    else go(dequant_kernel<AQMB_BF16, 1>);
+  } else {
+    if (w_dtype == AQMB_F32) go(dequant_kernel<AQMB_F32, 2>);
+    else if (w_dtype == AQMB_F16) go(dequant_kernel<AQMB_F16, 2>);
+    else go(dequant_kernel<AQMB_BF16, 2>);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace aqmb

@@ -1,0 +1,34 @@
+// Internal definitions shared by the host library and the kernel launchers.
+#pragma once
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/aqmb.h"
+
+namespace aqmb {
+
+// Codes are stored per plane as [S slices][d_out rows][J groups]: a slice holds J
+// consecutive groups of every row, so one 16-byte load brings the J codes of one
+// row (J = 16 uint8 codes or 8 uint16 codes). Groups past d_in/g in the last slice
+// are padding (code 0) and contribute nothing. Planes stay outermost: level k
+// reads the first k * plane_bytes bytes only.
+constexpr int kSliceBytes = 16;
+
+struct Layer {
+  uint32_t magic;
+  aqmb_desc d;
+  int device;
+  int G;                 // groups per row = d_in / g
+  int J;                 // groups per slice
+  int S;                 // slices per row = ceil(G / J)
+  size_t plane_bytes;    // S * d_out * 16
+  unsigned char* codes;  // [M][S][d_out][16 bytes]
+  uint16_t* codebooks;   // [M][2^B][g] fp16
+  uint16_t* scales;      // [d_out] fp16
+  float* ws;             // gemv split-K partial sums
+  size_t ws_floats;
+};
+
+constexpr uint32_t kMagic = 0x41514D42u;  // "AQMB"
+
+}  // namespace aqmb

@@ -1,0 +1,113 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol include/aqmb.h declares, and
+its host-side validation, status strings and bits-per-weight formula behave as documented.
+No test here launches anything on a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+A = pytest.importorskip("paper_2606_12876_amd", reason="libaqmb.so not built")
+
+
+def declared_symbols():
+    hdr = open(os.path.join(ROOT, "include", "aqmb.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    return sorted(set(re.findall(r"\b(aqmb_[a-z_]+)\s*\(", hdr)))
+
+
+def test_exports_every_declared_symbol():
+    syms = declared_symbols()
+    assert {"aqmb_create", "aqmb_gemv", "aqmb_gemm", "aqmb_dequant", "aqmb_destroy"} <= set(syms)
+    lib = ctypes.CDLL(A.LIB_PATH)
+    for s in syms:
+        assert hasattr(lib, s), s
+
+
+def test_strerror_and_last_error():
+    for st in A.Status:
+        assert A.strerror(st)
+    assert A.strerror(99) == "unknown status"
+    d = A.make_desc(64, 64, 4)
+    assert A.validate(d, 0, 0, 1, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EINVAL
+    assert "k = 0" in A.last_error()
+    assert A.validate(d, 0, 1, 1, A.DType.F16, A.DType.F16, 16, 32) == A.Status.OK
+    assert A.last_error() == ""
+
+
+@pytest.mark.parametrize("case,expect", [
+    (dict(d_out=0), A.Status.EINVAL),
+    (dict(d_in=12), A.Status.EINVAL),                     # not a multiple of g
+    (dict(d_in=0), A.Status.EINVAL),
+    (dict(group_size=4, d_in=64), A.Status.EUNSUPPORTED),
+    (dict(code_bits=4), A.Status.EUNSUPPORTED),
+    (dict(code_bits=12), A.Status.EUNSUPPORTED),
+    (dict(num_codebooks=0), A.Status.EINVAL),
+    (dict(num_codebooks=9), A.Status.EUNSUPPORTED),
+    (dict(d_out=1 << 18, d_in=1 << 13), A.Status.OK),
+    (dict(d_out=1 << 19, d_in=1 << 13), A.Status.EINVAL),  # d_out * d_in >= 2^32
+])
+def test_descriptor_validation(case, expect):
+    base = dict(d_out=64, d_in=64, group_size=8, num_codebooks=4, code_bits=8)
+    base.update(case)
+    d = A.Desc(base["d_out"], base["d_in"], base["group_size"], base["num_codebooks"], base["code_bits"])
+    assert A.validate(d, 2, 1, 0, A.DType.F16, A.DType.F16, None, 16) == expect
+
+
+@pytest.mark.parametrize("op,k,n,xdt,ydt,x,y,expect", [
+    (0, 1, 1, 0, 0, 16, 32, A.Status.OK),
+    (0, 4, 16, 1, 2, 16, 32, A.Status.OK),
+    (0, 0, 1, 0, 0, 16, 32, A.Status.EINVAL),       # k < 1
+    (0, 5, 1, 0, 0, 16, 32, A.Status.EINVAL),       # k > M
+    (0, 1, 0, 0, 0, 16, 32, A.Status.EINVAL),       # batch < 1
+    (0, 1, 17, 0, 0, 16, 32, A.Status.EUNSUPPORTED),  # batch > 16
+    (0, 1, 1, 2, 0, 16, 32, A.Status.EUNSUPPORTED),  # x must be f16/bf16
+    (0, 1, 1, 0, 7, 16, 32, A.Status.EUNSUPPORTED),  # bad y dtype
+    (0, 1, 1, 0, 0, None, 32, A.Status.EINVAL),
+    (0, 1, 1, 0, 0, 16, None, A.Status.EINVAL),
+    (0, 1, 1, 0, 0, 18, 32, A.Status.EINVAL),       # misaligned
+    (1, 2, 2048, 1, 1, 16, 32, A.Status.OK),
+    (1, 2, 0, 1, 1, 16, 32, A.Status.EINVAL),
+    (1, 2, 7, 1, 0, 16, 32, A.Status.EUNSUPPORTED),  # gemm output must be bf16/f32
+    (2, 3, 0, 0, 2, None, 32, A.Status.OK),
+    (2, 3, 0, 0, 2, None, None, A.Status.EINVAL),
+    (3, 1, 1, 0, 0, 16, 32, A.Status.EINVAL),       # unknown op
+])
+def test_call_validation(op, k, n, xdt, ydt, x, y, expect):
+    d = A.make_desc(256, 512, 4)
+    assert A.validate(d, op, k, n, xdt, ydt, x, y) == expect
+
+
+def test_gemm_rejects_16bit_codes():
+    d = A.make_desc(256, 512, 2, code_bits=16)
+    assert A.validate(d, 1, 1, 8, A.DType.BF16, A.DType.BF16, 16, 32) == A.Status.EUNSUPPORTED
+    assert A.validate(d, 0, 2, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.OK
+
+
+def test_bits_per_weight_matches_oracle():
+    for (d_out, d_in, M, B) in [(28672, 8192, 2, 8), (4096, 4096, 4, 8), (11008, 4096, 4, 8), (14336, 4096, 2, 16)]:
+        d = A.make_desc(d_out, d_in, M, B)
+        for k in range(1, M + 1):
+            assert A.bits_per_weight(d, k) == pytest.approx(oracle.bits_per_weight(d_out, d_in, 8, M, B, k), rel=1e-15)
+    d = A.make_desc(64, 64, 4)
+    assert A.bits_per_weight(d, 0) < 0 and A.bits_per_weight(d, 5) < 0
+
+
+def test_bad_handles_rejected_without_gpu():
+    assert A.lib.aqmb_destroy(None) == A.Status.OK
+    bogus = ctypes.c_void_p(0x1000)
+    assert A.lib.aqmb_destroy(bogus) == A.Status.EINVAL
+    assert A.lib.aqmb_gemv(bogus, 1, 16, 0, 1, 32, 0, None) == A.Status.EINVAL
+    assert A.lib.aqmb_gemm(bogus, 1, 16, 1, 32, 1, None) == A.Status.EINVAL
+    assert A.lib.aqmb_dequant(bogus, 1, 32, 0, None) == A.Status.EINVAL
+    d = A.Desc()
+    assert A.lib.aqmb_get_desc(bogus, ctypes.byref(d)) == A.Status.EINVAL
+    h = ctypes.c_void_p(0x1234)
+    desc = A.make_desc(64, 64, 4)
+    assert A.lib.aqmb_create(ctypes.byref(h), ctypes.byref(desc), None, 16, 16, None) == A.Status.EINVAL
+    assert h.value is None
+    bad = A.make_desc(64, 60, 4)
+    assert A.lib.aqmb_create(ctypes.byref(h), ctypes.byref(bad), 16, 16, 16, None) == A.Status.EINVAL

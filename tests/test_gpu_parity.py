@@ -1,0 +1,234 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, on seeded inputs.
+
+Dequantization is compared bit for bit with the oracle's stated evaluation order; GEMV and
+GEMM outputs are compared element by element under the tolerance in tests/gpu_helpers.py.
+Shapes cover several tiles with ragged tails in every dimension, batch 1..16, every k, the
+degenerate layers (one group, one row, one codebook) and the workload shapes.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import formats
+from workloads import CONFIGS, LayerSpec, make_layer, make_activations, config
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU hosts too; every test here is marked gpu
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2606_12876_amd as A  # noqa: E402
+from gpu_helpers import GpuLayer, out_values, check_close, to_dev, TORCH_DT, A_DT, act_values  # noqa: E402
+
+
+def _f64(L):
+    return formats.f16_bits_to_f64(L.codebooks), formats.f16_bits_to_f64(L.scales)
+
+
+def run_dequant(gl, k, dt):
+    d = gl.desc
+    W = torch.empty((d.d_out, d.d_in), dtype=TORCH_DT[dt], device="cuda")
+    A.dequant(gl.handle, k, W, A_DT[dt])
+    torch.cuda.synchronize()
+    W = W.cpu()
+    return W.numpy() if dt == "f32" else W.view(torch.int16).numpy().view(np.uint16)
+
+
+def run_gemv(gl, k, xbits, xdt, ydt):
+    b = xbits.shape[0]
+    x = to_dev(xbits).view(TORCH_DT[xdt])
+    y = torch.empty((b, gl.desc.d_out), dtype=TORCH_DT[ydt], device="cuda")
+    A.gemv(gl.handle, k, x, A_DT[xdt], b, y, A_DT[ydt])
+    torch.cuda.synchronize()
+    return out_values(y)
+
+
+def run_gemm(gl, k, Xbits, ydt):
+    n = Xbits.shape[0]
+    X = to_dev(Xbits).view(torch.bfloat16)
+    Y = torch.empty((n, gl.desc.d_out), dtype=TORCH_DT[ydt], device="cuda")
+    A.gemm(gl.handle, k, X, n, Y, A_DT[ydt])
+    torch.cuda.synchronize()
+    return out_values(Y)
+
+
+# ------------------------------------------------------------------------------------ dequant
+
+@pytest.mark.parametrize("spec", [
+    LayerSpec("ragged", 1000, 1032, seed=21),           # 129 groups: 9 slices, the last with 1 group
+    LayerSpec("M1", 37, 8, M=1, seed=22),               # one group per row, one codebook
+    LayerSpec("b16", 300, 136, M=2, B=16, seed=23),      # 16-bit codes, 17 groups
+], ids=lambda s: s.name)
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_dequant_bit_exact(spec, dt):
+    L = make_layer(spec)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in range(1, spec.M + 1):
+            got = run_dequant(gl, k, dt)
+            ref = oracle.dequant_canonical(L.codes, L.codebooks, L.scales, k, dt)
+            assert np.array_equal(got.view(np.uint32) if dt == "f32" else got,
+                                  ref.view(np.uint32) if dt == "f32" else ref), (spec.name, k, dt)
+
+
+def test_dequant_workload_layers_bit_exact():
+    for name in ("c1", "c2", "c4"):
+        spec = config(name)
+        L = make_layer(spec)
+        with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+            for k in spec.ks:
+                for dt in ("bf16", "f16"):
+                    got = run_dequant(gl, k, dt)
+                    ref = oracle.dequant_canonical(L.codes, L.codebooks, L.scales, k, dt)
+                    assert np.array_equal(got, ref), (name, k, dt)
+
+
+def test_dequant_index_revealing():
+    """C_0[c][t] = c + 256 t, s = 1: the dequantized matrix spells out plane 0's codes."""
+    rng = np.random.default_rng(0)
+    d_out, d_in = 515, 1048
+    codes = rng.integers(0, 256, size=(2, d_out, d_in // 8)).astype(np.uint8)
+    C = np.zeros((2, 256, 8)); C[0] = [[c + 256 * t for t in range(8)] for c in range(256)]; C[1] = 3.0
+    cb = C.astype(np.float16).view(np.uint16)
+    s = np.ones(d_out).astype(np.float16).view(np.uint16)
+    with GpuLayer(codes, cb, s) as gl:
+        W = run_dequant(gl, 1, "f32")
+        j, t = np.divmod(np.arange(d_in), 8)
+        assert np.array_equal(W.astype(np.float64), codes[0][:, j] + 256.0 * t[None, :])
+        W2 = run_dequant(gl, 2, "f32")
+        assert np.array_equal(W2.astype(np.float64), codes[0][:, j] + 256.0 * t[None, :] + 3.0)
+
+
+def test_dequant_subnormal_and_tie_cases():
+    """fp16 subnormal codebook entries and binary32 ties in the fold (the oracle's hand cases)."""
+    codes = np.zeros((3, 4, 2), dtype=np.uint8)
+    codes[:, 1] = 1
+    C = np.zeros((3, 256, 8))
+    C[0, 0], C[1, 0], C[2, 0] = 1.0, 2.0 ** -24, 2.0 ** -24
+    C[0, 1], C[1, 1], C[2, 1] = 2.0 ** -24, 2.0 ** -23, -(2.0 ** -24)
+    cb = C.astype(np.float16).view(np.uint16)
+    s = np.array([1.0, 1.0, 0.5, 3.0]).astype(np.float16).view(np.uint16)
+    with GpuLayer(codes, cb, s) as gl:
+        for k in (1, 2, 3):
+            for dt in ("f32", "f16", "bf16"):
+                got = run_dequant(gl, k, dt)
+                ref = oracle.dequant_canonical(codes, cb, s, k, dt)
+                assert np.array_equal(got.view(np.uint32) if dt == "f32" else got,
+                                      ref.view(np.uint32) if dt == "f32" else ref), (k, dt)
+
+
+# ------------------------------------------------------------------------------------ GEMV
+
+@pytest.mark.parametrize("spec,batches", [
+    (LayerSpec("ragged", 1000, 1032, seed=31), (1, 2, 3, 4, 5, 8, 13, 16)),
+    (LayerSpec("tiny", 1, 8, M=3, seed=32), (1, 4, 16)),
+    (LayerSpec("M1", 700, 264, M=1, seed=33), (1, 2, 7)),
+    (LayerSpec("M8", 520, 520, M=8, seed=34), (1, 4, 9)),
+    (LayerSpec("b16", 1030, 328, M=2, B=16, seed=35), (1, 3, 16)),
+], ids=lambda s: getattr(s, "name", str(s)))
+@pytest.mark.parametrize("xdt", ["f16", "bf16"])
+def test_gemv_small_shapes(spec, batches, xdt):
+    L = make_layer(spec)
+    C, s = _f64(L)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for b in batches:
+            xbits = make_activations(L, b, xdt, heavy_tail=(b % 2 == 1))
+            x = act_values(xbits, xdt)
+            for k in range(1, spec.M + 1):
+                ref = oracle.linear(x, L.codes, C, s, k)
+                for ydt in ("f32", "f16", "bf16"):
+                    got = run_gemv(gl, k, xbits, xdt, ydt)
+                    check_close(got, ref, ydt, f"{spec.name} b={b} k={k} {xdt}->{ydt}")
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3_up", "c3_down", "c4"])
+def test_gemv_workloads(name):
+    spec = config(name)
+    L = make_layer(spec)
+    C, s = _f64(L)
+    ydt = spec.act_dtype
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        xs = {b: make_activations(L, b) for b in spec.batches}
+        for k in spec.ks:
+            W = oracle.reconstruct(L.codes, C, s, k)
+            for b, xbits in xs.items():
+                ref = act_values(xbits, spec.act_dtype) @ W.T
+                got = run_gemv(gl, k, xbits, spec.act_dtype, ydt)
+                check_close(got, ref, ydt, f"{name} b={b} k={k}")
+            del W
+
+
+def test_gemv_plane_linearity():
+    """gemv(k) - gemv(k-1) equals the GEMV of a one-codebook layer holding plane k-1 alone."""
+    spec = LayerSpec("lin", 777, 1024, seed=36)
+    L = make_layer(spec)
+    xbits = make_activations(L, 2, "f16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        ys = [None] + [run_gemv(gl, k, xbits, "f16", "f32") for k in range(1, 5)]
+    for k in range(2, 5):
+        with GpuLayer(L.codes[k - 1:k].copy(), L.codebooks[k - 1:k].copy(), L.scales) as g1:
+            y1 = run_gemv(g1, 1, xbits, "f16", "f32")
+        check_close(ys[k] - ys[k - 1], y1, "f32", f"plane {k - 1}")
+
+
+def test_gemv_repeated_calls_and_errors_write_nothing():
+    """Counters re-arm: repeated calls agree; rejected calls leave y untouched."""
+    spec = LayerSpec("rep", 600, 512, seed=37)
+    L = make_layer(spec)
+    xbits = make_activations(L, 3, "f16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        first = run_gemv(gl, 3, xbits, "f16", "f32")
+        for _ in range(5):
+            assert np.array_equal(run_gemv(gl, 3, xbits, "f16", "f32"), first)
+        x = to_dev(xbits).view(torch.float16)
+        y = torch.full((3, 600), 7.0, dtype=torch.float32, device="cuda")
+        for k, b in ((0, 3), (5, 3), (1, 0), (1, 17)):
+            with pytest.raises(A.AqmbError):
+                A.gemv(gl.handle, k, x, A.DType.F16, b, y, A.DType.F32)
+        torch.cuda.synchronize()
+        assert torch.all(y == 7.0)
+
+
+# ------------------------------------------------------------------------------------ GEMM
+
+@pytest.mark.parametrize("shape", [(300, 200, 264, 4), (129, 130, 1032, 3), (1, 1, 8, 2), (17, 257, 520, 1)])
+def test_gemm_small_shapes(shape):
+    n, d_out, d_in, M = shape
+    spec = LayerSpec("g", d_out, d_in, M=M, seed=41, act_dtype="bf16")
+    L = make_layer(spec)
+    Xbits = make_activations(L, n, "bf16", heavy_tail=True)
+    X = act_values(Xbits, "bf16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in range(1, M + 1):
+            ref = oracle.gemm_reference(X, L.codes, L.codebooks, L.scales, k)
+            for ydt in ("f32", "bf16"):
+                got = run_gemm(gl, k, Xbits, ydt)
+                check_close(got, ref, ydt, f"gemm {shape} k={k} {ydt}")
+
+
+def test_gemm_workload_full_size():
+    spec = config("c5")
+    L = make_layer(spec)
+    Xbits = make_activations(L, spec.n_tokens, "bf16")
+    X = act_values(Xbits, "bf16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in spec.ks:
+            ref = oracle.gemm_reference(X, L.codes, L.codebooks, L.scales, k)
+            got = run_gemm(gl, k, Xbits, "bf16")
+            check_close(got, ref, "bf16", f"c5 k={k}")
+
+
+def test_gemm_matches_exact_layer_within_bf16_weight_rounding():
+    """Against the exact fp64 layer the only extra error is the bf16 rounding of the weight tile."""
+    spec = LayerSpec("gx", 256, 512, seed=42, act_dtype="bf16")
+    L = make_layer(spec)
+    C, s = _f64(L)
+    Xbits = make_activations(L, 64, "bf16")
+    X = act_values(Xbits, "bf16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in range(1, 5):
+            got = run_gemm(gl, k, Xbits, "f32")
+            exact = oracle.linear(X, L.codes, C, s, k)
+            W = oracle.reconstruct(L.codes, C, s, k)
+            bound = (np.abs(X) @ np.abs(W).T) * (2.0 ** -8 + 2.0 ** -20)
+            assert np.all(np.abs(got - exact) <= bound)
