@@ -1,4 +1,6 @@
 // Code re-tiling (layer creation) and the bit-exact dequantization kernel.
+#include <algorithm>
+
 #include "device.h"
 #include "launch.h"
 
@@ -80,43 +82,64 @@ __global__ __launch_bounds__(256) void dequant_kernel(const unsigned char* __res
     for (int q = threadIdx.x; q < k * 256; q += blockDim.x) cb_lds[q] = ((const uint4*)codebooks)[q];
     __syncthreads();
   }
-  const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int jj = (int)(t % J);
-  const size_t pair = t / J;             // (slice, row) pair, rows fastest
-  if (pair >= (size_t)S * d_out) return;
-  const int i = (int)(pair % d_out), s = (int)(pair / d_out);
-  const int j = s * J + jj;
-  if (j >= G) return;
-  const size_t chunk = pair * 16 + (size_t)(jj * CS / 4) * 4;  // the code word holding this group
-  const float scale = f16_to_f32(scales[i]);
-  float acc[8];
+  // Each thread takes U groups per pass and issues all their code loads before using any.
+  constexpr int U = 4;
+  const size_t n = (size_t)S * d_out * J;
+  const size_t stride = (size_t)gridDim.x * blockDim.x * U;
+  for (size_t base = (size_t)blockIdx.x * blockDim.x * U + threadIdx.x; base < n; base += stride) {
+    uint32_t words[U][8];
+    int row[U], grp[U];
 #pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    if (m < k) {
-      const uint32_t word = *(const uint32_t*)(codes + m * plane_bytes + chunk);
-      uint4 cw;
-      if constexpr (CS == 1) {
-        cw = cb_lds[m * 256 + ((word >> (8 * (jj & 3))) & 0xFFu)];
-      } else {
-        cw = ((const uint4*)codebooks)[((size_t)m << 16) + ((word >> (16 * (jj & 1))) & 0xFFFFu)];
+    for (int u = 0; u < U; ++u) {
+      const size_t t = base + (size_t)u * blockDim.x;
+      const int jj = (int)(t % J);
+      const size_t pair = t / J;  // (slice, row) pair, rows fastest
+      row[u] = (int)(pair % d_out);
+      const int s = (int)(pair / d_out);
+      grp[u] = (t < n) ? s * J + jj : G;
+      const size_t chunk = pair * 16 + (size_t)(jj * CS / 4) * 4;  // the code word holding this group
+#pragma unroll
+      for (int m = 0; m < 8; ++m) {
+        words[u][m] = 0;
+        if (m < k && grp[u] < G) words[u][m] = *(const uint32_t*)(codes + m * plane_bytes + chunk);
       }
-      fold_codeword(acc, cw, m == 0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (grp[u] >= G) continue;
+      const int jj = grp[u] % J;
+      float acc[8];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) {
+        if (m < k) {
+          uint4 cw;
+          if constexpr (CS == 1) {
+            cw = cb_lds[m * 256 + ((words[u][m] >> (8 * (jj & 3))) & 0xFFu)];
+          } else {
+            cw = ((const uint4*)codebooks)[((size_t)m << 16) + ((words[u][m] >> (16 * (jj & 1))) & 0xFFFFu)];
+          }
+          fold_codeword(acc, cw, m == 0);
+        }
+      }
+      const float scale = f16_to_f32(scales[row[u]]);
+      float w[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        w[e] = acc[e] * scale;
+        // Keep the binary32 product: without this the backend may fuse the multiply and the
+        // fp16 conversion into one mixed-precision instruction that rounds only once.
+        asm volatile("" : "+v"(w[e]));
+      }
+      store_group<OUT>(W, (size_t)row[u] * d_in + (size_t)grp[u] * 8, w);
     }
   }
-  float w[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    w[e] = acc[e] * scale;
-    // Keep the binary32 product: without this the backend may fuse the multiply and the
-    // fp16 conversion into one mixed-precision instruction that rounds only once.
-    asm volatile("" : "+v"(w[e]));
-  }
-  store_group<OUT>(W, (size_t)i * d_in + (size_t)j * 8, w);
 }
 
 hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hipStream_t st) {
   const size_t n = (size_t)L.S * L.d.d_out * L.J;  // one thread per (slice, row, group in slice)
-  const unsigned grid = (unsigned)((n + 255) / 256);
+  // Enough workgroups to fill the chip several times over, few enough that staging the
+  // codebooks in LDS stays small next to the output traffic.
+  const unsigned grid = (unsigned)std::min<size_t>((n + 1023) / 1024, 2048);
   const size_t lds = L.d.code_bits == 8 ? (size_t)k * 256 * 16 : 0;
   auto go = [&](auto kern) {
     kern<<<grid, 256, lds, st>>>(L.codes, L.codebooks, L.scales, W, L.d.d_out, L.d.d_in, L.G, L.S, k, L.plane_bytes);

@@ -2,10 +2,10 @@
 //
 // Work split: a workgroup owns a chunk of rows and one slice (16 consecutive groups for
 // 8-bit codes, 8 for 16-bit codes); every row's sum over slices is a split-K reduction.
-// Each workgroup writes fp32 partial sums for its rows to the layer's workspace; the last
-// workgroup to finish a row chunk (arrival counter) adds the partials of all slices in slice
-// order, applies the row scale and rounds once to the output dtype. The result therefore does
-// not depend on scheduling, and the counters are reset to zero for the next call.
+// Each workgroup writes fp32 partial sums for its rows to the layer's workspace; a second,
+// small kernel adds the partials of all slices in slice order, applies the row scale and
+// rounds once to the output dtype. The kernel boundary orders the two phases (no
+// device-wide fences inside the main kernel), and the result does not depend on scheduling.
 //
 // 8-bit codes (256 codewords): lookup tables in LDS. For the slice's groups and every used
 // plane m, LUT_m[j][c] = <x[b, group j], C_m[c]> is built once per workgroup (one codeword per
@@ -20,9 +20,10 @@
 
 namespace aqmb {
 
-constexpr int kThreads = 256;
-constexpr int kRowsPerThread = 2;
+constexpr int kThreads = 512;       // 8 waves: two per SIMD
+constexpr int kRowsPerThread = 1;
 constexpr int kRowsPerWG = kThreads * kRowsPerThread;
+constexpr int kReduceThreads = 256;
 
 struct GemvArgs {
   const unsigned char* codes;
@@ -31,7 +32,6 @@ struct GemvArgs {
   const void* x;
   void* y;
   float* partials;     // [S][batch][d_out]
-  unsigned* counters;  // [n_chunks]
   size_t plane_bytes;
   int d_out, d_in, G, S, k, batch;
   int y_dtype;
@@ -39,9 +39,7 @@ struct GemvArgs {
 
 size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S) {
   (void)G;
-  const size_t partials = (size_t)S * AQMB_MAX_BATCH * d.d_out;
-  const size_t chunks = ((size_t)d.d_out + kRowsPerWG - 1) / kRowsPerWG;
-  return partials + chunks + 64;
+  return (size_t)S * AQMB_MAX_BATCH * d.d_out + 64;
 }
 
 // Partial sums of one batch tile of this workgroup's rows.
@@ -61,66 +59,63 @@ __device__ __forceinline__ void store_partials(const GemvArgs& a, int b0, const 
   }
 }
 
-// After every partial of this workgroup is stored: the last arriving workgroup of the row
-// chunk reduces all slices in slice order, scales and writes y, and re-arms the counter.
-// The reduction reads four consecutive rows per 16-byte load and keeps kInflight loads in
-// flight per thread, so its latency is a few memory round trips, not one per slice.
-__device__ __forceinline__ void split_k_finish(const GemvArgs& a) {
-  constexpr int kInflight = 16;
-  const int tid = threadIdx.x;
-  const int chunk = blockIdx.x;
-  const int row0 = chunk * kRowsPerWG;
-  __shared__ unsigned s_last;
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const unsigned prev = atomicAdd(&a.counters[chunk], 1u);
-    s_last = (prev == (unsigned)a.S - 1) ? 1u : 0u;
-  }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  if (tid == 0) a.counters[chunk] = 0u;
-  const int rows = min(kRowsPerWG, a.d_out - row0);
-  const int quads = (rows + 3) / 4;
+// y[b][i] = s_i * sum over slices of the partials. A block takes 64 row quads (16-byte
+// loads of four consecutive rows); its four waves take interleaved quarters of the slices with
+// all their loads in flight, and the four quarter sums are added in a fixed order, so the
+// result does not depend on scheduling.
+__global__ __launch_bounds__(kReduceThreads) void gemv_reduce_kernel(GemvArgs a) {
+  constexpr int kQuads = 64, kParts = kReduceThreads / kQuads, kInflight = 8;
+  __shared__ float4 part_sum[kParts][kQuads];
+  const int quads = (a.d_out + 3) / 4;
+  const int lane = threadIdx.x % kQuads, part = threadIdx.x / kQuads;
+  const int item = blockIdx.x * kQuads + lane;     // (batch row, row quad)
+  const bool active = item < a.batch * quads;
+  const int b = active ? item / quads : 0, r0 = active ? (item % quads) * 4 : 0;
   const bool vec = (a.d_out % 4) == 0;  // 16-byte aligned row quads
-  for (int item = tid; item < a.batch * quads; item += kThreads) {
-    const int b = item / quads, q = item % quads;
-    const int r0 = row0 + q * 4;
-    float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s0 = 0; s0 < a.S; s0 += kInflight) {
-      float4 part[kInflight];
+  float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (active) {
+    for (int s0 = part; s0 < a.S; s0 += kParts * kInflight) {
+      float4 v[kInflight];
 #pragma unroll
       for (int u = 0; u < kInflight; ++u) {
-        part[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (s0 + u < a.S) {
-          const float* p = a.partials + ((size_t)(s0 + u) * a.batch + b) * a.d_out + r0;
+        const int sl = s0 + u * kParts;
+        v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (sl < a.S) {
+          const float* p = a.partials + ((size_t)sl * a.batch + b) * a.d_out + r0;
           if (vec) {
-            part[u] = *(const float4*)p;
+            v[u] = *(const float4*)p;
           } else {
-            part[u].x = p[0];
-            if (r0 + 1 < a.d_out) part[u].y = p[1];
-            if (r0 + 2 < a.d_out) part[u].z = p[2];
-            if (r0 + 3 < a.d_out) part[u].w = p[3];
+            v[u].x = p[0];
+            if (r0 + 1 < a.d_out) v[u].y = p[1];
+            if (r0 + 2 < a.d_out) v[u].z = p[2];
+            if (r0 + 3 < a.d_out) v[u].w = p[3];
           }
         }
       }
 #pragma unroll
-      for (int u = 0; u < kInflight; ++u) {  // slice order: deterministic
-        sum.x += part[u].x; sum.y += part[u].y; sum.z += part[u].z; sum.w += part[u].w;
+      for (int u = 0; u < kInflight; ++u) {
+        sum.x += v[u].x; sum.y += v[u].y; sum.z += v[u].z; sum.w += v[u].w;
       }
     }
-    const float v[4] = {sum.x, sum.y, sum.z, sum.w};
+  }
+  part_sum[part][lane] = sum;
+  __syncthreads();
+  if (part != 0 || !active) return;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int row = r0 + e;
-      if (row >= row0 + rows) break;
-      const float val = v[e] * f16_to_f32(a.scales[row]);
-      const size_t o = (size_t)b * a.d_out + row;
-      if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, o, val);
-      else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, o, val);
-      else OutT<AQMB_F32>::store(a.y, o, val);
-    }
+  for (int p2 = 1; p2 < kParts; ++p2) {
+    const float4 o = part_sum[p2][lane];
+    sum.x += o.x; sum.y += o.y; sum.z += o.z; sum.w += o.w;
+  }
+  const float v[4] = {sum.x, sum.y, sum.z, sum.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int row = r0 + e;
+    if (row >= a.d_out) break;
+    const float val = v[e] * f16_to_f32(a.scales[row]);
+    const size_t o = (size_t)b * a.d_out + row;
+    if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, o, val);
+    else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, o, val);
+    else OutT<AQMB_F32>::store(a.y, o, val);
   }
 }
 
@@ -169,6 +164,7 @@ __global__ __launch_bounds__(kThreads) void gemv_lut_kernel(GemvArgs a) {
   // 1. Loads, oldest first: x of the slice, then the code planes 0..K-1 of this thread's rows,
   //    then this thread's codeword of each codebook. The code loads stay in flight while the
   //    x staging and the LUT construction proceed.
+  static_assert(kThreads == 512, "the LUT build assigns two threads per codeword");
   uint4 xw = make_uint4(0, 0, 0, 0);
   const int xb = tid >> 4, xj = slice * 16 + (tid & 15);
   if (xb < a.batch && xj < a.G) xw = *(const uint4*)((const uint16_t*)a.x + (size_t)xb * a.d_in + (size_t)xj * 8);
@@ -183,10 +179,11 @@ __global__ __launch_bounds__(kThreads) void gemv_lut_kernel(GemvArgs a) {
         v[r][m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)slice * a.d_out + row) * 16);
     }
   }
+  const int c = tid & 255, jhalf = tid >> 8;  // LUT column and half of the groups this thread builds
   uint4 cw[K];
 #pragma unroll
-  for (int m = 0; m < K; ++m) cw[m] = ((const uint4*)a.codebooks)[m * 256 + tid];
-  xs[tid] = xw;  // groups past G and batch rows past `batch` are zero
+  for (int m = 0; m < K; ++m) cw[m] = ((const uint4*)a.codebooks)[m * 256 + c];
+  if (tid < AQMB_MAX_BATCH * 16) xs[tid] = xw;  // groups past G and batch rows past `batch` are zero
   __syncthreads();
 
   for (int b0 = 0; b0 < a.batch; b0 += BT) {
@@ -198,9 +195,11 @@ __global__ __launch_bounds__(kThreads) void gemv_lut_kernel(GemvArgs a) {
 #pragma unroll
     for (int h = 0; h < BT; ++h) {  // parts of JH groups
       if (b0 + h > 0) __syncthreads();  // the previous part's lookups are done
-      // 2. LUT entries of codeword c = tid for every plane, group and batch row of the part.
+      // 2. LUT entries of codeword c for every plane, batch row and this thread's half of
+      //    the part's groups (two threads per codeword).
 #pragma unroll
-      for (int jj = 0; jj < JH; ++jj) {
+      for (int j2 = 0; j2 < JH / 2; ++j2) {
+        const int jj = jhalf * (JH / 2) + j2;
         uint4 xv[BT];
 #pragma unroll
         for (int bt = 0; bt < BT; ++bt) xv[bt] = xs[(b0 + bt) * 16 + h * JH + jj];
@@ -209,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void gemv_lut_kernel(GemvArgs a) {
           float e[BT];
 #pragma unroll
           for (int bt = 0; bt < BT; ++bt) e[bt] = group_dot<XDT>(xv[bt], cw[m]);
-          float* dst = lut + ((m * JH + jj) * 256 + tid) * BT;
+          float* dst = lut + ((m * JH + jj) * 256 + c) * BT;
           if constexpr (BT == 1) dst[0] = e[0];
           else if constexpr (BT == 2) *(float2*)dst = make_float2(e[0], e[1]);
           else *(float4*)dst = make_float4(e[0], e[1], e[2], e[3]);
@@ -253,7 +252,6 @@ __global__ __launch_bounds__(kThreads) void gemv_lut_kernel(GemvArgs a) {
       for (int bt = 0; bt < BT; ++bt) out[r][bt] = acc[r][bt][0] + acc[r][bt][1];
     store_partials<BT>(a, b0, out);
   }
-  split_k_finish(a);
 }
 
 // 16-bit codes: codewords from global memory. One slice = 8 groups per row.
@@ -325,7 +323,6 @@ __global__ __launch_bounds__(kThreads) void gemv_b16_kernel(GemvArgs a) {
     }
   }
   store_partials<NB>(a, 0, acc);
-  split_k_finish(a);
 }
 
 template <int K, int XDT>
@@ -364,7 +361,6 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   a.x = x;
   a.y = y;
   a.partials = L.ws;
-  a.counters = (unsigned*)(L.ws + (size_t)L.S * AQMB_MAX_BATCH * L.d.d_out);
   a.plane_bytes = L.plane_bytes;
   a.d_out = L.d.d_out;
   a.d_in = L.d.d_in;
@@ -377,6 +373,10 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   const bool b16 = L.d.code_bits == 16;
   if (x_dtype == AQMB_F16) launch_x<AQMB_F16>(a, b16, grid, st);
   else launch_x<AQMB_BF16>(a, b16, grid, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int items = batch * ((L.d.d_out + 3) / 4);
+  gemv_reduce_kernel<<<(items + 63) / 64, kReduceThreads, 0, st>>>(a);
   return hipGetLastError();
 }
 
