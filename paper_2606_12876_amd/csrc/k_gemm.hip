@@ -2,43 +2,101 @@
 // reconstruction from the first k codebooks (binary32 left fold over planes), rounded to bf16,
 // and the products run on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16, fp32 accumulate).
 //
-// A workgroup computes a BM x BN tile of Y (BM = 256 tokens, BN = 128 output rows) with eight
-// waves in two roles that share each SIMD:
-//   - four consumer waves, each owning a 128 x 64 block of the tile (4 x 2 MFMA blocks of
-//     32 x 32), load their X fragments straight from global memory into registers one K step
-//     ahead and run the MFMAs;
-//   - four producer waves dequantize the next BK = 32 slab of the weight tile into a
-//     double-buffered LDS tile: per group, gather the k codewords from the codebooks held in
-//     LDS, fold them in binary32, round to bf16.
-// One barrier per K step hands a finished weight slab to the consumers and a consumed one back
-// to the producers. Within a step the MFMA K dimension is mapped so that each lane's X
-// fragments are one contiguous 32-byte piece of a row (K offsets 16h + 8i for half h and
-// sub-step i); the weight fragments follow the same mapping, which leaves the product unchanged.
-// (BK = 32 keeps the consumers' accumulators plus two steps of X fragments within the 256
-// registers a wave has at two waves per SIMD.)
-// Row scales are applied to the fp32 accumulators in the epilogue.
+// A workgroup computes a BM x BN tile of Y (BM = 256 tokens, BN = 128 output rows), walking
+// d_in in steps of BK = 64 (four MFMA K-blocks of 16). Eight waves share the four SIMDs in two
+// roles, handing data over through LDS with one barrier per step:
+//   - four consumer waves each own a 128 x 64 block of the tile (4 x 2 MFMA blocks of 32 x 32,
+//     fp32 accumulators in registers). They also stream X: direct global->LDS loads (16 bytes
+//     per lane, eight lanes per 128-byte row segment) fill a ring of X stages several steps
+//     ahead, so X reaches LDS without passing through registers. Within a step the fragments
+//     of K-block i + 1 are read from LDS while the MFMAs of block i run;
+//   - four producer waves dequantize the next step's weight slab into a double-buffered LDS
+//     buffer: per group, gather the k codewords from the codebooks held in LDS, fold them in
+//     binary32 and round to bf16. Each producer wave streams its own code words into its own
+//     LDS ring a few steps ahead with direct loads.
+// X stages are row-major with the eight 16-byte pieces of a row XOR-swizzled by the row index,
+// so the 32 rows of a fragment read hit distinct banks. Weight slabs are stored in MFMA operand
+// order (a 1 KiB chunk is one 32 x 16 fragment as the 64 lanes read it).
+// Column blocks start their K walk at different steps, so the workgroups that share an XCD
+// (and its L2) read different parts of their common X rows at any time. Row scales are applied
+// to the fp32 accumulators in the epilogue.
+//
+// Loads that fill LDS directly are issued as inline assembly and awaited with explicit vmcnt
+// waits before the barrier (or, for a wave's private code ring, before its own reads): the
+// compiler cannot see that their destinations are disjoint and would otherwise serialise them.
+// Every such load instruction is issued unconditionally (out-of-range rows and groups read a
+// valid address and are masked later), so each wait counts a fixed number of loads.
 #include "device.h"
 #include "launch.h"
 
 namespace aqmb {
 
 namespace gemm {
-constexpr int BM = 256, BN = 128, BK = 32;
-constexpr int kThreads = 512;          // waves 0-3 consume, waves 4-7 produce
-constexpr int LDB = BK + 8;            // weight tile pitch in bf16: 80 bytes, conflict-free fragment reads
-constexpr int kTileElems = BN * LDB;   // one weight slab buffer
+constexpr int BM = 256, BN = 128, BK = 64;
+constexpr int kThreads = 512;                        // waves 0-3 consume, waves 4-7 produce
+template <int K> constexpr int x_depth() { return K <= 4 ? 3 : 2; }   // X stages (LDS budget)
+constexpr int kXStage = BM * BK;                     // bf16 elements: 256 rows x 128 bytes
+constexpr int kChunk = 512;                          // one weight fragment: 64 lanes x 8 bf16
+constexpr int kSlab = (BN / 32) * (BK / 16) * kChunk;  // 4 column blocks x 4 K-blocks
+constexpr int kCodeDepth = 4;                        // steps of code words in flight per producer wave
+typedef __attribute__((address_space(3))) void* lds_ptr;
 }  // namespace gemm
 
-// Binary32 left fold of one group's k codewords (fp16) and rounding to bf16 pairs.
+#define AQMB_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x70 | 0xF00)
+
+// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at lds_base + 16 l.
+// Issued as inline assembly so the compiler does not serialise these loads against each other
+// and against later LDS reads (it cannot see that the destinations are disjoint); completion is
+// awaited explicitly with AQMB_WAIT_VMCNT before the barrier that publishes the data. Loads the
+// compiler issues itself are only ever over-waited by the extra outstanding count.
+__device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(gptr) : "memory", "m0");
+}
+
+// acc + fp16 value (low or high half of w), one binary32 rounding (fma with 1.0).
+__device__ __forceinline__ float add_f16_lo(uint32_t w, float acc) {
+  float d;
+  asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel_hi:[1,0,0]" : "=v"(d) : "v"(w), "v"(acc));
+  return d;
+}
+__device__ __forceinline__ float add_f16_hi(uint32_t w, float acc) {
+  float d;
+  asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(d) : "v"(w), "v"(acc));
+  return d;
+}
+
+// Direct global->LDS load of 4 bytes per lane: lane l's word lands at lds_base + 4 l.
+__device__ __forceinline__ void load_lds4(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(gptr) : "memory", "m0");
+}
+
+template <int K>
+__device__ __forceinline__ uint4 fold_bf16(const uint4 (&c)[K]) {
+  float w[8] = {f16lo(c[0].x), f16hi(c[0].x), f16lo(c[0].y), f16hi(c[0].y),
+                f16lo(c[0].z), f16hi(c[0].z), f16lo(c[0].w), f16hi(c[0].w)};
+#pragma unroll
+  for (int m = 1; m < K; ++m) {
+    w[0] = add_f16_lo(c[m].x, w[0]); w[1] = add_f16_hi(c[m].x, w[1]);
+    w[2] = add_f16_lo(c[m].y, w[2]); w[3] = add_f16_hi(c[m].y, w[3]);
+    w[4] = add_f16_lo(c[m].z, w[4]); w[5] = add_f16_hi(c[m].z, w[5]);
+    w[6] = add_f16_lo(c[m].w, w[6]); w[7] = add_f16_hi(c[m].w, w[7]);
+  }
+  return make_uint4(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]), pack_bf16x2(w[4], w[5]), pack_bf16x2(w[6], w[7]));
+}
+
 template <int K>
 __device__ __forceinline__ uint4 dequant_group_bf16(const uint4* __restrict__ cbs, const uint32_t (&word)[K], int sh) {
-  float w[8];
+  const uint4 c0 = cbs[(word[0] >> sh) & 0xFFu];
+  float w[8] = {f16lo(c0.x), f16hi(c0.x), f16lo(c0.y), f16hi(c0.y), f16lo(c0.z), f16hi(c0.z), f16lo(c0.w), f16hi(c0.w)};
 #pragma unroll
-  for (int m = 0; m < K; ++m) {
+  for (int m = 1; m < K; ++m) {
     const uint4 c = cbs[m * 256 + ((word[m] >> sh) & 0xFFu)];
-    const float f[8] = {f16lo(c.x), f16hi(c.x), f16lo(c.y), f16hi(c.y), f16lo(c.z), f16hi(c.z), f16lo(c.w), f16hi(c.w)};
-#pragma unroll
-    for (int t = 0; t < 8; ++t) w[t] = m == 0 ? f[t] : w[t] + f[t];
+    w[0] = add_f16_lo(c.x, w[0]); w[1] = add_f16_hi(c.x, w[1]);
+    w[2] = add_f16_lo(c.y, w[2]); w[3] = add_f16_hi(c.y, w[3]);
+    w[4] = add_f16_lo(c.z, w[4]); w[5] = add_f16_hi(c.z, w[5]);
+    w[6] = add_f16_lo(c.w, w[6]); w[7] = add_f16_hi(c.w, w[7]);
   }
   return make_uint4(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]), pack_bf16x2(w[4], w[5]), pack_bf16x2(w[6], w[7]));
 }
@@ -49,67 +107,123 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
                                                               const uint16_t* __restrict__ scales,
                                                               const uint16_t* __restrict__ X, void* __restrict__ Y,
                                                               int n_tokens, int d_out, int d_in, int G,
-                                                              size_t plane_bytes, int n_tb) {
+                                                              size_t plane_bytes, int n_tb, int n_cb) {
   using namespace gemm;
+  constexpr int kDepth = x_depth<K>();
   extern __shared__ uint4 smem[];
-  uint16_t* Bs = (uint16_t*)smem;                 // [2][BN][LDB] bf16
-  uint4* cbs = (uint4*)(Bs + 2 * kTileElems);     // [K][256] codewords (fp16 x 8)
+  uint16_t* Xs = (uint16_t*)smem;                  // [kDepth][256 rows][8 swizzled 16-byte pieces]
+  uint16_t* Bs = Xs + kDepth * kXStage;            // [2][4 col blocks][4 K-blocks][64 lanes][8]
+  uint4* cbs = (uint4*)(Bs + 2 * kSlab);           // [K][256] codewords (fp16 x 8)
+  uint32_t* cring = (uint32_t*)(cbs + K * 256);     // [kCodeDepth][4 producer waves][K][64 lanes] code words
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // Token blocks fastest: consecutive workgroup ids (which the dispatcher spreads over the
-  // XCDs) share a column block, and the workgroups of one token block land on one XCD when
-  // there are 8 token blocks, so that XCD's L2 keeps those X rows.
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform across the wave
+  const int half = lane >> 5, r32 = lane & 31;
   const int tb = blockIdx.x % n_tb, cb = blockIdx.x / n_tb;
   const int n0 = tb * BM, i0 = cb * BN;
   const int nsteps = (d_in + BK - 1) / BK;
+  const int s0 = (int)(((long long)cb * nsteps) / n_cb);
+  auto step_of = [&](int seq) { int st = s0 + seq; return st >= nsteps ? st - nsteps : st; };
 
   for (int q = tid; q < K * 256; q += kThreads) cbs[q] = ((const uint4*)codebooks)[q];
 
   if (wave >= 4) {
     // ------------------------------------------------------------------ producers
-    const int p = tid - 256;                       // 0..255
-    const int col = p >> 1, g2 = (p & 1) * 2;     // two groups of one weight row per step
+    const int p = tid - 256;
+    const int col = p & (BN - 1), gq = p >> 7;     // weight row; groups 4 gq .. 4 gq + 3 of a step
     const bool col_ok = i0 + col < d_out;
-    uint32_t cur[K], nxt[K];
-    auto load_codes = [&](int step, uint32_t (&w)[K]) {
-      const int j0 = step * (BK / 8) + g2;         // first of the two groups (same slice, even)
-#pragma unroll
-      for (int m = 0; m < K; ++m) {
-        w[m] = 0;
-        if (col_ok && j0 < G)
-          w[m] = *(const uint32_t*)(codes + m * plane_bytes + ((size_t)(j0 >> 4) * d_out + i0 + col) * 16 + (j0 & 12));
-      }
+    // Code words: each producer wave streams exactly the words its own lanes need (one 4-byte
+    // word per plane: the 4 groups of this thread's column in the step) straight into its own
+    // LDS ring, kCodeDepth steps ahead, and waits only for its own loads (no other wave reads
+    // them). Exactly K loads per step per wave, so "step q's words are in" is a fixed vmcnt.
+    const int pw = wave - 4;
+    const int col_ld = col_ok ? i0 + col : d_out - 1;
+    auto ring_base = [&](int seq) {
+      return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)(cring + ((seq % kCodeDepth) * 4 + pw) * K * 64);
     };
-    auto produce = [&](int step, const uint32_t (&w)[K]) {
-      uint16_t* dst = Bs + (step & 1) * kTileElems + col * LDB + g2 * 8;
-      const int j0 = step * (BK / 8) + g2;
+    auto load_codes = [&](int seq) {
+      int j0 = step_of(seq) * (BK / 8) + 4 * gq;   // 4-aligned: one code word per plane
+      if (j0 >= G) j0 = 0;                          // padding groups: any valid word, zeroed later
+      const uint32_t base = ring_base(seq);
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        uint4 v = dequant_group_bf16<K>(cbs, w, 8 * ((j0 & 3) + q));
+      for (int m = 0; m < K; ++m)
+        load_lds4(codes + m * plane_bytes + ((size_t)(j0 >> 4) * d_out + col_ld) * 16 + (j0 & 15), base + m * 256);
+    };
+    auto wait_codes = [&](int seq) {               // this wave's words of step seq are in LDS
+      const int after = min(kCodeDepth - 1, nsteps - 1 - seq);
+      if (after >= 3) AQMB_WAIT_VMCNT(3 * K);
+      else if (after == 2) AQMB_WAIT_VMCNT(2 * K);
+      else if (after == 1) AQMB_WAIT_VMCNT(K);
+      else AQMB_WAIT_VMCNT(0);
+    };
+    auto produce = [&](int seq) {
+      const int j0 = step_of(seq) * (BK / 8) + 4 * gq;
+      uint16_t* slab = Bs + (seq & 1) * kSlab;
+      const uint32_t* words = cring + ((seq % kCodeDepth) * 4 + pw) * K * 64 + lane;
+      uint32_t word[K];
+#pragma unroll
+      for (int m = 0; m < K; ++m) word[m] = words[m * 64];
+      // all 4K codeword gathers first, then the folds
+      uint4 cw[4][K];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int m = 0; m < K; ++m) cw[q][m] = cbs[m * 256 + ((word[m] >> (8 * q)) & 0xFFu)];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int g = 4 * gq + q;                   // group within the step: K-block g / 2, half g % 2
+        uint4 v = fold_bf16<K>(cw[q]);
         if (!col_ok || j0 + q >= G) v = make_uint4(0, 0, 0, 0);
-        *(uint4*)(dst + q * 8) = v;
+        *(uint4*)(slab + ((col >> 5) * 4 + (g >> 1)) * kChunk + ((col & 31) + 32 * (g & 1)) * 8) = v;
       }
     };
-    load_codes(0, cur);
-    if (nsteps > 1) load_codes(1, nxt);
-    __syncthreads();                                // codebooks staged
-    produce(0, cur);
-    __syncthreads();                                // slab 0 ready
-    for (int s = 0; s < nsteps; ++s) {
-      if (s + 1 < nsteps) {
-#pragma unroll
-        for (int m = 0; m < K; ++m) cur[m] = nxt[m];
-        if (s + 2 < nsteps) load_codes(s + 2, nxt);
-        produce(s + 1, cur);
+    for (int d = 0; d < kCodeDepth && d < nsteps; ++d) load_codes(d);
+    __syncthreads();                                 // codebooks staged
+    wait_codes(0);
+    produce(0);
+    if (kCodeDepth < nsteps) load_codes(kCodeDepth);   // refills the slot of step 0
+    for (int seq = 0; seq < nsteps; ++seq) {
+      __syncthreads();                               // slab seq published; slab seq+1 free
+      if (seq + 1 < nsteps) {
+        wait_codes(seq + 1);
+        produce(seq + 1);
+        if (seq + 1 + kCodeDepth < nsteps) load_codes(seq + 1 + kCodeDepth);
       }
-      __syncthreads();
     }
     return;
   }
 
   // -------------------------------------------------------------------- consumers
   const int wm = wave >> 1, wn = wave & 1;          // 128 x 64 block of the tile
-  const int half = lane >> 5, r32 = lane & 31;
+  // X stage layout: row r's 16-byte piece kc (8 bf16 of K) sits at r * 128 + ((kc ^ (r & 7)) * 16)
+  // bytes. A direct load covers 8 rows x 128 bytes (8 lanes per row, full cache lines); the
+  // XOR keeps fragment reads (32 rows, one piece each) on distinct banks.
+  auto load_x = [&](int seq) {
+    const int k0 = step_of(seq) * BK;
+    uint16_t* stage = Xs + (seq % kDepth) * kXStage;
+    const int pos = lane & 7, rsub = lane >> 3;
+    if (k0 + BK <= d_in) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {                 // this wave's rows 64 * wave .. + 63
+        const int r = wave * 64 + t * 8 + rsub;
+        const int kc = pos ^ (r & 7);
+        const int row = n0 + r < n_tokens ? n0 + r : n_tokens - 1;
+        uint16_t* base = stage + (wave * 64 + t * 8) * BK;   // 1 KiB: 8 rows, written lane-ordered
+        load_lds16(X + (size_t)row * d_in + k0 + kc * 8, (uint32_t)(uintptr_t)(lds_ptr)base);
+      }
+    } else {                                         // the ragged last step: zero past d_in
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int r = wave * 64 + t * 8 + rsub;
+        const int kc = pos ^ (r & 7);
+        const int row = n0 + r;
+        uint16_t* base = stage + (wave * 64 + t * 8) * BK;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (row < n_tokens && k0 + kc * 8 < d_in) v = *(const uint4*)(X + (size_t)row * d_in + k0 + kc * 8);
+        *(uint4*)(base + lane * 8) = v;
+      }
+    }
+  };
   f32x16_t acc[4][2];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
@@ -118,52 +232,54 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
 
-  // X fragments of one step: for each of the 4 row blocks, 16 bf16 (32 bytes) of one row.
-  uint4 xa[4][2], xn[4][2];
-  auto load_x = [&](int step, uint4 (&dst)[4][2]) {
-    const int kc = step * BK + half * 16;
+  struct Frags { bf16x8_t a[4], b[2]; };
+  auto read_frags = [&](const uint16_t* xst, const uint16_t* bsl, int i, Frags& f) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) f.b[b] = *(const bf16x8_t*)(bsl + ((wn * 2 + b) * 4 + i) * kChunk + lane * 8);
+    const int kc = 2 * i + half;
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
-      const int row = n0 + wm * 128 + a * 32 + r32;
-      const uint16_t* src = X + (size_t)row * d_in + kc;
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        dst[a][c] = make_uint4(0, 0, 0, 0);
-        if (row < n_tokens && kc + c * 8 < d_in) dst[a][c] = *(const uint4*)(src + c * 8);
-      }
+      const int r = wm * 128 + a * 32 + r32;
+      f.a[a] = *(const bf16x8_t*)(xst + r * BK + ((kc ^ (r & 7)) * 8));
     }
   };
-  load_x(0, xa);
-  __syncthreads();                                  // codebooks staged
-  __syncthreads();                                  // slab 0 ready
-  for (int s = 0; s < nsteps; ++s) {
-    if (s + 1 < nsteps) load_x(s + 1, xn);
-    const uint16_t* Bt = Bs + (s & 1) * kTileElems;
+  auto mfmas = [&](const Frags& f) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {                   // sub-step: K offsets 16 * half + 8 * i
-      bf16x8_t bf[2];
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int col = wn * 64 + b * 32 + r32;
-        bf[b] = *(const bf16x8_t*)(Bt + col * LDB + half * 16 + i * 8);
-      }
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const bf16x8_t af = __builtin_bit_cast(bf16x8_t, xa[a][i]);
-#pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf[b], acc[a][b], 0, 0, 0);
-      }
+      for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
+  };
+
+  for (int seq = 0; seq < kDepth - 1 && seq < nsteps; ++seq) load_x(seq);
+  __syncthreads();                                   // codebooks staged
+  for (int seq = 0; seq < nsteps; ++seq) {
+    {                                                // own X loads of step seq done
+      const int after = min(kDepth - 2, nsteps - 1 - seq);   // later steps already issued
+      if (after >= 1) AQMB_WAIT_VMCNT(8); else AQMB_WAIT_VMCNT(0);
     }
-    if (s + 1 < nsteps) {
+    __syncthreads();                                 // X stage seq and slab seq published
+    if (seq + kDepth - 1 < nsteps) load_x(seq + kDepth - 1);
+    const uint16_t* xst = Xs + (seq % kDepth) * kXStage;
+    const uint16_t* bsl = Bs + (seq & 1) * kSlab;
+    // K-blocks 0..3: the fragments of block i + 1 are read while block i's MFMAs run
+    // (one read, one MFMA, alternating); a scheduling barrier closes each block so the compiler
+    // cannot pull the next block's MFMAs (and their LDS waits) forward.
+    Frags f0, f1;
+    read_frags(xst, bsl, 0, f0);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int c = 0; c < 2; ++c) xa[a][c] = xn[a][c];
+    for (int i = 0; i < 4; ++i) {
+      Frags& cur = (i & 1) ? f1 : f0;
+      Frags& nxt = (i & 1) ? f0 : f1;
+      if (i < 3) read_frags(xst, bsl, i + 1, nxt);
+      mfmas(cur);
+      if (i < 3) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __syncthreads();
   }
-  // Epilogue. Accumulator element e of lane l in a 32 x 32 block holds
-  // row 8 * (e / 4) + 4 * (l / 32) + e % 4, column l % 32.
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int col = i0 + wn * 64 + b * 32 + r32;
@@ -183,15 +299,16 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 template <int K>
 static void launch_k(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
   using namespace gemm;
+  constexpr int kDepth = x_depth<K>();
   const int n_tb = (n_tokens + BM - 1) / BM, n_cb = (L.d.d_out + BN - 1) / BN;
-  const size_t lds = (size_t)2 * kTileElems * 2 + (size_t)K * 256 * 16;
+  const size_t lds = ((size_t)kDepth * kXStage + 2 * kSlab) * 2 + (size_t)K * 256 * 16 + (size_t)kCodeDepth * 4 * K * 64 * 4;
   const dim3 grid(n_tb * n_cb);
   if (y_dtype == AQMB_BF16)
     gemm_kernel<K, AQMB_BF16><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                            n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb);
+                                                            n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
   else
     gemm_kernel<K, AQMB_F32><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                           n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb);
+                                                           n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
 }
 
 hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,

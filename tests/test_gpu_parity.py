@@ -206,6 +206,26 @@ def test_gemm_small_shapes(shape):
                 check_close(got, ref, ydt, f"gemm {shape} k={k} {ydt}")
 
 
+def test_gemm_subnormal_codebook_entries():
+    """fp16 subnormal codebook entries enter the binary32 fold exactly in the GEMM's weight tile too."""
+    spec = LayerSpec("gs", 130, 136, M=4, seed=43, act_dtype="bf16")
+    L = make_layer(spec)
+    cb = formats.f16_bits_to_f64(L.codebooks)
+    rng = np.random.default_rng(1)
+    mask = rng.random(cb.shape) < 0.3
+    cb = np.where(mask, rng.integers(-1023, 1024, cb.shape) * 2.0 ** -24, cb)   # subnormal fp16 values
+    cbits = cb.astype(np.float16).view(np.uint16)
+    Xbits = make_activations(L, 70, "bf16")
+    X = act_values(Xbits, "bf16")
+    with GpuLayer(L.codes, cbits, L.scales) as gl:
+        for k in range(1, 5):
+            ref = oracle.gemm_reference(X, L.codes, cbits, L.scales, k)
+            got = run_gemm(gl, k, Xbits, "f32")
+            check_close(got, ref, "f32", f"subnormal k={k}")
+            # tighter: fp32 accumulation of bf16 products only
+            assert np.max(np.abs(got - ref)) <= 1e-5 * np.max(np.abs(ref)) + 1e-30
+
+
 def test_gemm_workload_full_size():
     spec = config("c5")
     L = make_layer(spec)
