@@ -15,6 +15,8 @@
 //
 // 16-bit codes (65536 codewords, 1 MiB per codebook): codewords are gathered from global
 // memory (resident in L2), summed over planes, and dotted with x staged in LDS.
+#include <cstdlib>
+
 #include "device.h"
 #include "launch.h"
 
@@ -25,6 +27,9 @@ constexpr int kRowsPerThread = 1;
 constexpr int kRowsPerWG = kThreads * kRowsPerThread;
 constexpr int kReduceThreads = 256;
 
+// vmcnt(0) only (expcnt and lgkmcnt left at their maxima), gfx9 encoding.
+#define AQMB_GEMV_WAIT_VMCNT0() __builtin_amdgcn_s_waitcnt(0x70 | 0xF00)
+
 struct GemvArgs {
   const unsigned char* codes;
   const uint16_t* codebooks;
@@ -32,6 +37,7 @@ struct GemvArgs {
   const void* x;
   void* y;
   float* partials;     // [S][batch][d_out]
+  const void* zero_page;  // 1 KiB of zeros, never written
   size_t plane_bytes;
   int d_out, d_in, G, S, k, batch;
   int y_dtype;
@@ -39,7 +45,7 @@ struct GemvArgs {
 
 size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S) {
   (void)G;
-  return (size_t)S * AQMB_MAX_BATCH * d.d_out + 64;
+  return 256 + (size_t)S * AQMB_MAX_BATCH * d.d_out + 64;   // zero page, then partial sums
 }
 
 // Partial sums of one batch tile of this workgroup's rows.
@@ -325,12 +331,205 @@ __global__ __launch_bounds__(kThreads) void gemv_b16_kernel(GemvArgs a) {
   store_partials<NB>(a, 0, acc);
 }
 
+// Direct-gather GEMV for 8-bit codes: one kernel, no partial sums. A workgroup of 1024 threads
+// owns 16 rows; the 64 threads of a row split its groups (thread `part` takes groups
+// 512 u + 8 part .. + 7 for u = 0, 1, ...), gather each code's codeword from the codebooks held
+// in LDS and accumulate <x_group, codeword> in fp32 (dot products of exact fp16 products).
+// A row's 64 partial sums are added in a fixed order (two shuffles, then the 16 waves through
+// LDS), so results are reproducible. Sixteen waves per CU keep the LDS and memory pipelines
+// busy while individual waves wait.
+// The codebooks are stored NREP times in LDS, interleaved so that codeword c of replica r sits
+// at (c * NREP + r) * 16 bytes: lane l reads replica l % NREP, which spreads the random 16-byte
+// reads of a wave over NREP bank groups instead of colliding at random.
+// x is staged in LDS once per batch tile of NB rows by direct global->LDS loads, each row padded
+// with zeros (read from the zero page at the head of the layer workspace) up to the padded group
+// count, so the group loops need no bounds tests: padding groups have code 0 and x = 0.
+namespace cw {
+constexpr int kThreads = 1024, kRows = 16, kParts = 64, kWaves = kThreads / 64;
+__host__ __device__ inline size_t row_stride(int S) {   // bytes per staged x row, whole KiB
+  return ((size_t)S * 16 * 16 + 1023) / 1024 * 1024;
+}
+}
+
+// 16-byte direct global->LDS load (lane l's bytes at lds_base + 16 l); awaited with vmcnt.
+__device__ __forceinline__ void gemv_load_lds16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(gptr) : "memory", "m0");
+}
+
+constexpr int kCwMaxBlocks = 4;   // 512-group blocks per row held in registers: d_in <= 16384
+
+template <int K, int NB, int XDT, int NREP>
+__global__ __launch_bounds__(cw::kThreads) void gemv_cw_kernel(GemvArgs a) {
+  extern __shared__ uint4 smem_cw[];
+  uint4* cb_rep = smem_cw;                               // [K][256][NREP] codewords
+  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * NREP);    // [NB][row_stride] x tile
+  __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rw = lane & 15, part = tid >> 4;              // row within the group, 0..63
+  const int row = blockIdx.x * cw::kRows + rw;
+  const bool row_ok = row < a.d_out;
+  const int rep = lane % NREP;
+  const int Gp = a.S * 16;                                 // padded groups per row
+  const int U = (Gp + 511) / 512;                          // 512-group blocks
+  const size_t rstride = cw::row_stride(a.S);
+  const uint32_t xs_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)xs;
+
+  // Code words: 8 groups (8 bytes) per plane for this thread's part of a 512-group block; the
+  // first two blocks are requested before anything else, later ones one block ahead.
+  auto load_block = [&](int u, uint2 (&c)[K]) {
+    const int j0 = u * 512 + part * 8;
+#pragma unroll
+    for (int m = 0; m < K; ++m) {
+      c[m] = make_uint2(0, 0);
+      if (u < U && row_ok && j0 < Gp)
+        c[m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 4) * a.d_out + row) * 16 + (j0 & 8));
+    }
+  };
+  uint2 cur[K], nxt[K];
+  load_block(0, cur);
+  load_block(1, nxt);
+
+  // x rows b0 .. b0 + NB - 1 into LDS; elements past d_in (and rows past `batch`) read zeros.
+  auto stage_x = [&](int b0) {
+    const int nch = (int)(rstride / 1024);
+    for (int q = wave; q < NB * nch; q += cw::kWaves) {
+      const int b = q / nch, ch = q % nch;
+      const int e = ch * 512 + lane * 8;                   // element offset in the row
+      const void* src = (b0 + b < a.batch && e < a.d_in)
+                            ? (const void*)((const uint16_t*)a.x + (size_t)(b0 + b) * a.d_in + e)
+                            : (const void*)a.zero_page;
+      gemv_load_lds16(src, xs_base + (uint32_t)(b * rstride + (size_t)ch * 1024));
+    }
+  };
+
+  for (int b0 = 0; b0 < a.batch; b0 += NB) {
+    if (b0 == 0) {
+      // Codebook replicas (the loads precede the x loads; the wait for them is vmcnt(0) below).
+      for (int q = tid; q < K * 256; q += cw::kThreads) {
+        const uint4 v = ((const uint4*)a.codebooks)[q];
+#pragma unroll
+        for (int r = 0; r < NREP; ++r) cb_rep[q * NREP + r] = v;
+      }
+    } else {
+      __syncthreads();                                     // the previous tile's reads of xs are done
+    }
+    stage_x(b0);
+    AQMB_GEMV_WAIT_VMCNT0();                               // this wave's x (and code) loads are in
+    __syncthreads();
+
+    float acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[b] = 0.f;
+    if (b0 > 0) { load_block(0, cur); load_block(1, nxt); }
+    for (int u = 0; u < U; ++u) {
+      const int j0 = u * 512 + part * 8;
+      if (j0 < Gp) {
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          uint4 xg[NB];
+#pragma unroll
+          for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)((const char*)xs + b * rstride + (size_t)(j0 + jj) * 16);
+#pragma unroll
+          for (int m = 0; m < K; ++m) {
+            const uint32_t word = jj < 4 ? cur[m].x : cur[m].y;
+            const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
+            const uint4 cwv = cb_rep[(m * 256 + c) * NREP + rep];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) acc[b] += group_dot<XDT>(xg[b], cwv);
+          }
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < K; ++m) cur[m] = nxt[m];
+      load_block(u + 2, nxt);
+    }
+    // row sum: lanes rw, rw + 16, rw + 32, rw + 48 of the wave, then the 16 waves in order
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float v = acc[b];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      acc[b] = v;
+    }
+    if (lane < 16) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) red[wave][rw][b] = acc[b];
+    }
+    __syncthreads();
+    if (wave == 0 && lane < 16 && row_ok) {
+      const float scale = f16_to_f32(a.scales[row]);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if (b0 + b < a.batch) {
+          float sum = 0.f;
+#pragma unroll
+          for (int w = 0; w < cw::kWaves; ++w) sum += red[w][rw][b];
+          const size_t o = (size_t)(b0 + b) * a.d_out + row;
+          const float v = sum * scale;
+          if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, o, v);
+          else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, o, v);
+          else OutT<AQMB_F32>::store(a.y, o, v);
+        }
+      }
+    }
+  }
+}
+
+// Replicas per codebook: as many as fit next to the x tile (LDS holds 160 KiB per workgroup).
+static int cw_nrep(int K, int nb, int S) {
+  const size_t budget = 160 * 1024 - (size_t)cw::kWaves * cw::kRows * 4 * nb - 512;  // minus the row sums
+  const size_t xb = (size_t)nb * cw::row_stride(S);
+  for (int r : {8, 4})
+    if ((size_t)K * 256 * r * 16 + xb <= budget) return r;
+  return 0;
+}
+
+template <int K, int NB, int XDT>
+static hipError_t launch_cw_nb(const GemvArgs& a, hipStream_t st) {
+  const int nrep = cw_nrep(K, NB, a.S);
+  const dim3 grid((a.d_out + cw::kRows - 1) / cw::kRows);
+  auto lds = [&](int r) { return (size_t)K * 256 * r * 16 + (size_t)NB * cw::row_stride(a.S); };
+  switch (nrep) {
+    case 8: gemv_cw_kernel<K, NB, XDT, 8><<<grid, cw::kThreads, lds(8), st>>>(a); break;
+    case 4: gemv_cw_kernel<K, NB, XDT, 4><<<grid, cw::kThreads, lds(4), st>>>(a); break;
+    default: return hipErrorInvalidValue;       // x tile does not fit: caller uses another path
+  }
+  return hipGetLastError();
+}
+
+template <int K, int XDT>
+static hipError_t launch_cw(const GemvArgs& a, hipStream_t st) {
+  if (a.batch == 1) return launch_cw_nb<K, 1, XDT>(a, st);
+  if (a.batch == 2) return launch_cw_nb<K, 2, XDT>(a, st);
+  return launch_cw_nb<K, 4, XDT>(a, st);         // batch 3..16: tiles of 4 rows
+}
+
+// The direct-gather kernel covers k <= 4 and d_in <= 16384 (the code words of a thread's
+// groups stay in registers); other shapes take the lookup-table path.
+static bool cw_fits(int K, int batch, int S) {
+  const int nb = batch == 1 ? 1 : batch == 2 ? 2 : 4;
+  return K <= 4 && (S * 16 + 511) / 512 <= kCwMaxBlocks && cw_nrep(K, nb, S) > 0;
+}
+
 template <int K, int XDT>
 static void launch_lut(const GemvArgs& a, dim3 grid, hipStream_t st) {
   const size_t lds = (size_t)K * 16 * 256 * sizeof(float);  // K * JH * 256 * BT floats, JH * BT = 16
   if (a.batch == 1) gemv_lut_kernel<K, 1, XDT><<<grid, kThreads, lds, st>>>(a);
   else if (a.batch == 2) gemv_lut_kernel<K, 2, XDT><<<grid, kThreads, lds, st>>>(a);
   else gemv_lut_kernel<K, 4, XDT><<<grid, kThreads, lds, st>>>(a);
+}
+
+template <int XDT>
+static hipError_t launch_cw_any(const GemvArgs& a, hipStream_t st) {
+  switch (a.k) {
+    case 1: return launch_cw<1, XDT>(a, st);
+    case 2: return launch_cw<2, XDT>(a, st);
+    case 3: return launch_cw<3, XDT>(a, st);
+    case 4: return launch_cw<4, XDT>(a, st);
+    default: return hipErrorInvalidValue;       // not reached: cw_fits requires k <= 4
+  }
 }
 
 template <int XDT>
@@ -352,6 +551,17 @@ static void launch_x(const GemvArgs& a, bool b16, dim3 grid, hipStream_t st) {
   }
 }
 
+// 8-bit GEMV variant: 1 = direct codeword gather (default), 0 = split-K lookup tables.
+// AQMB_GEMV=lut|cw overrides (read once).
+static int gemv_variant() {
+  static const int v = [] {
+    const char* e = getenv("AQMB_GEMV");
+    if (e && (e[0] == 'l' || e[0] == 'L')) return 0;
+    return 1;
+  }();
+  return v;
+}
+
 hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                        aqmb_dtype y_dtype, hipStream_t st) {
   GemvArgs a;
@@ -360,7 +570,8 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   a.scales = L.scales;
   a.x = x;
   a.y = y;
-  a.partials = L.ws;
+  a.zero_page = L.ws;                    // the first KiB of the workspace stays zero
+  a.partials = L.ws + 256;
   a.plane_bytes = L.plane_bytes;
   a.d_out = L.d.d_out;
   a.d_in = L.d.d_in;
@@ -371,6 +582,9 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   a.y_dtype = (int)y_dtype;
   const dim3 grid((L.d.d_out + kRowsPerWG - 1) / kRowsPerWG, L.S);
   const bool b16 = L.d.code_bits == 16;
+  if (!b16 && gemv_variant() == 1 && cw_fits(k, batch, L.S)) {   // direct gather: one kernel
+    return x_dtype == AQMB_F16 ? launch_cw_any<AQMB_F16>(a, st) : launch_cw_any<AQMB_BF16>(a, st);
+  }
   if (x_dtype == AQMB_F16) launch_x<AQMB_F16>(a, b16, grid, st);
   else launch_x<AQMB_BF16>(a, b16, grid, st);
   hipError_t e = hipGetLastError();
