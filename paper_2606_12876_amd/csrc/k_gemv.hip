@@ -41,6 +41,8 @@ struct GemvArgs {
   size_t plane_bytes;
   int d_out, d_in, G, S, k, batch;
   int y_dtype;
+  int nrep;            // codebook replicas in LDS (direct-gather kernel), a power of two
+  int cb_shift;        // log2(nrep * 16): byte shift from a code to its codeword
 };
 
 size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S) {
@@ -333,17 +335,20 @@ __global__ __launch_bounds__(kThreads) void gemv_b16_kernel(GemvArgs a) {
 
 // Direct-gather GEMV for 8-bit codes: one kernel, no partial sums. A workgroup of 1024 threads
 // owns 16 rows; the 64 threads of a row split its groups (thread `part` takes groups
-// 512 u + 8 part .. + 7 for u = 0, 1, ...), gather each code's codeword from the codebooks held
+// 512 u + 8 part .. + 7 for u = 0 .. UB - 1), gather each code's codeword from the codebooks held
 // in LDS and accumulate <x_group, codeword> in fp32 (dot products of exact fp16 products).
 // A row's 64 partial sums are added in a fixed order (two shuffles, then the 16 waves through
-// LDS), so results are reproducible. Sixteen waves per CU keep the LDS and memory pipelines
-// busy while individual waves wait.
-// The codebooks are stored NREP times in LDS, interleaved so that codeword c of replica r sits
-// at (c * NREP + r) * 16 bytes: lane l reads replica l % NREP, which spreads the random 16-byte
-// reads of a wave over NREP bank groups instead of colliding at random.
+// LDS), so results are reproducible.
+// The codebooks are stored nrep times in LDS, interleaved so that codeword c of replica r sits
+// at (c * nrep + r) * 16 bytes: lane l reads replica l % nrep, which spreads the random 16-byte
+// reads of a wave over nrep bank groups instead of colliding at random.
 // x is staged in LDS once per batch tile of NB rows by direct global->LDS loads, each row padded
 // with zeros (read from the zero page at the head of the layer workspace) up to the padded group
 // count, so the group loops need no bounds tests: padding groups have code 0 and x = 0.
+// Issue order: x, then the codebooks, then every code word the thread needs (all planes, all
+// blocks, addresses clamped into the layer so that each thread issues the same loads). Loads
+// complete in order, so the codebook replication waits for the codebook only while the code
+// planes stream in from HBM, and with one batch row the gather of plane m waits only for plane m.
 namespace cw {
 constexpr int kThreads = 1024, kRows = 16, kParts = 64, kWaves = kThreads / 64;
 __host__ __device__ inline size_t row_stride(int S) {   // bytes per staged x row, whole KiB
@@ -357,39 +362,35 @@ __device__ __forceinline__ void gemv_load_lds16(const void* gptr, uint32_t lds_b
                :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(gptr) : "memory", "m0");
 }
 
+// s_waitcnt vmcnt(N), other counters left at their maxima (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
 constexpr int kCwMaxBlocks = 4;   // 512-group blocks per row held in registers: d_in <= 16384
 
-template <int K, int NB, int XDT, int NREP>
-__global__ __launch_bounds__(cw::kThreads) void gemv_cw_kernel(GemvArgs a) {
+template <int K, int NB, int XDT, int UB>
+__global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_cw_kernel(GemvArgs a) {
   extern __shared__ uint4 smem_cw[];
-  uint4* cb_rep = smem_cw;                               // [K][256][NREP] codewords
-  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * NREP);    // [NB][row_stride] x tile
+  const int nrep = a.nrep;
+  uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords
+  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);    // [NB][row_stride] x tile
   __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rw = lane & 15, part = tid >> 4;              // row within the group, 0..63
   const int row = blockIdx.x * cw::kRows + rw;
   const bool row_ok = row < a.d_out;
-  const int rep = lane % NREP;
+  const int rowc = row_ok ? row : a.d_out - 1;
   const int Gp = a.S * 16;                                 // padded groups per row
-  const int U = (Gp + 511) / 512;                          // 512-group blocks
   const size_t rstride = cw::row_stride(a.S);
   const uint32_t xs_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)xs;
-
-  // Code words: 8 groups (8 bytes) per plane for this thread's part of a 512-group block; the
-  // first two blocks are requested before anything else, later ones one block ahead.
-  auto load_block = [&](int u, uint2 (&c)[K]) {
-    const int j0 = u * 512 + part * 8;
-#pragma unroll
-    for (int m = 0; m < K; ++m) {
-      c[m] = make_uint2(0, 0);
-      if (u < U && row_ok && j0 < Gp)
-        c[m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 4) * a.d_out + row) * 16 + (j0 & 8));
-    }
-  };
-  uint2 cur[K], nxt[K];
-  load_block(0, cur);
-  load_block(1, nxt);
+  const int cb_shift = a.cb_shift;                         // codeword c starts at c << cb_shift
+  const uint32_t cb_stride = 1u << cb_shift;
+  const uint32_t rep_off = (uint32_t)(lane % nrep) * 16;
 
   // x rows b0 .. b0 + NB - 1 into LDS; elements past d_in (and rows past `batch`) read zeros.
   auto stage_x = [&](int b0) {
@@ -404,46 +405,79 @@ __global__ __launch_bounds__(cw::kThreads) void gemv_cw_kernel(GemvArgs a) {
     }
   };
 
-  for (int b0 = 0; b0 < a.batch; b0 += NB) {
-    if (b0 == 0) {
-      // Codebook replicas (the loads precede the x loads; the wait for them is vmcnt(0) below).
-      for (int q = tid; q < K * 256; q += cw::kThreads) {
-        const uint4 v = ((const uint4*)a.codebooks)[q];
+  stage_x(0);
+  asm volatile("" ::: "memory");
+  const int q = tid % (K * 256);                           // K * 256 <= 1024 codewords
+  const uint4 cbv = ((const uint4*)a.codebooks)[q];
+  asm volatile("" ::: "memory");
+  uint2 code[UB][K];                                       // 8 codes per (block, plane)
 #pragma unroll
-        for (int r = 0; r < NREP; ++r) cb_rep[q * NREP + r] = v;
-      }
-    } else {
-      __syncthreads();                                     // the previous tile's reads of xs are done
-    }
-    stage_x(b0);
-    AQMB_GEMV_WAIT_VMCNT0();                               // this wave's x (and code) loads are in
-    __syncthreads();
+  for (int u = 0; u < UB; ++u) {
+    int j0 = u * 512 + part * 8;
+    j0 = j0 < Gp ? j0 : Gp - 8;                            // unused blocks reload a valid word
+#pragma unroll
+    for (int m = 0; m < K; ++m)
+      code[u][m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 4) * a.d_out + rowc) * 16 + (j0 & 8));
+  }
+  wait_vmcnt<UB * K>();                                    // x and the codebook word are in
+  if (tid < K * 256) {
+    // write i of thread q goes to replica (i + q / (16 / nrep)) % nrep: the 16 threads that share
+    // a 256-byte bank row write 16 distinct 16-byte slots of it, so the stores do not collide
+    const int rot = q >> (8 - cb_shift);                   // q / (16 / nrep); cb_shift = log2(16 nrep)
+    for (int i = 0; i < nrep; ++i) cb_rep[q * nrep + ((i + rot) & (nrep - 1))] = cbv;
+  }
+  __syncthreads();
 
+  // One batch tile of NB rows of x (already staged); the first tile is peeled out of the loop so
+  // that its waits for the code planes are exact.
+  auto tile = [&](int b0) {
     float acc[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[b] = 0.f;
-    if (b0 > 0) { load_block(0, cur); load_block(1, nxt); }
-    for (int u = 0; u < U; ++u) {
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
       const int j0 = u * 512 + part * 8;
-      if (j0 < Gp) {
+      if (j0 >= Gp) continue;                              // past the padded groups (short rows)
+      const char* xrow = (const char*)xs + (size_t)j0 * 16;
+      if constexpr (NB == 1) {
+        // plane-major: x for the 8 groups in registers, 8 independent gathers per plane
+        uint4 xg[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) xg[jj] = *(const uint4*)(xrow + jj * 16);
+#pragma unroll
+        for (int m = 0; m < K; ++m) {
+          // plane m's code word is awaited here, not earlier (the empty asm keeps its unpacking
+          // from being hoisted above the gathers of the previous planes)
+          uint2 cm = code[u][m];
+          asm volatile("" : "+v"(cm));
+          const uint32_t base = (uint32_t)(m * 256) * cb_stride + rep_off;
+          uint4 cw[8];
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) {
+            const uint32_t word = jj < 4 ? cm.x : cm.y;
+            const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
+            cw[jj] = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + base);
+          }
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) acc[0] += group_dot<XDT>(xg[jj], cw[jj]);
+        }
+      } else {
+        // group-major: the NB x vectors of a group are read once and used for every plane
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
           uint4 xg[NB];
 #pragma unroll
-          for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)((const char*)xs + b * rstride + (size_t)(j0 + jj) * 16);
+          for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xrow + b * rstride + jj * 16);
 #pragma unroll
           for (int m = 0; m < K; ++m) {
-            const uint32_t word = jj < 4 ? cur[m].x : cur[m].y;
+            const uint32_t word = jj < 4 ? code[u][m].x : code[u][m].y;
             const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
-            const uint4 cwv = cb_rep[(m * 256 + c) * NREP + rep];
+            const uint4 cwv = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + (uint32_t)(m * 256) * cb_stride + rep_off);
 #pragma unroll
             for (int b = 0; b < NB; ++b) acc[b] += group_dot<XDT>(xg[b], cwv);
           }
         }
       }
-#pragma unroll
-      for (int m = 0; m < K; ++m) cur[m] = nxt[m];
-      load_block(u + 2, nxt);
     }
     // row sum: lanes rw, rw + 16, rw + 32, rw + 48 of the wave, then the 16 waves in order
 #pragma unroll
@@ -474,28 +508,43 @@ __global__ __launch_bounds__(cw::kThreads) void gemv_cw_kernel(GemvArgs a) {
         }
       }
     }
+  };
+  tile(0);
+  for (int b0 = NB; b0 < a.batch; b0 += NB) {
+    __syncthreads();                                       // the previous tile's reads of xs are done
+    stage_x(b0);
+    wait_vmcnt<0>();
+    __syncthreads();
+    tile(b0);
   }
+}
+
+
+// LDS bytes of the direct-gather kernel: replicated codebooks plus the x tile.
+static size_t cw_lds(int K, int nb, int S, int nrep) {
+  return (size_t)K * 256 * nrep * 16 + (size_t)nb * cw::row_stride(S);
 }
 
 // Replicas per codebook: as many as fit next to the x tile (LDS holds 160 KiB per workgroup).
 static int cw_nrep(int K, int nb, int S) {
   const size_t budget = 160 * 1024 - (size_t)cw::kWaves * cw::kRows * 4 * nb - 512;  // minus the row sums
-  const size_t xb = (size_t)nb * cw::row_stride(S);
   for (int r : {8, 4})
-    if ((size_t)K * 256 * r * 16 + xb <= budget) return r;
+    if (cw_lds(K, nb, S, r) <= budget) return r;
   return 0;
 }
 
+static int cw_nb(int batch) { return batch == 1 ? 1 : batch == 2 ? 2 : 4; }
+static int cw_blocks(int S) { return (S * 16 + 511) / 512; }
+
 template <int K, int NB, int XDT>
-static hipError_t launch_cw_nb(const GemvArgs& a, hipStream_t st) {
-  const int nrep = cw_nrep(K, NB, a.S);
+static hipError_t launch_cw_nb(GemvArgs a, hipStream_t st) {
+  a.nrep = cw_nrep(K, NB, a.S);
+  if (a.nrep == 0) return hipErrorInvalidValue;  // x tile does not fit: caller uses another path
+  a.cb_shift = a.nrep == 8 ? 7 : 6;
   const dim3 grid((a.d_out + cw::kRows - 1) / cw::kRows);
-  auto lds = [&](int r) { return (size_t)K * 256 * r * 16 + (size_t)NB * cw::row_stride(a.S); };
-  switch (nrep) {
-    case 8: gemv_cw_kernel<K, NB, XDT, 8><<<grid, cw::kThreads, lds(8), st>>>(a); break;
-    case 4: gemv_cw_kernel<K, NB, XDT, 4><<<grid, cw::kThreads, lds(4), st>>>(a); break;
-    default: return hipErrorInvalidValue;       // x tile does not fit: caller uses another path
-  }
+  const size_t lds = cw_lds(K, NB, a.S, a.nrep);
+  if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
+  else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks><<<grid, cw::kThreads, lds, st>>>(a);
   return hipGetLastError();
 }
 
@@ -509,8 +558,7 @@ static hipError_t launch_cw(const GemvArgs& a, hipStream_t st) {
 // The direct-gather kernel covers k <= 4 and d_in <= 16384 (the code words of a thread's
 // groups stay in registers); other shapes take the lookup-table path.
 static bool cw_fits(int K, int batch, int S) {
-  const int nb = batch == 1 ? 1 : batch == 2 ? 2 : 4;
-  return K <= 4 && (S * 16 + 511) / 512 <= kCwMaxBlocks && cw_nrep(K, nb, S) > 0;
+  return K <= 4 && cw_blocks(S) <= kCwMaxBlocks && cw_nrep(K, cw_nb(batch), S) > 0;
 }
 
 template <int K, int XDT>
