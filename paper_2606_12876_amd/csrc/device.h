@@ -21,6 +21,13 @@ __device__ __forceinline__ uint4 load_stream16(const void* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// 8-byte streaming load (same cache policy as load_stream16).
+__device__ __forceinline__ uint2 load_stream8(const void* p) {
+  typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+  const u32x2_t v = __builtin_nontemporal_load((const u32x2_t*)p);
+  return make_uint2(v.x, v.y);
+}
+
 // fp16 bits -> fp32 (exact; fp16 subnormals become fp32 normals).
 __device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);

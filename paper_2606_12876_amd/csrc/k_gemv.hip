@@ -346,7 +346,9 @@ __global__ __launch_bounds__(kThreads) void gemv_b16_kernel(GemvArgs a) {
 // with zeros (read from the zero page at the head of the layer workspace) up to the padded group
 // count, so the group loops need no bounds tests: padding groups have code 0 and x = 0.
 // Issue order: x, then the codebooks, then every code word the thread needs (all planes, all
-// blocks, addresses clamped into the layer so that each thread issues the same loads). Loads
+// blocks, addresses clamped into the layer so that each thread issues the same loads). Code
+// words are read once, with a streaming (nontemporal) hint that keeps them from evicting the
+// codebooks and x, which every workgroup re-reads. Loads
 // complete in order, so the codebook replication waits for the codebook only while the code
 // planes stream in from HBM, and with one batch row the gather of plane m waits only for plane m.
 namespace cw {
@@ -417,7 +419,7 @@ void gemv_cw_kernel(GemvArgs a) {
     j0 = j0 < Gp ? j0 : Gp - 8;                            // unused blocks reload a valid word
 #pragma unroll
     for (int m = 0; m < K; ++m)
-      code[u][m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 4) * a.d_out + rowc) * 16 + (j0 & 8));
+      code[u][m] = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 4) * a.d_out + rowc) * 16 + (j0 & 8));
   }
   wait_vmcnt<UB * K>();                                    // x and the codebook word are in
   if (tid < K * 256) {
