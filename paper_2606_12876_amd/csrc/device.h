@@ -28,6 +28,29 @@ __device__ __forceinline__ uint2 load_stream8(const void* p) {
   return make_uint2(v.x, v.y);
 }
 
+// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at lds_base + 16 l (lds_base
+// is an LDS byte address, uniform across the wave). Issued as inline assembly so the compiler
+// neither serialises these loads against each other and against later LDS reads (it cannot see
+// that the destinations are disjoint) nor waits for them; completion is awaited explicitly with
+// wait_vmcnt before the barrier that publishes the data. Loads complete in issue order, so a
+// wait for the loads the compiler issues itself is never too short.
+__device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(gptr) : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N), the other counters left at their maxima (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// LDS byte address of a pointer into shared memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
 // fp16 bits -> fp32 (exact; fp16 subnormals become fp32 normals).
 __device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);

@@ -45,18 +45,24 @@ hipError_t launch_retile(const Layer& L, const void* codes, hipStream_t st) {
 // fused multiply-add is off so every step rounds on its own.
 #pragma clang fp contract(off)
 
+// The output is written once and not read back by this kernel: streaming (nontemporal) stores.
+__device__ __forceinline__ void store_stream16(void* p, uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  const u32x4_t v = {a, b, c, d};
+  __builtin_nontemporal_store(v, (u32x4_t*)p);
+}
+
 template <int OUT>
 __device__ __forceinline__ void store_group(void* W, size_t elem, const float (&w)[8]) {
   if constexpr (OUT == AQMB_F32) {
-    float4* p = (float4*)((float*)W + elem);
-    p[0] = make_float4(w[0], w[1], w[2], w[3]);
-    p[1] = make_float4(w[4], w[5], w[6], w[7]);
+    float* p = (float*)W + elem;
+    store_stream16(p, __float_as_uint(w[0]), __float_as_uint(w[1]), __float_as_uint(w[2]), __float_as_uint(w[3]));
+    store_stream16(p + 4, __float_as_uint(w[4]), __float_as_uint(w[5]), __float_as_uint(w[6]), __float_as_uint(w[7]));
   } else if constexpr (OUT == AQMB_F16) {
-    *(uint4*)((uint16_t*)W + elem) = make_uint4(pack_f16x2(w[0], w[1]), pack_f16x2(w[2], w[3]),
-                                                pack_f16x2(w[4], w[5]), pack_f16x2(w[6], w[7]));
+    store_stream16((uint16_t*)W + elem, pack_f16x2(w[0], w[1]), pack_f16x2(w[2], w[3]),
+                   pack_f16x2(w[4], w[5]), pack_f16x2(w[6], w[7]));
   } else {
-    *(uint4*)((uint16_t*)W + elem) = make_uint4(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]),
-                                                pack_bf16x2(w[4], w[5]), pack_bf16x2(w[6], w[7]));
+    store_stream16((uint16_t*)W + elem, pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]),
+                   pack_bf16x2(w[4], w[5]), pack_bf16x2(w[6], w[7]));
   }
 }
 
@@ -67,7 +73,7 @@ __device__ __forceinline__ void fold_codeword(float (&acc)[8], uint4 cw, bool fi
   for (int t = 0; t < 8; ++t) acc[t] = first ? v[t] : acc[t] + v[t];
 }
 
-// One thread per group: the J lanes of a (row, slice) pair take its J groups, so a wave writes
+// Used for 16-bit codes (and as the general fallback). One thread per group: the J lanes of a (row, slice) pair take its J groups, so a wave writes
 // whole row segments (J groups x 8 values) and the lanes of one row share one 16-byte code
 // chunk per plane (a single cache line). 256-entry codebooks are staged in LDS; 65536-entry
 // codebooks are read through the caches.
@@ -135,10 +141,116 @@ __global__ __launch_bounds__(256) void dequant_kernel(const unsigned char* __res
   }
 }
 
+// 8-bit codes, K = k planes, thread per group: the 16 lanes of a (slice, row) pair take its 16
+// groups, so every store instruction of a wave writes four whole 256-byte row segments. Each
+// thread takes U groups per pass (slots t, t + 256, ...; U = 1 measured best) and passes are
+// grid-strided; the code
+// words and row scales of the next pass are requested before the current pass is folded, with
+// two register sets used in turn so that no copy waits for them. The codebooks go straight to
+// LDS and the first pass's code words are requested right behind them; loads complete in order,
+// so the wait for the codebooks does not wait for the code words. Code words are read once,
+// with a streaming hint. The pointers are deliberately not restrict-qualified: that would let
+// the compiler treat the loads as invariant and move them next to their uses.
+template <int OUT, int K>
+__global__ __launch_bounds__(256) void dequant8_kernel(const unsigned char* codes, const uint16_t* codebooks,
+                                                       const uint16_t* scales, void* W,
+                                                       int d_out, int d_in, int G, int S, size_t plane_bytes) {
+  constexpr int U = 1;
+  extern __shared__ uint4 cb8[];  // [K][256] codewords
+  // group slots fit in 32 bits (the launcher checks 16 S d_out < 2^30)
+  const uint32_t nslot = (uint32_t)S * (uint32_t)d_out * 16u;
+  const uint32_t stride = gridDim.x * blockDim.x * U;
+  uint32_t t = blockIdx.x * blockDim.x * U + threadIdx.x;
+  // code words (the 4-byte word holding each group's code, per plane) and row scales of the U
+  // slots of pass tt; slots past the end re-read the last slot and are not used
+  auto load = [&](uint32_t tt, uint32_t (&w)[U][K], uint32_t (&sc)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      uint32_t slot = tt + u * blockDim.x;
+      slot = slot < nslot ? slot : nslot - 1;
+      const uint32_t pair = slot >> 4;
+      sc[u] = scales[pair % (uint32_t)d_out];
+#pragma unroll
+      for (int m = 0; m < K; ++m)
+        w[u][m] = __builtin_nontemporal_load(
+            (const uint32_t*)(codes + m * plane_bytes + (size_t)pair * 16 + (slot & 12)));
+    }
+  };
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+#pragma unroll
+  for (int i = 0; i < K; ++i)
+    load_lds16((const uint4*)codebooks + i * 256 + threadIdx.x, lds_addr(cb8 + i * 256 + wave * 64));
+  uint32_t wa[U][K], wb[U][K];
+  uint32_t sa[U], sb[U];                             // row scales (fp16 bits), one per register
+  load(t, wa, sa);
+  wait_vmcnt<U * (K + 1)>();
+  __syncthreads();
+  auto pass = [&](uint32_t tt, const uint32_t (&w)[U][K], const uint32_t (&sc)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t slot = tt + u * blockDim.x;
+      const uint32_t pair = slot >> 4;
+      const uint32_t slice = pair / (uint32_t)d_out;
+      const int row = (int)(pair - slice * (uint32_t)d_out);
+      const int grp = (int)slice * 16 + (int)(slot & 15);
+      if (slot >= nslot || grp >= G) continue;
+      const int sh = 8 * (int)(slot & 3);
+      float acc[8];
+#pragma unroll
+      for (int m = 0; m < K; ++m) fold_codeword(acc, cb8[m * 256 + ((w[u][m] >> sh) & 0xFFu)], m == 0);
+      const float scale = f16_to_f32((uint16_t)sc[u]);
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[e] = acc[e] * scale;
+        asm volatile("" : "+v"(v[e]));  // keep the binary32 product (see dequant_kernel)
+      }
+      store_group<OUT>(W, (size_t)row * d_in + (size_t)grp * 8, v);
+    }
+  };
+  for (; t < nslot; t += 2 * stride) {
+    load(t + stride, wb, sb);
+    __builtin_amdgcn_sched_barrier(0);
+    pass(t, wa, sa);
+    if (t + stride >= nslot) break;
+    load(t + 2 * stride, wa, sa);
+    __builtin_amdgcn_sched_barrier(0);
+    pass(t + stride, wb, sb);
+  }
+}
+
+template <int OUT>
+static void launch_dequant8(const Layer& L, int k, void* W, unsigned grid, hipStream_t st) {
+  const size_t lds = (size_t)k * 256 * 16;
+  auto go = [&](auto kern) {
+    kern<<<grid, 256, lds, st>>>(L.codes, L.codebooks, L.scales, W, L.d.d_out, L.d.d_in, L.G, L.S, L.plane_bytes);
+  };
+  switch (k) {
+    case 1: go(dequant8_kernel<OUT, 1>); break;
+    case 2: go(dequant8_kernel<OUT, 2>); break;
+    case 3: go(dequant8_kernel<OUT, 3>); break;
+    case 4: go(dequant8_kernel<OUT, 4>); break;
+    case 5: go(dequant8_kernel<OUT, 5>); break;
+    case 6: go(dequant8_kernel<OUT, 6>); break;
+    case 7: go(dequant8_kernel<OUT, 7>); break;
+    default: go(dequant8_kernel<OUT, 8>); break;
+  }
+}
+
 hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hipStream_t st) {
-  const size_t n = (size_t)L.S * L.d.d_out * L.J;  // one thread per (slice, row, group in slice)
-  // Enough workgroups to fill the chip several times over, few enough that staging the
-  // codebooks in LDS stays small next to the output traffic.
+  const size_t nslot = (size_t)L.S * L.d.d_out * 16;
+  if (L.d.code_bits == 8 && nslot < ((size_t)1 << 30)) {
+    // one thread per group slot and pass; at most 2048 workgroups (eight per CU), so large layers
+    // take several passes and the reads of one overlap the writes of another (t + 2 * stride
+    // stays below 2^31)
+    const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nslot + 255) / 256, 2048));
+    if (w_dtype == AQMB_F32) launch_dequant8<AQMB_F32>(L, k, W, grid, st);
+    else if (w_dtype == AQMB_F16) launch_dequant8<AQMB_F16>(L, k, W, grid, st);
+    else launch_dequant8<AQMB_BF16>(L, k, W, grid, st);
+    return hipGetLastError();
+  }
+  // 16-bit codes (and 8-bit layers too large for 32-bit thread indices): one thread per group
+  const size_t n = (size_t)L.S * L.d.d_out * L.J;
   const unsigned grid = (unsigned)std::min<size_t>((n + 1023) / 1024, 2048);
   const size_t lds = L.d.code_bits == 8 ? (size_t)k * 256 * 16 : 0;
   auto go = [&](auto kern) {

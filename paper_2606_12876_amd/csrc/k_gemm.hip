@@ -44,15 +44,6 @@ typedef __attribute__((address_space(3))) void* lds_ptr;
 
 #define AQMB_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x70 | 0xF00)
 
-// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at lds_base + 16 l.
-// Issued as inline assembly so the compiler does not serialise these loads against each other
-// and against later LDS reads (it cannot see that the destinations are disjoint); completion is
-// awaited explicitly with AQMB_WAIT_VMCNT before the barrier that publishes the data. Loads the
-// compiler issues itself are only ever over-waited by the extra outstanding count.
-__device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(gptr) : "memory", "m0");
-}
 
 // acc + fp16 value (low or high half of w), one binary32 rounding (fma with 1.0).
 __device__ __forceinline__ float add_f16_lo(uint32_t w, float acc) {

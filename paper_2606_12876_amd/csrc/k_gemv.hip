@@ -358,19 +358,6 @@ __host__ __device__ inline size_t row_stride(int S) {   // bytes per staged x ro
 }
 }
 
-// 16-byte direct global->LDS load (lane l's bytes at lds_base + 16 l); awaited with vmcnt.
-__device__ __forceinline__ void gemv_load_lds16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(gptr) : "memory", "m0");
-}
-
-// s_waitcnt vmcnt(N), other counters left at their maxima (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
-}
-
 constexpr int kCwMaxBlocks = 4;   // 512-group blocks per row held in registers: d_in <= 16384
 
 template <int K, int NB, int XDT, int UB>
@@ -403,7 +390,7 @@ void gemv_cw_kernel(GemvArgs a) {
       const void* src = (b0 + b < a.batch && e < a.d_in)
                             ? (const void*)((const uint16_t*)a.x + (size_t)(b0 + b) * a.d_in + e)
                             : (const void*)a.zero_page;
-      gemv_load_lds16(src, xs_base + (uint32_t)(b * rstride + (size_t)ch * 1024));
+      load_lds16(src, xs_base + (uint32_t)(b * rstride + (size_t)ch * 1024));
     }
   };
 
