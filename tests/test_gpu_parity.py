@@ -158,6 +158,23 @@ def test_gemv_workloads(name):
             del W
 
 
+@pytest.mark.parametrize("d_in", [16384, 16392])
+def test_gemv_wide_rows(d_in):
+    """Rows of 2048 groups (the widest the direct-gather kernel keeps in registers) and of 2049
+    groups (taken by the lookup-table kernel), batch 1 and 4, every k."""
+    spec = LayerSpec(f"wide{d_in}", 130, d_in, M=4, seed=38)
+    L = make_layer(spec)
+    C, s = _f64(L)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for b in (1, 4):
+            xbits = make_activations(L, b, "f16", heavy_tail=True)
+            x = act_values(xbits, "f16")
+            for k in range(1, 5):
+                ref = oracle.linear(x, L.codes, C, s, k)
+                got = run_gemv(gl, k, xbits, "f16", "f32")
+                check_close(got, ref, "f32", f"d_in={d_in} b={b} k={k}")
+
+
 def test_gemv_plane_linearity():
     """gemv(k) - gemv(k-1) equals the GEMV of a one-codebook layer holding plane k-1 alone."""
     spec = LayerSpec("lin", 777, 1024, seed=36)
