@@ -14,8 +14,9 @@
 //     buffer: per group, gather the k codewords from the codebooks held in LDS, fold them in
 //     binary32 and round to bf16. Each producer wave streams its own code words into its own
 //     LDS ring a few steps ahead with direct loads.
-// X stages are row-major with the eight 16-byte pieces of a row XOR-swizzled by the row index,
-// so the 32 rows of a fragment read hit distinct banks. Weight slabs are stored in MFMA operand
+// X stages are row-major with the eight 16-byte pieces of a row XOR-swizzled by (row / 2) mod 8:
+// rows are 128 bytes, so two consecutive rows fill one 256-byte bank row, and any 16 consecutive
+// rows of a fragment read (one LDS cycle's worth of 16-byte lanes) hit 16 distinct 16-byte slots. Weight slabs are stored in MFMA operand
 // order (a 1 KiB chunk is one 32 x 16 fragment as the 64 lanes read it).
 // Column blocks start their K walk at different steps, so the workgroups that share an XCD
 // (and its L2) read different parts of their common X rows at any time. Row scales are applied
@@ -186,7 +187,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 
   // -------------------------------------------------------------------- consumers
   const int wm = wave >> 1, wn = wave & 1;          // 128 x 64 block of the tile
-  // X stage layout: row r's 16-byte piece kc (8 bf16 of K) sits at r * 128 + ((kc ^ (r & 7)) * 16)
+  // X stage layout: row r's 16-byte piece kc (8 bf16 of K) sits at r * 128 + ((kc ^ ((r >> 1) & 7)) * 16)
   // bytes. A direct load covers 8 rows x 128 bytes (8 lanes per row, full cache lines); the
   // XOR keeps fragment reads (32 rows, one piece each) on distinct banks.
   auto load_x = [&](int seq) {
@@ -197,7 +198,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 #pragma unroll
       for (int t = 0; t < 8; ++t) {                 // this wave's rows 64 * wave .. + 63
         const int r = wave * 64 + t * 8 + rsub;
-        const int kc = pos ^ (r & 7);
+        const int kc = pos ^ ((r >> 1) & 7);
         const int row = n0 + r < n_tokens ? n0 + r : n_tokens - 1;
         uint16_t* base = stage + (wave * 64 + t * 8) * BK;   // 1 KiB: 8 rows, written lane-ordered
         load_lds16(X + (size_t)row * d_in + k0 + kc * 8, (uint32_t)(uintptr_t)(lds_ptr)base);
@@ -206,7 +207,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         const int r = wave * 64 + t * 8 + rsub;
-        const int kc = pos ^ (r & 7);
+        const int kc = pos ^ ((r >> 1) & 7);
         const int row = n0 + r;
         uint16_t* base = stage + (wave * 64 + t * 8) * BK;
         uint4 v = make_uint4(0, 0, 0, 0);
@@ -231,7 +232,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
       const int r = wm * 128 + a * 32 + r32;
-      f.a[a] = *(const bf16x8_t*)(xst + r * BK + ((kc ^ (r & 7)) * 8));
+      f.a[a] = *(const bf16x8_t*)(xst + r * BK + ((kc ^ ((r >> 1) & 7)) * 8));
     }
   };
   auto mfmas = [&](const Frags& f) {
