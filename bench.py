@@ -159,10 +159,22 @@ def main():
         for r in range(G_COPIES):
             A.gemm(glayers[r], k, Xg, n_tok, Yg[r], A.DType.BF16)
 
+    # The same R layers decoded with aqmb_gemv_multi, G layers per launch (layers that share their
+    # input, as fused q/k/v or gate/up projections do).
+    MULTI_G = (4, 16)
+
+    def gemv_multi_burst(k, b, G):
+        for r0 in range(0, R - G + 1, G):
+            xs, ys = (xs1, ys1) if b == 1 else (xs4, ys4)
+            A.gemv_multi(layers[r0:r0 + G], k, xs[r0], A.DType.F16, b, ys[r0:r0 + G], A.DType.F16)
+
     ops = []  # (name, k, b, fn, launches)
     for k in ks:
         ops.append(("gemv", k, 1, lambda k=k: gemv_burst(k, 1), R))
         ops.append(("gemv", k, 4, lambda k=k: gemv_burst(k, 4), R))
+        for G in MULTI_G:
+            for b in (1, 4):
+                ops.append((f"gemv_multi{G}", k, b, lambda k=k, b=b, G=G: gemv_multi_burst(k, b, G), R // G))
         ops.append(("dequant", k, 0, lambda k=k: dequant_burst(k), n_w))
         if not args.no_gemm:
             ops.append(("gemm", k, n_tok, lambda k=k: gemm_burst(k), G_COPIES))
@@ -242,6 +254,19 @@ def main():
             e["gemm_frac_bf16_peak"] = round(fl / (t * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)
         per_k[str(k)] = e
 
+    multi = {}
+    for G in MULTI_G:
+        mk = {}
+        for k in ks:
+            e = {}
+            for b in (1, 4):
+                t = per_launch_us[(f"gemv_multi{G}", k, b)] / G   # per layer
+                e[f"b{b}_us_per_layer"] = round(t, 3)
+                e[f"b{b}_GBps"] = round(gemv_bytes(k, b) / (t * 1e-6) / 1e9, 1)
+                e[f"b{b}_frac_hbm"] = round(gemv_bytes(k, b) / (t * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+            mk[str(k)] = e
+        multi[str(G)] = mk
+
     t_dom = per_launch_us[("gemv", 4, 1)]
     ach = gemv_bytes(4, 1) / (t_dom * 1e-6) / 1e9
     gemv_kernel = ("gemv_lut_kernel<K=4,BT=1> + gemv_reduce_kernel" if os.environ.get("AQMB_GEMV") == "lut"
@@ -268,6 +293,8 @@ def main():
                    "layer_copies": R, "launch": "HIP graph per burst of copies", "codes": "uint8",
                    "accumulate": "fp32"},
         "per_k": per_k,
+        "gemv_multi": {"layers_per_launch": list(MULTI_G), "note": "aqmb_gemv_multi over the same layer "
+                       "copies (one input per group); per-layer time and algorithmic GB/s", "per_G": multi},
         "roofline": roofline,
     }
     if not args.no_gemm:
@@ -279,9 +306,9 @@ def main():
                                 "traffic": None, "us_per_launch": round(tg, 2)}
         gemm_total_us = sum(per_launch_us[("gemm", k, n_tok)] for k in ks)
         out["gemm_TFLOPs"] = round(len(ks) * fl / (gemm_total_us * 1e-6) / 1e12, 1)
-    step_us = {n: 0.0 for n in ("gemv", "dequant", "gemm")}
+    step_us = {n: 0.0 for n in ("gemv", "gemv_multi", "dequant", "gemm")}
     for i, (name, k, b, fn, n) in enumerate(ops):
-        step_us[name] += per_op_ms[i] * 1e3 / args.steps
+        step_us["gemv_multi" if name.startswith("gemv_multi") else name] += per_op_ms[i] * 1e3 / args.steps
     tot = sum(step_us.values())
     out["time_share"] = {n: round(v / tot, 4) for n, v in step_us.items() if v > 0}
 

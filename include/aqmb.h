@@ -96,6 +96,28 @@ aqmb_status aqmb_get_desc(aqmb_layer_t layer, aqmb_desc* out);
 aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch,
                       void* y, aqmb_dtype y_dtype, aqmb_stream_t stream);
 
+/* Most layers accepted by one aqmb_gemv_multi call. */
+#define AQMB_MAX_MULTI 16
+
+/*
+ * Decode GEMV of several layers that read the same input (fused projections such as q/k/v or
+ * gate/up): for each l < n_layers, ys[l][b][i] = sum_t x[b][t] * W_k^(l)[i][t], exactly what
+ * aqmb_gemv(layers[l], k, x, x_dtype, batch, ys[l], y_dtype, stream) computes (same arithmetic,
+ * same rounding), in one launch when every layer has 8-bit codes, k <= 4 and batch <= 4 (one
+ * workgroup per row block walks through the layers, loading the next layer's codes while it
+ * works on the current one); otherwise the layers are launched one after another.
+ *   layers  n_layers live handles, all with the same d_in and on the same device
+ *   x       [batch][d_in], dtype x_dtype in {F16, BF16}
+ *   ys      n_layers device pointers, ys[l] is [batch][d_out of layer l], dtype y_dtype
+ * 1 <= n_layers <= AQMB_MAX_MULTI; k must be valid for every layer. Calls on a layer must be
+ * ordered as for aqmb_gemv. Nothing is launched when validation fails.
+ * Errors: EINVAL (null pointer, bad handle, n_layers < 1, d_in or device differ, k outside
+ * [1, M] of some layer, batch < 1), EUNSUPPORTED (n_layers > AQMB_MAX_MULTI, batch >
+ * AQMB_MAX_BATCH, dtype), EHIP.
+ */
+aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, const void* x, aqmb_dtype x_dtype,
+                            int batch, void* const* ys, aqmb_dtype y_dtype, aqmb_stream_t stream);
+
 /*
  * Prefill GEMM: Y[n][i] = s_i * sum_t X[n][t] * Wb_k[i][t] for n < n_tokens, where Wb_k is the
  * unscaled reconstruction sum_{m<k} C_m[b_{ijm}] formed as a binary32 left fold over m and

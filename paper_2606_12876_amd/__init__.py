@@ -61,6 +61,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_destroy.argtypes = [vp]
     L.aqmb_get_desc.argtypes = [vp, ctypes.POINTER(Desc)]
     L.aqmb_gemv.argtypes = [vp, i32, vp, i32, i32, vp, i32, vp]
+    L.aqmb_gemv_multi.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, i32, ctypes.POINTER(vp), i32, vp]
     L.aqmb_gemm.argtypes = [vp, i32, vp, i32, vp, i32, vp]
     L.aqmb_dequant.argtypes = [vp, i32, vp, i32, vp]
     L.aqmb_validate.argtypes = [ctypes.POINTER(Desc), i32, i32, i32, i32, i32, vp, vp]
@@ -70,8 +71,8 @@ def _load() -> ctypes.CDLL:
     L.aqmb_strerror.restype = ctypes.c_char_p
     L.aqmb_last_error.argtypes = []
     L.aqmb_last_error.restype = ctypes.c_char_p
-    for f in ("aqmb_create", "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemm", "aqmb_dequant",
-              "aqmb_validate"):
+    for f in ("aqmb_create", "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_multi", "aqmb_gemm",
+              "aqmb_dequant", "aqmb_validate"):
         getattr(L, f).restype = st
     return L
 
@@ -176,6 +177,26 @@ def gemv(layer: int, k: int, x, x_dtype, batch: int, y, y_dtype, stream=None) ->
         _need(y, batch * d.d_out, y_dtype, "y", "aqmb_gemv")
     _check(lib.aqmb_gemv(layer, k, _ptr(x), int(x_dtype), batch, _ptr(y), int(y_dtype), _stream(stream)),
            "aqmb_gemv")
+
+
+MAX_MULTI = 16
+
+
+def gemv_multi(layers, k: int, x, x_dtype, batch: int, ys, y_dtype, stream=None) -> None:
+    """aqmb_gemv_multi: the GEMV of every layer in `layers` (same d_in) on the same x, one output each."""
+    layers, ys = list(layers), list(ys)
+    if len(layers) != len(ys):
+        raise AqmbError(Status.EINVAL, "aqmb_gemv_multi", "one output per layer")
+    if 1 <= batch <= 16 and 1 <= len(layers) <= MAX_MULTI:
+        for layer, y in zip(layers, ys):
+            d = get_desc(layer)
+            _need(x, batch * d.d_in, x_dtype, "x", "aqmb_gemv_multi")
+            _need(y, batch * d.d_out, y_dtype, "y", "aqmb_gemv_multi")
+    n = len(layers)
+    la = (ctypes.c_void_p * max(n, 1))(*[ctypes.c_void_p(h) for h in layers])
+    ya = (ctypes.c_void_p * max(n, 1))(*[ctypes.c_void_p(_ptr(y)) for y in ys])
+    _check(lib.aqmb_gemv_multi(la, n, k, _ptr(x), int(x_dtype), batch, ya, int(y_dtype), _stream(stream)),
+           "aqmb_gemv_multi")
 
 
 def gemm(layer: int, k: int, X, n_tokens: int, Y, y_dtype, stream=None) -> None:

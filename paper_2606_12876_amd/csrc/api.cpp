@@ -147,6 +147,28 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv: launch");
 }
 
+aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, const void* x, aqmb_dtype x_dtype,
+                            int batch, void* const* ys, aqmb_dtype y_dtype, aqmb_stream_t stream) {
+  clear_error();
+  if (!layers || !ys) return fail(AQMB_EINVAL, "gemv_multi: null layers or outputs");
+  if (n_layers < 1) return fail(AQMB_EINVAL, "gemv_multi: n_layers < 1");
+  if (n_layers > AQMB_MAX_MULTI) return fail(AQMB_EUNSUPPORTED, "gemv_multi: more than AQMB_MAX_MULTI layers");
+  const Layer* Ls[AQMB_MAX_MULTI];
+  for (int i = 0; i < n_layers; ++i) {
+    const Layer* L = (const Layer*)layers[i];
+    if (!is_live((Layer*)L)) return fail(AQMB_EINVAL, "gemv_multi: not a live layer");
+    if (i > 0 && (L->d.d_in != Ls[0]->d.d_in || L->device != Ls[0]->device))
+      return fail(AQMB_EINVAL, "gemv_multi: layers differ in d_in or device");
+    aqmb_status s = validate_call(&L->d, 0, k, batch, x_dtype, y_dtype, x, ys[i]);
+    if (s != AQMB_OK) return s;
+    Ls[i] = L;
+  }
+  aqmb_status s = check_device((Layer*)Ls[0]);
+  if (s != AQMB_OK) return s;
+  hipError_t e = launch_gemv_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv_multi: launch");
+}
+
 aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
                       aqmb_stream_t stream) {
   clear_error();

@@ -360,6 +360,143 @@ __host__ __device__ inline size_t row_stride(int S) {   // bytes per staged x ro
 
 constexpr int kCwMaxBlocks = 4;   // 512-group blocks per row held in registers: d_in <= 16384
 
+// The gather-and-reduce part shared by the direct-gather kernels. For this thread's row and part,
+// gather the codewords of its groups (code words in `code`: UB blocks x K planes, already
+// requested), dot them with the NB staged x rows, reduce each row in a fixed order (a butterfly
+// over the wave's parts, then the waves in order), scale by `scale` (the row's, loaded by the
+// caller with the code words) and store y rows b0 .. b0 + NB - 1 (those below `batch`) of output
+// row `row`. `red` is reused: the caller separates calls with a barrier.
+template <int K, int NB, int XDT, int UB>
+__device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4* cb_rep, const uint16_t* xs,
+                                        size_t rstride, int Gp, int cb_shift, uint32_t rep_off,
+                                        float (&red)[cw::kWaves][cw::kRows][NB], int b0, int batch, int row,
+                                        bool row_ok, float scale, void* y, int d_out, int y_dtype) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rw = lane & 15, part = tid >> 4;
+  const uint32_t cb_stride = 1u << cb_shift;
+  float acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = 0.f;
+#pragma unroll
+  for (int u = 0; u < UB; ++u) {
+    const int j0 = u * 512 + part * 8;
+    if (j0 >= Gp) continue;                                // past the padded groups (short rows)
+    const char* xrow = (const char*)xs + (size_t)j0 * 16;
+    if constexpr (NB == 1) {
+      // plane-major: x for the 8 groups in registers, 8 independent gathers per plane
+      uint4 xg[8];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) xg[jj] = *(const uint4*)(xrow + jj * 16);
+#pragma unroll
+      for (int m = 0; m < K; ++m) {
+        // plane m's code word is awaited here, not earlier (the empty asm keeps its unpacking
+        // from being hoisted above the gathers of the previous planes)
+        uint2 cm = code[u][m];
+        asm volatile("" : "+v"(cm));
+        const uint32_t base = (uint32_t)(m * 256) * cb_stride + rep_off;
+        uint4 cw[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const uint32_t word = jj < 4 ? cm.x : cm.y;
+          const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
+          cw[jj] = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + base);
+        }
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) acc[0] += group_dot<XDT>(xg[jj], cw[jj]);
+      }
+    } else {
+      // group-major: the NB x vectors of a group are read once and used for every plane
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        uint4 xg[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xrow + b * rstride + jj * 16);
+#pragma unroll
+        for (int m = 0; m < K; ++m) {
+          const uint32_t word = jj < 4 ? code[u][m].x : code[u][m].y;
+          const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
+          const uint4 cwv = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + (uint32_t)(m * 256) * cb_stride + rep_off);
+#pragma unroll
+          for (int b = 0; b < NB; ++b) acc[b] += group_dot<XDT>(xg[b], cwv);
+        }
+      }
+    }
+  }
+  // row sum: lanes rw, rw + 16, rw + 32, rw + 48 of the wave, then the 16 waves in order
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    float v = acc[b];
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    acc[b] = v;
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) red[wave][rw][b] = acc[b];
+  }
+  __syncthreads();
+  if (wave == 0 && lane < 16 && row_ok) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (b0 + b < batch) {
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < cw::kWaves; ++w) sum += red[w][rw][b];
+        const size_t o = (size_t)(b0 + b) * d_out + row;
+        const float v = sum * scale;
+        if (y_dtype == AQMB_F16) OutT<AQMB_F16>::store(y, o, v);
+        else if (y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(y, o, v);
+        else OutT<AQMB_F32>::store(y, o, v);
+      }
+    }
+  }
+}
+
+// Write this thread's codebook word (codeword q = tid, q < K * 256) to its nrep replicas. Write i
+// goes to replica (i + q / (16 / nrep)) % nrep: the 16 threads that share a 256-byte bank row
+// write 16 distinct 16-byte slots of it, so the stores do not collide.
+template <int K>
+__device__ __forceinline__ void cw_replicate(uint4* cb_rep, uint4 cbv, int nrep, int cb_shift) {
+  const int q = threadIdx.x;
+  if (q < K * 256) {
+    const int rot = q >> (8 - cb_shift);                   // q / (16 / nrep); cb_shift = log2(16 nrep)
+    for (int i = 0; i < nrep; ++i) cb_rep[q * nrep + ((i + rot) & (nrep - 1))] = cbv;
+  }
+}
+
+// x rows b0 .. b0 + NB - 1 into LDS by direct loads; elements past d_in (and rows past `batch`)
+// read zeros from the zero page.
+template <int NB>
+__device__ __forceinline__ void cw_stage_x(const void* x, const void* zero_page, int b0, int batch, int d_in,
+                                           size_t rstride, uint32_t xs_base) {
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int nch = (int)(rstride / 1024);
+  for (int q = wave; q < NB * nch; q += cw::kWaves) {
+    const int b = q / nch, ch = q % nch;
+    const int e = ch * 512 + lane * 8;                     // element offset in the row
+    const void* src = (b0 + b < batch && e < d_in) ? (const void*)((const uint16_t*)x + (size_t)(b0 + b) * d_in + e)
+                                                   : zero_page;
+    load_lds16(src, xs_base + (uint32_t)(b * rstride + (size_t)ch * 1024));
+  }
+}
+
+// This thread's code words (UB blocks x K planes) of row `rowc`: 8 groups per (block, plane),
+// streaming loads, addresses clamped so that every thread issues the same loads.
+template <int K, int UB>
+__device__ __forceinline__ void cw_load_codes(uint2 (&code)[UB][K], const unsigned char* codes, size_t plane_bytes,
+                                              int d_out, int rowc, int Gp) {
+  const int part = threadIdx.x >> 4;
+#pragma unroll
+  for (int u = 0; u < UB; ++u) {
+    int j0 = u * 512 + part * 8;
+    j0 = j0 < Gp ? j0 : Gp - 8;                            // unused blocks reload a valid word
+#pragma unroll
+    for (int m = 0; m < K; ++m)
+      code[u][m] = load_stream8(codes + m * plane_bytes + ((size_t)(j0 >> 4) * d_out + rowc) * 16 + (j0 & 8));
+  }
+}
+
 template <int K, int NB, int XDT, int UB>
 __global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_cw_kernel(GemvArgs a) {
@@ -369,145 +506,132 @@ void gemv_cw_kernel(GemvArgs a) {
   uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);    // [NB][row_stride] x tile
   __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int rw = lane & 15, part = tid >> 4;              // row within the group, 0..63
+  const int rw = lane & 15;
   const int row = blockIdx.x * cw::kRows + rw;
   const bool row_ok = row < a.d_out;
   const int rowc = row_ok ? row : a.d_out - 1;
   const int Gp = a.S * 16;                                 // padded groups per row
   const size_t rstride = cw::row_stride(a.S);
-  const uint32_t xs_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)xs;
-  const int cb_shift = a.cb_shift;                         // codeword c starts at c << cb_shift
-  const uint32_t cb_stride = 1u << cb_shift;
+  const uint32_t xs_base = lds_addr(xs);
   const uint32_t rep_off = (uint32_t)(lane % nrep) * 16;
 
-  // x rows b0 .. b0 + NB - 1 into LDS; elements past d_in (and rows past `batch`) read zeros.
-  auto stage_x = [&](int b0) {
-    const int nch = (int)(rstride / 1024);
-    for (int q = wave; q < NB * nch; q += cw::kWaves) {
-      const int b = q / nch, ch = q % nch;
-      const int e = ch * 512 + lane * 8;                   // element offset in the row
-      const void* src = (b0 + b < a.batch && e < a.d_in)
-                            ? (const void*)((const uint16_t*)a.x + (size_t)(b0 + b) * a.d_in + e)
-                            : (const void*)a.zero_page;
-      load_lds16(src, xs_base + (uint32_t)(b * rstride + (size_t)ch * 1024));
-    }
-  };
-
-  stage_x(0);
+  cw_stage_x<NB>(a.x, a.zero_page, 0, a.batch, a.d_in, rstride, xs_base);
   asm volatile("" ::: "memory");
-  const int q = tid % (K * 256);                           // K * 256 <= 1024 codewords
-  const uint4 cbv = ((const uint4*)a.codebooks)[q];
+  const uint4 cbv = ((const uint4*)a.codebooks)[tid % (K * 256)];   // K * 256 <= 1024 codewords
   asm volatile("" ::: "memory");
-  uint2 code[UB][K];                                       // 8 codes per (block, plane)
-#pragma unroll
-  for (int u = 0; u < UB; ++u) {
-    int j0 = u * 512 + part * 8;
-    j0 = j0 < Gp ? j0 : Gp - 8;                            // unused blocks reload a valid word
-#pragma unroll
-    for (int m = 0; m < K; ++m)
-      code[u][m] = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 4) * a.d_out + rowc) * 16 + (j0 & 8));
-  }
-  wait_vmcnt<UB * K>();                                    // x and the codebook word are in
-  if (tid < K * 256) {
-    // write i of thread q goes to replica (i + q / (16 / nrep)) % nrep: the 16 threads that share
-    // a 256-byte bank row write 16 distinct 16-byte slots of it, so the stores do not collide
-    const int rot = q >> (8 - cb_shift);                   // q / (16 / nrep); cb_shift = log2(16 nrep)
-    for (int i = 0; i < nrep; ++i) cb_rep[q * nrep + ((i + rot) & (nrep - 1))] = cbv;
-  }
+  const uint16_t sbits = a.scales[rowc];                   // the row scale, needed only at the end
+  uint2 code[UB][K];
+  cw_load_codes<K, UB>(code, a.codes, a.plane_bytes, a.d_out, rowc, Gp);
+  wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in (older than the scale and codes)
+  cw_replicate<K>(cb_rep, cbv, nrep, a.cb_shift);
   __syncthreads();
 
-  // One batch tile of NB rows of x (already staged); the first tile is peeled out of the loop so
-  // that its waits for the code planes are exact.
-  auto tile = [&](int b0) {
-    float acc[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) acc[b] = 0.f;
-#pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const int j0 = u * 512 + part * 8;
-      if (j0 >= Gp) continue;                              // past the padded groups (short rows)
-      const char* xrow = (const char*)xs + (size_t)j0 * 16;
-      if constexpr (NB == 1) {
-        // plane-major: x for the 8 groups in registers, 8 independent gathers per plane
-        uint4 xg[8];
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) xg[jj] = *(const uint4*)(xrow + jj * 16);
-#pragma unroll
-        for (int m = 0; m < K; ++m) {
-          // plane m's code word is awaited here, not earlier (the empty asm keeps its unpacking
-          // from being hoisted above the gathers of the previous planes)
-          uint2 cm = code[u][m];
-          asm volatile("" : "+v"(cm));
-          const uint32_t base = (uint32_t)(m * 256) * cb_stride + rep_off;
-          uint4 cw[8];
-#pragma unroll
-          for (int jj = 0; jj < 8; ++jj) {
-            const uint32_t word = jj < 4 ? cm.x : cm.y;
-            const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
-            cw[jj] = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + base);
-          }
-#pragma unroll
-          for (int jj = 0; jj < 8; ++jj) acc[0] += group_dot<XDT>(xg[jj], cw[jj]);
-        }
-      } else {
-        // group-major: the NB x vectors of a group are read once and used for every plane
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          uint4 xg[NB];
-#pragma unroll
-          for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xrow + b * rstride + jj * 16);
-#pragma unroll
-          for (int m = 0; m < K; ++m) {
-            const uint32_t word = jj < 4 ? code[u][m].x : code[u][m].y;
-            const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
-            const uint4 cwv = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + (uint32_t)(m * 256) * cb_stride + rep_off);
-#pragma unroll
-            for (int b = 0; b < NB; ++b) acc[b] += group_dot<XDT>(xg[b], cwv);
-          }
-        }
-      }
-    }
-    // row sum: lanes rw, rw + 16, rw + 32, rw + 48 of the wave, then the 16 waves in order
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      float v = acc[b];
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
-      acc[b] = v;
-    }
-    if (lane < 16) {
-#pragma unroll
-      for (int b = 0; b < NB; ++b) red[wave][rw][b] = acc[b];
-    }
-    __syncthreads();
-    if (wave == 0 && lane < 16 && row_ok) {
-      const float scale = f16_to_f32(a.scales[row]);
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        if (b0 + b < a.batch) {
-          float sum = 0.f;
-#pragma unroll
-          for (int w = 0; w < cw::kWaves; ++w) sum += red[w][rw][b];
-          const size_t o = (size_t)(b0 + b) * a.d_out + row;
-          const float v = sum * scale;
-          if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, o, v);
-          else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, o, v);
-          else OutT<AQMB_F32>::store(a.y, o, v);
-        }
-      }
-    }
-  };
-  tile(0);
+  // The first batch tile is peeled out of the loop so that its waits for the code planes are exact.
+  const float scale = f16_to_f32(sbits);
+  cw_tile<K, NB, XDT, UB>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row, row_ok,
+                          scale, a.y, a.d_out, a.y_dtype);
   for (int b0 = NB; b0 < a.batch; b0 += NB) {
     __syncthreads();                                       // the previous tile's reads of xs are done
-    stage_x(b0);
+    cw_stage_x<NB>(a.x, a.zero_page, b0, a.batch, a.d_in, rstride, xs_base);
     wait_vmcnt<0>();
     __syncthreads();
-    tile(b0);
+    cw_tile<K, NB, XDT, UB>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, b0, a.batch, row, row_ok,
+                            scale, a.y, a.d_out, a.y_dtype);
   }
 }
 
+// ------------------------------------------------------------------ several layers, one launch
+// Layers that share the input x (fused projections such as q/k/v or gate/up): one persistent
+// workgroup per 16-row block walks through the layers that have that block. x is staged once;
+// the replicas of the next layer's codebooks are written right after the reduction barrier of
+// the current one (every wave has finished its gathers by then; wave 0 still reads only the row
+// sums), and one more barrier publishes them;
+// while a layer's codewords are gathered, the codebook word and code words of the next layer are
+// already on their way (two register sets used in turn), so a layer costs its gathers and the
+// replica writes of its codebooks, not a launch and the load latency. Results are those of one
+// aqmb_gemv call per layer (same arithmetic, same reduction order).
+struct GemvMultiLayer {
+  const unsigned char* codes;
+  const uint16_t* codebooks;
+  const uint16_t* scales;
+  void* y;
+  size_t plane_bytes;
+  int d_out;
+  int row_blocks;                                          // ceil(d_out / 16)
+};
+
+struct GemvMultiArgs {
+  GemvMultiLayer L[AQMB_MAX_MULTI];
+  const void* x;
+  const void* zero_page;
+  int n_layers, d_in, S, batch, y_dtype, nrep, cb_shift;
+};
+
+template <int K, int NB, int XDT, int UB>
+__global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_cw_multi_kernel(GemvMultiArgs a) {
+  extern __shared__ uint4 smem_cw[];
+  const int nrep = a.nrep;
+  uint4* cb_rep = smem_cw;
+  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);
+  __shared__ float red[cw::kWaves][cw::kRows][NB];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int rw = lane & 15;
+  const int row = blockIdx.x * cw::kRows + rw;
+  const int Gp = a.S * 16;
+  const size_t rstride = cw::row_stride(a.S);
+  const uint32_t xs_base = lds_addr(xs);
+  const uint32_t rep_off = (uint32_t)(lane % nrep) * 16;
+  // next layer (after l) that has this workgroup's row block, or -1 (uniform)
+  auto next_layer = [&](int l) {
+    for (int j = l + 1; j < a.n_layers; ++j)
+      if ((int)blockIdx.x < a.L[j].row_blocks) return j;
+    return -1;
+  };
+  // the layer's codebook word (first), row scale and code words
+  auto load_layer = [&](int l, uint4& cbv, uint32_t& sbits, uint2 (&code)[UB][K]) {
+    cbv = ((const uint4*)a.L[l].codebooks)[tid % (K * 256)];
+    asm volatile("" ::: "memory");                        // the codebook word goes out first
+    const int d_out = a.L[l].d_out;
+    const int rowc = row < d_out ? row : d_out - 1;
+    sbits = a.L[l].scales[rowc];
+    cw_load_codes<K, UB>(code, a.L[l].codes, a.L[l].plane_bytes, d_out, rowc, Gp);
+  };
+  auto run_layer = [&](int l, uint32_t sbits, const uint2 (&code)[UB][K]) {
+    const int d_out = a.L[l].d_out;
+    cw_tile<K, NB, XDT, UB>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
+                            row < d_out, f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype);
+  };
+
+  int cur = next_layer(-1);                                // the grid never exceeds the largest layer
+  cw_stage_x<NB>(a.x, a.zero_page, 0, a.batch, a.d_in, rstride, xs_base);
+  asm volatile("" ::: "memory");
+  uint4 cba, cbb;
+  uint32_t sa, sb;
+  uint2 ca[UB][K], cb[UB][K];
+  load_layer(cur, cba, sa, ca);
+  wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
+  cw_replicate<K>(cb_rep, cba, nrep, a.cb_shift);
+  __syncthreads();
+  for (;;) {
+    int nxt = next_layer(cur);
+    load_layer(nxt >= 0 ? nxt : cur, cbb, sb, cb);         // without a next layer: a harmless reload
+    run_layer(cur, sa, ca);                                // its reduction barrier: all gathers done
+    if (nxt < 0) break;
+    wait_vmcnt<UB * K + 1>();                              // the next codebook word is in
+    cw_replicate<K>(cb_rep, cbb, nrep, a.cb_shift);
+    __syncthreads();
+    cur = nxt;
+    nxt = next_layer(cur);
+    load_layer(nxt >= 0 ? nxt : cur, cba, sa, ca);
+    run_layer(cur, sb, cb);
+    if (nxt < 0) break;
+    wait_vmcnt<UB * K + 1>();
+    cw_replicate<K>(cb_rep, cba, nrep, a.cb_shift);
+    __syncthreads();
+    cur = nxt;
+  }
+}
 
 // LDS bytes of the direct-gather kernel: replicated codebooks plus the x tile.
 static size_t cw_lds(int K, int nb, int S, int nrep) {
@@ -629,6 +753,71 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   const int items = batch * ((L.d.d_out + 3) / 4);
   gemv_reduce_kernel<<<(items + 63) / 64, kReduceThreads, 0, st>>>(a);
   return hipGetLastError();
+}
+
+
+template <int K, int NB, int XDT>
+static hipError_t launch_multi_nb(GemvMultiArgs a, int grid, hipStream_t st) {
+  a.nrep = cw_nrep(K, NB, a.S);
+  a.cb_shift = a.nrep == 8 ? 7 : 6;
+  const size_t lds = cw_lds(K, NB, a.S, a.nrep);
+  if (cw_blocks(a.S) == 1) gemv_cw_multi_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
+  else gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks><<<grid, cw::kThreads, lds, st>>>(a);
+  return hipGetLastError();
+}
+
+template <int K, int XDT>
+static hipError_t launch_multi_k(const GemvMultiArgs& a, int grid, hipStream_t st) {
+  if (a.batch == 1) return launch_multi_nb<K, 1, XDT>(a, grid, st);
+  if (a.batch == 2) return launch_multi_nb<K, 2, XDT>(a, grid, st);
+  return launch_multi_nb<K, 4, XDT>(a, grid, st);  // batch 3..4: one tile of 4 rows
+}
+
+template <int XDT>
+static hipError_t launch_multi_x(const GemvMultiArgs& a, int k, int grid, hipStream_t st) {
+  switch (k) {
+    case 1: return launch_multi_k<1, XDT>(a, grid, st);
+    case 2: return launch_multi_k<2, XDT>(a, grid, st);
+    case 3: return launch_multi_k<3, XDT>(a, grid, st);
+    default: return launch_multi_k<4, XDT>(a, grid, st);   // k <= 4 checked by the caller
+  }
+}
+
+hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x, aqmb_dtype x_dtype, int batch,
+                             void* const* ys, aqmb_dtype y_dtype, hipStream_t st) {
+  // One launch when every layer takes the direct-gather path in a single batch tile (8-bit codes,
+  // k <= 4, batch <= 4); otherwise the layers are launched one after another.
+  const Layer& L0 = *Ls[0];
+  bool one = batch <= 4 && gemv_variant() == 1 && cw_fits(k, batch, L0.S);
+  for (int i = 0; i < n && one; ++i) one = Ls[i]->d.code_bits == 8;
+  if (!one) {
+    for (int i = 0; i < n; ++i) {
+      hipError_t e = launch_gemv(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, st);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  GemvMultiArgs a{};
+  int grid = 0;
+  for (int i = 0; i < n; ++i) {
+    const Layer& L = *Ls[i];
+    a.L[i].codes = L.codes;
+    a.L[i].codebooks = L.codebooks;
+    a.L[i].scales = L.scales;
+    a.L[i].y = ys[i];
+    a.L[i].plane_bytes = L.plane_bytes;
+    a.L[i].d_out = L.d.d_out;
+    a.L[i].row_blocks = (L.d.d_out + cw::kRows - 1) / cw::kRows;
+    grid = a.L[i].row_blocks > grid ? a.L[i].row_blocks : grid;
+  }
+  a.x = x;
+  a.zero_page = L0.ws;
+  a.n_layers = n;
+  a.d_in = L0.d.d_in;
+  a.S = L0.S;
+  a.batch = batch;
+  a.y_dtype = (int)y_dtype;
+  return x_dtype == AQMB_F16 ? launch_multi_x<AQMB_F16>(a, k, grid, st) : launch_multi_x<AQMB_BF16>(a, k, grid, st);
 }
 
 }  // namespace aqmb

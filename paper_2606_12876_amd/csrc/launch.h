@@ -11,6 +11,9 @@ hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hi
 hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                        aqmb_dtype y_dtype, hipStream_t st);
 size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S);
+// Several layers with the same d_in and device, already validated; n <= AQMB_MAX_MULTI.
+hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x, aqmb_dtype x_dtype, int batch,
+                             void* const* ys, aqmb_dtype y_dtype, hipStream_t st);
 hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
                        hipStream_t st);
 

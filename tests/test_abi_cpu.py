@@ -111,3 +111,20 @@ def test_bad_handles_rejected_without_gpu():
     assert h.value is None
     bad = A.make_desc(64, 60, 4)
     assert A.lib.aqmb_create(ctypes.byref(h), ctypes.byref(bad), 16, 16, 16, None) == A.Status.EINVAL
+
+
+def test_gemv_multi_rejects_before_any_launch():
+    vp = ctypes.c_void_p
+    bogus = (vp * 2)(vp(0x1000), vp(0x2000))
+    ys = (vp * 2)(vp(64), vp(128))
+    f = A.lib.aqmb_gemv_multi
+    assert f(None, 1, 1, 16, 0, 1, ys, 0, None) == A.Status.EINVAL                 # null layer array
+    assert f(bogus, 1, 1, 16, 0, 1, None, 0, None) == A.Status.EINVAL              # null output array
+    assert f(bogus, 0, 1, 16, 0, 1, ys, 0, None) == A.Status.EINVAL                # no layers
+    many = (vp * 17)(*[vp(0x1000 + 64 * i) for i in range(17)])
+    many_y = (vp * 17)(*[vp(64) for _ in range(17)])
+    assert f(many, 17, 1, 16, 0, 1, many_y, 0, None) == A.Status.EUNSUPPORTED     # over AQMB_MAX_MULTI
+    assert f(bogus, 2, 1, 16, 0, 1, ys, 0, None) == A.Status.EINVAL                # not live layers
+    assert "live" in A.last_error()
+    with pytest.raises(A.AqmbError):
+        A.gemv_multi([0x1000], 1, 16, A.DType.F16, 1, [64, 128], A.DType.F16)    # one output per layer
