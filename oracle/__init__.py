@@ -10,8 +10,8 @@ checked against the paper by eye:
                   even encodings (own bit manipulation for bf16, numpy for fp16,
                   plus a format-generic rounding used to pin both);
 * ``aq``        - the partial reconstruction, the linear layer, the canonical
-                  rounded dequantization, the GEMM reference, the weighted MSE
-                  and the average-bits formula;
+                  rounded dequantization, the GEMM reference, the weighted MSE,
+                  the distortion of every prefix level and the average-bits formula;
 * ``search``    - residual k-means encoding and exhaustive / beam code search on
                   tiny groups (fixture generators and pins, not on the hot path).
 
@@ -20,5 +20,5 @@ Every function cites the passage of the paper it follows. Pins live in
 """
 from . import formats, aq, search  # noqa: F401
 from .aq import (reconstruct, linear, dequant_canonical, gemm_reference, wmse_frobenius,
-                 wmse_trace, bits_per_weight, code_bits_per_weight)  # noqa: F401
+                 wmse_trace, prefix_distortions, bits_per_weight, code_bits_per_weight)  # noqa: F401
 from .search import encode_residual_kmeans, brute_force_codes, beam_search_codes  # noqa: F401

@@ -142,6 +142,18 @@ def wmse_trace(W, W_hat, X) -> float:
     return float(np.trace(E @ H @ E.T) / d_out)
 
 
+def prefix_distortions(W, codes, codebooks, scales, X_rows) -> np.ndarray:
+    """D^(k) for k = 1..M (§5, the distortion of each partial reconstruction): the weighted MSE
+    of Eq. (1), ||(W - W^(k)) X||_F^2 / (d_out n), with W^(k) from the first k codebooks.
+
+    X_rows holds the n calibration inputs as rows, [n][d_in] (X of the paper is its transpose).
+    Returns an array of M values, entry k - 1 for level k.
+    """
+    X = np.asarray(X_rows, dtype=np.float64).T
+    M = np.asarray(codes).shape[0]
+    return np.array([wmse_frobenius(W, reconstruct(codes, codebooks, scales, k), X) for k in range(1, M + 1)])
+
+
 def bits_per_weight(d_out: int, d_in: int, g: int, M: int, B: int, k=None) -> float:
     """Average bits per weight of a stored layer, Eq. (avg_bits) of App. C.
 

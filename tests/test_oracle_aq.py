@@ -175,6 +175,32 @@ def test_wmse_forms_agree_and_reduce_to_mse():
     assert abs(oracle.wmse_frobenius(W, Wh, np.concatenate([X, X], axis=1)) - a) <= 1e-12 * a
 
 
+def test_prefix_distortions_explicit_sums():
+    """D^(k) written out as a quintuple sum over rows, samples, groups, positions and planes."""
+    rng = np.random.default_rng(9)
+    M, d_out, G, g, n = 3, 4, 3, 8, 5
+    codes = rng.integers(0, 4, size=(M, d_out, G))
+    C = rng.integers(-8, 9, size=(M, 256, g)).astype(np.float64) / 16   # exact in fp16 and fp64
+    s = np.array([1.0, 0.5, 2.0, 1.5])
+    W = rng.integers(-32, 33, size=(d_out, G * g)).astype(np.float64) / 32
+    Xr = rng.integers(-4, 5, size=(n, G * g)).astype(np.float64) / 4
+    got = oracle.prefix_distortions(W, codes, C, s, Xr)
+    for k in range(1, M + 1):
+        tot = Fraction(0)
+        for i in range(d_out):
+            for t in range(n):
+                r = Fraction(0)
+                for j in range(G):
+                    for q in range(g):
+                        w_hat = Fraction(s[i]) * sum(Fraction(C[m, codes[m, i, j], q]) for m in range(k))
+                        r += (Fraction(W[i, j * g + q]) - w_hat) * Fraction(Xr[t, j * g + q])
+                tot += r * r
+        assert got[k - 1] == float(tot / (d_out * n)), k
+    # with every plane reproducing W exactly the full level has zero distortion
+    Wm = oracle.reconstruct(codes, C, s, M)
+    assert oracle.prefix_distortions(Wm, codes, C, s, Xr)[-1] == 0.0
+
+
 # ----------------------------------------------------------------------------- dequant
 
 def _f16bits(a):
