@@ -142,6 +142,29 @@ aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, vo
 aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype, aqmb_stream_t stream);
 
 /*
+ * Distortion of every precision level in one pass (section 5: the error of each partial
+ * reconstruction, which the training loop of Alg. 1 drives down level by level; the weighted
+ * MSE of section 2.2, Eq. wmse-task): for k = 1..M,
+ *   D[k-1] = ||(W - W_k) X||_F^2 / (d_out * n)
+ * with the calibration inputs given as the rows of Xt = X^T.
+ *   W   [d_out][d_in] fp16: the weights being quantized (w_dtype must be F16)
+ *   Xt  [n][d_in]     fp16: one calibration input per row (x_dtype must be F16)
+ *   D   M doubles in device memory, written in stream order
+ * The products W X and C_m[b_m] X run on fp16 matrix cores (each product of two fp16 values
+ * exact, sums in fp32), the per-output differences W X - s_i sum_{m<k} (C_m[b_m] X) in fp32, the
+ * sums of their squares in fp64, added in a fixed order: the result is reproducible.
+ * The Hessian form of the same quantity, tr[(W - W_k) H (W - W_k)^T] / d_out with H = X X^T / n,
+ * is obtained by passing any factor F with F F^T = H (e.g. a Cholesky factor) as Xt = F^T,
+ * n = d_in, and multiplying D by d_in.
+ * Requires B = 8. Uses the layer's workspace: calls on a layer must be ordered with each other
+ * and with aqmb_gemv / aqmb_gemv_multi calls on that layer.
+ * Errors: EINVAL (bad handle, null pointer, n < 1, misaligned pointer), EUNSUPPORTED (B = 16,
+ * dtype other than F16, n > 2^30), EHIP.
+ */
+aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* Xt,
+                                   aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream);
+
+/*
  * Average storage bits per weight at level k (appendix C, Eq. avg_bits): codebooks
  * 16*g*k*2^B bits, codes d_out*(d_in/g)*B bits per used plane, scales 16*d_out bits,
  * over d_out*d_in weights. The printed codes term lacks the per-plane factor; the
@@ -157,10 +180,12 @@ const char* aqmb_strerror(aqmb_status status);
 const char* aqmb_last_error(void);
 
 /* Validate arguments exactly as the entry points do, without touching the GPU.
- * op: 0 = gemv, 1 = gemm, 2 = dequant. For gemv `n` is the batch, for gemm the
- * token count, ignored for dequant; `in_dtype` is x's dtype (gemv only) and
- * `out_dtype` the output dtype. Returns the status the entry point would return
- * before launching anything. */
+ * op: 0 = gemv, 1 = gemm, 2 = dequant, 3 = prefix distortion. For gemv `n` is the batch, for
+ * gemm the token count, for the distortion the number of inputs, ignored for dequant;
+ * `in_dtype` is x's dtype (gemv) or Xt's (distortion), `out_dtype` the output dtype or, for
+ * the distortion, W's dtype; `in`/`out` are x/y, X/Y, -/W, or Xt/D. `k` is not checked for
+ * the distortion. Returns the status the entry point would return before launching anything
+ * (the distortion's W pointer is checked by the entry point itself). */
 aqmb_status aqmb_validate(const aqmb_desc* desc, int op, int k, int n, aqmb_dtype in_dtype,
                           aqmb_dtype out_dtype, const void* in, const void* out);
 

@@ -64,6 +64,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_gemv_multi.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, i32, ctypes.POINTER(vp), i32, vp]
     L.aqmb_gemm.argtypes = [vp, i32, vp, i32, vp, i32, vp]
     L.aqmb_dequant.argtypes = [vp, i32, vp, i32, vp]
+    L.aqmb_prefix_distortion.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
     L.aqmb_validate.argtypes = [ctypes.POINTER(Desc), i32, i32, i32, i32, i32, vp, vp]
     L.aqmb_bits_per_weight.argtypes = [ctypes.POINTER(Desc), i32]
     L.aqmb_bits_per_weight.restype = ctypes.c_double
@@ -72,7 +73,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_last_error.argtypes = []
     L.aqmb_last_error.restype = ctypes.c_char_p
     for f in ("aqmb_create", "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_multi", "aqmb_gemm",
-              "aqmb_dequant", "aqmb_validate"):
+              "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_validate"):
         getattr(L, f).restype = st
     return L
 
@@ -211,6 +212,21 @@ def dequant(layer: int, k: int, W, w_dtype, stream=None) -> None:
     d = get_desc(layer)
     _need(W, d.d_out * d.d_in, w_dtype, "W", "aqmb_dequant")
     _check(lib.aqmb_dequant(layer, k, _ptr(W), int(w_dtype), _stream(stream)), "aqmb_dequant")
+
+
+def prefix_distortion(layer: int, W, w_dtype, Xt, x_dtype, n: int, D, stream=None) -> None:
+    """aqmb_prefix_distortion: D[k-1] = ||(W - W_k) X||_F^2 / (d_out n) for k = 1..M, with the n
+    calibration inputs as the rows of Xt [n][d_in] (fp16) and W [d_out][d_in] fp16; D holds M
+    float64 values in device memory."""
+    d = get_desc(layer)
+    _need(W, d.d_out * d.d_in, w_dtype, "W", "aqmb_prefix_distortion")
+    if n >= 1:
+        _need(Xt, n * d.d_in, x_dtype, "Xt", "aqmb_prefix_distortion")
+    nd = _nbytes(D)
+    if nd is not None and nd < 8 * d.num_codebooks:
+        raise AqmbError(Status.EINVAL, "aqmb_prefix_distortion", f"D holds {nd} bytes, needs {8 * d.num_codebooks}")
+    _check(lib.aqmb_prefix_distortion(layer, _ptr(W), int(w_dtype), _ptr(Xt), int(x_dtype), n, _ptr(D),
+                                      _stream(stream)), "aqmb_prefix_distortion")
 
 
 def bits_per_weight(desc: Desc, k: int) -> float:

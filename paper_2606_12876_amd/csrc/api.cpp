@@ -75,6 +75,7 @@ aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* co
   const size_t n_codewords = (size_t)1 << desc->code_bits;
   const size_t cb_bytes = (size_t)desc->num_codebooks * n_codewords * desc->group_size * 2;
   L->ws_floats = gemv_workspace_floats(*desc, L->G, L->S);
+  if (L->ws_floats < 256 + distortion_workspace_floats()) L->ws_floats = 256 + distortion_workspace_floats();
 
   struct { void** p; size_t n; const char* what; } allocs[] = {
       {(void**)&L->codes, (size_t)desc->num_codebooks * L->plane_bytes, "codes"},
@@ -91,8 +92,8 @@ aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* co
       return fail(AQMB_ENOMEM, "create: hipMalloc(%zu) for %s failed: %s", a.n, a.what, hipGetErrorString(e));
     }
   }
-  // The workspace holds per-call partial sums and arrival counters that every gemv
-  // call leaves at zero; they start at zero here.
+  // The workspace's first KiB is a zero page that kernels read in place of out-of-range
+  // inputs (never written); the rest holds per-call partial sums (gemv, prefix distortion).
   if ((e = hipMemsetAsync(L->ws, 0, L->ws_floats * sizeof(float), st)) != hipSuccess ||
       (e = hipMemcpyAsync(L->codebooks, codebooks, cb_bytes, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
       (e = hipMemcpyAsync(L->scales, scales, (size_t)desc->d_out * 2, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
@@ -179,6 +180,20 @@ aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, vo
   if ((s = check_device(L)) != AQMB_OK) return s;
   hipError_t e = launch_gemm(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemm: launch");
+}
+
+aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* X,
+                                   aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "prefix_distortion: not a live layer");
+  if (!W) return fail(AQMB_EINVAL, "prefix_distortion: W is NULL");
+  if ((uintptr_t)W % 16) return fail(AQMB_EINVAL, "prefix_distortion: W must be 16-byte aligned");
+  aqmb_status s = validate_call(&L->d, 3, 0, n, x_dtype, w_dtype, X, D);
+  if (s != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  hipError_t e = launch_distortion(*L, W, X, n, D, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "prefix_distortion: launch");
 }
 
 aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype, aqmb_stream_t stream) {

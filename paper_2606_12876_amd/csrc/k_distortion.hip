@@ -1,0 +1,259 @@
+// Distortion of every prefix level in one pass (the quantity the training loop of Drop-by-Drop
+// evaluates after each new codebook, section 5 and Alg. 1, with the weighted MSE of section 2.2,
+// Eq. wmse-task): for k = 1..M,
+//   D^(k) = ||(W - W^(k)) X||_F^2 / (d_out n),  W^(k)[i, j g + t] = s_i sum_{m<k} C_m[b_{ijm}][t],
+// with the n calibration inputs given as rows X^T = [n][d_in].
+//
+// For an output tile (samples x weight rows) the kernel accumulates, over d_in, the dense product
+// P = X^T W^T and one product per code plane, Q_m = X^T C_m[b_m]^T (unscaled). Then
+//   R_k = P - s_i (Q_0 + ... + Q_{k-1}),   D^(k) = sum of R_k^2 / (d_out n).
+// W, X and the codebooks are fp16 and the products run on the fp16 matrix cores
+// (v_mfma_f32_32x32x16_f16): every product of two fp16 values is exact in the fp32 accumulator,
+// so the only roundings are those of the fp32 sums, of s_i Q and of the differences.
+//
+// Work item: kTok = 32 NA samples x 128 weight rows. Each of the four waves owns 32 rows (one
+// MFMA column block) and all NA sample blocks, so the B fragment of a row block (a W piece or a
+// codeword) feeds NA MFMAs. d_in is walked in steps of 32 (two K-blocks of 16 = four groups):
+//   - the kTok x 32 slice of X is staged in LDS (direct loads, double-buffered, swizzled so that
+//     the 32 rows of an A fragment read hit distinct banks) and read by all four waves;
+//   - the W pieces of the next step come from global memory into registers (16 bytes per lane),
+//     together with the next step's code words (one 4-byte word = 4 groups per plane);
+//   - the B fragment of plane m is the codeword itself: lane l of a K-block needs the 8 values of
+//     one group of one row, i.e. C_m[code], gathered from codebooks replicated in LDS.
+// Each lane keeps fp64 sums of R_k^2 over its outputs; each workgroup writes its sums and a
+// second kernel adds them in workgroup order, so the result does not depend on scheduling.
+#include "device.h"
+#include "launch.h"
+
+namespace aqmb {
+
+namespace dist {
+constexpr int kThreads = 256;                // four waves
+constexpr int kRows = 128;                   // weight rows per work item (32 per wave)
+constexpr int kStep = 32;                    // d_in per step: two K-blocks of 16
+constexpr int kMaxGrid = 256;                // one workgroup per CU; each loops over work items
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+template <int M> struct Cfg {
+  static constexpr int NA = M <= 6 ? 2 : 1;  // 32-sample blocks per wave (accumulators: 16 NA (M+1))
+  static constexpr int kTok = 32 * NA;
+  static constexpr int kNrep = M <= 4 ? 8 : 4;                 // codebook replicas in LDS
+  static constexpr int kShift = kNrep == 8 ? 7 : 6;            // log2(16 kNrep)
+  static constexpr size_t kCbBytes = (size_t)M * 256 * kNrep * 16;
+  static constexpr size_t kXBytes = (size_t)kTok * kStep * 2;  // one X stage
+  static constexpr size_t kLds = kCbBytes + 2 * kXBytes;
+};
+}  // namespace dist
+
+size_t distortion_workspace_floats() { return (size_t)dist::kMaxGrid * 8 * 2; }
+
+struct DistArgs {
+  const unsigned char* codes;
+  const uint16_t* codebooks;
+  const uint16_t* scales;
+  const uint16_t* W;      // [d_out][d_in] fp16
+  const uint16_t* X;      // [n][d_in] fp16
+  double* partials;       // [gridDim.x][8]
+  const void* zero_page;  // >= 16 zero bytes
+  size_t plane_bytes;
+  int d_out, d_in, n, n_rb, n_items;
+};
+
+template <int M>
+__global__ __launch_bounds__(dist::kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void distortion_kernel(DistArgs a) {
+  using namespace dist;
+  using C = Cfg<M>;
+  constexpr int NA = C::NA, kTok = C::kTok, kNrep = C::kNrep, kShift = C::kShift;
+  extern __shared__ uint4 smem_d[];
+  uint4* cbr = smem_d;                                          // [M][256][kNrep] codewords
+  char* xs = (char*)smem_d + C::kCbBytes;                       // [2][kTok][64 bytes]
+  __shared__ double red[4][M];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5, r32 = lane & 31;
+  const int nsteps = (a.d_in + kStep - 1) / kStep;
+
+  // Codebooks, replicated: replica r of codeword q (= m * 256 + c) at slot q * kNrep + r. The
+  // writers of one store instruction are rotated so that 16 consecutive q fill a bank row.
+  for (int q = tid; q < M * 256; q += kThreads) {
+    const uint4 v = ((const uint4*)a.codebooks)[q];
+    const int rot = q >> (8 - kShift);
+#pragma unroll
+    for (int i = 0; i < kNrep; ++i) cbr[q * kNrep + ((i + rot) & (kNrep - 1))] = v;
+  }
+  const char* cbase = (const char*)cbr + (lane & (kNrep - 1)) * 16;   // this lane's replica
+
+  double part[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) part[m] = 0.0;
+
+  for (int item = blockIdx.x; item < a.n_items; item += gridDim.x) {
+    const int rb = item % a.n_rb, t0 = (item / a.n_rb) * kTok;
+    const int row = rb * kRows + wave * 32 + r32;
+    const bool row_ok = row < a.d_out;
+    const int rowc = row_ok ? row : a.d_out - 1;
+
+    // X stage of step st into buffer buf: 16-byte slot p of the stage (p = 64 w + lane) holds
+    // sample p / 4, piece (p % 4) ^ ((sample / 4) % 4) of the step's 64 bytes. Waves 0 .. 2 NA - 1
+    // load (kTok samples x 4 pieces = 64 * 2 NA slots).
+    auto stage_x = [&](int st, int buf) {
+      if (wave < 2 * NA) {
+        const int p = wave * 64 + lane, srow = p >> 2;
+        const int piece = (p & 3) ^ ((srow >> 2) & 3);
+        const int t = t0 + srow, k = st * kStep + piece * 8;
+        const void* src = (t < a.n && k < a.d_in) ? (const void*)(a.X + (size_t)t * a.d_in + k) : a.zero_page;
+        load_lds16(src, lds_addr(xs + buf * C::kXBytes + wave * 1024));
+      }
+    };
+    struct Frag { f16x8_t w[2]; uint32_t c[M]; };
+    // W pieces (K-blocks 0, 1: values 16 kb + 8 h .. + 7 of the step) and the code words of
+    // groups 4 st .. 4 st + 3 of this lane's row. Past the last step: reload the last (unused).
+    auto load_frag = [&](int st, Frag& f) {
+      const int stc = st < nsteps ? st : nsteps - 1;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        int k = stc * kStep + kb * 16 + h * 8;
+        k = k < a.d_in ? k : 0;                                // zeroed before use
+        f.w[kb] = *(const f16x8_t*)(a.W + (size_t)rowc * a.d_in + k);
+      }
+      const int g0 = stc * 4;
+#pragma unroll
+      for (int m = 0; m < M; ++m)
+        f.c[m] = *(const uint32_t*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 12));
+    };
+
+    f32x16_t acc[M + 1][NA];
+#pragma unroll
+    for (int s = 0; s <= M; ++s)
+#pragma unroll
+      for (int na = 0; na < NA; ++na)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[s][na][e] = 0.f;
+
+    auto step = [&](int st, const Frag& f, Frag& nxt) {
+      wait_vmcnt<0>();                                         // this wave's X slots of step st
+      __syncthreads();                                         // all slots; buffer st + 1 free
+      if (st + 1 < nsteps) stage_x(st + 1, (st + 1) & 1);
+      load_frag(st + 1, nxt);
+      const char* xst = xs + (st & 1) * C::kXBytes;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bool kin = st * kStep + kb * 16 + h * 8 < a.d_in;     // ragged last step
+        const int piece = kb * 2 + h, gi = piece;                   // group gi of the step
+        f16x8_t xa[NA];
+#pragma unroll
+        for (int na = 0; na < NA; ++na) {
+          const int s = na * 32 + r32;
+          xa[na] = *(const f16x8_t*)(xst + s * 64 + ((piece ^ ((s >> 2) & 3)) << 4));
+        }
+        f16x8_t bw = f.w[kb];
+        if (!kin) bw = f16x8_t{};
+#pragma unroll
+        for (int na = 0; na < NA; ++na)
+          acc[0][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa[na], bw, acc[0][na], 0, 0, 0);
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          const uint32_t code = (f.c[m] >> (8 * gi)) & 0xFFu;
+          f16x8_t bq = *(const f16x8_t*)(cbase + ((uint32_t)(m * 256 + code) << kShift));
+          if (!kin) bq = f16x8_t{};
+#pragma unroll
+          for (int na = 0; na < NA; ++na)
+            acc[m + 1][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa[na], bq, acc[m + 1][na], 0, 0, 0);
+        }
+      }
+    };
+
+    Frag fa, fb;
+    stage_x(0, 0);
+    load_frag(0, fa);
+    for (int st = 0; st < nsteps; st += 2) {
+      step(st, fa, fb);
+      if (st + 1 < nsteps) step(st + 1, fb, fa);
+    }
+    // R_k = P - s (Q_0 + ... + Q_{k-1}) for each output (sample t, row), summed squared over the
+    // outputs inside the matrix. Element e of an accumulator is sample 8 (e / 4) + 4 h + e % 4 of
+    // its block, row r32 of the wave's block.
+    const float sc = f16_to_f32(a.scales[rowc]);
+#pragma unroll
+    for (int na = 0; na < NA; ++na) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int t = t0 + na * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+        const bool ok = row_ok && t < a.n;
+        float r = acc[0][na][e];
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          r -= sc * acc[m + 1][na][e];
+          if (ok) part[m] += (double)r * (double)r;
+        }
+      }
+    }
+    __syncthreads();                                           // X buffers are restaged next item
+  }
+  // Workgroup sums in a fixed order: butterfly within each wave, then waves 0..3.
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    double v = part[m];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    if (lane == 0) red[wave][m] = v;
+  }
+  __syncthreads();
+  if (tid < M) a.partials[(size_t)blockIdx.x * 8 + tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+}
+
+// D[m] = (sum of the workgroup sums, in workgroup order) / (d_out n).
+__global__ void distortion_reduce_kernel(const double* partials, int grid, int M, double inv, double* D) {
+  const int m = threadIdx.x;
+  if (m < M) {
+    double s = 0.0;
+    for (int b = 0; b < grid; ++b) s += partials[(size_t)b * 8 + m];
+    D[m] = s * inv;
+  }
+}
+
+template <int M>
+static hipError_t launch_dist_m(DistArgs& a, hipStream_t st, int* grid_out) {
+  using C = dist::Cfg<M>;
+  a.n_rb = (a.d_out + dist::kRows - 1) / dist::kRows;
+  a.n_items = a.n_rb * ((a.n + C::kTok - 1) / C::kTok);
+  const int grid = a.n_items < dist::kMaxGrid ? a.n_items : dist::kMaxGrid;
+  static_assert(C::kLds <= 160 * 1024 - 512, "LDS budget");
+  distortion_kernel<M><<<grid, dist::kThreads, C::kLds, st>>>(a);
+  *grid_out = grid;
+  return hipGetLastError();
+}
+
+hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n, double* D, hipStream_t st) {
+  DistArgs a{};
+  a.codes = L.codes;
+  a.codebooks = L.codebooks;
+  a.scales = L.scales;
+  a.W = (const uint16_t*)W;
+  a.X = (const uint16_t*)X;
+  a.partials = (double*)(L.ws + 256);
+  a.zero_page = L.ws;
+  a.plane_bytes = L.plane_bytes;
+  a.d_out = L.d.d_out;
+  a.d_in = L.d.d_in;
+  a.n = n;
+  int grid = 0;
+  hipError_t e;
+  switch (L.d.num_codebooks) {
+    case 1: e = launch_dist_m<1>(a, st, &grid); break;
+    case 2: e = launch_dist_m<2>(a, st, &grid); break;
+    case 3: e = launch_dist_m<3>(a, st, &grid); break;
+    case 4: e = launch_dist_m<4>(a, st, &grid); break;
+    case 5: e = launch_dist_m<5>(a, st, &grid); break;
+    case 6: e = launch_dist_m<6>(a, st, &grid); break;
+    case 7: e = launch_dist_m<7>(a, st, &grid); break;
+    default: e = launch_dist_m<8>(a, st, &grid); break;
+  }
+  if (e != hipSuccess) return e;
+  distortion_reduce_kernel<<<1, 64, 0, st>>>(a.partials, grid, L.d.num_codebooks,
+                                             1.0 / ((double)L.d.d_out * (double)n), D);
+  return hipGetLastError();
+}
+
+}  // namespace aqmb

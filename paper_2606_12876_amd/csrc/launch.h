@@ -14,6 +14,10 @@ size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S);
 // Several layers with the same d_in and device, already validated; n <= AQMB_MAX_MULTI.
 hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x, aqmb_dtype x_dtype, int batch,
                              void* const* ys, aqmb_dtype y_dtype, hipStream_t st);
+// All prefix distortions D[0..M-1] of the layer against fp16 W [d_out][d_in] and fp16 inputs
+// X [n][d_in]; uses the layer's workspace after its first KiB.
+hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n, double* D, hipStream_t st);
+size_t distortion_workspace_floats();
 hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
                        hipStream_t st);
 

@@ -46,7 +46,7 @@ aqmb_status validate_call(const aqmb_desc* d, int op, int k, int n, aqmb_dtype i
                           const void* in, const void* out) {
   aqmb_status s = validate_desc(d);
   if (s != AQMB_OK) return s;
-  if (k < 1 || k > d->num_codebooks)
+  if (op != 3 && (k < 1 || k > d->num_codebooks))   // the distortion covers every k at once
     return fail(AQMB_EINVAL, "k = %d outside [1, M = %d]", k, d->num_codebooks);
   if (!valid_dtype(out_dt)) return fail(AQMB_EUNSUPPORTED, "output dtype %d is not F16, BF16 or F32", (int)out_dt);
   switch (op) {
@@ -71,6 +71,16 @@ aqmb_status validate_call(const aqmb_desc* d, int op, int k, int n, aqmb_dtype i
     case 2:  // dequant
       if (!out) return fail(AQMB_EINVAL, "dequant: W is NULL");
       if ((uintptr_t)out % 16) return fail(AQMB_EINVAL, "dequant: W must be 16-byte aligned");
+      return AQMB_OK;
+    case 3:  // prefix distortion: in = X (dtype in_dt), out = D, out_dt = W's dtype
+      if (!in || !out) return fail(AQMB_EINVAL, "prefix_distortion: X or D is NULL");
+      if (n < 1) return fail(AQMB_EINVAL, "prefix_distortion: n = %d must be >= 1", n);
+      if (n > (1 << 30)) return fail(AQMB_EUNSUPPORTED, "prefix_distortion: n = %d above 2^30", n);
+      if (d->code_bits != 8) return fail(AQMB_EUNSUPPORTED, "prefix_distortion: only B = 8 layers are supported");
+      if (in_dt != AQMB_F16 || out_dt != AQMB_F16)
+        return fail(AQMB_EUNSUPPORTED, "prefix_distortion: W and X must be F16");
+      if ((uintptr_t)in % 16) return fail(AQMB_EINVAL, "prefix_distortion: X must be 16-byte aligned");
+      if ((uintptr_t)out % 8) return fail(AQMB_EINVAL, "prefix_distortion: D must be 8-byte aligned");
       return AQMB_OK;
     default:
       return fail(AQMB_EINVAL, "unknown op %d", op);

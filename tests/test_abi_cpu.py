@@ -74,7 +74,17 @@ def test_descriptor_validation(case, expect):
     (1, 2, 7, 1, 0, 16, 32, A.Status.EUNSUPPORTED),  # gemm output must be bf16/f32
     (2, 3, 0, 0, 2, None, 32, A.Status.OK),
     (2, 3, 0, 0, 2, None, None, A.Status.EINVAL),
-    (3, 1, 1, 0, 0, 16, 32, A.Status.EINVAL),       # unknown op
+    (4, 1, 1, 0, 0, 16, 32, A.Status.EINVAL),       # unknown op
+    (3, 0, 4096, 0, 0, 16, 32, A.Status.OK),        # distortion: k is not checked
+    (3, 9, 1, 0, 0, 16, 8, A.Status.OK),            # D needs 8-byte alignment only
+    (3, 1, 0, 0, 0, 16, 32, A.Status.EINVAL),       # n < 1
+    (3, 1, (1 << 30) + 1, 0, 0, 16, 32, A.Status.EUNSUPPORTED),
+    (3, 1, 8, 1, 0, 16, 32, A.Status.EUNSUPPORTED),  # X must be f16
+    (3, 1, 8, 0, 1, 16, 32, A.Status.EUNSUPPORTED),  # W must be f16
+    (3, 1, 8, 0, 0, None, 32, A.Status.EINVAL),
+    (3, 1, 8, 0, 0, 16, None, A.Status.EINVAL),
+    (3, 1, 8, 0, 0, 24, 32, A.Status.EINVAL),       # X misaligned
+    (3, 1, 8, 0, 0, 16, 36, A.Status.EINVAL),       # D misaligned
 ])
 def test_call_validation(op, k, n, xdt, ydt, x, y, expect):
     d = A.make_desc(256, 512, 4)
@@ -85,6 +95,7 @@ def test_gemm_rejects_16bit_codes():
     d = A.make_desc(256, 512, 2, code_bits=16)
     assert A.validate(d, 1, 1, 8, A.DType.BF16, A.DType.BF16, 16, 32) == A.Status.EUNSUPPORTED
     assert A.validate(d, 0, 2, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.OK
+    assert A.validate(d, 3, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EUNSUPPORTED
 
 
 def test_bits_per_weight_matches_oracle():
@@ -103,6 +114,8 @@ def test_bad_handles_rejected_without_gpu():
     assert A.lib.aqmb_gemv(bogus, 1, 16, 0, 1, 32, 0, None) == A.Status.EINVAL
     assert A.lib.aqmb_gemm(bogus, 1, 16, 1, 32, 1, None) == A.Status.EINVAL
     assert A.lib.aqmb_dequant(bogus, 1, 32, 0, None) == A.Status.EINVAL
+    assert A.lib.aqmb_prefix_distortion(bogus, 16, 0, 32, 0, 8, 64, None) == A.Status.EINVAL
+    assert "live" in A.last_error()
     d = A.Desc()
     assert A.lib.aqmb_get_desc(bogus, ctypes.byref(d)) == A.Status.EINVAL
     h = ctypes.c_void_p(0x1234)

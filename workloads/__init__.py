@@ -19,7 +19,15 @@ order):
 4. activations ``normal(0, 1, (batch, d_in))`` -> fp16 or bf16 (round to
    nearest even); the heavy-tailed variant multiplies
    ``round(0.001*batch*d_in)`` positions, chosen without replacement, by 20
-   before the cast.
+   before the cast. Calibration inputs of the distortion evaluator are drawn
+   the same way (fp16, one input per row);
+5. dense weights (distortion evaluator) ``normal(0, 0.02, (d_out, d_in))`` -> fp16.
+
+Integer-valued variant (exactness tests of the distortion evaluator): the same
+steps with codebook entries ``integers(-4, 5)``, scales drawn from {0.5, 1, 2},
+inputs ``integers(-4, 5)`` and weights ``integers(-16, 17)``. Every product and
+every partial sum of products of such values is an integer (or half-integer)
+far below 2^24, so it is exact in fp32 whatever the summation order.
 
 The shapes stand in for the projections of Llama-7B-class models (4096x4096,
 11008x4096, 4096x11008, 14336x4096) quantized with M codebooks of 2**B
@@ -32,8 +40,8 @@ from typing import List, Optional
 
 import numpy as np
 
-__all__ = ["Layer", "LayerSpec", "make_layer", "make_activations", "float_to_bf16_bits",
-           "float_to_f16_bits", "CONFIGS", "config"]
+__all__ = ["Layer", "LayerSpec", "make_layer", "make_activations", "make_weights", "make_integer_layer",
+           "make_integer_rows", "float_to_bf16_bits", "float_to_f16_bits", "CONFIGS", "config"]
 
 
 def float_to_f16_bits(a: np.ndarray) -> np.ndarray:
@@ -117,6 +125,30 @@ def make_activations(layer: Layer, rows: int, dtype: Optional[str] = None,
     if dtype == "bf16":
         return float_to_bf16_bits(x)
     raise ValueError(dtype)
+
+
+def make_weights(layer: Layer, std: float = 0.02) -> np.ndarray:
+    """Draw a dense weight matrix [d_out][d_in], normal(0, std), as fp16 bits (step 5)."""
+    spec = layer.spec
+    return float_to_f16_bits(layer.rng.normal(0.0, std, size=(spec.d_out, spec.d_in)))
+
+
+def make_integer_layer(spec: LayerSpec, seed: Optional[int] = None) -> Layer:
+    """Integer-valued layer: codebook entries in [-4, 4], codes uniform, scales in {0.5, 1, 2}."""
+    rng = np.random.Generator(np.random.PCG64(spec.seed if seed is None else seed))
+    M, B, g = spec.M, spec.B, spec.g
+    if spec.d_in % g:
+        raise ValueError("d_in must be a multiple of g")
+    codebooks = float_to_f16_bits(rng.integers(-4, 5, size=(M, 1 << B, g)).astype(np.float64))
+    code_dt = np.uint8 if B <= 8 else np.uint16
+    codes = rng.integers(0, 1 << B, size=(M, spec.d_out, spec.d_in // g), dtype=np.int64).astype(code_dt)
+    scales = float_to_f16_bits(rng.choice(np.array([0.5, 1.0, 2.0]), size=spec.d_out))
+    return Layer(spec, codes, codebooks, scales, rng)
+
+
+def make_integer_rows(layer: Layer, rows: int, lim: int) -> np.ndarray:
+    """``rows`` x d_in integers in [-lim, lim] as fp16 bits (inputs: lim 4, weights: lim 16)."""
+    return float_to_f16_bits(layer.rng.integers(-lim, lim + 1, size=(rows, layer.spec.d_in)).astype(np.float64))
 
 
 # The five workloads. Config 3 is a pair of layers (up and down projection).
