@@ -7,6 +7,8 @@ exceeds the 256 MB Infinity Cache and every launch streams its codes from HBM):
   for k in 1..4:   decode GEMV at batch 1 and batch 4   (4096 x 4096, M = 4, uint8 codes, fp16 x/y)
                    dequantization to bf16                 (same layers)
                    prefill GEMM, 2048 bf16 tokens          (4096 x 4096 layer, bf16 out)
+  once:            prefix distortions D^(1..4) of the decode layer against a dense fp16 W
+                   over 4096 fp16 calibration inputs
 
 Each (operation, k, batch) runs as a burst of R launches captured in a HIP graph and timed
 with HIP events on the launch stream; the per-launch time is burst time / R.
@@ -14,7 +16,9 @@ with HIP events on the launch stream; the per-launch time is burst time / R.
 `value` is the decode GEMV throughput in algorithmic GB/s (code planes 0..k-1, their
 codebooks, scales, x and y) over all GEMV launches of the timed steps. `roofline` describes the
 GEMV kernel at batch 1, k = 4 (HBM-bound); `roofline_gemm` the prefill GEMM at k = 4
-(MFMA-bound). The CPU baseline is the fp64 oracle timed on a bounded sample.
+(MFMA-bound); `roofline_distortion` the distortion evaluator (fp16 MFMA-bound, algorithmic
+flops 2 (M + 1) d_out d_in n: W X and one product per code plane). The CPU baseline is the fp64
+oracle timed on a bounded sample.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -33,6 +37,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+F16_PEAK_TFLOPS = 2500.0        # MI355X dense fp16 MFMA
 
 
 def log(*a):
@@ -142,6 +147,13 @@ def main():
                             to_dev(gl.codebooks), to_dev(gl.scales)) for r in range(G_COPIES)]
         Xg = to_dev(make_activations(gl, n_tok, "bf16")).view(torch.bfloat16)
         Yg = [torch.empty((n_tok, gspec.d_out), dtype=torch.bfloat16, device=dev) for _ in range(G_COPIES)]
+    # ---------------------------------------------------------------- distortion workload
+    n_cal = 4096
+    from workloads import make_weights
+    Wd = to_dev(make_weights(base)).view(torch.float16)
+    Xd = to_dev(make_activations(base, n_cal, "f16")).view(torch.float16)
+    D_COPIES = 4
+    Ds = [torch.empty((M,), dtype=torch.float64, device=dev) for _ in range(D_COPIES)]
     torch.cuda.synchronize()
 
     ks = list(spec.ks)
@@ -168,7 +180,11 @@ def main():
             xs, ys = (xs1, ys1) if b == 1 else (xs4, ys4)
             A.gemv_multi(layers[r0:r0 + G], k, xs[r0], A.DType.F16, b, ys[r0:r0 + G], A.DType.F16)
 
-    ops = []  # (name, k, b, fn, launches)
+    def distortion_burst():
+        for r in range(D_COPIES):
+            A.prefix_distortion(layers[r], Wd, A.DType.F16, Xd, A.DType.F16, n_cal, Ds[r])
+
+    ops = [("distortion", M, n_cal, distortion_burst, D_COPIES)]  # (name, k, b, fn, launches)
     for k in ks:
         ops.append(("gemv", k, 1, lambda k=k: gemv_burst(k, 1), R))
         ops.append(("gemv", k, 4, lambda k=k: gemv_burst(k, 4), R))
@@ -306,7 +322,16 @@ def main():
                                 "traffic": None, "us_per_launch": round(tg, 2)}
         gemm_total_us = sum(per_launch_us[("gemm", k, n_tok)] for k in ks)
         out["gemm_TFLOPs"] = round(len(ks) * fl / (gemm_total_us * 1e-6) / 1e12, 1)
-    step_us = {n: 0.0 for n in ("gemv", "gemv_multi", "dequant", "gemm")}
+    td = per_launch_us[("distortion", M, n_cal)]
+    fld = 2.0 * (M + 1) * d_out * d_in * n_cal
+    achd = fld / (td * 1e-6) / 1e12
+    out["roofline_distortion"] = {"bound": "mfma", "kernel": f"distortion_kernel<M={M}> + distortion_reduce_kernel",
+                                  "achieved": round(achd, 1), "peak": F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                  "frac": round(achd / F16_PEAK_TFLOPS, 4), "traffic": None,
+                                  "us_per_launch": round(td, 2),
+                                  "workload": f"D^(1..{M}) of a {d_out}x{d_in} layer, dense fp16 W, "
+                                              f"{n_cal} fp16 calibration inputs"}
+    step_us = {n: 0.0 for n in ("gemv", "gemv_multi", "dequant", "gemm", "distortion")}
     for i, (name, k, b, fn, n) in enumerate(ops):
         step_us["gemv_multi" if name.startswith("gemv_multi") else name] += per_op_ms[i] * 1e3 / args.steps
     tot = sum(step_us.values())

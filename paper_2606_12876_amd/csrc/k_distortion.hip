@@ -13,11 +13,12 @@
 //
 // Work item: kTok = 32 NA samples x 128 weight rows. Each of the four waves owns 32 rows (one
 // MFMA column block) and all NA sample blocks, so the B fragment of a row block (a W piece or a
-// codeword) feeds NA MFMAs. d_in is walked in steps of 32 (two K-blocks of 16 = four groups):
-//   - the kTok x 32 slice of X is staged in LDS (direct loads, double-buffered, swizzled so that
-//     the 32 rows of an A fragment read hit distinct banks) and read by all four waves;
-//   - the W pieces of the next step come from global memory into registers (16 bytes per lane),
-//     together with the next step's code words (one 4-byte word = 4 groups per plane);
+// codeword) feeds NA MFMAs. d_in is walked in steps of 64 (four K-blocks of 16 = eight groups),
+// with the loads of the next kPre steps in flight while a step computes:
+//   - the kTok x 64 slice of X is staged in LDS (direct loads into kPre + 1 buffers, swizzled
+//     so that the 32 rows of an A fragment read hit distinct banks) and read by all four waves;
+//   - the W pieces come from global memory into registers (16 bytes per lane and K-block),
+//     together with the code bytes (8 bytes = 8 groups per plane), in kPre + 1 register sets;
 //   - the B fragment of plane m is the codeword itself: lane l of a K-block needs the 8 values of
 //     one group of one row, i.e. C_m[code], gathered from codebooks replicated in LDS.
 // Each lane keeps fp64 sums of R_k^2 over its outputs; each workgroup writes its sums and a
@@ -30,7 +31,9 @@ namespace aqmb {
 namespace dist {
 constexpr int kThreads = 256;                // four waves
 constexpr int kRows = 128;                   // weight rows per work item (32 per wave)
-constexpr int kStep = 32;                    // d_in per step: two K-blocks of 16
+constexpr int kStep = 64;                    // d_in per step: four K-blocks of 16 = eight groups
+constexpr int kPre = 2;                      // steps whose loads are in flight ahead of the computed one
+constexpr int kBufs = kPre + 1;              // X buffers and register sets
 constexpr int kMaxGrid = 256;                // one workgroup per CU; each loops over work items
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 template <int M> struct Cfg {
@@ -40,8 +43,11 @@ template <int M> struct Cfg {
   static constexpr int kShift = kNrep == 8 ? 7 : 6;            // log2(16 kNrep)
   static constexpr size_t kCbBytes = (size_t)M * 256 * kNrep * 16;
   static constexpr size_t kXBytes = (size_t)kTok * kStep * 2;  // one X stage
-  static constexpr size_t kLds = kCbBytes + 2 * kXBytes;
+  static constexpr size_t kLds = kCbBytes + kBufs * kXBytes;
+  static constexpr int kLoads = NA + 4 + M;                    // loads per wave per step
 };
+// One step's operands in registers: the W pieces of the four K-blocks and 8 code bytes per plane.
+template <int M> struct Frag { f16x8_t w[4]; uint2 c[M]; };
 }  // namespace dist
 
 size_t distortion_workspace_floats() { return (size_t)dist::kMaxGrid * 8 * 2; }
@@ -63,10 +69,10 @@ __global__ __launch_bounds__(dist::kThreads) __attribute__((amdgpu_waves_per_eu(
 void distortion_kernel(DistArgs a) {
   using namespace dist;
   using C = Cfg<M>;
-  constexpr int NA = C::NA, kTok = C::kTok, kNrep = C::kNrep, kShift = C::kShift;
+  constexpr int NA = C::NA, kTok = C::kTok, kNrep = C::kNrep, kShift = C::kShift, kLoads = C::kLoads;
   extern __shared__ uint4 smem_d[];
   uint4* cbr = smem_d;                                          // [M][256][kNrep] codewords
-  char* xs = (char*)smem_d + C::kCbBytes;                       // [2][kTok][64 bytes]
+  char* xs = (char*)smem_d + C::kCbBytes;                       // [kBufs][kTok][128 bytes]
   __shared__ double red[4][M];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -94,33 +100,35 @@ void distortion_kernel(DistArgs a) {
     const bool row_ok = row < a.d_out;
     const int rowc = row_ok ? row : a.d_out - 1;
 
-    // X stage of step st into buffer buf: 16-byte slot p of the stage (p = 64 w + lane) holds
-    // sample p / 4, piece (p % 4) ^ ((sample / 4) % 4) of the step's 64 bytes. Waves 0 .. 2 NA - 1
-    // load (kTok samples x 4 pieces = 64 * 2 NA slots).
+    // X stage of step st into buffer buf: 16-byte slot q of the stage holds sample q / 8,
+    // piece (q % 8) ^ ((sample / 2) % 8) of the step's 128 bytes (two 128-byte sample rows share
+    // a bank row, so the 32 samples an A fragment reads land on distinct banks). Each wave loads
+    // NA runs of 64 slots. Past d_in (and past the last step) the zero page is loaded.
     auto stage_x = [&](int st, int buf) {
-      if (wave < 2 * NA) {
-        const int p = wave * 64 + lane, srow = p >> 2;
-        const int piece = (p & 3) ^ ((srow >> 2) & 3);
-        const int t = t0 + srow, k = st * kStep + piece * 8;
+#pragma unroll
+      for (int j = 0; j < NA; ++j) {
+        const int q = (wave * NA + j) * 64 + lane, smp = q >> 3;
+        const int piece = (q & 7) ^ ((smp >> 1) & 7);
+        const int t = t0 + smp, k = st * kStep + piece * 8;
         const void* src = (t < a.n && k < a.d_in) ? (const void*)(a.X + (size_t)t * a.d_in + k) : a.zero_page;
-        load_lds16(src, lds_addr(xs + buf * C::kXBytes + wave * 1024));
+        load_lds16(src, lds_addr(xs + buf * C::kXBytes + (wave * NA + j) * 1024));
       }
     };
-    struct Frag { f16x8_t w[2]; uint32_t c[M]; };
-    // W pieces (K-blocks 0, 1: values 16 kb + 8 h .. + 7 of the step) and the code words of
-    // groups 4 st .. 4 st + 3 of this lane's row. Past the last step: reload the last (unused).
-    auto load_frag = [&](int st, Frag& f) {
+    // W pieces (K-block kb: values 16 kb + 8 h .. + 7 of the step) and the code bytes of groups
+    // 8 st .. 8 st + 7 of this lane's row (one 8-byte half of a 16-group slice). Past the last
+    // step the last one is loaded again (never used), so every step issues the same loads.
+    auto load_frag = [&](int st, Frag<M>& f) {
       const int stc = st < nsteps ? st : nsteps - 1;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 4; ++kb) {
         int k = stc * kStep + kb * 16 + h * 8;
         k = k < a.d_in ? k : 0;                                // zeroed before use
         f.w[kb] = *(const f16x8_t*)(a.W + (size_t)rowc * a.d_in + k);
       }
-      const int g0 = stc * 4;
+      const int g0 = stc * 8;
 #pragma unroll
       for (int m = 0; m < M; ++m)
-        f.c[m] = *(const uint32_t*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 12));
+        f.c[m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 8));
     };
 
     f32x16_t acc[M + 1][NA];
@@ -131,46 +139,73 @@ void distortion_kernel(DistArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[s][na][e] = 0.f;
 
-    auto step = [&](int st, const Frag& f, Frag& nxt) {
-      wait_vmcnt<0>();                                         // this wave's X slots of step st
-      __syncthreads();                                         // all slots; buffer st + 1 free
-      if (st + 1 < nsteps) stage_x(st + 1, (st + 1) & 1);
-      load_frag(st + 1, nxt);
-      const char* xst = xs + (st & 1) * C::kXBytes;
+    // One step: for each K-block, NA A fragments from the X stage and M codewords gathered from
+    // the codebooks, read one K-block ahead of the MFMAs that use them. No lane is masked: past
+    // d_in the staged X is zero, so whatever W piece or codeword sits in the B operand there
+    // contributes nothing (W and the codebooks hold finite values).
+    struct Ops { f16x8_t xa[NA]; f16x8_t bq[M]; };
+    auto read_ops = [&](const char* xst, const Frag<M>& f, int kb, Ops& o) {
+      const int piece = kb * 2 + h;                            // = group of the step
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bool kin = st * kStep + kb * 16 + h * 8 < a.d_in;     // ragged last step
-        const int piece = kb * 2 + h, gi = piece;                   // group gi of the step
-        f16x8_t xa[NA];
+      for (int na = 0; na < NA; ++na) {
+        const int smp = na * 32 + r32;
+        o.xa[na] = *(const f16x8_t*)(xst + smp * 128 + ((piece ^ ((smp >> 1) & 7)) << 4));
+      }
 #pragma unroll
-        for (int na = 0; na < NA; ++na) {
-          const int s = na * 32 + r32;
-          xa[na] = *(const f16x8_t*)(xst + s * 64 + ((piece ^ ((s >> 2) & 3)) << 4));
-        }
-        f16x8_t bw = f.w[kb];
-        if (!kin) bw = f16x8_t{};
+      for (int m = 0; m < M; ++m) {
+        const uint32_t word = kb < 2 ? f.c[m].x : f.c[m].y;
+        const uint32_t code = (word >> (16 * (kb & 1) + 8 * h)) & 0xFFu;
+        o.bq[m] = *(const f16x8_t*)(cbase + ((uint32_t)(m * 256 + code) << kShift));
+      }
+    };
+    auto compute = [&](const Frag<M>& f, int buf) {
+      const char* xst = xs + buf * C::kXBytes;
+      Ops o[2];
+      read_ops(xst, f, 0, o[0]);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        if (kb < 3) read_ops(xst, f, kb + 1, o[(kb + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);                     // reads of kb + 1 before the MFMAs of kb
+        const Ops& c = o[kb & 1];
 #pragma unroll
         for (int na = 0; na < NA; ++na)
-          acc[0][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa[na], bw, acc[0][na], 0, 0, 0);
+          acc[0][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(c.xa[na], f.w[kb], acc[0][na], 0, 0, 0);
 #pragma unroll
-        for (int m = 0; m < M; ++m) {
-          const uint32_t code = (f.c[m] >> (8 * gi)) & 0xFFu;
-          f16x8_t bq = *(const f16x8_t*)(cbase + ((uint32_t)(m * 256 + code) << kShift));
-          if (!kin) bq = f16x8_t{};
+        for (int m = 0; m < M; ++m)
 #pragma unroll
           for (int na = 0; na < NA; ++na)
-            acc[m + 1][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xa[na], bq, acc[m + 1][na], 0, 0, 0);
-        }
+            acc[m + 1][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(c.xa[na], c.bq[m], acc[m + 1][na], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     };
 
-    Frag fa, fb;
-    stage_x(0, 0);
-    load_frag(0, fa);
-    for (int st = 0; st < nsteps; st += 2) {
-      step(st, fa, fb);
-      if (st + 1 < nsteps) step(st + 1, fb, fa);
+    // Software pipeline: the loads of step st + kPre are issued when step st starts, into X
+    // buffer and register set (st + kPre) % kBufs; kLoads loads per step, completing in order.
+    Frag<M> f[kBufs];
+#pragma unroll
+    for (int j = 0; j < kPre; ++j) {
+      stage_x(j, j);
+      load_frag(j, f[j]);
     }
+    auto step = [&](int st, int j) {                         // j = st % kBufs, a constant
+      wait_vmcnt<(kPre - 1) * kLoads>();                       // this wave's loads of step st
+      __syncthreads();                                         // every wave's; step st - 1 done
+      stage_x(st + kPre, (j + kPre) % kBufs);
+      load_frag(st + kPre, f[(j + kPre) % kBufs]);
+      __builtin_amdgcn_sched_barrier(0);                       // issue the loads before the MFMAs
+      compute(f[j], j);
+    };
+    // Whole rounds of kBufs steps, then the last nsteps % kBufs steps: a loop body without
+    // skipped steps lets the compiler see that the register set a step uses was loaded kPre
+    // steps earlier (a conditional step would make it wait for the newer loads too).
+    int st0 = 0;
+    for (; st0 + kBufs <= nsteps; st0 += kBufs) {
+#pragma unroll
+      for (int j = 0; j < kBufs; ++j) step(st0 + j, j);
+    }
+#pragma unroll
+    for (int j = 0; j < kBufs - 1; ++j)
+      if (st0 + j < nsteps) step(st0 + j, j);
     // R_k = P - s (Q_0 + ... + Q_{k-1}) for each output (sample t, row), summed squared over the
     // outputs inside the matrix. Element e of an accumulator is sample 8 (e / 4) + 4 h + e % 4 of
     // its block, row r32 of the wave's block.
@@ -189,6 +224,7 @@ void distortion_kernel(DistArgs a) {
         }
       }
     }
+    wait_vmcnt<0>();                                           // loads past the last step
     __syncthreads();                                           // X buffers are restaged next item
   }
   // Workgroup sums in a fixed order: butterfly within each wave, then waves 0..3.
