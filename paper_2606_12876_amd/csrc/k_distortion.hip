@@ -117,18 +117,24 @@ void distortion_kernel(DistArgs a) {
     // W pieces (K-block kb: values 16 kb + 8 h .. + 7 of the step) and the code bytes of groups
     // 8 st .. 8 st + 7 of this lane's row (one 8-byte half of a 16-group slice). Past the last
     // step the last one is loaded again (never used), so every step issues the same loads.
-    auto load_frag = [&](int st, Frag<M>& f) {
+    auto load_w = [&](int st, Frag<M>& f, int kb) {
       const int stc = st < nsteps ? st : nsteps - 1;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        int k = stc * kStep + kb * 16 + h * 8;
-        k = k < a.d_in ? k : 0;                                // zeroed before use
-        f.w[kb] = *(const f16x8_t*)(a.W + (size_t)rowc * a.d_in + k);
-      }
-      const int g0 = stc * 8;
+      int k = stc * kStep + kb * 16 + h * 8;
+      k = k < a.d_in ? k : 0;                                  // only meets zero X
+      f.w[kb] = *(const f16x8_t*)(a.W + (size_t)rowc * a.d_in + k);
+    };
+    auto load_codes = [&](int st, Frag<M>& f) {
+      const int g0 = (st < nsteps ? st : nsteps - 1) * 8;
 #pragma unroll
       for (int m = 0; m < M; ++m)
         f.c[m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 8));
+    };
+    // The loads of one step, issued in three parts (with the MFMAs of K-blocks 0, 1, 2 of the step
+    // kPre earlier), kLoads in all.
+    auto issue_part = [&](int st, int buf, Frag<M>& f, int part) {
+      if (part == 0) { stage_x(st, buf); load_w(st, f, 0); load_w(st, f, 1); }
+      if (part == 1) { load_w(st, f, 2); load_w(st, f, 3); }
+      if (part == 2) load_codes(st, f);
     };
 
     f32x16_t acc[M + 1][NA];
@@ -139,12 +145,12 @@ void distortion_kernel(DistArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[s][na][e] = 0.f;
 
-    // One step: for each K-block, NA A fragments from the X stage and M codewords gathered from
-    // the codebooks, read one K-block ahead of the MFMAs that use them. No lane is masked: past
-    // d_in the staged X is zero, so whatever W piece or codeword sits in the B operand there
-    // contributes nothing (W and the codebooks hold finite values).
+    // For each K-block: NA A fragments from the X stage and M codewords gathered from the
+    // codebooks. No lane is masked: past d_in the staged X is zero, so whatever W piece or
+    // codeword sits in the B operand there contributes nothing (W and the codebooks are finite).
     struct Ops { f16x8_t xa[NA]; f16x8_t bq[M]; };
-    auto read_ops = [&](const char* xst, const Frag<M>& f, int kb, Ops& o) {
+    auto read_ops = [&](int buf, const Frag<M>& f, int kb, Ops& o) {
+      const char* xst = xs + buf * C::kXBytes;
       const int piece = kb * 2 + h;                            // = group of the step
 #pragma unroll
       for (int na = 0; na < NA; ++na) {
@@ -158,18 +164,41 @@ void distortion_kernel(DistArgs a) {
         o.bq[m] = *(const f16x8_t*)(cbase + ((uint32_t)(m * 256 + code) << kShift));
       }
     };
-    auto compute = [&](const Frag<M>& f, int buf) {
-      const char* xst = xs + buf * C::kXBytes;
-      Ops o[2];
-      read_ops(xst, f, 0, o[0]);
+
+    // Software pipeline over steps (j = st % kBufs selects X buffer and register set):
+    //   K-block kb of step st: read the operands of the next K-block, issue part kb of the loads of
+    //   step st + kPre, then the MFMAs of kb. Before the MFMAs of K-block 3 each wave waits for its
+    //   loads of step st + 1 and the workgroup synchronises (every wave's X slots of step st + 1
+    //   are in; every wave has read step st's operands, whose buffer the loads issued during step
+    //   st + 1 overwrite), and K-block 0 of step st + 1 is read: the MFMA stream never waits for
+    //   the first reads of a step.
+    Frag<M> f[kBufs];
+    Ops o[2];
+#pragma unroll
+    for (int j = 0; j < kPre; ++j)
+#pragma unroll
+      for (int part = 0; part < 3; ++part) issue_part(j, j, f[j], part);
+    wait_vmcnt<(kPre - 1) * kLoads>();
+    __syncthreads();
+    read_ops(0, f[0], 0, o[0]);
+
+    auto step = [&](int st, int j) {                           // j = st % kBufs, a constant
+      const int jn = (j + 1) % kBufs, jl = (j + kPre) % kBufs;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        if (kb < 3) read_ops(xst, f, kb + 1, o[(kb + 1) & 1]);
-        __builtin_amdgcn_sched_barrier(0);                     // reads of kb + 1 before the MFMAs of kb
+        if (kb < 3) {
+          read_ops(j, f[j], kb + 1, o[(kb + 1) & 1]);
+          issue_part(st + kPre, jl, f[jl], kb);
+        } else {
+          wait_vmcnt<(kPre - 1) * kLoads>();                   // this wave's loads of step st + 1
+          __syncthreads();
+          read_ops(jn, f[jn], 0, o[0]);                        // past the last step: unused
+        }
+        __builtin_amdgcn_sched_barrier(0);
         const Ops& c = o[kb & 1];
 #pragma unroll
         for (int na = 0; na < NA; ++na)
-          acc[0][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(c.xa[na], f.w[kb], acc[0][na], 0, 0, 0);
+          acc[0][na] = __builtin_amdgcn_mfma_f32_32x32x16_f16(c.xa[na], f[j].w[kb], acc[0][na], 0, 0, 0);
 #pragma unroll
         for (int m = 0; m < M; ++m)
 #pragma unroll
@@ -178,26 +207,8 @@ void distortion_kernel(DistArgs a) {
         __builtin_amdgcn_sched_barrier(0);
       }
     };
-
-    // Software pipeline: the loads of step st + kPre are issued when step st starts, into X
-    // buffer and register set (st + kPre) % kBufs; kLoads loads per step, completing in order.
-    Frag<M> f[kBufs];
-#pragma unroll
-    for (int j = 0; j < kPre; ++j) {
-      stage_x(j, j);
-      load_frag(j, f[j]);
-    }
-    auto step = [&](int st, int j) {                         // j = st % kBufs, a constant
-      wait_vmcnt<(kPre - 1) * kLoads>();                       // this wave's loads of step st
-      __syncthreads();                                         // every wave's; step st - 1 done
-      stage_x(st + kPre, (j + kPre) % kBufs);
-      load_frag(st + kPre, f[(j + kPre) % kBufs]);
-      __builtin_amdgcn_sched_barrier(0);                       // issue the loads before the MFMAs
-      compute(f[j], j);
-    };
     // Whole rounds of kBufs steps, then the last nsteps % kBufs steps: a loop body without
-    // skipped steps lets the compiler see that the register set a step uses was loaded kPre
-    // steps earlier (a conditional step would make it wait for the newer loads too).
+    // skipped steps lets the compiler see when each register set was loaded.
     int st0 = 0;
     for (; st0 + kBufs <= nsteps; st0 += kBufs) {
 #pragma unroll
