@@ -22,7 +22,7 @@
 //   - the B fragment of plane m is the codeword itself: lane l of a K-block needs the 8 values of
 //     one group of one row, i.e. C_m[code], gathered from codebooks replicated in LDS.
 // Each lane keeps fp64 sums of R_k^2 over its outputs; each workgroup writes its sums and a
-// second kernel adds them in workgroup order, so the result does not depend on scheduling.
+// second kernel adds them in a fixed order, so the result does not depend on scheduling.
 #include "device.h"
 #include "launch.h"
 
@@ -250,14 +250,22 @@ void distortion_kernel(DistArgs a) {
   if (tid < M) a.partials[(size_t)blockIdx.x * 8 + tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
 }
 
-// D[m] = (sum of the workgroup sums, in workgroup order) / (d_out n).
-__global__ void distortion_reduce_kernel(const double* partials, int grid, int M, double inv, double* D) {
-  const int m = threadIdx.x;
-  if (m < M) {
-    double s = 0.0;
-    for (int b = 0; b < grid; ++b) s += partials[(size_t)b * 8 + m];
-    D[m] = s * inv;
+// D[m] = (sum of the workgroup sums) / (d_out n): thread b loads workgroup b's sums, then a tree
+// with a fixed pairing (b + half into b) adds them, so the result does not depend on scheduling.
+__global__ __launch_bounds__(dist::kMaxGrid) void distortion_reduce_kernel(const double* partials, int grid, int M,
+                                                                          double inv, double* D) {
+  __shared__ double s[8][dist::kMaxGrid];
+  const int b = threadIdx.x;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) s[m][b] = (b < grid && m < M) ? partials[(size_t)b * 8 + m] : 0.0;
+  __syncthreads();
+  for (int half = dist::kMaxGrid / 2; half >= 1; half >>= 1) {
+    if (b < half)
+#pragma unroll
+      for (int m = 0; m < 8; ++m) s[m][b] += s[m][b + half];
+    __syncthreads();
   }
+  if (b < M) D[b] = s[b][0] * inv;
 }
 
 template <int M>
@@ -298,7 +306,7 @@ hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n
     default: e = launch_dist_m<8>(a, st, &grid); break;
   }
   if (e != hipSuccess) return e;
-  distortion_reduce_kernel<<<1, 64, 0, st>>>(a.partials, grid, L.d.num_codebooks,
+  distortion_reduce_kernel<<<1, dist::kMaxGrid, 0, st>>>(a.partials, grid, L.d.num_codebooks,
                                              1.0 / ((double)L.d.d_out * (double)n), D);
   return hipGetLastError();
 }
