@@ -136,3 +136,58 @@ def beam_search_codes(W, codebooks, scales, k: int, beam: int):
             codes[:, i, j] = kept[0]
             total += float(_group_errors(w, codebooks, scales[i], kept)[0])
     return codes, total
+
+
+def beam_search_codes_f32(W, codebooks, scales, k: int, beam: int, groups=None):
+    """Beam search of App. C (code optimisation) with every comparison decided in binary32.
+
+    The paper fixes no precision for the search. Reading: the candidate errors are evaluated
+    in binary32 in one stated order, the order the GPU search uses, so that both sides take
+    the same decisions. Inputs are fp16-representable values (weights, codewords, scales).
+
+    Per group (row i, group j), with s = s_i and S_m[c][t] = s * C_m[c][t] (a product of two
+    fp16 values, exact in binary32) and the residual r = w (the group's g weights):
+      stage m = 0..k-1 extends every kept entry (tuple, r) by every codeword c of codebook m:
+          d_t = fl32(r_t - S_m[c][t]),
+          e   = fl32(...fl32(fl32(d_0 * d_0) + fl32(d_1 * d_1)) ... + fl32(d_{g-1} * d_{g-1}))
+                (added left to right, no fused multiply-add);
+      and keeps the `beam` candidates with the smallest e, equal e ordered by the tuple
+      (lexicographically); a kept candidate's residual is its d. The last stage keeps one.
+    Stage 0 starts from the single empty tuple, so it ranks the 2^B codewords of codebook 0.
+
+    Returns (codes [k][d_out][d_in/g] int64, errors [d_out][d_in/g] float32: e of the kept
+    tuple). With `groups` (an iterable of (i, j)) only those groups are searched; the others
+    keep code 0 and error NaN.
+    """
+    f32 = np.float32
+    W32 = np.asarray(W, dtype=np.float64).astype(f32)
+    C32 = np.asarray(codebooks, dtype=np.float64).astype(f32)
+    s32 = np.asarray(scales, dtype=np.float64).astype(f32)
+    n_cw, g = C32.shape[1], C32.shape[2]
+    d_out, d_in = W32.shape
+    G = d_in // g
+    codes = np.zeros((k, d_out, G), dtype=np.int64)
+    errors = np.full((d_out, G), np.nan, dtype=f32)
+    if groups is None:
+        groups = [(i, j) for i in range(d_out) for j in range(G)]
+    for (i, j) in groups:
+        S = [s32[i] * C32[m] for m in range(k)]                   # exact products
+        kept = [((), W32[i, j * g:(j + 1) * g])]                  # (tuple, residual)
+        for m in range(k):
+            tuples, resid, errs = [], [], []
+            for tup, r in kept:
+                D = r[None, :] - S[m]                             # [n_cw][g], binary32
+                e = D[:, 0] * D[:, 0]
+                for t in range(1, g):
+                    e = e + D[:, t] * D[:, t]                     # binary32, left to right
+                for c in range(n_cw):
+                    tuples.append(tup + (c,))
+                    resid.append(D[c])
+                    errs.append(e[c])
+            order = sorted(range(len(tuples)), key=lambda q: (errs[q], tuples[q]))
+            n_keep = beam if m < k - 1 else 1
+            kept = [(tuples[q], resid[q]) for q in order[:n_keep]]
+            best_err = errs[order[0]]
+        codes[:, i, j] = kept[0][0]
+        errors[i, j] = best_err
+    return codes, errors

@@ -86,3 +86,80 @@ def test_brute_force_is_optimal_and_consistent(k, nb, g):
     full_codes, full = oracle.beam_search_codes(W, C, s, k, beam=nb ** (k - 1))
     assert abs(full - err) <= 1e-12 * max(1.0, err)
     assert np.array_equal(full_codes, codes)      # same tie-break: lexicographically smallest
+
+
+# ---- beam search with decisions in binary32 (the reference of the GPU search) ----
+
+def _int_case(rng, M, nb, g, d_out, G):
+    C = rng.integers(-4, 5, size=(M, nb, g)).astype(np.float64)
+    s = rng.choice(np.array([0.5, 1.0, 2.0]), size=d_out)
+    W = rng.integers(-16, 17, size=(d_out, G * g)).astype(np.float64)
+    return C, s, W
+
+
+@pytest.mark.parametrize("k,nb,beam", [(1, 16, 4), (2, 16, 1), (2, 16, 3), (3, 8, 4), (3, 8, 64), (4, 4, 2)])
+def test_f32_beam_equals_exact_beam_on_integer_data(k, nb, beam):
+    """On integer-valued inputs every binary32 operation of the search is exact, so its decisions
+    are those of the fp64 search (itself pinned against exhaustive search below)."""
+    rng = np.random.default_rng(100 + 10 * k + beam)
+    C, s, W = _int_case(rng, 4, nb, 4, 5, 6)
+    c32, e32 = oracle.beam_search_codes_f32(W, C, s, k, beam)
+    c64, t64 = oracle.beam_search_codes(W, C, s, k, beam)
+    assert np.array_equal(c32, c64)
+    assert float(e32.astype(np.float64).sum()) == t64
+
+
+def test_f32_full_beam_is_exhaustive_on_integer_data():
+    rng = np.random.default_rng(7)
+    C, s, W = _int_case(rng, 3, 8, 4, 4, 5)
+    codes, best = oracle.brute_force_codes(W, C, s, 3)
+    c32, e32 = oracle.beam_search_codes_f32(W, C, s, 3, beam=8 * 8)
+    assert np.array_equal(c32, codes)
+    assert float(e32.astype(np.float64).sum()) == best
+
+
+def test_f32_beam_recovers_signed_digit_codes():
+    """Codebook m holds the codewords (d * 16^(2-m)) * (1, ..., 1) with signed digits d in [-7, 8];
+    a weight group built from one codeword per codebook is recovered exactly by any beam, greedy
+    included (every stage's nearest codeword is the true digit), with error 0."""
+    rng = np.random.default_rng(8)
+    g, k = 8, 3
+    digits = np.arange(-7, 9, dtype=np.float64)                       # 16 codewords
+    C = np.stack([np.repeat((digits * 16.0 ** (k - 1 - m))[:, None], g, axis=1) for m in range(k)])
+    true = rng.integers(0, 16, size=(k, 3, 4))
+    s = np.array([1.0, 0.5, 0.25])
+    W = oracle.reconstruct(true, C, s, k)
+    for beam in (1, 2, 5):
+        c32, e32 = oracle.beam_search_codes_f32(W, C, s, k, beam)
+        assert np.array_equal(c32, true)
+        assert np.all(e32 == 0)
+
+
+def test_f32_beam_reported_error_reevaluates():
+    """On Gaussian data the reported binary32 error is the squared error of the returned codes'
+    reconstruction, up to binary32 rounding of the residual chain and of the sum."""
+    rng = np.random.default_rng(9)
+    f16 = lambda a: a.astype(np.float16).astype(np.float64)
+    C = f16(rng.normal(0, 0.02, size=(3, 32, 8)))
+    s = f16(rng.uniform(0.5, 1.5, size=6))
+    W = f16(rng.normal(0, 0.02, size=(6, 40)))
+    codes, e32 = oracle.beam_search_codes_f32(W, C, s, 3, beam=4)
+    R = W - oracle.reconstruct(codes, C, s, 3)
+    e64 = (R.reshape(6, 5, 8) ** 2).sum(axis=2)
+    u = 2.0 ** -24
+    # each d carries at most k roundings relative to |r| + |s c| terms; the sum g more
+    mag = (np.abs(W) + np.abs(oracle.reconstruct(codes, C, s, 3))).reshape(6, 5, 8)
+    bound = 2 * (3 + 1) * u * (np.sqrt(e64) * np.sqrt((mag ** 2).sum(axis=2))) * 2 + 10 * u * e64
+    assert np.all(np.abs(e32.astype(np.float64) - e64) <= bound + 1e-30)
+
+
+def test_f32_beam_groups_subset():
+    """Searching a subset of groups gives the same results for those groups."""
+    rng = np.random.default_rng(10)
+    C, s, W = _int_case(rng, 2, 16, 4, 3, 4)
+    full_c, full_e = oracle.beam_search_codes_f32(W, C, s, 2, 3)
+    sub = [(0, 1), (2, 3)]
+    c, e = oracle.beam_search_codes_f32(W, C, s, 2, 3, groups=sub)
+    for (i, j) in sub:
+        assert np.array_equal(c[:, i, j], full_c[:, i, j]) and e[i, j] == full_e[i, j]
+    assert np.isnan(e[1, 0])
