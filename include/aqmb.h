@@ -164,6 +164,35 @@ aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype,
 aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* Xt,
                                    aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream);
 
+/* Widest beam accepted by aqmb_beam_search. */
+#define AQMB_MAX_BEAM 16
+
+/*
+ * Code search (Appendix C, code optimisation: a beam search over combinations of codewords that
+ * minimise the quantization error; Algorithm 1 updates the assignments b this way): for every
+ * group (row i, group j) of a dense weight matrix, beam search over codebooks 0..k-1 for the
+ * codes c_0..c_{k-1} that minimise the group's squared error ||w_ij - s_i sum_m C_m[c_m]||^2.
+ * Stage m extends each kept partial tuple by every codeword of codebook m and keeps the `beam`
+ * best; the last stage keeps the best one (beam 1 is greedy residual coding). Groups are
+ * independent (the plain squared error of the weights, X = I in the weighted MSE of §2.2).
+ * Every comparison is decided in binary32 in this order: S_m[c][t] = s_i * C_m[c][t] (exact for
+ * fp16 operands); the residual of a kept tuple is w - S_0[c_0] - ... with each subtraction
+ * rounded; a candidate's d_t = fl(r_t - S_m[c][t]) and e = d_0 d_0 + d_1 d_1 + ... + d_7 d_7
+ * with every product and every sum rounded, left to right, no fused multiply-add; candidates are
+ * ordered by e, equal e by the code tuple (lexicographically).
+ *   desc       the layer shape: d_out, d_in, g = 8, M codebooks, B = 8
+ *   W          [d_out][d_in] fp16 (device, 16-byte aligned): the weights to encode
+ *   codebooks  [M][256][8] fp16 (device, 16-byte aligned); codebooks 0..k-1 are used
+ *   scales     [d_out] fp16 (device)
+ *   codes      [k][d_out][d_in/8] uint8 (device, output): plane-major, the layout aqmb_create takes
+ *   errors     [d_out][d_in/8] float (device, output; may be NULL): e of the chosen tuple
+ * 1 <= k <= M, 1 <= beam <= AQMB_MAX_BEAM. Work: 256 (1 + (k - 1) beam) candidates per group.
+ * Errors: EINVAL (null pointer, misaligned W or codebooks, k outside [1, M], beam < 1),
+ * EUNSUPPORTED (B = 16, beam > AQMB_MAX_BEAM), EHIP.
+ */
+aqmb_status aqmb_beam_search(const aqmb_desc* desc, int k, int beam, const void* W, const uint16_t* codebooks,
+                             const uint16_t* scales, uint8_t* codes, float* errors, aqmb_stream_t stream);
+
 /*
  * Average storage bits per weight at level k (appendix C, Eq. avg_bits): codebooks
  * 16*g*k*2^B bits, codes d_out*(d_in/g)*B bits per used plane, scales 16*d_out bits,
@@ -180,8 +209,9 @@ const char* aqmb_strerror(aqmb_status status);
 const char* aqmb_last_error(void);
 
 /* Validate arguments exactly as the entry points do, without touching the GPU.
- * op: 0 = gemv, 1 = gemm, 2 = dequant, 3 = prefix distortion. For gemv `n` is the batch, for
- * gemm the token count, for the distortion the number of inputs, ignored for dequant;
+ * op: 0 = gemv, 1 = gemm, 2 = dequant, 3 = prefix distortion, 4 = beam search. For gemv `n` is
+ * the batch, for gemm the token count, for the distortion the number of inputs, for the beam
+ * search the beam width (in = W, out = codes, dtypes ignored), ignored for dequant;
  * `in_dtype` is x's dtype (gemv) or Xt's (distortion), `out_dtype` the output dtype or, for
  * the distortion, W's dtype; `in`/`out` are x/y, X/Y, -/W, or Xt/D. `k` is not checked for
  * the distortion. Returns the status the entry point would return before launching anything

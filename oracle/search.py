@@ -174,20 +174,28 @@ def beam_search_codes_f32(W, codebooks, scales, k: int, beam: int, groups=None):
         S = [s32[i] * C32[m] for m in range(k)]                   # exact products
         kept = [((), W32[i, j * g:(j + 1) * g])]                  # (tuple, residual)
         for m in range(k):
-            tuples, resid, errs = [], [], []
-            for tup, r in kept:
+            # the kept tuples' ranks in lexicographic order: (parent rank, c) orders the
+            # extended tuples lexicographically
+            lex = {tup: q for q, tup in enumerate(sorted(tup for tup, _ in kept))}
+            E, parent, cw = [], [], []
+            for p, (tup, r) in enumerate(kept):
                 D = r[None, :] - S[m]                             # [n_cw][g], binary32
                 e = D[:, 0] * D[:, 0]
                 for t in range(1, g):
                     e = e + D[:, t] * D[:, t]                     # binary32, left to right
-                for c in range(n_cw):
-                    tuples.append(tup + (c,))
-                    resid.append(D[c])
-                    errs.append(e[c])
-            order = sorted(range(len(tuples)), key=lambda q: (errs[q], tuples[q]))
+                E.append(e)
+                parent.append(np.full(n_cw, p))
+                cw.append(np.arange(n_cw))
+            E, parent, cw = np.concatenate(E), np.concatenate(parent), np.concatenate(cw)
+            prank = np.array([lex[kept[p][0]] for p in parent])
+            order = np.lexsort((cw, prank, E))                    # by e, then the tuple
             n_keep = beam if m < k - 1 else 1
-            kept = [(tuples[q], resid[q]) for q in order[:n_keep]]
-            best_err = errs[order[0]]
+            new = []
+            for q in order[:n_keep]:
+                tup, r = kept[parent[q]]
+                new.append((tup + (int(cw[q]),), r - S[m][cw[q]]))  # the candidate's d
+            kept = new
+            best_err = E[order[0]]
         codes[:, i, j] = kept[0][0]
         errors[i, j] = best_err
     return codes, errors

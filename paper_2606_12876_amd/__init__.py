@@ -65,6 +65,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_gemm.argtypes = [vp, i32, vp, i32, vp, i32, vp]
     L.aqmb_dequant.argtypes = [vp, i32, vp, i32, vp]
     L.aqmb_prefix_distortion.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
+    L.aqmb_beam_search.argtypes = [ctypes.POINTER(Desc), i32, i32, vp, vp, vp, vp, vp, vp]
     L.aqmb_validate.argtypes = [ctypes.POINTER(Desc), i32, i32, i32, i32, i32, vp, vp]
     L.aqmb_bits_per_weight.argtypes = [ctypes.POINTER(Desc), i32]
     L.aqmb_bits_per_weight.restype = ctypes.c_double
@@ -73,7 +74,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_last_error.argtypes = []
     L.aqmb_last_error.restype = ctypes.c_char_p
     for f in ("aqmb_create", "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_multi", "aqmb_gemm",
-              "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_validate"):
+              "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_beam_search", "aqmb_validate"):
         getattr(L, f).restype = st
     return L
 
@@ -227,6 +228,24 @@ def prefix_distortion(layer: int, W, w_dtype, Xt, x_dtype, n: int, D, stream=Non
         raise AqmbError(Status.EINVAL, "aqmb_prefix_distortion", f"D holds {nd} bytes, needs {8 * d.num_codebooks}")
     _check(lib.aqmb_prefix_distortion(layer, _ptr(W), int(w_dtype), _ptr(Xt), int(x_dtype), n, _ptr(D),
                                       _stream(stream)), "aqmb_prefix_distortion")
+
+
+MAX_BEAM = 16
+
+
+def beam_search(desc: Desc, k: int, beam: int, W, codebooks, scales, codes, errors=None, stream=None) -> None:
+    """aqmb_beam_search: codes [k][d_out][d_in/8] uint8 (and errors [d_out][d_in/8] float32 if given)
+    from a beam search over codebooks 0..k-1 for every group of W [d_out][d_in] fp16."""
+    G = desc.d_in // max(desc.group_size, 1)
+    _need(W, desc.d_out * desc.d_in, DType.F16, "W", "aqmb_beam_search")
+    nc = _nbytes(codes)
+    if nc is not None and 1 <= k and nc < k * desc.d_out * G:
+        raise AqmbError(Status.EINVAL, "aqmb_beam_search", f"codes holds {nc} bytes, needs {k * desc.d_out * G}")
+    ne = _nbytes(errors) if errors is not None else None
+    if ne is not None and ne < 4 * desc.d_out * G:
+        raise AqmbError(Status.EINVAL, "aqmb_beam_search", f"errors holds {ne} bytes, needs {4 * desc.d_out * G}")
+    _check(lib.aqmb_beam_search(ctypes.byref(desc), k, beam, _ptr(W), _ptr(codebooks), _ptr(scales), _ptr(codes),
+                                _ptr(errors) if errors is not None else None, _stream(stream)), "aqmb_beam_search")
 
 
 def bits_per_weight(desc: Desc, k: int) -> float:

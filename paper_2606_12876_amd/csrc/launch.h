@@ -18,6 +18,9 @@ hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x
 // X [n][d_in]; uses the layer's workspace after its first KiB.
 hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n, double* D, hipStream_t st);
 size_t distortion_workspace_floats();
+// Beam search of codes for every group of W [d_out][d_in] fp16 over codebooks 0..k-1 (8-bit).
+hipError_t launch_beam_search(const aqmb_desc& d, int k, int beam_width, const void* W, const uint16_t* codebooks,
+                              const uint16_t* scales, unsigned char* codes, float* errors, hipStream_t st);
 hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
                        hipStream_t st);
 

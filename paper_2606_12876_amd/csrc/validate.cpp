@@ -48,6 +48,16 @@ aqmb_status validate_call(const aqmb_desc* d, int op, int k, int n, aqmb_dtype i
   if (s != AQMB_OK) return s;
   if (op != 3 && (k < 1 || k > d->num_codebooks))   // the distortion covers every k at once
     return fail(AQMB_EINVAL, "k = %d outside [1, M = %d]", k, d->num_codebooks);
+  if (op == 4) {  // beam search: n = beam width, in = W, out = codes
+    if (!in || !out) return fail(AQMB_EINVAL, "beam_search: W or codes is NULL");
+    if (n < 1) return fail(AQMB_EINVAL, "beam_search: beam = %d must be >= 1", n);
+    if (n > AQMB_MAX_BEAM) return fail(AQMB_EUNSUPPORTED, "beam_search: beam = %d above %d", n, AQMB_MAX_BEAM);
+    if (d->code_bits != 8) return fail(AQMB_EUNSUPPORTED, "beam_search: only B = 8 codebooks are supported");
+    if ((uintptr_t)in % 16) return fail(AQMB_EINVAL, "beam_search: W must be 16-byte aligned");
+    const uint64_t chunks = ((uint64_t)(d->d_in / d->group_size) + 255) / 256;
+    if (chunks * (uint64_t)d->d_out >= (1ull << 31)) return fail(AQMB_EINVAL, "beam_search: matrix too large");
+    return AQMB_OK;
+  }
   if (!valid_dtype(out_dt)) return fail(AQMB_EUNSUPPORTED, "output dtype %d is not F16, BF16 or F32", (int)out_dt);
   switch (op) {
     case 0:  // gemv

@@ -74,7 +74,15 @@ def test_descriptor_validation(case, expect):
     (1, 2, 7, 1, 0, 16, 32, A.Status.EUNSUPPORTED),  # gemm output must be bf16/f32
     (2, 3, 0, 0, 2, None, 32, A.Status.OK),
     (2, 3, 0, 0, 2, None, None, A.Status.EINVAL),
-    (4, 1, 1, 0, 0, 16, 32, A.Status.EINVAL),       # unknown op
+    (5, 1, 1, 0, 0, 16, 32, A.Status.EINVAL),       # unknown op
+    (4, 4, 8, 0, 0, 16, 32, A.Status.OK),           # beam search: n = beam
+    (4, 4, 16, 0, 0, 16, 7, A.Status.OK),           # codes need no alignment
+    (4, 5, 8, 0, 0, 16, 32, A.Status.EINVAL),       # k > M
+    (4, 1, 0, 0, 0, 16, 32, A.Status.EINVAL),       # beam < 1
+    (4, 1, 17, 0, 0, 16, 32, A.Status.EUNSUPPORTED),  # beam > 16
+    (4, 1, 8, 0, 0, None, 32, A.Status.EINVAL),
+    (4, 1, 8, 0, 0, 16, None, A.Status.EINVAL),
+    (4, 1, 8, 0, 0, 24, 32, A.Status.EINVAL),       # W misaligned
     (3, 0, 4096, 0, 0, 16, 32, A.Status.OK),        # distortion: k is not checked
     (3, 9, 1, 0, 0, 16, 8, A.Status.OK),            # D needs 8-byte alignment only
     (3, 1, 0, 0, 0, 16, 32, A.Status.EINVAL),       # n < 1
@@ -96,6 +104,7 @@ def test_gemm_rejects_16bit_codes():
     assert A.validate(d, 1, 1, 8, A.DType.BF16, A.DType.BF16, 16, 32) == A.Status.EUNSUPPORTED
     assert A.validate(d, 0, 2, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.OK
     assert A.validate(d, 3, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EUNSUPPORTED
+    assert A.validate(d, 4, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EUNSUPPORTED
 
 
 def test_bits_per_weight_matches_oracle():
@@ -116,6 +125,7 @@ def test_bad_handles_rejected_without_gpu():
     assert A.lib.aqmb_dequant(bogus, 1, 32, 0, None) == A.Status.EINVAL
     assert A.lib.aqmb_prefix_distortion(bogus, 16, 0, 32, 0, 8, 64, None) == A.Status.EINVAL
     assert "live" in A.last_error()
+    assert A.lib.aqmb_beam_search(None, 1, 1, 16, 16, 16, 16, None, None) == A.Status.EINVAL   # null desc
     d = A.Desc()
     assert A.lib.aqmb_get_desc(bogus, ctypes.byref(d)) == A.Status.EINVAL
     h = ctypes.c_void_p(0x1234)
