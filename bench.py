@@ -9,6 +9,7 @@ exceeds the 256 MB Infinity Cache and every launch streams its codes from HBM):
                    prefill GEMM, 2048 bf16 tokens          (4096 x 4096 layer, bf16 out)
   once:            prefix distortions D^(1..4) of the decode layer against a dense fp16 W
                    over 4096 fp16 calibration inputs
+                   beam search (k = 4, beam 8) of codes for every group of that W
 
 Each (operation, k, batch) runs as a burst of R launches captured in a HIP graph and timed
 with HIP events on the launch stream; the per-launch time is burst time / R.
@@ -17,7 +18,9 @@ with HIP events on the launch stream; the per-launch time is burst time / R.
 codebooks, scales, x and y) over all GEMV launches of the timed steps. `roofline` describes the
 GEMV kernel at batch 1, k = 4 (HBM-bound); `roofline_gemm` the prefill GEMM at k = 4
 (MFMA-bound); `roofline_distortion` the distortion evaluator (fp16 MFMA-bound, algorithmic
-flops 2 (M + 1) d_out d_in n: W X and one product per code plane). The CPU baseline is the fp64
+flops 2 (M + 1) d_out d_in n: W X and one product per code plane); `roofline_beam` the code search
+(ALU-bound: 23 binary32 operations per candidate, against the chip's non-packed, non-fused fp32
+rate 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3 Tops/s). The CPU baseline is the fp64
 oracle timed on a bounded sample.
 
 Prints one JSON line on stdout; progress goes to stderr.
@@ -38,6 +41,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
 F16_PEAK_TFLOPS = 2500.0        # MI355X dense fp16 MFMA
+FP32_PLAIN_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # one non-packed fp32 op per lane and clock
+BEAM_K, BEAM_WIDTH = 4, 8
 
 
 def log(*a):
@@ -154,6 +159,10 @@ def main():
     Xd = to_dev(make_activations(base, n_cal, "f16")).view(torch.float16)
     D_COPIES = 4
     Ds = [torch.empty((M,), dtype=torch.float64, device=dev) for _ in range(D_COPIES)]
+    G_groups = d_in // 8
+    beam_codes = torch.empty((BEAM_K, d_out, G_groups), dtype=torch.uint8, device=dev)
+    beam_errs = torch.empty((d_out, G_groups), dtype=torch.float32, device=dev)
+    cb_dev, sc_dev = to_dev(base.codebooks), to_dev(base.scales)
     torch.cuda.synchronize()
 
     ks = list(spec.ks)
@@ -184,7 +193,11 @@ def main():
         for r in range(D_COPIES):
             A.prefix_distortion(layers[r], Wd, A.DType.F16, Xd, A.DType.F16, n_cal, Ds[r])
 
-    ops = [("distortion", M, n_cal, distortion_burst, D_COPIES)]  # (name, k, b, fn, launches)
+    def beam_burst():
+        A.beam_search(desc, BEAM_K, BEAM_WIDTH, Wd, cb_dev, sc_dev, beam_codes, beam_errs)
+
+    ops = [("distortion", M, n_cal, distortion_burst, D_COPIES),   # (name, k, b, fn, launches)
+           ("beam", BEAM_K, BEAM_WIDTH, beam_burst, 1)]
     for k in ks:
         ops.append(("gemv", k, 1, lambda k=k: gemv_burst(k, 1), R))
         ops.append(("gemv", k, 4, lambda k=k: gemv_burst(k, 4), R))
@@ -331,7 +344,16 @@ def main():
                                   "us_per_launch": round(td, 2),
                                   "workload": f"D^(1..{M}) of a {d_out}x{d_in} layer, dense fp16 W, "
                                               f"{n_cal} fp16 calibration inputs"}
-    step_us = {n: 0.0 for n in ("gemv", "gemv_multi", "dequant", "gemm", "distortion")}
+    tb = per_launch_us[("beam", BEAM_K, BEAM_WIDTH)]
+    cands = d_out * G_groups * 256 * (1 + (BEAM_K - 1) * BEAM_WIDTH)
+    achb = cands * 23 / (tb * 1e-6) / 1e12
+    out["roofline_beam"] = {"bound": "alu", "kernel": f"beam_kernel<{BEAM_WIDTH}> (k={BEAM_K})", "achieved": round(achb, 2),
+                            "peak": round(FP32_PLAIN_PEAK_TOPS, 2), "unit": "TFLOP/s",
+                            "frac": round(achb / FP32_PLAIN_PEAK_TOPS, 4), "traffic": None,
+                            "us_per_launch": round(tb, 1), "candidates_per_s": round(cands / (tb * 1e-6), 1),
+                            "workload": f"codes for the {d_out * G_groups} groups of a {d_out}x{d_in} fp16 W, "
+                                        f"k={BEAM_K} codebooks of 256, beam {BEAM_WIDTH}"}
+    step_us = {n: 0.0 for n in ("gemv", "gemv_multi", "dequant", "gemm", "distortion", "beam")}
     for i, (name, k, b, fn, n) in enumerate(ops):
         step_us["gemv_multi" if name.startswith("gemv_multi") else name] += per_op_ms[i] * 1e3 / args.steps
     tot = sum(step_us.values())
