@@ -67,9 +67,8 @@ aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* co
   L->d = *desc;
   hipError_t e = hipGetDevice(&L->device);
   if (e != hipSuccess) { free_layer(L); return hip_fail(e, "create: hipGetDevice"); }
-  const int code_size = desc->code_bits == 8 ? 1 : 2;
   L->G = desc->d_in / desc->group_size;
-  L->J = kSliceBytes / code_size;
+  L->J = kSliceBytes * 8 / desc->code_bits;     // groups per 16-byte slice: 32, 16 or 8
   L->S = (L->G + L->J - 1) / L->J;
   L->plane_bytes = (size_t)L->S * desc->d_out * kSliceBytes;
   const size_t n_codewords = (size_t)1 << desc->code_bits;
@@ -97,9 +96,21 @@ aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* co
   if ((e = hipMemsetAsync(L->ws, 0, L->ws_floats * sizeof(float), st)) != hipSuccess ||
       (e = hipMemcpyAsync(L->codebooks, codebooks, cb_bytes, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
       (e = hipMemcpyAsync(L->scales, scales, (size_t)desc->d_out * 2, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
-      (e = launch_retile(*L, codes, st)) != hipSuccess || (e = hipStreamSynchronize(st)) != hipSuccess) {
+      (e = launch_retile(*L, codes, (int*)(L->ws + 256), st)) != hipSuccess ||
+      (e = hipStreamSynchronize(st)) != hipSuccess) {
     free_layer(L);
     return hip_fail(e, "create: upload");
+  }
+  if (desc->code_bits == 4) {  // the re-tiling flags 4-bit codes above 15 in the workspace
+    int bad = 0;
+    if ((e = hipMemcpy(&bad, L->ws + 256, sizeof(int), hipMemcpyDeviceToHost)) != hipSuccess) {
+      free_layer(L);
+      return hip_fail(e, "create: code check");
+    }
+    if (bad) {
+      free_layer(L);
+      return fail(AQMB_EINVAL, "create: a 4-bit code is above 15");
+    }
   }
   {
     std::lock_guard<std::mutex> lk(g_mu);
@@ -144,7 +155,8 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
   aqmb_status s = validate_call(&L->d, 0, k, batch, x_dtype, y_dtype, x, y);
   if (s != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
-  hipError_t e = launch_gemv(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream);
+  hipError_t e = L->d.code_bits == 4 ? launch_gemv_b4(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream)
+                                     : launch_gemv(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv: launch");
 }
 
@@ -166,7 +178,16 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
   }
   aqmb_status s = check_device((Layer*)Ls[0]);
   if (s != AQMB_OK) return s;
-  hipError_t e = launch_gemv_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
+  bool any4 = false;
+  for (int i = 0; i < n_layers; ++i) any4 = any4 || Ls[i]->d.code_bits == 4;
+  hipError_t e = hipSuccess;
+  if (any4) {  // layers with 4-bit codes have their own kernel: one launch per layer
+    for (int i = 0; i < n_layers && e == hipSuccess; ++i)
+      e = Ls[i]->d.code_bits == 4 ? launch_gemv_b4(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, (hipStream_t)stream)
+                                  : launch_gemv(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, (hipStream_t)stream);
+  } else {
+    e = launch_gemv_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
+  }
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv_multi: launch");
 }
 

@@ -6,23 +6,39 @@
 
 namespace aqmb {
 
-// [M][d_out][G] plane-major codes (1 or 2 bytes each) -> [M][S][d_out][16 bytes].
-template <int CS>
+// [M][d_out][G] plane-major codes -> [M][S][d_out][16 bytes]. CB = code bits: 16-bit codes are
+// 2 bytes each, 8-bit and 4-bit codes 1 byte each in the input; a slice holds J = 128 / CB
+// consecutive groups of one row, 4-bit codes packed two to a byte (group 2b in the low nibble of
+// byte b, group 2b + 1 in the high nibble). A 4-bit code above 15 sets *bad (the layer is refused).
+template <int CB>
 __global__ __launch_bounds__(256) void retile_kernel(const unsigned char* __restrict__ in, unsigned char* __restrict__ out,
-                                                     int M, int d_out, int G, int S) {
-  constexpr int J = 16 / CS;
+                                                     int M, int d_out, int G, int S, int* bad) {
+  constexpr int J = 128 / CB, CS = CB == 16 ? 2 : 1;
   const size_t total = (size_t)M * S * d_out;
   for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
     const int i = (int)(q % d_out);
     const size_t ms = q / d_out;
     const int s = (int)(ms % S), m = (int)(ms / S);
     unsigned char chunk[16];
+    if constexpr (CB == 4) {
+      unsigned high = 0;
 #pragma unroll
-    for (int jj = 0; jj < J; ++jj) {
-      const int j = s * J + jj;
+      for (int b = 0; b < 16; ++b) {
+        const int j0 = s * J + 2 * b, j1 = j0 + 1;
+        const unsigned c0 = j0 < G ? in[((size_t)m * d_out + i) * G + j0] : 0u;
+        const unsigned c1 = j1 < G ? in[((size_t)m * d_out + i) * G + j1] : 0u;
+        high |= (c0 | c1) >> 4;
+        chunk[b] = (unsigned char)((c0 & 15u) | ((c1 & 15u) << 4));
+      }
+      if (high) *bad = 1;
+    } else {
 #pragma unroll
-      for (int b = 0; b < CS; ++b)
-        chunk[jj * CS + b] = j < G ? in[(((size_t)m * d_out + i) * G + j) * CS + b] : (unsigned char)0;
+      for (int jj = 0; jj < J; ++jj) {
+        const int j = s * J + jj;
+#pragma unroll
+        for (int b = 0; b < CS; ++b)
+          chunk[jj * CS + b] = j < G ? in[(((size_t)m * d_out + i) * G + j) * CS + b] : (unsigned char)0;
+      }
     }
     uint4 v;
     __builtin_memcpy(&v, chunk, 16);
@@ -30,13 +46,16 @@ __global__ __launch_bounds__(256) void retile_kernel(const unsigned char* __rest
   }
 }
 
-hipError_t launch_retile(const Layer& L, const void* codes, hipStream_t st) {
+hipError_t launch_retile(const Layer& L, const void* codes, int* bad, hipStream_t st) {
   const size_t total = (size_t)L.d.num_codebooks * L.S * L.d.d_out;
   const unsigned grid = (unsigned)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
+  const auto* in = (const unsigned char*)codes;
   if (L.d.code_bits == 8)
-    retile_kernel<1><<<grid, 256, 0, st>>>((const unsigned char*)codes, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S);
+    retile_kernel<8><<<grid, 256, 0, st>>>(in, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S, bad);
+  else if (L.d.code_bits == 4)
+    retile_kernel<4><<<grid, 256, 0, st>>>(in, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S, bad);
   else
-    retile_kernel<2><<<grid, 256, 0, st>>>((const unsigned char*)codes, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S);
+    retile_kernel<16><<<grid, 256, 0, st>>>(in, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S, bad);
   return hipGetLastError();
 }
 
@@ -73,19 +92,20 @@ __device__ __forceinline__ void fold_codeword(float (&acc)[8], uint4 cw, bool fi
   for (int t = 0; t < 8; ++t) acc[t] = first ? v[t] : acc[t] + v[t];
 }
 
-// Used for 16-bit codes (and as the general fallback). One thread per group: the J lanes of a (row, slice) pair take its J groups, so a wave writes
-// whole row segments (J groups x 8 values) and the lanes of one row share one 16-byte code
-// chunk per plane (a single cache line). 256-entry codebooks are staged in LDS; 65536-entry
+// Used for 16-bit and 4-bit codes (and as the general fallback). CB = code bits. One thread per
+// group: the J = 128 / CB lanes of a (row, slice) pair take its J groups, so a wave writes whole
+// row segments (J groups x 8 values) and the lanes of one row share one 16-byte code chunk per
+// plane (a single cache line). 16- and 256-entry codebooks are staged in LDS; 65536-entry
 // codebooks are read through the caches.
-template <int OUT, int CS>
+template <int OUT, int CB>
 __global__ __launch_bounds__(256) void dequant_kernel(const unsigned char* __restrict__ codes,
                                                       const uint16_t* __restrict__ codebooks,
                                                       const uint16_t* __restrict__ scales, void* __restrict__ W,
                                                       int d_out, int d_in, int G, int S, int k, size_t plane_bytes) {
-  constexpr int J = 16 / CS;
-  extern __shared__ uint4 cb_lds[];  // [k][256] codewords (B = 8 only)
-  if constexpr (CS == 1) {
-    for (int q = threadIdx.x; q < k * 256; q += blockDim.x) cb_lds[q] = ((const uint4*)codebooks)[q];
+  constexpr int J = 128 / CB, PER_WORD = 32 / CB;
+  extern __shared__ uint4 cb_lds[];  // [k][2^CB] codewords (CB <= 8)
+  if constexpr (CB <= 8) {
+    for (int q = threadIdx.x; q < (k << CB); q += blockDim.x) cb_lds[q] = ((const uint4*)codebooks)[q];
     __syncthreads();
   }
   // Each thread takes U groups per pass and issues all their code loads before using any.
@@ -103,7 +123,7 @@ __global__ __launch_bounds__(256) void dequant_kernel(const unsigned char* __res
       row[u] = (int)(pair % d_out);
       const int s = (int)(pair / d_out);
       grp[u] = (t < n) ? s * J + jj : G;
-      const size_t chunk = pair * 16 + (size_t)(jj * CS / 4) * 4;  // the code word holding this group
+      const size_t chunk = pair * 16 + (size_t)(jj / PER_WORD) * 4;  // the code word holding this group
 #pragma unroll
       for (int m = 0; m < 8; ++m) {
         words[u][m] = 0;
@@ -119,10 +139,11 @@ __global__ __launch_bounds__(256) void dequant_kernel(const unsigned char* __res
       for (int m = 0; m < 8; ++m) {
         if (m < k) {
           uint4 cw;
-          if constexpr (CS == 1) {
-            cw = cb_lds[m * 256 + ((words[u][m] >> (8 * (jj & 3))) & 0xFFu)];
+          const uint32_t code = (words[u][m] >> (CB * (jj % PER_WORD))) & ((1u << CB) - 1u);
+          if constexpr (CB <= 8) {
+            cw = cb_lds[(m << CB) + code];
           } else {
-            cw = ((const uint4*)codebooks)[((size_t)m << 16) + ((words[u][m] >> (16 * (jj & 1))) & 0xFFFFu)];
+            cw = ((const uint4*)codebooks)[((size_t)m << 16) + code];
           }
           fold_codeword(acc, cw, m == 0);
         }
@@ -249,22 +270,21 @@ hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hi
     else launch_dequant8<AQMB_BF16>(L, k, W, grid, st);
     return hipGetLastError();
   }
-  // 16-bit codes (and 8-bit layers too large for 32-bit thread indices): one thread per group
+  // 16- and 4-bit codes (and 8-bit layers too large for 32-bit thread indices): one thread per group
   const size_t n = (size_t)L.S * L.d.d_out * L.J;
   const unsigned grid = (unsigned)std::min<size_t>((n + 1023) / 1024, 2048);
-  const size_t lds = L.d.code_bits == 8 ? (size_t)k * 256 * 16 : 0;
+  const size_t lds = L.d.code_bits <= 8 ? ((size_t)k << L.d.code_bits) * 16 : 0;
   auto go = [&](auto kern) {
     kern<<<grid, 256, lds, st>>>(L.codes, L.codebooks, L.scales, W, L.d.d_out, L.d.d_in, L.G, L.S, k, L.plane_bytes);
   };
-  if (L.d.code_bits == 8) {
-    if (w_dtype == AQMB_F32) go(dequant_kernel<AQMB_F32, 1>);
-    else if (w_dtype == AQMB_F16) go(dequant_kernel<AQMB_F16, 1>);
-    else go(dequant_kernel<AQMB_BF16, 1>);
-  } else {
-    if (w_dtype == AQMB_F32) go(dequant_kernel<AQMB_F32, 2>);
-    else if (w_dtype == AQMB_F16) go(dequant_kernel<AQMB_F16, 2>);
-    else go(dequant_kernel<AQMB_BF16, 2>);
-  }
+  auto pick = [&](auto f32, auto f16, auto bf16) {
+    if (w_dtype == AQMB_F32) go(f32);
+    else if (w_dtype == AQMB_F16) go(f16);
+    else go(bf16);
+  };
+  if (L.d.code_bits == 8) pick(dequant_kernel<AQMB_F32, 8>, dequant_kernel<AQMB_F16, 8>, dequant_kernel<AQMB_BF16, 8>);
+  else if (L.d.code_bits == 4) pick(dequant_kernel<AQMB_F32, 4>, dequant_kernel<AQMB_F16, 4>, dequant_kernel<AQMB_BF16, 4>);
+  else pick(dequant_kernel<AQMB_F32, 16>, dequant_kernel<AQMB_F16, 16>, dequant_kernel<AQMB_BF16, 16>);
   return hipGetLastError();
 }
 

@@ -6,11 +6,15 @@
 
 namespace aqmb {
 
-hipError_t launch_retile(const Layer& L, const void* codes_plane_major, hipStream_t st);
+// Re-tile plane-major codes into the layer; for 4-bit codes a value above 15 sets *bad (device int).
+hipError_t launch_retile(const Layer& L, const void* codes_plane_major, int* bad, hipStream_t st);
 hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hipStream_t st);
 hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                        aqmb_dtype y_dtype, hipStream_t st);
 size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S);
+// Decode GEMV of a layer with 4-bit codes (16-codeword codebooks).
+hipError_t launch_gemv_b4(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                          aqmb_dtype y_dtype, hipStream_t st);
 // Several layers with the same d_in and device, already validated; n <= AQMB_MAX_MULTI.
 hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x, aqmb_dtype x_dtype, int batch,
                              void* const* ys, aqmb_dtype y_dtype, hipStream_t st);

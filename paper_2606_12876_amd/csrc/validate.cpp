@@ -30,8 +30,8 @@ aqmb_status validate_desc(const aqmb_desc* d) {
   if (d->group_size != 8) return fail(AQMB_EUNSUPPORTED, "group_size = %d: only g = 8 is supported", d->group_size);
   if (d->d_in < d->group_size || d->d_in % d->group_size)
     return fail(AQMB_EINVAL, "d_in = %d must be a positive multiple of g = %d", d->d_in, d->group_size);
-  if (d->code_bits != 8 && d->code_bits != 16)
-    return fail(AQMB_EUNSUPPORTED, "code_bits = %d: only B = 8 and B = 16 are supported", d->code_bits);
+  if (d->code_bits != 4 && d->code_bits != 8 && d->code_bits != 16)
+    return fail(AQMB_EUNSUPPORTED, "code_bits = %d: only B = 4, 8 and 16 are supported", d->code_bits);
   if (d->num_codebooks < 1) return fail(AQMB_EINVAL, "num_codebooks = %d must be >= 1", d->num_codebooks);
   if (d->num_codebooks > 8) return fail(AQMB_EUNSUPPORTED, "num_codebooks = %d: at most 8", d->num_codebooks);
   if ((uint64_t)d->d_out * (uint64_t)d->d_in >= (1ull << 32))

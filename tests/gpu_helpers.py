@@ -31,9 +31,10 @@ def to_dev(a: np.ndarray) -> torch.Tensor:
 
 
 class GpuLayer:
-    def __init__(self, codes, codebooks, scales):
+    def __init__(self, codes, codebooks, scales, B=None):
         M, d_out, G = codes.shape
-        B = 8 if codes.dtype == np.uint8 else 16
+        if B is None:          # from the codebook size: 16, 256 or 65536 codewords
+            B = {16: 4, 256: 8, 65536: 16}[codebooks.shape[1]]
         self.desc = A.make_desc(d_out, G * 8, M, B)
         self.codes, self.codebooks, self.scales = codes, codebooks, scales
         c, cb, s = to_dev(codes), to_dev(codebooks), to_dev(scales)

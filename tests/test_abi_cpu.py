@@ -43,8 +43,9 @@ def test_strerror_and_last_error():
     (dict(d_in=12), A.Status.EINVAL),                     # not a multiple of g
     (dict(d_in=0), A.Status.EINVAL),
     (dict(group_size=4, d_in=64), A.Status.EUNSUPPORTED),
-    (dict(code_bits=4), A.Status.EUNSUPPORTED),
+    (dict(code_bits=4), A.Status.OK),
     (dict(code_bits=12), A.Status.EUNSUPPORTED),
+    (dict(code_bits=2), A.Status.EUNSUPPORTED),
     (dict(num_codebooks=0), A.Status.EINVAL),
     (dict(num_codebooks=9), A.Status.EUNSUPPORTED),
     (dict(d_out=1 << 18, d_in=1 << 13), A.Status.OK),
@@ -151,3 +152,26 @@ def test_gemv_multi_rejects_before_any_launch():
     assert "live" in A.last_error()
     with pytest.raises(A.AqmbError):
         A.gemv_multi([0x1000], 1, 16, A.DType.F16, 1, [64, 128], A.DType.F16)    # one output per layer
+
+
+def test_four_bit_codes_validation():
+    """B = 4 (16-codeword codebooks): GEMV and dequant accept it; the GEMM, the distortion
+    evaluator and the beam search take 8-bit codes only."""
+    d = A.make_desc(256, 512, 4, code_bits=4)
+    assert A.validate(d, 0, 4, 16, A.DType.BF16, A.DType.F32, 16, 32) == A.Status.OK
+    assert A.validate(d, 2, 2, 0, A.DType.F16, A.DType.BF16, None, 16) == A.Status.OK
+    assert A.validate(d, 1, 1, 8, A.DType.BF16, A.DType.BF16, 16, 32) == A.Status.EUNSUPPORTED
+    assert A.validate(d, 3, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EUNSUPPORTED
+    assert A.validate(d, 4, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EUNSUPPORTED
+    assert A.validate(A.make_desc(256, 512, 4, code_bits=2), 0, 1, 1, 0, 0, 16, 32) == A.Status.EUNSUPPORTED
+
+
+def test_ablation_budgets_are_two_bits():
+    """The ablation on codebook precision against count compares 2 x 8-bit and 4 x 4-bit codebooks
+    at about 2 bits per weight: both follow from Eq. avg_bits (codes term with the plane count)."""
+    for (M, B) in [(2, 8), (4, 4)]:
+        for (d_out, d_in) in [(2048, 2048), (16384, 2048)]:
+            d = A.make_desc(d_out, d_in, M, code_bits=B)
+            v = A.bits_per_weight(d, M)
+            assert v == pytest.approx(oracle.bits_per_weight(d_out, d_in, 8, M, B, M), rel=1e-15)
+            assert 2.0 < v < 2.1

@@ -1,0 +1,105 @@
+"""Layers with 4-bit codes (codebooks of 16 codewords): create, dequant and decode GEMV on the GPU
+against the oracle.
+
+The 4 x 4-bit configuration is the one the paper's ablation on codebook precision against
+codebook count compares with 2 x 8 bits. The oracle is the same fp64 reconstruction and product
+for any codebook size; dequant must be bit-exact under the canonical rounding, the GEMV within
+the normwise tolerance of the other GEMV tests.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import formats
+from workloads import LayerSpec, make_layer, make_activations
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU hosts too; every test here is marked gpu
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2606_12876_amd as A  # noqa: E402
+from gpu_helpers import GpuLayer, out_values, check_close, to_dev, TORCH_DT, A_DT, act_values  # noqa: E402
+
+
+def _vals(L):
+    return formats.f16_bits_to_f64(L.codebooks), formats.f16_bits_to_f64(L.scales)
+
+
+@pytest.mark.parametrize("shape", [(77, 360, 4), (256, 1024, 4), (33, 8, 2), (130, 20000, 3), (64, 512, 8)])
+def test_dequant_bit_exact(shape):
+    d_out, d_in, M = shape
+    L = make_layer(LayerSpec("b4", d_out, d_in, M=M, B=4, seed=300 + d_out))
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in range(1, M + 1):
+            for dt in ("bf16", "f16", "f32"):
+                W = torch.empty((d_out, d_in), dtype=TORCH_DT[dt], device="cuda")
+                A.dequant(gl.handle, k, W, A_DT[dt])
+                torch.cuda.synchronize()
+                ref = oracle.dequant_canonical(L.codes, L.codebooks, L.scales, k, dt)
+                if dt == "f32":                              # binary32 values: compare their bits
+                    got, ref = W.cpu().numpy().view(np.uint32), np.asarray(ref, dtype=np.float32).view(np.uint32)
+                else:
+                    got = W.cpu().view(torch.int16).numpy().view(np.uint16)
+                assert np.array_equal(got, ref), f"{shape} k={k} {dt}"
+
+
+@pytest.mark.parametrize("shape,batches", [((77, 360, 4), (1, 3, 16)), ((4096, 4096, 4), (1, 4)),
+                                           ((130, 20000, 3), (1, 5)), ((64, 512, 8), (1, 8))])
+def test_gemv_matches_oracle(shape, batches):
+    """Ragged rows and groups (360 = 45 groups: one partial 32-group slice), the benchmarked shape,
+    a row longer than one 2048-group stage of x (20000 = 2500 groups), and M = 8."""
+    d_out, d_in, M = shape
+    L = make_layer(LayerSpec("b4g", d_out, d_in, M=M, B=4, seed=310 + d_in))
+    C, s = _vals(L)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for b in batches:
+            for xdt in ("f16", "bf16"):
+                xbits = make_activations(L, b, xdt, heavy_tail=(b % 2 == 1))
+                x = to_dev(xbits).view(TORCH_DT[xdt])
+                xv = act_values(xbits, xdt)
+                for k in sorted({1, M // 2 or 1, M}):
+                    ref = oracle.linear(xv, L.codes, C, s, k)
+                    for ydt in ("f32", "f16") if xdt == "f16" else ("bf16",):
+                        y = torch.full((b, d_out), 7.0, dtype=TORCH_DT[ydt], device="cuda")
+                        A.gemv(gl.handle, k, x, A_DT[xdt], b, y, A_DT[ydt])
+                        torch.cuda.synchronize()
+                        check_close(out_values(y), ref, ydt, f"{shape} b={b} k={k} {xdt}->{ydt}")
+
+
+def test_codes_above_15_rejected():
+    L = make_layer(LayerSpec("bad", 8, 64, M=2, B=4, seed=320))
+    codes = L.codes.copy()
+    codes[1, 5, 3] = 16
+    desc = A.make_desc(8, 64, 2, 4)
+    with pytest.raises(A.AqmbError) as ei:
+        A.create(desc, to_dev(codes), to_dev(L.codebooks), to_dev(L.scales))
+    assert ei.value.status == A.Status.EINVAL and "15" in A.last_error()
+
+
+def test_unsupported_operations_and_multi():
+    """GEMM, the distortion evaluator and the beam search take 8-bit codes only; aqmb_gemv_multi
+    runs 4-bit layers one launch each, with results equal to aqmb_gemv."""
+    L4 = make_layer(LayerSpec("m4", 96, 256, M=2, B=4, seed=330))
+    L8 = make_layer(LayerSpec("m8", 40, 256, M=2, B=8, seed=331))
+    with GpuLayer(L4.codes, L4.codebooks, L4.scales) as g4, GpuLayer(L8.codes, L8.codebooks, L8.scales) as g8:
+        X = torch.zeros((8, 256), dtype=torch.bfloat16, device="cuda")
+        Y = torch.zeros((8, 96), dtype=torch.float32, device="cuda")
+        assert A.lib.aqmb_gemm(g4.handle, 1, X.data_ptr(), 8, Y.data_ptr(), int(A.DType.F32), None) == A.Status.EUNSUPPORTED
+        W = torch.zeros((96, 256), dtype=torch.float16, device="cuda")
+        D = torch.zeros(2, dtype=torch.float64, device="cuda")
+        Xc = torch.zeros((8, 256), dtype=torch.float16, device="cuda")
+        assert A.lib.aqmb_prefix_distortion(g4.handle, W.data_ptr(), 0, Xc.data_ptr(), 0, 8, D.data_ptr(), None) \
+            == A.Status.EUNSUPPORTED
+        xbits = make_activations(L4, 2, "f16")
+        x = to_dev(xbits).view(torch.float16)
+        ys = [torch.empty((2, 96), dtype=torch.float32, device="cuda"), torch.empty((2, 40), dtype=torch.float32, device="cuda")]
+        A.gemv_multi([g4.handle, g8.handle], 2, x, A.DType.F16, 2, ys, A.DType.F32)
+        y1 = [torch.empty_like(t) for t in ys]
+        A.gemv(g4.handle, 2, x, A.DType.F16, 2, y1[0], A.DType.F32)
+        A.gemv(g8.handle, 2, x, A.DType.F16, 2, y1[1], A.DType.F32)
+        torch.cuda.synchronize()
+        assert torch.equal(ys[0], y1[0]) and torch.equal(ys[1], y1[1])
