@@ -10,6 +10,8 @@ exceeds the 256 MB Infinity Cache and every launch streams its codes from HBM):
   once:            prefix distortions D^(1..4) of the decode layer against a dense fp16 W
                    over 4096 fp16 calibration inputs
                    beam search (k = 4, beam 8) of codes for every group of that W
+  for k in 1..4:   decode GEMV at batch 1 of the same shape stored as 4 codebooks of 16
+                   codewords (4-bit codes, 64 copies)
 
 Each (operation, k, batch) runs as a burst of R launches captured in a HIP graph and timed
 with HIP events on the launch stream; the per-launch time is burst time / R.
@@ -163,6 +165,13 @@ def main():
     beam_codes = torch.empty((BEAM_K, d_out, G_groups), dtype=torch.uint8, device=dev)
     beam_errs = torch.empty((d_out, G_groups), dtype=torch.float32, device=dev)
     cb_dev, sc_dev = to_dev(base.codebooks), to_dev(base.scales)
+    # the same shape with 4-bit codes (4 codebooks of 16 codewords), R copies
+    import dataclasses
+    spec4 = dataclasses.replace(spec, name="c2_b4", B=4, seed=spec.seed + 100)
+    base4 = make_layer(spec4)
+    desc4 = A.make_desc(d_out, d_in, M, 4)
+    layers4 = [A.create(desc4, to_dev(base4.codes if r == 0 else np.ascontiguousarray(np.roll(base4.codes, r * 61, axis=1))),
+                        to_dev(base4.codebooks), to_dev(base4.scales)) for r in range(R)]
     torch.cuda.synchronize()
 
     ks = list(spec.ks)
@@ -196,8 +205,14 @@ def main():
     def beam_burst():
         A.beam_search(desc, BEAM_K, BEAM_WIDTH, Wd, cb_dev, sc_dev, beam_codes, beam_errs)
 
+    def gemv4_burst(k):
+        for r in range(R):
+            A.gemv(layers4[r], k, xs1[r], A.DType.F16, 1, ys1[r], A.DType.F16)
+
     ops = [("distortion", M, n_cal, distortion_burst, D_COPIES),   # (name, k, b, fn, launches)
            ("beam", BEAM_K, BEAM_WIDTH, beam_burst, 1)]
+    for k in ks:
+        ops.append(("gemv4", k, 1, lambda k=k: gemv4_burst(k), R))
     for k in ks:
         ops.append(("gemv", k, 1, lambda k=k: gemv_burst(k, 1), R))
         ops.append(("gemv", k, 4, lambda k=k: gemv_burst(k, 4), R))
@@ -353,7 +368,14 @@ def main():
                             "us_per_launch": round(tb, 1), "candidates_per_s": round(cands / (tb * 1e-6), 1),
                             "workload": f"codes for the {d_out * G_groups} groups of a {d_out}x{d_in} fp16 W, "
                                         f"k={BEAM_K} codebooks of 256, beam {BEAM_WIDTH}"}
-    step_us = {n: 0.0 for n in ("gemv", "gemv_multi", "dequant", "gemm", "distortion", "beam")}
+    def gemv4_bytes(k):
+        return k * (d_out * d_in // 16) + k * 16 * 8 * 2 + 2 * d_out + 2 * (d_in + d_out)
+    out["gemv_4bit"] = {"note": "the same shape with 4-bit codes (M = 4 codebooks of 16 codewords), batch 1, "
+                        "fp16 x/y; algorithmic bytes k*d_out*d_in/16 + codebooks + scales + x + y",
+                        "per_k": {str(k): {"us": round(per_launch_us[("gemv4", k, 1)], 3),
+                                           "GBps": round(gemv4_bytes(k) / (per_launch_us[("gemv4", k, 1)] * 1e-6) / 1e9, 1)}
+                                  for k in ks}}
+    step_us = {n: 0.0 for n in ("gemv", "gemv_multi", "gemv4", "dequant", "gemm", "distortion", "beam")}
     for i, (name, k, b, fn, n) in enumerate(ops):
         step_us["gemv_multi" if name.startswith("gemv_multi") else name] += per_op_ms[i] * 1e3 / args.steps
     tot = sum(step_us.values())
@@ -362,7 +384,7 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(base, x1, x4, ks, gemv_bytes)
 
-    for h in layers:
+    for h in layers + layers4:
         A.destroy(h)
     if not args.no_gemm:
         for h in glayers:

@@ -18,7 +18,6 @@ namespace aqmb {
 
 namespace b4 {
 constexpr int kThreads = 1024, kRows = 16, kWaves = 16;
-constexpr int kChunk = 2048;                 // groups per x stage (4 blocks of 512)
 }  // namespace b4
 
 struct Gemv4Args {
@@ -53,9 +52,12 @@ __device__ __forceinline__ float dot8(uint4 xw, uint4 cw) {
   }
 }
 
-template <int K, int NB, int XDT>
+// UB = 512-group blocks per x stage: 1 when a row has at most 512 groups (no load is issued for
+// blocks past the row), else 4.
+template <int K, int NB, int XDT, int UB>
 __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
   constexpr int kTiles = NB == 1 ? 1 : 4;    // batch <= 16
+  constexpr int kChunk = UB * 512;
   extern __shared__ uint4 smem_b4[];
   uint4* cb = smem_b4;                                       // [K][16] codewords
   char* xs = (char*)(smem_b4 + K * 16);                      // [NB][kChunk][16 bytes]
@@ -78,11 +80,11 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[t][b] = 0.f;
 
-  for (int g0 = 0; g0 < Gp; g0 += b4::kChunk) {
+  for (int g0 = 0; g0 < Gp; g0 += kChunk) {
     // code words of this chunk: block u, plane m -> 8 groups g0 + 512 u + 8 part .. + 7
-    uint32_t code[4][K];
+    uint32_t code[UB][K];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < UB; ++u) {
       int j0 = g0 + u * 512 + part * 8;
       j0 = j0 < Gp ? j0 : Gp - 8;                            // unused blocks reload a valid word
 #pragma unroll
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
         code[u][m] = __builtin_nontemporal_load(
             (const uint32_t*)(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 5) * a.d_out + rowc) * 16 + ((j0 & 31) >> 1)));
     }
-    const int n_ch = ((Gp - g0 < b4::kChunk ? Gp - g0 : b4::kChunk) + 63) / 64;   // 1 KiB pieces per x row
+    const int n_ch = ((Gp - g0 < kChunk ? Gp - g0 : kChunk) + 63) / 64;   // 1 KiB pieces per x row
 #pragma unroll
     for (int t = 0; t < kTiles; ++t) {
       if (t < n_tiles) {
@@ -101,18 +103,18 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
           const int e = (g0 + ch * 64 + lane) * 8;           // element offset in the row
           const void* src = (xb < a.batch && e < a.d_in) ? (const void*)((const uint16_t*)a.x + (size_t)xb * a.d_in + e)
                                                          : a.zero_page;
-          load_lds16(src, xs_base + (uint32_t)(b * b4::kChunk * 16 + ch * 1024));
+          load_lds16(src, xs_base + (uint32_t)(b * kChunk * 16 + ch * 1024));
         }
         wait_vmcnt<0>();
         __syncthreads();
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < UB; ++u) {
           const int j0 = u * 512 + part * 8;                 // group within the chunk
           if (g0 + j0 < Gp) {
             auto group = [&](int jj) {
               uint4 xg[NB];
 #pragma unroll
-              for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xs + (size_t)b * b4::kChunk * 16 + (size_t)(j0 + jj) * 16);
+              for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xs + (size_t)b * kChunk * 16 + (size_t)(j0 + jj) * 16);
 #pragma unroll
               for (int m = 0; m < K; ++m) {
                 const uint4 cwv = cb[m * 16 + ((code[u][m] >> (4 * jj)) & 15u)];
@@ -169,17 +171,18 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
   }
 }
 
+template <int K, int XDT, int UB>
+static hipError_t launch_b4_ub(const Gemv4Args& a, hipStream_t st) {
+  const unsigned grid = (unsigned)((a.d_out + b4::kRows - 1) / b4::kRows);
+  const size_t row_bytes = (size_t)UB * 512 * 16;
+  if (a.batch == 1) gemv_b4_kernel<K, 1, XDT, UB><<<grid, b4::kThreads, (size_t)K * 256 + row_bytes, st>>>(a);
+  else gemv_b4_kernel<K, 4, XDT, UB><<<grid, b4::kThreads, (size_t)K * 256 + 4 * row_bytes, st>>>(a);
+  return hipGetLastError();
+}
+
 template <int K, int XDT>
 static hipError_t launch_b4_k(const Gemv4Args& a, hipStream_t st) {
-  const unsigned grid = (unsigned)((a.d_out + b4::kRows - 1) / b4::kRows);
-  if (a.batch == 1) {
-    const size_t lds = (size_t)K * 256 + (size_t)b4::kChunk * 16;
-    gemv_b4_kernel<K, 1, XDT><<<grid, b4::kThreads, lds, st>>>(a);
-  } else {
-    const size_t lds = (size_t)K * 256 + 4 * (size_t)b4::kChunk * 16;
-    gemv_b4_kernel<K, 4, XDT><<<grid, b4::kThreads, lds, st>>>(a);
-  }
-  return hipGetLastError();
+  return a.S * 32 <= 512 ? launch_b4_ub<K, XDT, 1>(a, st) : launch_b4_ub<K, XDT, 4>(a, st);
 }
 
 template <int XDT>
