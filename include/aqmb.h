@@ -54,7 +54,7 @@ typedef struct {
   int32_t d_in;           /* input columns of W, >= g, a multiple of g */
   int32_t group_size;     /* g: weights per group; 8 is supported */
   int32_t num_codebooks;  /* M: 1..8 */
-  int32_t code_bits;      /* B: 8 (uint8 codes, 256 codewords) or 16 (uint16 codes, 65536 codewords) */
+  int32_t code_bits;      /* B: 4 (16 codewords), 8 (uint8 codes, 256 codewords) or 16 (uint16 codes, 65536 codewords) */
 } aqmb_desc;
 
 /* Largest batch accepted by aqmb_gemv. */
@@ -62,19 +62,44 @@ typedef struct {
 
 /*
  * Create a layer from device buffers (Alg. 1 stores a layer as AQLMFormat(C, b, s)).
- *   codes     [M][d_out][d_in/g] uint8 (B = 8) or uint16 (B = 16): plane-major.
+ *   codes     [M][d_out][d_in/g] uint8 (B = 8), uint16 (B = 16), or uint8 holding values 0..15
+ *             (B = 4; stored two per byte): plane-major.
  *   codebooks [M][2^B][g] fp16 bit patterns; codeword c of codebook m is g contiguous values.
  *   scales    [d_out] fp16 bit patterns.
  * The library copies everything into device memory it owns, re-tiling the codes
  * inside each plane for coalesced reads while keeping planes outermost, so that
  * level k reads only the first k planes. Synchronous: returns after the copy on
  * `stream` has finished; the caller may free its buffers afterwards.
- * Code values >= 2^B cannot occur for B = 8 or 16 (they fill their type).
- * Errors: EINVAL (null pointer, bad sizes), EUNSUPPORTED (g, B or M not supported),
+ * Code values >= 2^B cannot occur for B = 8 or 16 (they fill their type); for B = 4 they are
+ * refused (EINVAL).
+ * Errors: EINVAL (null pointer, bad sizes, 4-bit codes above 15), EUNSUPPORTED (g, B or M not supported),
  * ENOMEM, EHIP. On error *out is set to NULL.
  */
 aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* codes,
                         const uint16_t* codebooks, const uint16_t* scales, aqmb_stream_t stream);
+
+/*
+ * Run-time loading of code planes (the dynamic loading the paper's discussion of future work
+ * names as an application of droppable codebooks: a device keeps only the planes its precision
+ * level needs). Planes are stored outermost, so level k needs exactly planes 0..k-1.
+ *   aqmb_create_prefix  like aqmb_create with only the first `resident` planes in device memory
+ *                       (1 <= resident <= M); codes is [resident][d_out][d_in/g], codebooks and
+ *                       scales are complete ([M][2^B][g], [d_out]).
+ *   aqmb_load_planes    append the next n_planes planes (codes [n_planes][d_out][d_in/g], plane
+ *                       `resident` first); the layer's code memory is reallocated.
+ *   aqmb_drop_planes    keep planes 0..keep-1 (1 <= keep <= resident) and free the others.
+ *   aqmb_resident_planes  the number of resident planes.
+ * Every compute call with k above the resident count returns EINVAL; aqmb_prefix_distortion
+ * covers the resident levels. load and drop are synchronous, wait for the device before the old
+ * code memory is freed, and must not run concurrently with other calls on the same layer.
+ * Errors: EINVAL (bad handle, null pointer, plane counts out of range, 4-bit codes above 15),
+ * ENOMEM, EHIP. On error the layer is unchanged.
+ */
+aqmb_status aqmb_create_prefix(aqmb_layer_t* out, const aqmb_desc* desc, int resident, const void* codes,
+                               const uint16_t* codebooks, const uint16_t* scales, aqmb_stream_t stream);
+aqmb_status aqmb_load_planes(aqmb_layer_t layer, int n_planes, const void* codes, aqmb_stream_t stream);
+aqmb_status aqmb_drop_planes(aqmb_layer_t layer, int keep);
+aqmb_status aqmb_resident_planes(aqmb_layer_t layer, int* resident);
 
 /* Free a layer and its device memory (waits for the device first). NULL is a no-op.
  * EINVAL for a handle that is not a live layer. */
@@ -149,7 +174,7 @@ aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype,
  * with the calibration inputs given as the rows of Xt = X^T.
  *   W   [d_out][d_in] fp16: the weights being quantized (w_dtype must be F16)
  *   Xt  [n][d_in]     fp16: one calibration input per row (x_dtype must be F16)
- *   D   M doubles in device memory, written in stream order
+ *   D   one double per resident level (M unless planes were dropped or never loaded), device memory
  * The products W X and C_m[b_m] X run on fp16 matrix cores (each product of two fp16 values
  * exact, sums in fp32), the per-output differences W X - s_i sum_{m<k} (C_m[b_m] X) in fp32, the
  * sums of their squares in fp64, added in a fixed order: the result is reproducible.

@@ -59,6 +59,10 @@ def _load() -> ctypes.CDLL:
     vp, i32, st = ctypes.c_void_p, ctypes.c_int, ctypes.c_int
     L.aqmb_create.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(Desc), vp, vp, vp, vp]
     L.aqmb_destroy.argtypes = [vp]
+    L.aqmb_create_prefix.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(Desc), i32, vp, vp, vp, vp]
+    L.aqmb_load_planes.argtypes = [vp, i32, vp, vp]
+    L.aqmb_drop_planes.argtypes = [vp, i32]
+    L.aqmb_resident_planes.argtypes = [vp, ctypes.POINTER(i32)]
     L.aqmb_get_desc.argtypes = [vp, ctypes.POINTER(Desc)]
     L.aqmb_gemv.argtypes = [vp, i32, vp, i32, i32, vp, i32, vp]
     L.aqmb_gemv_multi.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, i32, ctypes.POINTER(vp), i32, vp]
@@ -73,7 +77,8 @@ def _load() -> ctypes.CDLL:
     L.aqmb_strerror.restype = ctypes.c_char_p
     L.aqmb_last_error.argtypes = []
     L.aqmb_last_error.restype = ctypes.c_char_p
-    for f in ("aqmb_create", "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_multi", "aqmb_gemm",
+    for f in ("aqmb_create", "aqmb_create_prefix", "aqmb_load_planes", "aqmb_drop_planes", "aqmb_resident_planes",
+              "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_multi", "aqmb_gemm",
               "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_beam_search", "aqmb_validate"):
         getattr(L, f).restype = st
     return L
@@ -153,6 +158,40 @@ def create(desc: Desc, codes, codebooks, scales, stream=None) -> int:
     return h.value
 
 
+def _need_planes(desc: Desc, codes, n_planes: int, where: str):
+    g = desc.group_size if desc.group_size > 0 else 1
+    need = max(n_planes, 0) * desc.d_out * (desc.d_in // g) * (1 if desc.code_bits <= 8 else 2)
+    n = _nbytes(codes)
+    if n is not None and n < need:
+        raise AqmbError(Status.EINVAL, where, f"codes holds {n} bytes, {n_planes} planes need {need}")
+
+
+def create_prefix(desc: Desc, resident: int, codes, codebooks, scales, stream=None) -> int:
+    """aqmb_create_prefix: a layer holding only code planes 0..resident-1 (codes [resident][d_out][d_in/g])."""
+    _need_planes(desc, codes, resident, "aqmb_create_prefix")
+    h = ctypes.c_void_p()
+    _check(lib.aqmb_create_prefix(ctypes.byref(h), ctypes.byref(desc), resident, _ptr(codes), _ptr(codebooks),
+                                  _ptr(scales), _stream(stream)), "aqmb_create_prefix")
+    return h.value
+
+
+def load_planes(layer: int, n_planes: int, codes, stream=None) -> None:
+    """aqmb_load_planes: append the next n_planes code planes (codes [n_planes][d_out][d_in/g])."""
+    _need_planes(get_desc(layer), codes, n_planes, "aqmb_load_planes")
+    _check(lib.aqmb_load_planes(layer, n_planes, _ptr(codes), _stream(stream)), "aqmb_load_planes")
+
+
+def drop_planes(layer: int, keep: int) -> None:
+    """aqmb_drop_planes: keep code planes 0..keep-1 and free the others."""
+    _check(lib.aqmb_drop_planes(layer, keep), "aqmb_drop_planes")
+
+
+def resident_planes(layer: int) -> int:
+    r = ctypes.c_int32()
+    _check(lib.aqmb_resident_planes(layer, ctypes.byref(r)), "aqmb_resident_planes")
+    return r.value
+
+
 def destroy(layer: int) -> None:
     _check(lib.aqmb_destroy(layer), "aqmb_destroy")
 
@@ -224,8 +263,9 @@ def prefix_distortion(layer: int, W, w_dtype, Xt, x_dtype, n: int, D, stream=Non
     if n >= 1:
         _need(Xt, n * d.d_in, x_dtype, "Xt", "aqmb_prefix_distortion")
     nd = _nbytes(D)
-    if nd is not None and nd < 8 * d.num_codebooks:
-        raise AqmbError(Status.EINVAL, "aqmb_prefix_distortion", f"D holds {nd} bytes, needs {8 * d.num_codebooks}")
+    need = 8 * resident_planes(layer)
+    if nd is not None and nd < need:
+        raise AqmbError(Status.EINVAL, "aqmb_prefix_distortion", f"D holds {nd} bytes, needs {need}")
     _check(lib.aqmb_prefix_distortion(layer, _ptr(W), int(w_dtype), _ptr(Xt), int(x_dtype), n, _ptr(D),
                                       _stream(stream)), "aqmb_prefix_distortion")
 

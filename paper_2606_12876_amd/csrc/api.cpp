@@ -51,13 +51,36 @@ using namespace aqmb;
 
 extern "C" {
 
-aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* codes, const uint16_t* codebooks,
-                        const uint16_t* scales, aqmb_stream_t stream) {
-  clear_error();
+}  // extern "C"
+
+namespace aqmb {
+
+// Re-tile n plane-major code planes into dst (n tiled planes) and, for 4-bit codes, refuse values
+// above 15 (the re-tiling flags them in the workspace). Synchronous.
+static aqmb_status upload_planes(Layer* L, const void* codes, int n, unsigned char* dst, hipStream_t st,
+                                 const char* where) {
+  int* flag = (int*)(L->ws + 256);
+  hipError_t e;
+  if ((e = hipMemsetAsync(flag, 0, sizeof(int), st)) != hipSuccess ||
+      (e = launch_retile(*L, codes, n, dst, flag, st)) != hipSuccess || (e = hipStreamSynchronize(st)) != hipSuccess)
+    return fail(AQMB_EHIP, "%s: upload: %s", where, hipGetErrorString(e));
+  if (L->d.code_bits == 4) {
+    int bad = 0;
+    if ((e = hipMemcpy(&bad, flag, sizeof(int), hipMemcpyDeviceToHost)) != hipSuccess)
+      return fail(AQMB_EHIP, "%s: code check: %s", where, hipGetErrorString(e));
+    if (bad) return fail(AQMB_EINVAL, "%s: a 4-bit code is above 15", where);
+  }
+  return AQMB_OK;
+}
+
+static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int resident, const void* codes,
+                               const uint16_t* codebooks, const uint16_t* scales, aqmb_stream_t stream) {
   if (!out) return fail(AQMB_EINVAL, "create: out is NULL");
   *out = nullptr;
   aqmb_status s = validate_desc(desc);
   if (s != AQMB_OK) return s;
+  if (resident < 1 || resident > desc->num_codebooks)
+    return fail(AQMB_EINVAL, "create: resident planes = %d outside [1, M = %d]", resident, desc->num_codebooks);
   if (!codes || !codebooks || !scales) return fail(AQMB_EINVAL, "create: codes, codebooks or scales is NULL");
   hipStream_t st = (hipStream_t)stream;
 
@@ -71,13 +94,14 @@ aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* co
   L->J = kSliceBytes * 8 / desc->code_bits;     // groups per 16-byte slice: 32, 16 or 8
   L->S = (L->G + L->J - 1) / L->J;
   L->plane_bytes = (size_t)L->S * desc->d_out * kSliceBytes;
+  L->resident = resident;
   const size_t n_codewords = (size_t)1 << desc->code_bits;
   const size_t cb_bytes = (size_t)desc->num_codebooks * n_codewords * desc->group_size * 2;
   L->ws_floats = gemv_workspace_floats(*desc, L->G, L->S);
   if (L->ws_floats < 256 + distortion_workspace_floats()) L->ws_floats = 256 + distortion_workspace_floats();
 
   struct { void** p; size_t n; const char* what; } allocs[] = {
-      {(void**)&L->codes, (size_t)desc->num_codebooks * L->plane_bytes, "codes"},
+      {(void**)&L->codes, (size_t)resident * L->plane_bytes, "codes"},
       {(void**)&L->codebooks, cb_bytes, "codebooks"},
       {(void**)&L->scales, (size_t)desc->d_out * 2, "scales"},
       {(void**)&L->ws, L->ws_floats * sizeof(float), "workspace"},
@@ -95,28 +119,109 @@ aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* co
   // inputs (never written); the rest holds per-call partial sums (gemv, prefix distortion).
   if ((e = hipMemsetAsync(L->ws, 0, L->ws_floats * sizeof(float), st)) != hipSuccess ||
       (e = hipMemcpyAsync(L->codebooks, codebooks, cb_bytes, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
-      (e = hipMemcpyAsync(L->scales, scales, (size_t)desc->d_out * 2, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
-      (e = launch_retile(*L, codes, (int*)(L->ws + 256), st)) != hipSuccess ||
-      (e = hipStreamSynchronize(st)) != hipSuccess) {
+      (e = hipMemcpyAsync(L->scales, scales, (size_t)desc->d_out * 2, hipMemcpyDeviceToDevice, st)) != hipSuccess) {
     free_layer(L);
     return hip_fail(e, "create: upload");
   }
-  if (desc->code_bits == 4) {  // the re-tiling flags 4-bit codes above 15 in the workspace
-    int bad = 0;
-    if ((e = hipMemcpy(&bad, L->ws + 256, sizeof(int), hipMemcpyDeviceToHost)) != hipSuccess) {
-      free_layer(L);
-      return hip_fail(e, "create: code check");
-    }
-    if (bad) {
-      free_layer(L);
-      return fail(AQMB_EINVAL, "create: a 4-bit code is above 15");
-    }
+  if ((s = upload_planes(L, codes, resident, L->codes, st, "create")) != AQMB_OK) {
+    free_layer(L);
+    return s;
   }
   {
     std::lock_guard<std::mutex> lk(g_mu);
     g_live.insert(L);
   }
   *out = (aqmb_layer_t)L;
+  return AQMB_OK;
+}
+
+// k must name resident planes.
+static aqmb_status check_resident(const Layer* L, int k, const char* where) {
+  if (k > L->resident)
+    return fail(AQMB_EINVAL, "%s: k = %d needs planes that are not resident (%d of %d loaded)", where, k, L->resident,
+                L->d.num_codebooks);
+  return AQMB_OK;
+}
+
+// Replace the layer's planes by the first `keep` of them followed by n new planes from `codes`.
+static aqmb_status resize_planes(Layer* L, int keep, const void* codes, int n, hipStream_t st, const char* where) {
+  unsigned char* fresh = nullptr;
+  hipError_t e = hipMalloc(&fresh, (size_t)(keep + n) * L->plane_bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AQMB_ENOMEM, "%s: hipMalloc(%zu) failed: %s", where, (size_t)(keep + n) * L->plane_bytes,
+                hipGetErrorString(e));
+  }
+  // no kernel may still read the old planes when they are freed: wait for the device
+  if ((e = hipDeviceSynchronize()) != hipSuccess ||
+      (e = hipMemcpyAsync(fresh, L->codes, (size_t)keep * L->plane_bytes, hipMemcpyDeviceToDevice, st)) != hipSuccess) {
+    (void)hipFree(fresh);
+    return hip_fail(e, where);
+  }
+  if (n > 0) {
+    aqmb_status s = upload_planes(L, codes, n, fresh + (size_t)keep * L->plane_bytes, st, where);
+    if (s != AQMB_OK) {
+      (void)hipStreamSynchronize(st);
+      (void)hipFree(fresh);
+      return s;
+    }
+  } else if ((e = hipStreamSynchronize(st)) != hipSuccess) {
+    (void)hipFree(fresh);
+    return hip_fail(e, where);
+  }
+  (void)hipFree(L->codes);
+  L->codes = fresh;
+  L->resident = keep + n;
+  return AQMB_OK;
+}
+
+}  // namespace aqmb
+
+extern "C" {
+
+aqmb_status aqmb_create(aqmb_layer_t* out, const aqmb_desc* desc, const void* codes, const uint16_t* codebooks,
+                        const uint16_t* scales, aqmb_stream_t stream) {
+  clear_error();
+  return create_impl(out, desc, desc ? desc->num_codebooks : 1, codes, codebooks, scales, stream);
+}
+
+aqmb_status aqmb_create_prefix(aqmb_layer_t* out, const aqmb_desc* desc, int resident, const void* codes,
+                               const uint16_t* codebooks, const uint16_t* scales, aqmb_stream_t stream) {
+  clear_error();
+  return create_impl(out, desc, resident, codes, codebooks, scales, stream);
+}
+
+aqmb_status aqmb_load_planes(aqmb_layer_t layer, int n_planes, const void* codes, aqmb_stream_t stream) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "load_planes: not a live layer");
+  if (!codes) return fail(AQMB_EINVAL, "load_planes: codes is NULL");
+  if (n_planes < 1 || L->resident + n_planes > L->d.num_codebooks)
+    return fail(AQMB_EINVAL, "load_planes: %d more planes do not fit (%d of %d resident)", n_planes, L->resident,
+                L->d.num_codebooks);
+  aqmb_status s = check_device(L);
+  if (s != AQMB_OK) return s;
+  return resize_planes(L, L->resident, codes, n_planes, (hipStream_t)stream, "load_planes");
+}
+
+aqmb_status aqmb_drop_planes(aqmb_layer_t layer, int keep) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "drop_planes: not a live layer");
+  if (keep < 1 || keep > L->resident)
+    return fail(AQMB_EINVAL, "drop_planes: keep = %d outside [1, %d resident]", keep, L->resident);
+  if (keep == L->resident) return AQMB_OK;
+  aqmb_status s = check_device(L);
+  if (s != AQMB_OK) return s;
+  return resize_planes(L, keep, nullptr, 0, nullptr, "drop_planes");
+}
+
+aqmb_status aqmb_resident_planes(aqmb_layer_t layer, int* resident) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "resident_planes: not a live layer");
+  if (!resident) return fail(AQMB_EINVAL, "resident_planes: resident is NULL");
+  *resident = L->resident;
   return AQMB_OK;
 }
 
@@ -154,6 +259,7 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
   if (!is_live(L)) return fail(AQMB_EINVAL, "gemv: not a live layer");
   aqmb_status s = validate_call(&L->d, 0, k, batch, x_dtype, y_dtype, x, y);
   if (s != AQMB_OK) return s;
+  if ((s = check_resident(L, k, "gemv")) != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
   hipError_t e = L->d.code_bits == 4 ? launch_gemv_b4(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream)
                                      : launch_gemv(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream);
@@ -174,6 +280,7 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
       return fail(AQMB_EINVAL, "gemv_multi: layers differ in d_in or device");
     aqmb_status s = validate_call(&L->d, 0, k, batch, x_dtype, y_dtype, x, ys[i]);
     if (s != AQMB_OK) return s;
+    if ((s = check_resident(L, k, "gemv_multi")) != AQMB_OK) return s;
     Ls[i] = L;
   }
   aqmb_status s = check_device((Layer*)Ls[0]);
@@ -198,6 +305,7 @@ aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, vo
   if (!is_live(L)) return fail(AQMB_EINVAL, "gemm: not a live layer");
   aqmb_status s = validate_call(&L->d, 1, k, n_tokens, AQMB_BF16, y_dtype, X, Y);
   if (s != AQMB_OK) return s;
+  if ((s = check_resident(L, k, "gemm")) != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
   hipError_t e = launch_gemm(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemm: launch");
@@ -235,6 +343,7 @@ aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype,
   if (!is_live(L)) return fail(AQMB_EINVAL, "dequant: not a live layer");
   aqmb_status s = validate_call(&L->d, 2, k, 0, AQMB_F16, w_dtype, nullptr, W);
   if (s != AQMB_OK) return s;
+  if ((s = check_resident(L, k, "dequant")) != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
   hipError_t e = launch_dequant(*L, k, W, w_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "dequant: launch");

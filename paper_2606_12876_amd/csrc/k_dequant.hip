@@ -46,16 +46,17 @@ __global__ __launch_bounds__(256) void retile_kernel(const unsigned char* __rest
   }
 }
 
-hipError_t launch_retile(const Layer& L, const void* codes, int* bad, hipStream_t st) {
-  const size_t total = (size_t)L.d.num_codebooks * L.S * L.d.d_out;
+hipError_t launch_retile(const Layer& L, const void* codes, int n_planes, unsigned char* out, int* bad,
+                         hipStream_t st) {
+  const size_t total = (size_t)n_planes * L.S * L.d.d_out;
   const unsigned grid = (unsigned)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
   const auto* in = (const unsigned char*)codes;
   if (L.d.code_bits == 8)
-    retile_kernel<8><<<grid, 256, 0, st>>>(in, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S, bad);
+    retile_kernel<8><<<grid, 256, 0, st>>>(in, out, n_planes, L.d.d_out, L.G, L.S, bad);
   else if (L.d.code_bits == 4)
-    retile_kernel<4><<<grid, 256, 0, st>>>(in, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S, bad);
+    retile_kernel<4><<<grid, 256, 0, st>>>(in, out, n_planes, L.d.d_out, L.G, L.S, bad);
   else
-    retile_kernel<16><<<grid, 256, 0, st>>>(in, L.codes, L.d.num_codebooks, L.d.d_out, L.G, L.S, bad);
+    retile_kernel<16><<<grid, 256, 0, st>>>(in, out, n_planes, L.d.d_out, L.G, L.S, bad);
   return hipGetLastError();
 }
 

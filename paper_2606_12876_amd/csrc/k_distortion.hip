@@ -295,7 +295,7 @@ hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n
   a.n = n;
   int grid = 0;
   hipError_t e;
-  switch (L.d.num_codebooks) {
+  switch (L.resident) {                            // the resident levels
     case 1: e = launch_dist_m<1>(a, st, &grid); break;
     case 2: e = launch_dist_m<2>(a, st, &grid); break;
     case 3: e = launch_dist_m<3>(a, st, &grid); break;
@@ -306,7 +306,7 @@ hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n
     default: e = launch_dist_m<8>(a, st, &grid); break;
   }
   if (e != hipSuccess) return e;
-  distortion_reduce_kernel<<<1, dist::kMaxGrid, 0, st>>>(a.partials, grid, L.d.num_codebooks,
+  distortion_reduce_kernel<<<1, dist::kMaxGrid, 0, st>>>(a.partials, grid, L.resident,
                                              1.0 / ((double)L.d.d_out * (double)n), D);
   return hipGetLastError();
 }

@@ -6,8 +6,10 @@
 
 namespace aqmb {
 
-// Re-tile plane-major codes into the layer; for 4-bit codes a value above 15 sets *bad (device int).
-hipError_t launch_retile(const Layer& L, const void* codes_plane_major, int* bad, hipStream_t st);
+// Re-tile n_planes plane-major code planes [n_planes][d_out][G] into out (n_planes tiled planes);
+// for 4-bit codes a value above 15 sets *bad (device int).
+hipError_t launch_retile(const Layer& L, const void* codes_plane_major, int n_planes, unsigned char* out, int* bad,
+                         hipStream_t st);
 hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hipStream_t st);
 hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                        aqmb_dtype y_dtype, hipStream_t st);

@@ -22,7 +22,8 @@ struct Layer {
   int J;                 // groups per slice
   int S;                 // slices per row = ceil(G / J)
   size_t plane_bytes;    // S * d_out * 16
-  unsigned char* codes;  // [M][S][d_out][16 bytes]
+  int resident;          // planes 0..resident-1 are in memory (the others were never loaded or were dropped)
+  unsigned char* codes;  // [resident][S][d_out][16 bytes]
   uint16_t* codebooks;   // [M][2^B][g] fp16
   uint16_t* scales;      // [d_out] fp16
   float* ws;             // gemv split-K partial sums

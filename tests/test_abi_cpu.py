@@ -175,3 +175,16 @@ def test_ablation_budgets_are_two_bits():
             v = A.bits_per_weight(d, M)
             assert v == pytest.approx(oracle.bits_per_weight(d_out, d_in, 8, M, B, M), rel=1e-15)
             assert 2.0 < v < 2.1
+
+
+def test_plane_calls_reject_without_gpu():
+    bogus = ctypes.c_void_p(0x1000)
+    r = ctypes.c_int32(-1)
+    assert A.lib.aqmb_load_planes(bogus, 1, 16, None) == A.Status.EINVAL
+    assert A.lib.aqmb_drop_planes(bogus, 1) == A.Status.EINVAL
+    assert A.lib.aqmb_resident_planes(bogus, ctypes.byref(r)) == A.Status.EINVAL and r.value == -1
+    h = ctypes.c_void_p(0x1234)
+    d = A.make_desc(64, 64, 4)
+    for resident in (0, 5):
+        assert A.lib.aqmb_create_prefix(ctypes.byref(h), ctypes.byref(d), resident, 16, 16, 16, None) == A.Status.EINVAL
+        assert h.value is None
