@@ -1,6 +1,7 @@
 // The C-ABI entry points: layer registry, creation (copy + re-tile), dispatch.
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
 #include <mutex>
 #include <new>
 #include <unordered_set>
@@ -135,6 +136,32 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
   return AQMB_OK;
 }
 
+// GEMV kernel choice. Default: 4-bit codes -> their kernel; 8-bit codes at batch >= 3 -> the
+// matrix-core kernel (measured faster from batch 3 or 4 on, equal at 2); otherwise the direct-gather
+// kernel (k <= 4, rows <= 16384) or the lookup table kernel, as k_gemv.hip decides. AQMB_GEMV=mma uses the matrix-core kernel at batch 1 too,
+// AQMB_GEMV=cw or =lut keep 8-bit layers on k_gemv.hip's kernels (read once).
+static int gemv_mode() {
+  static const int v = [] {
+    const char* e = getenv("AQMB_GEMV");
+    if (!e) return 0;
+    if (e[0] == 'm' || e[0] == 'M') return 3;
+    if (e[0] == 'c' || e[0] == 'C' || e[0] == 'l' || e[0] == 'L') return 2;
+    return 0;
+  }();
+  return v;
+}
+
+static bool gemv_uses_mma(const Layer& L, int batch) {
+  return L.d.code_bits == 8 && (gemv_mode() == 3 || (gemv_mode() == 0 && batch >= 3));
+}
+
+static hipError_t launch_gemv_any(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                                  aqmb_dtype y_dtype, hipStream_t st) {
+  if (L.d.code_bits == 4) return launch_gemv_b4(L, k, x, x_dtype, batch, y, y_dtype, st);
+  if (gemv_uses_mma(L, batch)) return launch_gemv_mma(L, k, x, x_dtype, batch, y, y_dtype, st);
+  return launch_gemv(L, k, x, x_dtype, batch, y, y_dtype, st);
+}
+
 // k must name resident planes.
 static aqmb_status check_resident(const Layer* L, int k, const char* where) {
   if (k > L->resident)
@@ -261,8 +288,7 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
   if (s != AQMB_OK) return s;
   if ((s = check_resident(L, k, "gemv")) != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
-  hipError_t e = L->d.code_bits == 4 ? launch_gemv_b4(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream)
-                                     : launch_gemv(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream);
+  hipError_t e = launch_gemv_any(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv: launch");
 }
 
@@ -285,13 +311,15 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
   }
   aqmb_status s = check_device((Layer*)Ls[0]);
   if (s != AQMB_OK) return s;
-  bool any4 = false;
-  for (int i = 0; i < n_layers; ++i) any4 = any4 || Ls[i]->d.code_bits == 4;
+  // The one-launch kernel shares the direct-gather kernel's arithmetic; layers that a single call
+  // would send to another kernel (4-bit codes, the matrix-core kernel) run one launch each, so the
+  // results are always those of aqmb_gemv.
+  bool per_layer = false;
+  for (int i = 0; i < n_layers; ++i) per_layer = per_layer || Ls[i]->d.code_bits == 4 || gemv_uses_mma(*Ls[i], batch);
   hipError_t e = hipSuccess;
-  if (any4) {  // layers with 4-bit codes have their own kernel: one launch per layer
+  if (per_layer) {
     for (int i = 0; i < n_layers && e == hipSuccess; ++i)
-      e = Ls[i]->d.code_bits == 4 ? launch_gemv_b4(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, (hipStream_t)stream)
-                                  : launch_gemv(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, (hipStream_t)stream);
+      e = launch_gemv_any(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, (hipStream_t)stream);
   } else {
     e = launch_gemv_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
   }

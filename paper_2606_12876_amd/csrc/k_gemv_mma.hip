@@ -1,0 +1,214 @@
+// Decode GEMV on the matrix cores (8-bit codes, any batch up to 16; used from batch 3 on): y[b][i] = s_i sum_j sum_{m<k}
+// <x[b, group j], C_m[b_{ijm}]>, the per-plane products computed by v_mfma_f32_16x16x32 with the
+// batch in the 16 rows of the A operand and 16 weight rows in the columns of the B operand.
+//
+// A workgroup of 16 waves owns 16 weight rows; the waves take interleaved runs of 4 K-steps of 32
+// inputs (a run is the 16 groups of one code slice, one 16-byte load per plane). In a K-step lane l
+// of a wave stands for weight row l % 16 and group l / 16 of the step: it gathers that group's
+// codeword of every plane from the codebooks replicated in LDS, which is the B fragment of that
+// plane's MFMA as it is (8 fp16 values of one row and group). The A fragment is x itself: lane l
+// holds 8 values of batch row l % 16 (rows past the batch read zeros). So every code costs one
+// codeword gather, as at batch 1, and the dot products run on the matrix cores whatever the batch.
+// Products are exact: fp16 x by the fp16 codeword directly; bf16 x by the codeword split exactly
+// into two bf16 parts (an fp16 value has 11 significant bits: hi = RNE_bf16(c) and lo = c - hi has
+// at most 3, both exact), split once per codeword when the codebooks are copied into LDS (a book
+// of high parts and a book of low parts), so a code costs two gathers and two MFMAs.
+// Sums are fp32. The 16 waves' partial tiles are added in wave order, scaled once and rounded
+// once, so results are reproducible.
+#include "device.h"
+#include "launch.h"
+
+namespace aqmb {
+
+namespace mg {
+constexpr int kThreads = 1024, kWaves = 16, kRows = 16;
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 b16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+}  // namespace mg
+
+struct GemvMmaArgs {
+  const unsigned char* codes;
+  const uint16_t* codebooks;
+  const uint16_t* scales;
+  const uint16_t* x;
+  void* y;
+  const void* zero_page;      // >= 16 zero bytes
+  size_t plane_bytes;
+  int d_out, d_in, G, batch, y_dtype, nrep, cb_shift;
+};
+
+
+// A run: 4 consecutive K-steps = the 16 groups of one code slice. Per lane: x of its batch row
+// for the 4 steps (8 values each) and one 16-byte slice word per plane (groups of its weight row).
+template <int K>
+struct MgRun {
+  uint4 xa[4];
+  uint4 c[K];
+};
+
+template <int K, int XDT>
+__global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_mma_kernel(GemvMmaArgs a) {
+  using namespace mg;
+  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;            // fp16 codewords, or bf16 high and low parts
+  extern __shared__ uint4 smem_mg[];
+  uint4* cb_rep = smem_mg;                                   // [kBooks][K][256][nrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * 256 * a.nrep);   // [kWaves][64] partial tiles
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15, kc = lane >> 4;                 // weight row in the block, group in a step
+  const int row0 = blockIdx.x * kRows;
+  const int rowc = row0 + col < a.d_out ? row0 + col : a.d_out - 1;
+  const int n_runs = (a.G + 15) / 16;                        // code slices per row
+  const uint32_t rep_off = (uint32_t)(lane & (a.nrep - 1)) * 16;
+  const bool brow = col < a.batch;                           // this lane's x row exists
+
+  // Loads of run r (past the end: the last run again, never used): x of batch row `col` at
+  // inputs 128 r + 32 j + 8 kc .. + 7 for steps j = 0..3 (zeros past d_in and past the batch),
+  // and slice r of weight row `rowc` in every plane.
+  auto load_run = [&](int r, MgRun<K>& R) {
+    const int rc = r < n_runs ? r : n_runs - 1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = rc * 128 + j * 32 + kc * 8;
+      const void* src = (brow && e < a.d_in) ? (const void*)(a.x + (size_t)col * a.d_in + e) : a.zero_page;
+      R.xa[j] = *(const uint4*)src;
+    }
+#pragma unroll
+    for (int m = 0; m < K; ++m) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+  };
+
+  // The wave's runs are wave, wave + 16, ...; the first two are requested before the codebooks are
+  // replicated into LDS (a 4096-wide row has 32 runs: two per wave).
+  MgRun<K> ra, rb;
+  int r = wave;
+  load_run(r, ra);
+  load_run(r + kWaves, rb);
+  for (int q = tid; q < K * 256; q += kThreads) {
+    const uint4 v = ((const uint4*)a.codebooks)[q];
+    const int rot = q >> (8 - a.cb_shift);
+    if constexpr (kBooks == 1) {
+      for (int i = 0; i < a.nrep; ++i) cb_rep[q * a.nrep + ((i + rot) & (a.nrep - 1))] = v;
+    } else {
+      const f16x8_t c = __builtin_bit_cast(f16x8_t, v);
+      b16x8_t hi, lo;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float cf = (float)c[t];
+        hi[t] = (__bf16)cf;                                  // round to nearest even
+        lo[t] = (__bf16)(cf - (float)hi[t]);                 // exact: at most 3 significant bits
+      }
+      const uint4 vh = __builtin_bit_cast(uint4, hi), vl = __builtin_bit_cast(uint4, lo);
+      for (int i = 0; i < a.nrep; ++i) {
+        cb_rep[q * a.nrep + ((i + rot) & (a.nrep - 1))] = vh;
+        cb_rep[(K * 256 + q) * a.nrep + ((i + rot) & (a.nrep - 1))] = vl;
+      }
+    }
+  }
+  __syncthreads();
+
+  f32x4_t acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // Step j of a run: group 4 j + kc of the slice, code byte 4 j + kc of each plane's word.
+  auto compute = [&](const MgRun<K>& R) {
+#pragma unroll
+    for (int m = 0; m < K; ++m) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
+        const uint32_t code = (word >> (8 * kc)) & 0xFFu;
+        const uint32_t off = (((uint32_t)(m * 256) + code) << a.cb_shift) + rep_off;
+        const uint4 cw = *(const uint4*)((const char*)cb_rep + off);
+        if constexpr (XDT == AQMB_F16) {
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, R.xa[j]),
+                                                          __builtin_bit_cast(f16x8_t, cw), acc[j], 0, 0, 0);
+        } else {
+          const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * 256) << a.cb_shift) + off);
+          const b16x8_t xb = __builtin_bit_cast(b16x8_t, R.xa[j]);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cw), acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cl), acc[j], 0, 0, 0);
+        }
+      }
+    }
+  };
+  // Two register sets in turn: the loads of the wave's run after next are requested while it
+  // computes one.
+  for (; r < n_runs; r += 2 * kWaves) {
+    compute(ra);
+    if (r + kWaves >= n_runs) break;
+    if (r + 2 * kWaves < n_runs) load_run(r + 2 * kWaves, ra);
+    compute(rb);
+    if (r + 3 * kWaves < n_runs) load_run(r + 3 * kWaves, rb);
+  }
+  // Partial tiles in wave order; element e of lane l is batch row 4 (l / 16) + e, weight row l % 16.
+  red[wave * 64 + lane] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  __syncthreads();
+  if (wave == 0) {
+    f32x4_t sum = red[lane];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) sum += red[w * 64 + lane];
+    const int row = row0 + col;
+    if (row < a.d_out) {
+      const float scale = f16_to_f32(a.scales[row]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int b = 4 * kc + e;
+        if (b < a.batch) {
+          const size_t o = (size_t)b * a.d_out + row;
+          const float v = sum[e] * scale;
+          if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, o, v);
+          else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, o, v);
+          else OutT<AQMB_F32>::store(a.y, o, v);
+        }
+      }
+    }
+  }
+}
+
+template <int K, int XDT>
+static hipError_t launch_mma_k(GemvMmaArgs a, hipStream_t st) {
+  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * 256 * 16;
+  const size_t budget = 160 * 1024 - 1024 - red;
+  a.nrep = book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
+  a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : 5;
+  const size_t lds = book * a.nrep + red;
+  const unsigned grid = (unsigned)((a.d_out + mg::kRows - 1) / mg::kRows);
+  gemv_mma_kernel<K, XDT><<<grid, mg::kThreads, lds, st>>>(a);
+  return hipGetLastError();
+}
+
+template <int XDT>
+static hipError_t launch_mma_x(const GemvMmaArgs& a, int k, hipStream_t st) {
+  switch (k) {
+    case 1: return launch_mma_k<1, XDT>(a, st);
+    case 2: return launch_mma_k<2, XDT>(a, st);
+    case 3: return launch_mma_k<3, XDT>(a, st);
+    case 4: return launch_mma_k<4, XDT>(a, st);
+    case 5: return launch_mma_k<5, XDT>(a, st);
+    case 6: return launch_mma_k<6, XDT>(a, st);
+    case 7: return launch_mma_k<7, XDT>(a, st);
+    default: return launch_mma_k<8, XDT>(a, st);
+  }
+}
+
+hipError_t launch_gemv_mma(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                           aqmb_dtype y_dtype, hipStream_t st) {
+  GemvMmaArgs a{};
+  a.codes = L.codes;
+  a.codebooks = L.codebooks;
+  a.scales = L.scales;
+  a.x = (const uint16_t*)x;
+  a.y = y;
+  a.zero_page = L.ws;                                       // the first KiB of the workspace stays zero
+  a.plane_bytes = L.plane_bytes;
+  a.d_out = L.d.d_out;
+  a.d_in = L.d.d_in;
+  a.G = L.G;
+  a.batch = batch;
+  a.y_dtype = (int)y_dtype;
+  return x_dtype == AQMB_F16 ? launch_mma_x<AQMB_F16>(a, k, st) : launch_mma_x<AQMB_BF16>(a, k, st);
+}
+
+}  // namespace aqmb

@@ -1,0 +1,57 @@
+"""Every GEMV kernel for 8-bit codes, whatever batch the default dispatch sends to it.
+
+By default batch 1..2 runs the direct-gather kernel and batch 3..16 the matrix-core kernel; the
+AQMB_GEMV variable (read once per process) forces one of them for every batch. A child process
+with the variable set runs the small GEMV cases against the oracle, so both kernels stay
+parity-tested at every batch. Oracle and tolerance as in the other GEMV tests.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU hosts too; every test here is marked gpu
+    pytest.skip("no GPU", allow_module_level=True)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+CHILD = r"""
+import sys
+sys.path.insert(0, {root!r}); sys.path.insert(0, {tests!r})
+import numpy as np, torch
+import oracle
+from oracle import formats
+from workloads import LayerSpec, make_layer, make_activations
+from gpu_helpers import GpuLayer, check_close, act_values, to_dev, out_values, TORCH_DT, A_DT
+import paper_2606_12876_amd as A
+for spec in [LayerSpec("ragged", 1000, 1032, seed=31), LayerSpec("M8", 520, 520, M=8, seed=34),
+             LayerSpec("wide", 130, 16392, M=4, seed=38)]:
+    L = make_layer(spec)
+    C, s = formats.f16_bits_to_f64(L.codebooks), formats.f16_bits_to_f64(L.scales)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for b in (1, 2, 3, 16):
+            for xdt in ("f16", "bf16"):
+                xbits = make_activations(L, b, xdt, heavy_tail=(b % 2 == 1))
+                x = act_values(xbits, xdt)
+                for k in sorted({{1, spec.M}}):
+                    ref = oracle.linear(x, L.codes, C, s, k)
+                    y = torch.empty((b, spec.d_out), dtype=torch.float32, device="cuda")
+                    A.gemv(gl.handle, k, to_dev(xbits).view(TORCH_DT[xdt]), A_DT[xdt], b, y, A.DType.F32)
+                    torch.cuda.synchronize()
+                    check_close(out_values(y), ref, "f32", f"{{spec.name}} b={{b}} k={{k}} {{xdt}}")
+print("variant ok", flush=True)
+"""
+
+
+@pytest.mark.parametrize("variant", ["mma", "cw"])
+def test_forced_variant_matches_oracle(variant):
+    env = dict(os.environ, AQMB_GEMV=variant)
+    code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"))
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "variant ok" in r.stdout, f"AQMB_GEMV={variant}:\n{r.stdout[-2000:]}\n{r.stderr[-3000:]}"
