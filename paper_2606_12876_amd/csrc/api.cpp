@@ -162,6 +162,20 @@ static hipError_t launch_gemv_any(const Layer& L, int k, const void* x, aqmb_dty
   return launch_gemv(L, k, x, x_dtype, batch, y, y_dtype, st);
 }
 
+// GEMM tiling: small token counts take the 16-row tiling (every CU busy), larger ones the
+// 256 x 128 tiles. AQMB_GEMM=small or =big forces one (read once).
+static int gemm_mode() {
+  static const int v = [] {
+    const char* e = getenv("AQMB_GEMM");
+    if (!e) return 0;
+    if (e[0] == 's' || e[0] == 'S') return 1;
+    if (e[0] == 'b' || e[0] == 'B') return 2;
+    return 0;
+  }();
+  return v;
+}
+constexpr int kGemmSmallMax = 192;   // tokens: the 16-row tiling re-gathers per 64 tokens; measured break-even near 256
+
 // k must name resident planes.
 static aqmb_status check_resident(const Layer* L, int k, const char* where) {
   if (k > L->resident)
@@ -335,7 +349,9 @@ aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, vo
   if (s != AQMB_OK) return s;
   if ((s = check_resident(L, k, "gemm")) != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
-  hipError_t e = launch_gemm(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream);
+  const bool small = gemm_mode() == 1 || (gemm_mode() == 0 && n_tokens <= kGemmSmallMax);
+  hipError_t e = small ? launch_gemm_small(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream)
+                       : launch_gemm(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemm: launch");
 }
 

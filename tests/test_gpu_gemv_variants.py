@@ -1,4 +1,4 @@
-"""Every GEMV kernel for 8-bit codes, whatever batch the default dispatch sends to it.
+"""Every GEMV kernel for 8-bit codes and both GEMM tilings, whatever the default dispatch picks.
 
 By default batch 1..2 runs the direct-gather kernel and batch 3..16 the matrix-core kernel; the
 AQMB_GEMV variable (read once per process) forces one of them for every batch. A child process
@@ -55,3 +55,35 @@ def test_forced_variant_matches_oracle(variant):
     code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"))
     r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
     assert r.returncode == 0 and "variant ok" in r.stdout, f"AQMB_GEMV={variant}:\n{r.stdout[-2000:]}\n{r.stderr[-3000:]}"
+
+
+GEMM_CHILD = r"""
+import sys
+sys.path.insert(0, {root!r}); sys.path.insert(0, {tests!r})
+import numpy as np, torch
+import oracle
+from workloads import LayerSpec, make_layer, make_activations
+from gpu_helpers import GpuLayer, check_close, act_values, to_dev, out_values
+import paper_2606_12876_amd as A
+for (n, d_out, d_in, M) in [(1, 40, 264, 2), (17, 257, 520, 3), (300, 200, 264, 4), (600, 130, 1032, 8)]:
+    L = make_layer(LayerSpec("g", d_out, d_in, M=M, seed=41 + n, act_dtype="bf16"))
+    Xbits = make_activations(L, n, "bf16", heavy_tail=True)
+    X = act_values(Xbits, "bf16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in sorted({{1, M}}):
+            ref = oracle.gemm_reference(X, L.codes, L.codebooks, L.scales, k)
+            Y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+            A.gemm(gl.handle, k, to_dev(Xbits).view(torch.bfloat16), n, Y, A.DType.F32)
+            torch.cuda.synchronize()
+            check_close(out_values(Y), ref, "f32", f"gemm n={{n}} {{d_out}}x{{d_in}} k={{k}}")
+print("variant ok", flush=True)
+"""
+
+
+@pytest.mark.parametrize("variant", ["small", "big"])
+def test_forced_gemm_tiling_matches_oracle(variant):
+    """Both GEMM tilings at token counts the default dispatch sends to the other one."""
+    env = dict(os.environ, AQMB_GEMM=variant)
+    code = GEMM_CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"))
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "variant ok" in r.stdout, f"AQMB_GEMM={variant}:\n{r.stdout[-2000:]}\n{r.stderr[-3000:]}"
