@@ -383,6 +383,9 @@ def main():
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(base, x1, x4, ks, gemv_bytes)
+        dist_cpu, beam_cpu = cpu_oracle_widened(base, make_weights, make_activations, M, d_in)
+        out["roofline_distortion"]["cpu_oracle"] = dist_cpu
+        out["roofline_beam"]["cpu_oracle"] = beam_cpu
 
     for h in layers + layers4:
         A.destroy(h)
@@ -423,6 +426,43 @@ def cpu_baseline(layer, x1bits, x4bits, ks, gemv_bytes):
             "sample": f"{passes} pass(es) of: reconstruct W_k in fp64 and multiply, batch 1 and 4, k=1..4, "
                       f"one {layer.spec.d_out}x{layer.spec.d_in} layer (gather single-threaded, product on BLAS)",
             "seconds": round(t_total, 2), "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def cpu_oracle_widened(layer, make_weights, make_activations, M, d_in):
+    """The oracle beside the distortion evaluator and the beam search, on bounded samples of the
+    same workloads (a few seconds each): the fp64 prefix distortions of the first 2048 rows over 1024
+    calibration inputs (in TFLOP/s of the same 2 (M + 1) d_out d_in n count), and the binary32
+    beam search of 64 groups (in candidates/s)."""
+    import oracle
+    from oracle import formats
+    from workloads import LayerSpec, make_layer
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    rows, n = 2048, 1024
+    C = formats.f16_bits_to_f64(layer.codebooks)
+    s = formats.f16_bits_to_f64(layer.scales)
+    W = formats.f16_bits_to_f64(make_weights(layer))[:rows]
+    X = formats.f16_bits_to_f64(make_activations(layer, n, "f16"))
+    t0 = time.perf_counter()
+    oracle.prefix_distortions(W, layer.codes[:, :rows], C, s[:rows], X)
+    td = time.perf_counter() - t0
+    dist = {"value": round(2.0 * (M + 1) * rows * d_in * n / td / 1e12, 4), "unit": "TFLOP/s",
+            "cores": int(blas_threads), "kind": "oracle", "seconds": round(td, 2),
+            "sample": f"fp64 prefix distortions of {rows} rows x {d_in} over {n} inputs (reconstruction "
+                      f"single-threaded, products on BLAS)"}
+    groups = [(i, j) for i in range(8) for j in range(8)]
+    t0 = time.perf_counter()
+    oracle.beam_search_codes_f32(formats.f16_bits_to_f64(make_weights(layer)[:8]), C[:BEAM_K], s[:8], BEAM_K,
+                                 BEAM_WIDTH, groups=groups)
+    tb = time.perf_counter() - t0
+    cands = len(groups) * 256 * (1 + (BEAM_K - 1) * BEAM_WIDTH)
+    beam = {"value": round(cands / tb, 1), "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "seconds": round(tb, 2), "sample": f"binary32 beam search (k={BEAM_K}, beam {BEAM_WIDTH}) of "
+                                                f"{len(groups)} groups, one thread"}
+    return dist, beam
 
 
 if __name__ == "__main__":
