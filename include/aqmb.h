@@ -149,8 +149,8 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
  * rounded to nearest-even bf16 (the operand fed to bf16 matrix cores); accumulation is fp32.
  *   X  [n_tokens][d_in]  bf16
  *   Y  [n_tokens][d_out] dtype y_dtype in {BF16, F32}
- * Requires B = 8. Errors: EINVAL (bad handle, null pointer, k outside [1, M], n_tokens < 1),
- * EUNSUPPORTED (B = 16, dtype), EHIP.
+ * Requires B = 8 or B = 4. Errors: EINVAL (bad handle, null pointer, k outside [1, M],
+ * n_tokens < 1), EUNSUPPORTED (B = 16, dtype), EHIP.
  */
 aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y,
                       aqmb_dtype y_dtype, aqmb_stream_t stream);
@@ -181,8 +181,8 @@ aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype,
  * The Hessian form of the same quantity, tr[(W - W_k) H (W - W_k)^T] / d_out with H = X X^T / n,
  * is obtained by passing any factor F with F F^T = H (e.g. a Cholesky factor) as Xt = F^T,
  * n = d_in, and multiplying D by d_in.
- * Requires B = 8. Uses the layer's workspace: calls on a layer must be ordered with each other
- * and with aqmb_gemv / aqmb_gemv_multi calls on that layer.
+ * Requires B = 8 or B = 4. Uses the layer's workspace: calls on a layer must be ordered with each
+ * other and with aqmb_gemv / aqmb_gemv_multi calls on that layer.
  * Errors: EINVAL (bad handle, null pointer, n < 1, misaligned pointer), EUNSUPPORTED (B = 16,
  * dtype other than F16, n > 2^30), EHIP.
  */
@@ -205,13 +205,14 @@ aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype
  * rounded; a candidate's d_t = fl(r_t - S_m[c][t]) and e = d_0 d_0 + d_1 d_1 + ... + d_7 d_7
  * with every product and every sum rounded, left to right, no fused multiply-add; candidates are
  * ordered by e, equal e by the code tuple (lexicographically).
- *   desc       the layer shape: d_out, d_in, g = 8, M codebooks, B = 8
+ *   desc       the layer shape: d_out, d_in, g = 8, M codebooks, B = 8 or 4
  *   W          [d_out][d_in] fp16 (device, 16-byte aligned): the weights to encode
- *   codebooks  [M][256][8] fp16 (device, 16-byte aligned); codebooks 0..k-1 are used
+ *   codebooks  [M][2^B][8] fp16 (device, 16-byte aligned); codebooks 0..k-1 are used
  *   scales     [d_out] fp16 (device)
- *   codes      [k][d_out][d_in/8] uint8 (device, output): plane-major, the layout aqmb_create takes
+ *   codes      [k][d_out][d_in/8] uint8 (device, output; values < 2^B): plane-major, the layout
+ *              aqmb_create takes
  *   errors     [d_out][d_in/8] float (device, output; may be NULL): e of the chosen tuple
- * 1 <= k <= M, 1 <= beam <= AQMB_MAX_BEAM. Work: 256 (1 + (k - 1) beam) candidates per group.
+ * 1 <= k <= M, 1 <= beam <= AQMB_MAX_BEAM. Work: 2^B (1 + (k - 1) beam) candidates per group.
  * Errors: EINVAL (null pointer, misaligned W or codebooks, k outside [1, M], beam < 1),
  * EUNSUPPORTED (B = 16, beam > AQMB_MAX_BEAM), EHIP.
  */

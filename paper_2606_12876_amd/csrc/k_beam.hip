@@ -1,5 +1,6 @@
 // Code search by beam search (Appendix C, code optimisation; Alg. 1 updates the assignments b by
-// beam search): for every group (row i, group j) of a dense weight matrix, the tuple
+// beam search), for codebooks of 256 (8-bit codes) or 16 (4-bit codes) codewords: for every group
+// (row i, group j) of a dense weight matrix, the tuple
 // (c_0, ..., c_{k-1}) of codewords of codebooks 0..k-1 that minimises the group's squared error
 // ||w - s_i sum_m C_m[c_m]||^2 is searched stage by stage, keeping the `beam` best partial tuples.
 //
@@ -77,17 +78,19 @@ __device__ __forceinline__ void insert(float (&le)[B], uint32_t (&lk)[B], float 
 
 }  // namespace
 
-template <int B>
+// NCW = codewords per codebook (256 for 8-bit codes, 16 for 4-bit codes).
+template <int B, int NCW>
 __global__ __launch_bounds__(beam::kThreads) void beam_kernel(BeamArgs a) {
-  __shared__ float4 sc[256][2];         // scaled codewords of the stage being searched
-  extern __shared__ uint4 cb_dyn[];     // fp16 codebooks 0..k-1: [k][256] 16-byte codewords
-  uint4 (*cb)[256] = (uint4 (*)[256])cb_dyn;
+  __shared__ float4 sc[NCW][2];         // scaled codewords of the stage being searched
+  extern __shared__ uint4 cb_dyn[];     // fp16 codebooks 0..k-1: [k][NCW] 16-byte codewords
+  uint4 (*cb)[NCW] = (uint4 (*)[NCW])cb_dyn;
   const int n_chunks = (a.G + beam::kThreads - 1) / beam::kThreads;
   const int tid = threadIdx.x, i = blockIdx.x / n_chunks, j = (blockIdx.x % n_chunks) * beam::kThreads + tid;
   const bool ok = j < a.G;
   const int jc = ok ? j : a.G - 1;
   const float s = f16_to_f32(a.scales[i]);
-  for (int m = 0; m < a.k; ++m) cb[m][tid] = ((const uint4*)a.codebooks)[m * 256 + tid];
+  if (tid < NCW)
+    for (int m = 0; m < a.k; ++m) cb[m][tid] = ((const uint4*)a.codebooks)[m * NCW + tid];
 
   float w[8];
   {
@@ -113,7 +116,7 @@ __global__ __launch_bounds__(beam::kThreads) void beam_kernel(BeamArgs a) {
 
   for (int m = 0; m < a.k; ++m) {
     __syncthreads();                    // codebooks written; previous stage done with sc
-    {
+    if (tid < NCW) {
       const uint4 v = cb[m][tid];
       const uint32_t u[4] = {v.x, v.y, v.z, v.w};
       float x[8];
@@ -136,7 +139,7 @@ __global__ __launch_bounds__(beam::kThreads) void beam_kernel(BeamArgs a) {
     }
     if (last) {
       // Only the best candidate is kept.
-      for (int c = 0; c < 256; ++c) {
+      for (int c = 0; c < NCW; ++c) {
         const float4 s0 = sc[c][0], s1 = sc[c][1];
 #pragma unroll
         for (int p = 0; p < B; ++p) {
@@ -150,7 +153,7 @@ __global__ __launch_bounds__(beam::kThreads) void beam_kernel(BeamArgs a) {
         }
       }
     } else {
-      for (int c = 0; c < 256; ++c) {
+      for (int c = 0; c < NCW; ++c) {
         const float4 s0 = sc[c][0], s1 = sc[c][1];
 #pragma unroll
         for (int p = 0; p < B; ++p) {
@@ -221,9 +224,10 @@ __global__ __launch_bounds__(beam::kThreads) void beam_kernel(BeamArgs a) {
 }
 
 template <int B>
-static hipError_t launch_beam_b(const BeamArgs& a, hipStream_t st) {
+static hipError_t launch_beam_b(const BeamArgs& a, int ncw, hipStream_t st) {
   const int grid = ((a.G + beam::kThreads - 1) / beam::kThreads) * a.d_out;   // validated below 2^31
-  beam_kernel<B><<<grid, beam::kThreads, (size_t)a.k * 256 * 16, st>>>(a);
+  if (ncw == 16) beam_kernel<B, 16><<<grid, beam::kThreads, (size_t)a.k * 16 * 16, st>>>(a);
+  else beam_kernel<B, 256><<<grid, beam::kThreads, (size_t)a.k * 256 * 16, st>>>(a);
   return hipGetLastError();
 }
 
@@ -239,23 +243,24 @@ hipError_t launch_beam_search(const aqmb_desc& d, int k, int beam_width, const v
   a.d_in = d.d_in;
   a.G = d.d_in / d.group_size;
   a.k = k;
+  const int ncw = 1 << d.code_bits;
   switch (beam_width) {
-    case 1: return launch_beam_b<1>(a, st);
-    case 2: return launch_beam_b<2>(a, st);
-    case 3: return launch_beam_b<3>(a, st);
-    case 4: return launch_beam_b<4>(a, st);
-    case 5: return launch_beam_b<5>(a, st);
-    case 6: return launch_beam_b<6>(a, st);
-    case 7: return launch_beam_b<7>(a, st);
-    case 8: return launch_beam_b<8>(a, st);
-    case 9: return launch_beam_b<9>(a, st);
-    case 10: return launch_beam_b<10>(a, st);
-    case 11: return launch_beam_b<11>(a, st);
-    case 12: return launch_beam_b<12>(a, st);
-    case 13: return launch_beam_b<13>(a, st);
-    case 14: return launch_beam_b<14>(a, st);
-    case 15: return launch_beam_b<15>(a, st);
-    default: return launch_beam_b<16>(a, st);
+    case 1: return launch_beam_b<1>(a, ncw, st);
+    case 2: return launch_beam_b<2>(a, ncw, st);
+    case 3: return launch_beam_b<3>(a, ncw, st);
+    case 4: return launch_beam_b<4>(a, ncw, st);
+    case 5: return launch_beam_b<5>(a, ncw, st);
+    case 6: return launch_beam_b<6>(a, ncw, st);
+    case 7: return launch_beam_b<7>(a, ncw, st);
+    case 8: return launch_beam_b<8>(a, ncw, st);
+    case 9: return launch_beam_b<9>(a, ncw, st);
+    case 10: return launch_beam_b<10>(a, ncw, st);
+    case 11: return launch_beam_b<11>(a, ncw, st);
+    case 12: return launch_beam_b<12>(a, ncw, st);
+    case 13: return launch_beam_b<13>(a, ncw, st);
+    case 14: return launch_beam_b<14>(a, ncw, st);
+    case 15: return launch_beam_b<15>(a, ncw, st);
+    default: return launch_beam_b<16>(a, ncw, st);
   }
 }
 

@@ -1,4 +1,4 @@
-// Distortion of every prefix level in one pass (the quantity the training loop of Drop-by-Drop
+// Distortion of every prefix level in one pass (8- or 4-bit codes) (the quantity the training loop of Drop-by-Drop
 // evaluates after each new codebook, section 5 and Alg. 1, with the weighted MSE of section 2.2,
 // Eq. wmse-task): for k = 1..M,
 //   D^(k) = ||(W - W^(k)) X||_F^2 / (d_out n),  W^(k)[i, j g + t] = s_i sum_{m<k} C_m[b_{ijm}][t],
@@ -36,12 +36,15 @@ constexpr int kPre = 2;                      // steps whose loads are in flight 
 constexpr int kBufs = kPre + 1;              // X buffers and register sets
 constexpr int kMaxGrid = 256;                // one workgroup per CU; each loops over work items
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
-template <int M> struct Cfg {
+// CB = code bits: 8 (256 codewords, replicated) or 4 (16 codewords: they fill the LDS banks once,
+// so one copy is read without conflicts).
+template <int M, int CB> struct Cfg {
   static constexpr int NA = M <= 6 ? 2 : 1;  // 32-sample blocks per wave (accumulators: 16 NA (M+1))
   static constexpr int kTok = 32 * NA;
-  static constexpr int kNrep = M <= 4 ? 8 : 4;                 // codebook replicas in LDS
-  static constexpr int kShift = kNrep == 8 ? 7 : 6;            // log2(16 kNrep)
-  static constexpr size_t kCbBytes = (size_t)M * 256 * kNrep * 16;
+  static constexpr int NCW = 1 << CB;
+  static constexpr int kNrep = CB == 4 ? 1 : M <= 4 ? 8 : 4;   // codebook replicas in LDS
+  static constexpr int kShift = kNrep == 8 ? 7 : kNrep == 4 ? 6 : 4;   // log2(16 kNrep)
+  static constexpr size_t kCbBytes = (size_t)M * NCW * kNrep * 16;
   static constexpr size_t kXBytes = (size_t)kTok * kStep * 2;  // one X stage
   static constexpr size_t kLds = kCbBytes + kBufs * kXBytes;
   static constexpr int kLoads = NA + 4 + M;                    // loads per wave per step
@@ -64,14 +67,15 @@ struct DistArgs {
   int d_out, d_in, n, n_rb, n_items;
 };
 
-template <int M>
+template <int M, int CB>
 __global__ __launch_bounds__(dist::kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void distortion_kernel(DistArgs a) {
   using namespace dist;
-  using C = Cfg<M>;
+  using C = Cfg<M, CB>;
   constexpr int NA = C::NA, kTok = C::kTok, kNrep = C::kNrep, kShift = C::kShift, kLoads = C::kLoads;
+  constexpr int NCW = C::NCW;
   extern __shared__ uint4 smem_d[];
-  uint4* cbr = smem_d;                                          // [M][256][kNrep] codewords
+  uint4* cbr = smem_d;                                          // [M][NCW][kNrep] codewords
   char* xs = (char*)smem_d + C::kCbBytes;                       // [kBufs][kTok][128 bytes]
   __shared__ double red[4][M];
 
@@ -80,9 +84,9 @@ void distortion_kernel(DistArgs a) {
   const int h = lane >> 5, r32 = lane & 31;
   const int nsteps = (a.d_in + kStep - 1) / kStep;
 
-  // Codebooks, replicated: replica r of codeword q (= m * 256 + c) at slot q * kNrep + r. The
+  // Codebooks, replicated: replica r of codeword q (= m * NCW + c) at slot q * kNrep + r. The
   // writers of one store instruction are rotated so that 16 consecutive q fill a bank row.
-  for (int q = tid; q < M * 256; q += kThreads) {
+  for (int q = tid; q < M * NCW; q += kThreads) {
     const uint4 v = ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - kShift);
 #pragma unroll
@@ -127,7 +131,9 @@ void distortion_kernel(DistArgs a) {
       const int g0 = (st < nsteps ? st : nsteps - 1) * 8;
 #pragma unroll
       for (int m = 0; m < M; ++m)
-        f.c[m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 8));
+        f.c[m] = CB == 8 ? *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 8))
+                         : make_uint2(*(const uint32_t*)(a.codes + m * a.plane_bytes +
+                                                         ((size_t)(g0 >> 5) * a.d_out + rowc) * 16 + ((g0 & 31) >> 1)), 0u);
     };
     // The loads of one step, issued in three parts (with the MFMAs of K-blocks 0, 1, 2 of the step
     // kPre earlier), kLoads in all.
@@ -159,9 +165,14 @@ void distortion_kernel(DistArgs a) {
       }
 #pragma unroll
       for (int m = 0; m < M; ++m) {
-        const uint32_t word = kb < 2 ? f.c[m].x : f.c[m].y;
-        const uint32_t code = (word >> (16 * (kb & 1) + 8 * h)) & 0xFFu;
-        o.bq[m] = *(const f16x8_t*)(cbase + ((uint32_t)(m * 256 + code) << kShift));
+        uint32_t code;
+        if constexpr (CB == 8) {
+          const uint32_t word = kb < 2 ? f.c[m].x : f.c[m].y;
+          code = (word >> (16 * (kb & 1) + 8 * h)) & 0xFFu;
+        } else {                                               // nibble `piece` of the step's word
+          code = (f.c[m].x >> (4 * piece)) & 15u;
+        }
+        o.bq[m] = *(const f16x8_t*)(cbase + ((uint32_t)(m * NCW + code) << kShift));
       }
     };
 
@@ -268,16 +279,21 @@ __global__ __launch_bounds__(dist::kMaxGrid) void distortion_reduce_kernel(const
   if (b < M) D[b] = s[b][0] * inv;
 }
 
-template <int M>
-static hipError_t launch_dist_m(DistArgs& a, hipStream_t st, int* grid_out) {
-  using C = dist::Cfg<M>;
+template <int M, int CB>
+static hipError_t launch_dist_mc(DistArgs& a, hipStream_t st, int* grid_out) {
+  using C = dist::Cfg<M, CB>;
   a.n_rb = (a.d_out + dist::kRows - 1) / dist::kRows;
   a.n_items = a.n_rb * ((a.n + C::kTok - 1) / C::kTok);
   const int grid = a.n_items < dist::kMaxGrid ? a.n_items : dist::kMaxGrid;
   static_assert(C::kLds <= 160 * 1024 - 512, "LDS budget");
-  distortion_kernel<M><<<grid, dist::kThreads, C::kLds, st>>>(a);
+  distortion_kernel<M, CB><<<grid, dist::kThreads, C::kLds, st>>>(a);
   *grid_out = grid;
   return hipGetLastError();
+}
+
+template <int M>
+static hipError_t launch_dist_m(DistArgs& a, int code_bits, hipStream_t st, int* grid_out) {
+  return code_bits == 4 ? launch_dist_mc<M, 4>(a, st, grid_out) : launch_dist_mc<M, 8>(a, st, grid_out);
 }
 
 hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n, double* D, hipStream_t st) {
@@ -296,14 +312,14 @@ hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n
   int grid = 0;
   hipError_t e;
   switch (L.resident) {                            // the resident levels
-    case 1: e = launch_dist_m<1>(a, st, &grid); break;
-    case 2: e = launch_dist_m<2>(a, st, &grid); break;
-    case 3: e = launch_dist_m<3>(a, st, &grid); break;
-    case 4: e = launch_dist_m<4>(a, st, &grid); break;
-    case 5: e = launch_dist_m<5>(a, st, &grid); break;
-    case 6: e = launch_dist_m<6>(a, st, &grid); break;
-    case 7: e = launch_dist_m<7>(a, st, &grid); break;
-    default: e = launch_dist_m<8>(a, st, &grid); break;
+    case 1: e = launch_dist_m<1>(a, L.d.code_bits, st, &grid); break;
+    case 2: e = launch_dist_m<2>(a, L.d.code_bits, st, &grid); break;
+    case 3: e = launch_dist_m<3>(a, L.d.code_bits, st, &grid); break;
+    case 4: e = launch_dist_m<4>(a, L.d.code_bits, st, &grid); break;
+    case 5: e = launch_dist_m<5>(a, L.d.code_bits, st, &grid); break;
+    case 6: e = launch_dist_m<6>(a, L.d.code_bits, st, &grid); break;
+    case 7: e = launch_dist_m<7>(a, L.d.code_bits, st, &grid); break;
+    default: e = launch_dist_m<8>(a, L.d.code_bits, st, &grid); break;
   }
   if (e != hipSuccess) return e;
   distortion_reduce_kernel<<<1, dist::kMaxGrid, 0, st>>>(a.partials, grid, L.resident,

@@ -1,4 +1,4 @@
-// Prefill GEMM for small token counts (8-bit codes): Y[n][i] = s_i sum_t X[n][t] Wb_k[i][t], with
+// Prefill GEMM for small token counts (8-bit codes; every token count for 4-bit codes): Y[n][i] = s_i sum_t X[n][t] Wb_k[i][t], with
 // Wb_k = RNE_bf16(binary32 left fold of C_m[b_{ijm}] over m < k), bf16 matrix cores, fp32 sums:
 // the arithmetic of the large-tile GEMM, on a tiling that keeps every CU busy when n is small.
 //
@@ -17,8 +17,10 @@ namespace aqmb {
 
 namespace gs {
 constexpr int kThreads = 512, kWaves = 8, kRows = 16;
-template <int K> struct Rep {                                // codebook replicas in LDS
-  static constexpr int kNrep = K <= 6 ? 4 : 2, kShift = K <= 6 ? 6 : 5;
+template <int K, int CB> struct Rep {                       // codebook replicas in LDS
+  // 16-codeword codebooks fill the LDS banks once: one copy reads without conflicts
+  static constexpr int kNrep = CB == 4 ? 1 : K <= 6 ? 4 : 2;
+  static constexpr int kShift = kNrep == 4 ? 6 : kNrep == 2 ? 5 : 4;
 };
 typedef __bf16 b16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -41,21 +43,22 @@ struct GsRun {
   uint4 c[K];
 };
 
-template <int K, int NA>
+// CB = code bits (8: a run is one 16-byte slice; 4: a run is half a slice, 8 bytes).
+template <int K, int NA, int CB>
 __global__ __launch_bounds__(gs::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_small_kernel(GemmSmallArgs a) {
   using namespace gs;
-  constexpr int kNrep = Rep<K>::kNrep, kShift = Rep<K>::kShift;
+  constexpr int kNrep = Rep<K, CB>::kNrep, kShift = Rep<K, CB>::kShift, NCW = 1 << CB;
   extern __shared__ uint4 smem_gs[];
-  uint4* cb_rep = smem_gs;                                   // [K][256][kNrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_gs + K * 256 * kNrep);      // [kWaves][NA][64] partial tiles
+  uint4* cb_rep = smem_gs;                                   // [K][NCW][kNrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_gs + K * NCW * kNrep);      // [kWaves][NA][64] partial tiles
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15, kc = lane >> 4;
   const int row0 = blockIdx.x * kRows;
   const int rowc = row0 + col < a.d_out ? row0 + col : a.d_out - 1;
   const int t0 = blockIdx.y * 16 * NA;                       // first token of the pass
-  const int n_runs = (a.G + 15) / 16;
+  const int n_runs = (a.G + 15) / 16;                        // 16-group runs (4-bit slices hold two)
   const uint32_t rep_off = (uint32_t)(lane & (kNrep - 1)) * 16;
 
   // Loads of run r (past the end: the last run again, never used).
@@ -72,14 +75,21 @@ void gemm_small_kernel(GemmSmallArgs a) {
       }
     }
 #pragma unroll
-    for (int m = 0; m < K; ++m) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+    for (int m = 0; m < K; ++m) {
+      if constexpr (CB == 8) {
+        R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+      } else {                                               // groups 16 rc .. + 15: half of slice rc / 2
+        const uint2 h = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(rc >> 1) * a.d_out + rowc) * 16 + (rc & 1) * 8);
+        R.c[m] = make_uint4(h.x, h.y, 0u, 0u);
+      }
+    }
   };
 
   GsRun<K, NA> ra, rb;
   int r = wave;
   load_run(r, ra);
   load_run(r + kWaves, rb);
-  for (int q = tid; q < K * 256; q += kThreads) {
+  for (int q = tid; q < K * NCW; q += kThreads) {
     const uint4 v = ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - kShift);
 #pragma unroll
@@ -97,9 +107,15 @@ void gemm_small_kernel(GemmSmallArgs a) {
       float w[8];
 #pragma unroll
       for (int m = 0; m < K; ++m) {
-        const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
-        const uint32_t code = (word >> (8 * kc)) & 0xFFu;
-        const uint4 cw = *(const uint4*)((const char*)cb_rep + (((uint32_t)(m * 256) + code) << kShift) + rep_off);
+        uint32_t code;
+        if constexpr (CB == 8) {
+          const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
+          code = (word >> (8 * kc)) & 0xFFu;
+        } else {                                             // nibble 4 j + kc of the run's 8 bytes
+          const uint32_t word = j < 2 ? R.c[m].x : R.c[m].y;
+          code = (word >> (4 * (4 * (j & 1) + kc))) & 15u;
+        }
+        const uint4 cw = *(const uint4*)((const char*)cb_rep + (((uint32_t)(m * NCW) + code) << kShift) + rep_off);
         const uint32_t u[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
@@ -153,19 +169,24 @@ void gemm_small_kernel(GemmSmallArgs a) {
   }
 }
 
-template <int K, int NA>
+template <int K, int NA, int CB>
 static hipError_t launch_small(const GemmSmallArgs& a, hipStream_t st) {
-  const size_t lds = (size_t)K * 256 * 16 * gs::Rep<K>::kNrep + (size_t)gs::kWaves * NA * 64 * 16;
+  const size_t lds = (size_t)K * (1 << CB) * 16 * gs::Rep<K, CB>::kNrep + (size_t)gs::kWaves * NA * 64 * 16;
   const dim3 grid((a.d_out + gs::kRows - 1) / gs::kRows, (a.n + 16 * NA - 1) / (16 * NA));
-  gemm_small_kernel<K, NA><<<grid, gs::kThreads, lds, st>>>(a);
+  gemm_small_kernel<K, NA, CB><<<grid, gs::kThreads, lds, st>>>(a);
   return hipGetLastError();
 }
 
+template <int K, int CB>
+static hipError_t launch_small_cb(const GemmSmallArgs& a, hipStream_t st) {
+  if (a.n <= 16) return launch_small<K, 1, CB>(a, st);
+  if (a.n <= 32) return launch_small<K, 2, CB>(a, st);
+  return launch_small<K, 4, CB>(a, st);
+}
+
 template <int K>
-static hipError_t launch_small_k(const GemmSmallArgs& a, hipStream_t st) {
-  if (a.n <= 16) return launch_small<K, 1>(a, st);
-  if (a.n <= 32) return launch_small<K, 2>(a, st);
-  return launch_small<K, 4>(a, st);
+static hipError_t launch_small_k(const GemmSmallArgs& a, int code_bits, hipStream_t st) {
+  return code_bits == 4 ? launch_small_cb<K, 4>(a, st) : launch_small_cb<K, 8>(a, st);
 }
 
 hipError_t launch_gemm_small(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
@@ -183,15 +204,16 @@ hipError_t launch_gemm_small(const Layer& L, int k, const void* X, int n_tokens,
   a.G = L.G;
   a.n = n_tokens;
   a.y_dtype = (int)y_dtype;
+  const int cb = L.d.code_bits;
   switch (k) {
-    case 1: return launch_small_k<1>(a, st);
-    case 2: return launch_small_k<2>(a, st);
-    case 3: return launch_small_k<3>(a, st);
-    case 4: return launch_small_k<4>(a, st);
-    case 5: return launch_small_k<5>(a, st);
-    case 6: return launch_small_k<6>(a, st);
-    case 7: return launch_small_k<7>(a, st);
-    default: return launch_small_k<8>(a, st);
+    case 1: return launch_small_k<1>(a, cb, st);
+    case 2: return launch_small_k<2>(a, cb, st);
+    case 3: return launch_small_k<3>(a, cb, st);
+    case 4: return launch_small_k<4>(a, cb, st);
+    case 5: return launch_small_k<5>(a, cb, st);
+    case 6: return launch_small_k<6>(a, cb, st);
+    case 7: return launch_small_k<7>(a, cb, st);
+    default: return launch_small_k<8>(a, cb, st);
   }
 }
 

@@ -52,7 +52,7 @@ aqmb_status validate_call(const aqmb_desc* d, int op, int k, int n, aqmb_dtype i
     if (!in || !out) return fail(AQMB_EINVAL, "beam_search: W or codes is NULL");
     if (n < 1) return fail(AQMB_EINVAL, "beam_search: beam = %d must be >= 1", n);
     if (n > AQMB_MAX_BEAM) return fail(AQMB_EUNSUPPORTED, "beam_search: beam = %d above %d", n, AQMB_MAX_BEAM);
-    if (d->code_bits != 8) return fail(AQMB_EUNSUPPORTED, "beam_search: only B = 8 codebooks are supported");
+    if (d->code_bits == 16) return fail(AQMB_EUNSUPPORTED, "beam_search: only B = 4 and B = 8 codebooks are supported");
     if ((uintptr_t)in % 16) return fail(AQMB_EINVAL, "beam_search: W must be 16-byte aligned");
     const uint64_t chunks = ((uint64_t)(d->d_in / d->group_size) + 255) / 256;
     if (chunks * (uint64_t)d->d_out >= (1ull << 31)) return fail(AQMB_EINVAL, "beam_search: matrix too large");
@@ -71,7 +71,7 @@ aqmb_status validate_call(const aqmb_desc* d, int op, int k, int n, aqmb_dtype i
     case 1:  // gemm
       if (!in || !out) return fail(AQMB_EINVAL, "gemm: X or Y is NULL");
       if (n < 1) return fail(AQMB_EINVAL, "gemm: n_tokens = %d must be >= 1", n);
-      if (d->code_bits != 8) return fail(AQMB_EUNSUPPORTED, "gemm: only B = 8 layers are supported");
+      if (d->code_bits == 16) return fail(AQMB_EUNSUPPORTED, "gemm: only B = 4 and B = 8 layers are supported");
       if (out_dt != AQMB_BF16 && out_dt != AQMB_F32)
         return fail(AQMB_EUNSUPPORTED, "gemm: Y dtype must be BF16 or F32");
       if ((uint64_t)n * (uint64_t)(d->d_in > d->d_out ? d->d_in : d->d_out) >= (1ull << 32))
@@ -86,7 +86,7 @@ aqmb_status validate_call(const aqmb_desc* d, int op, int k, int n, aqmb_dtype i
       if (!in || !out) return fail(AQMB_EINVAL, "prefix_distortion: X or D is NULL");
       if (n < 1) return fail(AQMB_EINVAL, "prefix_distortion: n = %d must be >= 1", n);
       if (n > (1 << 30)) return fail(AQMB_EUNSUPPORTED, "prefix_distortion: n = %d above 2^30", n);
-      if (d->code_bits != 8) return fail(AQMB_EUNSUPPORTED, "prefix_distortion: only B = 8 layers are supported");
+      if (d->code_bits == 16) return fail(AQMB_EUNSUPPORTED, "prefix_distortion: only B = 4 and B = 8 layers are supported");
       if (in_dt != AQMB_F16 || out_dt != AQMB_F16)
         return fail(AQMB_EUNSUPPORTED, "prefix_distortion: W and X must be F16");
       if ((uintptr_t)in % 16) return fail(AQMB_EINVAL, "prefix_distortion: X must be 16-byte aligned");

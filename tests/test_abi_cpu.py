@@ -155,14 +155,18 @@ def test_gemv_multi_rejects_before_any_launch():
 
 
 def test_four_bit_codes_validation():
-    """B = 4 (16-codeword codebooks): GEMV and dequant accept it; the GEMM, the distortion
-    evaluator and the beam search take 8-bit codes only."""
+    """B = 4 (16-codeword codebooks) is accepted by every operation; B = 16 by the GEMV and the
+    dequant only."""
     d = A.make_desc(256, 512, 4, code_bits=4)
     assert A.validate(d, 0, 4, 16, A.DType.BF16, A.DType.F32, 16, 32) == A.Status.OK
     assert A.validate(d, 2, 2, 0, A.DType.F16, A.DType.BF16, None, 16) == A.Status.OK
-    assert A.validate(d, 1, 1, 8, A.DType.BF16, A.DType.BF16, 16, 32) == A.Status.EUNSUPPORTED
-    assert A.validate(d, 3, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EUNSUPPORTED
-    assert A.validate(d, 4, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.EUNSUPPORTED
+    assert A.validate(d, 1, 1, 8, A.DType.BF16, A.DType.BF16, 16, 32) == A.Status.OK
+    assert A.validate(d, 3, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.OK
+    assert A.validate(d, 4, 1, 8, A.DType.F16, A.DType.F16, 16, 32) == A.Status.OK
+    d16 = A.make_desc(256, 512, 2, code_bits=16)
+    for op in (1, 3, 4):
+        assert A.validate(d16, op, 1, 8, A.DType.F16 if op != 1 else A.DType.BF16, A.DType.F16 if op != 1 else A.DType.BF16,
+                          16, 32) == A.Status.EUNSUPPORTED
     assert A.validate(A.make_desc(256, 512, 4, code_bits=2), 0, 1, 1, 0, 0, 16, 32) == A.Status.EUNSUPPORTED
 
 

@@ -1,5 +1,5 @@
-"""Layers with 4-bit codes (codebooks of 16 codewords): create, dequant and decode GEMV on the GPU
-against the oracle.
+"""Layers with 4-bit codes (codebooks of 16 codewords): create, dequant, decode GEMV, prefill GEMM
+and the prefix distortions on the GPU against the oracle.
 
 The 4 x 4-bit configuration is the one the paper's ablation on codebook precision against
 codebook count compares with 2 x 8 bits. The oracle is the same fp64 reconstruction and product
@@ -80,26 +80,50 @@ def test_codes_above_15_rejected():
     assert ei.value.status == A.Status.EINVAL and "15" in A.last_error()
 
 
-def test_unsupported_operations_and_multi():
-    """GEMM, the distortion evaluator and the beam search take 8-bit codes only; aqmb_gemv_multi
-    runs 4-bit layers one launch each, with results equal to aqmb_gemv."""
+@pytest.mark.parametrize("n", [1, 70, 300])
+def test_gemm_matches_oracle(n):
+    """4-bit layers run the 16-row GEMM tiling at every token count; same weight rounding (the
+    binary32 fold rounded to bf16) as the reference."""
+    L = make_layer(LayerSpec("g4", 200, 520, M=4, B=4, seed=340 + n, act_dtype="bf16"))
+    Xbits = make_activations(L, n, "bf16", heavy_tail=True)
+    X = act_values(Xbits, "bf16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in (1, 2, 4):
+            ref = oracle.gemm_reference(X, L.codes, L.codebooks, L.scales, k)
+            for ydt in ("f32", "bf16"):
+                Y = torch.empty((n, 200), dtype=TORCH_DT[ydt], device="cuda")
+                A.gemm(gl.handle, k, to_dev(Xbits).view(torch.bfloat16), n, Y, A_DT[ydt])
+                torch.cuda.synchronize()
+                check_close(out_values(Y), ref, ydt, f"gemm n={n} k={k} {ydt}")
+
+
+def test_prefix_distortion_matches_oracle():
+    from workloads import make_weights
+    L = make_layer(LayerSpec("d4", 257, 520, M=4, B=4, seed=350))
+    Wb = make_weights(L)
+    Xb = make_activations(L, 150, "f16")
+    C, s = _vals(L)
+    ref = oracle.prefix_distortions(formats.f16_bits_to_f64(Wb), L.codes, C, s, formats.f16_bits_to_f64(Xb))
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        D = torch.empty(4, dtype=torch.float64, device="cuda")
+        A.prefix_distortion(gl.handle, to_dev(Wb).view(torch.float16), A.DType.F16, to_dev(Xb).view(torch.float16),
+                            A.DType.F16, 150, D)
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(D.cpu().numpy(), ref, rtol=1e-5)
+
+
+def test_multi_layer_calls_mix_code_widths():
+    """aqmb_gemv_multi runs 4-bit layers one launch each, with results equal to aqmb_gemv."""
     L4 = make_layer(LayerSpec("m4", 96, 256, M=2, B=4, seed=330))
     L8 = make_layer(LayerSpec("m8", 40, 256, M=2, B=8, seed=331))
     with GpuLayer(L4.codes, L4.codebooks, L4.scales) as g4, GpuLayer(L8.codes, L8.codebooks, L8.scales) as g8:
-        X = torch.zeros((8, 256), dtype=torch.bfloat16, device="cuda")
-        Y = torch.zeros((8, 96), dtype=torch.float32, device="cuda")
-        assert A.lib.aqmb_gemm(g4.handle, 1, X.data_ptr(), 8, Y.data_ptr(), int(A.DType.F32), None) == A.Status.EUNSUPPORTED
-        W = torch.zeros((96, 256), dtype=torch.float16, device="cuda")
-        D = torch.zeros(2, dtype=torch.float64, device="cuda")
-        Xc = torch.zeros((8, 256), dtype=torch.float16, device="cuda")
-        assert A.lib.aqmb_prefix_distortion(g4.handle, W.data_ptr(), 0, Xc.data_ptr(), 0, 8, D.data_ptr(), None) \
-            == A.Status.EUNSUPPORTED
-        xbits = make_activations(L4, 2, "f16")
-        x = to_dev(xbits).view(torch.float16)
-        ys = [torch.empty((2, 96), dtype=torch.float32, device="cuda"), torch.empty((2, 40), dtype=torch.float32, device="cuda")]
-        A.gemv_multi([g4.handle, g8.handle], 2, x, A.DType.F16, 2, ys, A.DType.F32)
-        y1 = [torch.empty_like(t) for t in ys]
-        A.gemv(g4.handle, 2, x, A.DType.F16, 2, y1[0], A.DType.F32)
-        A.gemv(g8.handle, 2, x, A.DType.F16, 2, y1[1], A.DType.F32)
-        torch.cuda.synchronize()
-        assert torch.equal(ys[0], y1[0]) and torch.equal(ys[1], y1[1])
+        for b in (1, 2, 5):
+            xbits = make_activations(L4, b, "f16")
+            x = to_dev(xbits).view(torch.float16)
+            ys = [torch.empty((b, 96), dtype=torch.float32, device="cuda"), torch.empty((b, 40), dtype=torch.float32, device="cuda")]
+            A.gemv_multi([g4.handle, g8.handle], 2, x, A.DType.F16, b, ys, A.DType.F32)
+            y1 = [torch.empty_like(t) for t in ys]
+            A.gemv(g4.handle, 2, x, A.DType.F16, b, y1[0], A.DType.F32)
+            A.gemv(g8.handle, 2, x, A.DType.F16, b, y1[1], A.DType.F32)
+            torch.cuda.synchronize()
+            assert torch.equal(ys[0], y1[0]) and torch.equal(ys[1], y1[1])

@@ -28,7 +28,7 @@ from gpu_helpers import GpuLayer, to_dev  # noqa: E402
 def _gpu(L, Wbits, k, beam):
     spec = L.spec
     G = spec.d_in // 8
-    desc = A.make_desc(spec.d_out, spec.d_in, spec.M, 8)
+    desc = A.make_desc(spec.d_out, spec.d_in, spec.M, spec.B)
     codes = torch.full((k, spec.d_out, G), 0xAB, dtype=torch.uint8, device="cuda")
     errs = torch.full((spec.d_out, G), -1.0, dtype=torch.float32, device="cuda")
     A.beam_search(desc, k, beam, to_dev(Wbits).view(torch.float16), to_dev(L.codebooks), to_dev(L.scales),
@@ -73,6 +73,20 @@ def test_gaussian_bit_exact(k, beam):
     L = make_layer(LayerSpec("g", 5, 2400, M=4, seed=210 + k + beam))
     Wb = make_weights(L)
     _check(L, Wb, k, beam, f"gaussian k={k} beam={beam}")
+
+
+@pytest.mark.parametrize("k,beam", [(1, 3), (2, 4), (4, 16)])
+def test_four_bit_codebooks(k, beam):
+    """Codebooks of 16 codewords: integer inputs (codes of the fp64 search) and Gaussian ones."""
+    L = make_integer_layer(LayerSpec("int4", 9, 64, M=4, B=4, seed=250 + k))
+    Wb = make_integer_rows(L, 9, 16)
+    codes, errs = _check(L, Wb, k, beam, f"4-bit integer k={k} beam={beam}")
+    C = formats.f16_bits_to_f64(L.codebooks)
+    s = formats.f16_bits_to_f64(L.scales)
+    c64, t64 = oracle.beam_search_codes(formats.f16_bits_to_f64(Wb), C, s, k, beam)
+    assert np.array_equal(codes, c64) and float(errs.astype(np.float64).sum()) == t64
+    Lg = make_layer(LayerSpec("g4", 33, 2400, M=4, B=4, seed=260 + k))
+    _check(Lg, make_weights(Lg), k, beam, f"4-bit gaussian k={k} beam={beam}")
 
 
 def test_eight_codebooks_and_one_row():
