@@ -349,8 +349,7 @@ aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, vo
   if (s != AQMB_OK) return s;
   if ((s = check_resident(L, k, "gemm")) != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
-  // 4-bit codes: the 16-row tiling at every token count (the large tiles take 8-bit codes only)
-  const bool small = L->d.code_bits == 4 || gemm_mode() == 1 || (gemm_mode() == 0 && n_tokens <= kGemmSmallMax);
+  const bool small = gemm_mode() == 1 || (gemm_mode() == 0 && n_tokens <= kGemmSmallMax);
   hipError_t e = small ? launch_gemm_small(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream)
                        : launch_gemm(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemm: launch");

@@ -13,7 +13,9 @@
 //   - four producer waves dequantize the next step's weight slab into a double-buffered LDS
 //     buffer: per group, gather the k codewords from the codebooks held in LDS, fold them in
 //     binary32 and round to bf16. Each producer wave streams its own code words into its own
-//     LDS ring a few steps ahead with direct loads.
+//     LDS ring a few steps ahead with direct loads (8-bit codes: the 4 groups of its thread in one
+//     word per plane; 4-bit codes: the step's 8 groups in one word per plane, of which the thread
+//     takes its 4 nibbles).
 // X stages are row-major with the eight 16-byte pieces of a row XOR-swizzled by (row / 2) mod 8:
 // rows are 128 bytes, so two consecutive rows fill one 256-byte bank row, and any 16 consecutive
 // rows of a fragment read (one LDS cycle's worth of 16-byte lanes) hit 16 distinct 16-byte slots. Weight slabs are stored in MFMA operand
@@ -93,7 +95,8 @@ __device__ __forceinline__ uint4 dequant_group_bf16(const uint4* __restrict__ cb
   return make_uint4(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]), pack_bf16x2(w[4], w[5]), pack_bf16x2(w[6], w[7]));
 }
 
-template <int K, int YDT>
+// CB = code bits: 8 (256 codewords per codebook) or 4 (16 codewords).
+template <int K, int YDT, int CB>
 __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned char* __restrict__ codes,
                                                               const uint16_t* __restrict__ codebooks,
                                                               const uint16_t* __restrict__ scales,
@@ -102,11 +105,12 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
                                                               size_t plane_bytes, int n_tb, int n_cb) {
   using namespace gemm;
   constexpr int kDepth = x_depth<K>();
+  constexpr int NCW = 1 << CB;
   extern __shared__ uint4 smem[];
   uint16_t* Xs = (uint16_t*)smem;                  // [kDepth][256 rows][8 swizzled 16-byte pieces]
   uint16_t* Bs = Xs + kDepth * kXStage;            // [2][4 col blocks][4 K-blocks][64 lanes][8]
-  uint4* cbs = (uint4*)(Bs + 2 * kSlab);           // [K][256] codewords (fp16 x 8)
-  uint32_t* cring = (uint32_t*)(cbs + K * 256);     // [kCodeDepth][4 producer waves][K][64 lanes] code words
+  uint4* cbs = (uint4*)(Bs + 2 * kSlab);           // [K][NCW] codewords (fp16 x 8)
+  uint32_t* cring = (uint32_t*)(cbs + K * NCW);     // [kCodeDepth][4 producer waves][K][64 lanes] code words
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform across the wave
@@ -117,7 +121,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   const int s0 = (int)(((long long)cb * nsteps) / n_cb);
   auto step_of = [&](int seq) { int st = s0 + seq; return st >= nsteps ? st - nsteps : st; };
 
-  for (int q = tid; q < K * 256; q += kThreads) cbs[q] = ((const uint4*)codebooks)[q];
+  for (int q = tid; q < K * NCW; q += kThreads) cbs[q] = ((const uint4*)codebooks)[q];
 
   if (wave >= 4) {
     // ------------------------------------------------------------------ producers
@@ -134,12 +138,20 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
       return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)(cring + ((seq % kCodeDepth) * 4 + pw) * K * 64);
     };
     auto load_codes = [&](int seq) {
-      int j0 = step_of(seq) * (BK / 8) + 4 * gq;   // 4-aligned: one code word per plane
-      if (j0 >= G) j0 = 0;                          // padding groups: any valid word, zeroed later
       const uint32_t base = ring_base(seq);
+      if constexpr (CB == 8) {
+        int j0 = step_of(seq) * (BK / 8) + 4 * gq;   // 4-aligned: one code word per plane
+        if (j0 >= G) j0 = 0;                          // padding groups: any valid word, zeroed later
 #pragma unroll
-      for (int m = 0; m < K; ++m)
-        load_lds4(codes + m * plane_bytes + ((size_t)(j0 >> 4) * d_out + col_ld) * 16 + (j0 & 15), base + m * 256);
+        for (int m = 0; m < K; ++m)
+          load_lds4(codes + m * plane_bytes + ((size_t)(j0 >> 4) * d_out + col_ld) * 16 + (j0 & 15), base + m * 256);
+      } else {                                        // groups 8 s .. 8 s + 7: one word of a 32-group slice
+        int j0 = step_of(seq) * (BK / 8);
+        if (j0 >= G) j0 = 0;
+#pragma unroll
+        for (int m = 0; m < K; ++m)
+          load_lds4(codes + m * plane_bytes + ((size_t)(j0 >> 5) * d_out + col_ld) * 16 + ((j0 & 31) >> 1), base + m * 256);
+      }
     };
     auto wait_codes = [&](int seq) {               // this wave's words of step seq are in LDS
       const int after = min(kCodeDepth - 1, nsteps - 1 - seq);
@@ -160,7 +172,10 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int m = 0; m < K; ++m) cw[q][m] = cbs[m * 256 + ((word[m] >> (8 * q)) & 0xFFu)];
+        for (int m = 0; m < K; ++m) {
+          const uint32_t code = CB == 8 ? (word[m] >> (8 * q)) & 0xFFu : (word[m] >> (4 * (4 * gq + q))) & 15u;
+          cw[q][m] = cbs[m * NCW + code];
+        }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int g = 4 * gq + q;                   // group within the step: K-block g / 2, half g % 2
@@ -288,19 +303,25 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   }
 }
 
-template <int K>
-static void launch_k(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
+template <int K, int CB>
+static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
   using namespace gemm;
   constexpr int kDepth = x_depth<K>();
   const int n_tb = (n_tokens + BM - 1) / BM, n_cb = (L.d.d_out + BN - 1) / BN;
-  const size_t lds = ((size_t)kDepth * kXStage + 2 * kSlab) * 2 + (size_t)K * 256 * 16 + (size_t)kCodeDepth * 4 * K * 64 * 4;
+  const size_t lds = ((size_t)kDepth * kXStage + 2 * kSlab) * 2 + (size_t)K * (1 << CB) * 16 + (size_t)kCodeDepth * 4 * K * 64 * 4;
   const dim3 grid(n_tb * n_cb);
   if (y_dtype == AQMB_BF16)
-    gemm_kernel<K, AQMB_BF16><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                            n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+    gemm_kernel<K, AQMB_BF16, CB><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
+                                                                n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
   else
-    gemm_kernel<K, AQMB_F32><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                           n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+    gemm_kernel<K, AQMB_F32, CB><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
+                                                               n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+}
+
+template <int K>
+static void launch_k(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
+  if (L.d.code_bits == 4) launch_kc<K, 4>(L, X, n_tokens, Y, y_dtype, st);
+  else launch_kc<K, 8>(L, X, n_tokens, Y, y_dtype, st);
 }
 
 hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,

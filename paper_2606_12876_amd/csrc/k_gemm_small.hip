@@ -1,4 +1,4 @@
-// Prefill GEMM for small token counts (8-bit codes; every token count for 4-bit codes): Y[n][i] = s_i sum_t X[n][t] Wb_k[i][t], with
+// Prefill GEMM for small token counts (8- and 4-bit codes): Y[n][i] = s_i sum_t X[n][t] Wb_k[i][t], with
 // Wb_k = RNE_bf16(binary32 left fold of C_m[b_{ijm}] over m < k), bf16 matrix cores, fp32 sums:
 // the arithmetic of the large-tile GEMM, on a tiling that keeps every CU busy when n is small.
 //

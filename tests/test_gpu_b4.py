@@ -80,11 +80,12 @@ def test_codes_above_15_rejected():
     assert ei.value.status == A.Status.EINVAL and "15" in A.last_error()
 
 
-@pytest.mark.parametrize("n", [1, 70, 300])
+@pytest.mark.parametrize("n", [1, 70, 300, 1100])
 def test_gemm_matches_oracle(n):
-    """4-bit layers run the 16-row GEMM tiling at every token count; same weight rounding (the
-    binary32 fold rounded to bf16) as the reference."""
-    L = make_layer(LayerSpec("g4", 200, 520, M=4, B=4, seed=340 + n, act_dtype="bf16"))
+    """Both tilings (16-row up to 192 tokens, large tiles above: 300 and 1100 tokens span ragged
+    token and row tiles and a ragged last K step); same weight rounding (the binary32 fold rounded
+    to bf16) as the reference."""
+    L = make_layer(LayerSpec("g4", 200, 1032, M=4, B=4, seed=340 + n, act_dtype="bf16"))
     Xbits = make_activations(L, n, "bf16", heavy_tail=True)
     X = act_values(Xbits, "bf16")
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
@@ -95,6 +96,24 @@ def test_gemm_matches_oracle(n):
                 A.gemm(gl.handle, k, to_dev(Xbits).view(torch.bfloat16), n, Y, A_DT[ydt])
                 torch.cuda.synchronize()
                 check_close(out_values(Y), ref, ydt, f"gemm n={n} k={k} {ydt}")
+
+
+def test_gemm_full_size_sampled():
+    """The prefill shape (2048 tokens x 4096 x 4096, 4 codebooks of 16 codewords): every output
+    of 24 sampled token rows against the reference, at k = 1 and 4."""
+    L = make_layer(LayerSpec("g4full", 4096, 4096, M=4, B=4, seed=345, act_dtype="bf16"))
+    n = 2048
+    Xbits = make_activations(L, n, "bf16")
+    rows = np.sort(np.random.default_rng(9).choice(n, 24, replace=False))
+    X = act_values(Xbits[rows], "bf16")
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        Xd = to_dev(Xbits).view(torch.bfloat16)
+        for k in (1, 4):
+            Y = torch.empty((n, 4096), dtype=torch.bfloat16, device="cuda")
+            A.gemm(gl.handle, k, Xd, n, Y, A.DType.BF16)
+            torch.cuda.synchronize()
+            ref = oracle.gemm_reference(X, L.codes, L.codebooks, L.scales, k)
+            check_close(out_values(Y)[rows], ref, "bf16", f"gemm 2048x4096x4096 B=4 k={k}")
 
 
 def test_prefix_distortion_matches_oracle():

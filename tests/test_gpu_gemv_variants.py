@@ -1,4 +1,4 @@
-"""Every GEMV kernel for 8-bit codes and both GEMM tilings, whatever the default dispatch picks.
+"""Every GEMV kernel for 8-bit codes and both GEMM tilings (8- and 4-bit codes), whatever the default dispatch picks.
 
 By default batch 1..2 runs the direct-gather kernel and batch 3..16 the matrix-core kernel; the
 AQMB_GEMV variable (read once per process) forces one of them for every batch. A child process
@@ -65,8 +65,9 @@ import oracle
 from workloads import LayerSpec, make_layer, make_activations
 from gpu_helpers import GpuLayer, check_close, act_values, to_dev, out_values
 import paper_2606_12876_amd as A
-for (n, d_out, d_in, M) in [(1, 40, 264, 2), (17, 257, 520, 3), (300, 200, 264, 4), (600, 130, 1032, 8)]:
-    L = make_layer(LayerSpec("g", d_out, d_in, M=M, seed=41 + n, act_dtype="bf16"))
+for (n, d_out, d_in, M, B) in [(1, 40, 264, 2, 8), (17, 257, 520, 3, 8), (300, 200, 264, 4, 8), (600, 130, 1032, 8, 8),
+                               (17, 257, 520, 3, 4), (300, 200, 264, 4, 4), (600, 130, 1032, 8, 4)]:
+    L = make_layer(LayerSpec("g", d_out, d_in, M=M, B=B, seed=41 + n + B, act_dtype="bf16"))
     Xbits = make_activations(L, n, "bf16", heavy_tail=True)
     X = act_values(Xbits, "bf16")
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
@@ -75,7 +76,7 @@ for (n, d_out, d_in, M) in [(1, 40, 264, 2), (17, 257, 520, 3), (300, 200, 264, 
             Y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
             A.gemm(gl.handle, k, to_dev(Xbits).view(torch.bfloat16), n, Y, A.DType.F32)
             torch.cuda.synchronize()
-            check_close(out_values(Y), ref, "f32", f"gemm n={{n}} {{d_out}}x{{d_in}} k={{k}}")
+            check_close(out_values(Y), ref, "f32", f"gemm n={{n}} {{d_out}}x{{d_in}} B={{B}} k={{k}}")
 print("variant ok", flush=True)
 """
 
