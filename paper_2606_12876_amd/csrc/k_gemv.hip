@@ -360,17 +360,30 @@ __host__ __device__ inline size_t row_stride(int S) {   // bytes per staged x ro
 
 constexpr int kCwMaxBlocks = 4;   // 512-group blocks per row held in registers: d_in <= 16384
 
+// <x group, codeword> of fp16 values added to s (a group's running sum over the planes).
+__device__ __forceinline__ float group_dot_acc(uint4 xw, uint4 cw, float s) {
+  s = dot2_f16(xw.x, cw.x, s);
+  s = dot2_f16(xw.y, cw.y, s);
+  s = dot2_f16(xw.z, cw.z, s);
+  return dot2_f16(xw.w, cw.w, s);
+}
+
 // The gather-and-reduce part shared by the direct-gather kernels. For this thread's row and part,
 // gather the codewords of its groups (code words in `code`: UB blocks x K planes, already
 // requested), dot them with the NB staged x rows, reduce each row in a fixed order (a butterfly
 // over the wave's parts, then the waves in order), scale by `scale` (the row's, loaded by the
 // caller with the code words) and store y rows b0 .. b0 + NB - 1 (those below `batch`) of output
 // row `row`. `red` is reused: the caller separates calls with a barrier.
-template <int K, int NB, int XDT, int UB>
+// The staged x holds fp16 values: the input itself, or (XS) bf16 input converted by
+// cw_convert_own_bf16 to x / scl[group] (scl rows of rstride / 16 floats). A group's dot products
+// are chained over the planes into one partial sum (independent chains, one v_dot2 per code word
+// pair), which is then added to the row's accumulator (XS: multiplied by the group's scale).
+template <int K, int NB, int UB, bool XS>
 __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4* cb_rep, const uint16_t* xs,
                                         size_t rstride, int Gp, int cb_shift, uint32_t rep_off,
                                         float (&red)[cw::kWaves][cw::kRows][NB], int b0, int batch, int row,
-                                        bool row_ok, float scale, void* y, int d_out, int y_dtype) {
+                                        bool row_ok, float scale, void* y, int d_out, int y_dtype,
+                                        const float* scl) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rw = lane & 15, part = tid >> 4;
@@ -388,6 +401,9 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
       uint4 xg[8];
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) xg[jj] = *(const uint4*)(xrow + jj * 16);
+      float t[8];                                          // per-group sums over the planes
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) t[jj] = 0.f;
 #pragma unroll
       for (int m = 0; m < K; ++m) {
         // plane m's code word is awaited here, not earlier (the empty asm keeps its unpacking
@@ -403,22 +419,41 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
           cw[jj] = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + base);
         }
 #pragma unroll
-        for (int jj = 0; jj < 8; ++jj) acc[0] += group_dot<XDT>(xg[jj], cw[jj]);
+        for (int jj = 0; jj < 8; ++jj) t[jj] = group_dot_acc(xg[jj], cw[jj], t[jj]);
+      }
+      if constexpr (XS) {                                  // the group scales, read once the sums are done
+        const float4 s0 = *(const float4*)(scl + j0), s1 = *(const float4*)(scl + j0 + 4);
+        const float xsc[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) acc[0] = __builtin_fmaf(t[jj], xsc[jj], acc[0]);
+      } else {
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) acc[0] += t[jj];
       }
     } else {
       // group-major: the NB x vectors of a group are read once and used for every plane
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) {
         uint4 xg[NB];
+        float t[NB], xsc[NB];
 #pragma unroll
-        for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xrow + b * rstride + jj * 16);
+        for (int b = 0; b < NB; ++b) {
+          xg[b] = *(const uint4*)(xrow + b * rstride + jj * 16);
+          if constexpr (XS) xsc[b] = scl[(size_t)b * (rstride / 16) + j0 + jj];
+          t[b] = 0.f;
+        }
 #pragma unroll
         for (int m = 0; m < K; ++m) {
           const uint32_t word = jj < 4 ? code[u][m].x : code[u][m].y;
           const uint32_t c = (word >> (8 * (jj & 3))) & 0xFFu;
           const uint4 cwv = *(const uint4*)((const char*)cb_rep + (c << cb_shift) + (uint32_t)(m * 256) * cb_stride + rep_off);
 #pragma unroll
-          for (int b = 0; b < NB; ++b) acc[b] += group_dot<XDT>(xg[b], cwv);
+          for (int b = 0; b < NB; ++b) t[b] = group_dot_acc(xg[b], cwv, t[b]);
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          if constexpr (XS) acc[b] = __builtin_fmaf(t[b], xsc[b], acc[b]);
+          else acc[b] += t[b];
         }
       }
     }
@@ -481,6 +516,38 @@ __device__ __forceinline__ void cw_stage_x(const void* x, const void* zero_page,
   }
 }
 
+// bf16 x -> fp16, one power-of-two scale per 8-value group: this thread converts in place the
+// 16-byte groups its own cw_stage_x loads brought in (so no barrier is needed before it; the
+// caller's barrier publishes the result) and writes the group's scale 2^e to scl. e puts the
+// group's largest magnitude in [2^14, 2^15), where a bf16 value (8 significant bits) is exact in
+// fp16; only values below 2^-29 of the group maximum fall in the fp16 subnormal range and are
+// rounded, to a multiple of 2^-39 of it (far below the rounding of the fp32 sums). The fp16 dot
+// products then apply and cw_tile multiplies each group's sum by its scale.
+template <int NB>
+__device__ __forceinline__ void cw_convert_own_bf16(uint16_t* xs, float* scl, size_t rstride) {
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int nch = (int)(rstride / 1024);
+  for (int q = wave; q < NB * nch; q += cw::kWaves) {
+    const int b = q / nch, ch = q % nch;
+    const int g = ch * 64 + lane;                          // group of the row (the one this lane loaded)
+    char* p = (char*)xs + (size_t)b * rstride + (size_t)g * 16;
+    const uint4 v = *(const uint4*)p;
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t e = 0;                                        // largest exponent field (bf16 subnormals: 0)
+#pragma unroll
+    for (int h = 0; h < 4; ++h) e = max(e, max((w[h] >> 7) & 0xFFu, (w[h] >> 23) & 0xFFu));
+    const int sh = (int)e - 141;                           // (e - 127) - 14
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const _Float16 lo = (_Float16)ldexpf(bf16lo(w[h]), -sh);
+      const _Float16 hi = (_Float16)ldexpf(bf16hi(w[h]), -sh);
+      w[h] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+    }
+    *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
+    scl[(size_t)b * (rstride / 16) + g] = ldexpf(1.0f, sh);
+  }
+}
+
 // This thread's code words (UB blocks x K planes) of row `rowc`: 8 groups per (block, plane),
 // streaming loads, addresses clamped so that every thread issues the same loads.
 template <int K, int UB>
@@ -505,6 +572,7 @@ void gemv_cw_kernel(GemvArgs a) {
   uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords
   uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);    // [NB][row_stride] x tile
   __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
+  constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group
   const int tid = threadIdx.x, lane = tid & 63;
   const int rw = lane & 15;
   const int row = blockIdx.x * cw::kRows + rw;
@@ -523,20 +591,23 @@ void gemv_cw_kernel(GemvArgs a) {
   uint2 code[UB][K];
   cw_load_codes<K, UB>(code, a.codes, a.plane_bytes, a.d_out, rowc, Gp);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in (older than the scale and codes)
+  float* scl = (float*)((char*)xs + NB * rstride);         // bf16 x: [NB][rstride / 16] group scales
+  if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
   cw_replicate<K>(cb_rep, cbv, nrep, a.cb_shift);
   __syncthreads();
 
   // The first batch tile is peeled out of the loop so that its waits for the code planes are exact.
   const float scale = f16_to_f32(sbits);
-  cw_tile<K, NB, XDT, UB>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row, row_ok,
-                          scale, a.y, a.d_out, a.y_dtype);
+  cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row, row_ok,
+                          scale, a.y, a.d_out, a.y_dtype, scl);
   for (int b0 = NB; b0 < a.batch; b0 += NB) {
     __syncthreads();                                       // the previous tile's reads of xs are done
     cw_stage_x<NB>(a.x, a.zero_page, b0, a.batch, a.d_in, rstride, xs_base);
     wait_vmcnt<0>();
+    if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
     __syncthreads();
-    cw_tile<K, NB, XDT, UB>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, b0, a.batch, row, row_ok,
-                            scale, a.y, a.d_out, a.y_dtype);
+    cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, b0, a.batch, row, row_ok,
+                            scale, a.y, a.d_out, a.y_dtype, scl);
   }
 }
 
@@ -597,10 +668,12 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
     sbits = a.L[l].scales[rowc];
     cw_load_codes<K, UB>(code, a.L[l].codes, a.L[l].plane_bytes, d_out, rowc, Gp);
   };
+  constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group, once
+  float* scl = (float*)((char*)xs + NB * rstride);         // [NB][rstride / 16] group scales
   auto run_layer = [&](int l, uint32_t sbits, const uint2 (&code)[UB][K]) {
     const int d_out = a.L[l].d_out;
-    cw_tile<K, NB, XDT, UB>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
-                            row < d_out, f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype);
+    cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
+                            row < d_out, f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype, scl);
   };
 
   int cur = next_layer(-1);                                // the grid never exceeds the largest layer
@@ -611,6 +684,7 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   uint2 ca[UB][K], cb[UB][K];
   load_layer(cur, cba, sa, ca);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
+  if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
   cw_replicate<K>(cb_rep, cba, nrep, a.cb_shift);
   __syncthreads();
   for (;;) {
@@ -633,16 +707,18 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   }
 }
 
-// LDS bytes of the direct-gather kernel: replicated codebooks plus the x tile.
-static size_t cw_lds(int K, int nb, int S, int nrep) {
-  return (size_t)K * 256 * nrep * 16 + (size_t)nb * cw::row_stride(S);
+// LDS bytes of the direct-gather kernel: replicated codebooks plus the x tile (plus one float
+// per staged group for bf16 x).
+static size_t cw_lds(int K, int nb, int S, int nrep, bool bf16) {
+  const size_t xt = (size_t)nb * cw::row_stride(S);
+  return (size_t)K * 256 * nrep * 16 + xt + (bf16 ? xt / 4 : 0);
 }
 
 // Replicas per codebook: as many as fit next to the x tile (LDS holds 160 KiB per workgroup).
-static int cw_nrep(int K, int nb, int S) {
+static int cw_nrep(int K, int nb, int S, bool bf16) {
   const size_t budget = 160 * 1024 - (size_t)cw::kWaves * cw::kRows * 4 * nb - 512;  // minus the row sums
   for (int r : {8, 4})
-    if (cw_lds(K, nb, S, r) <= budget) return r;
+    if (cw_lds(K, nb, S, r, bf16) <= budget) return r;
   return 0;
 }
 
@@ -651,11 +727,11 @@ static int cw_blocks(int S) { return (S * 16 + 511) / 512; }
 
 template <int K, int NB, int XDT>
 static hipError_t launch_cw_nb(GemvArgs a, hipStream_t st) {
-  a.nrep = cw_nrep(K, NB, a.S);
+  a.nrep = cw_nrep(K, NB, a.S, XDT == AQMB_BF16);
   if (a.nrep == 0) return hipErrorInvalidValue;  // x tile does not fit: caller uses another path
   a.cb_shift = a.nrep == 8 ? 7 : 6;
   const dim3 grid((a.d_out + cw::kRows - 1) / cw::kRows);
-  const size_t lds = cw_lds(K, NB, a.S, a.nrep);
+  const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
   if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
   else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks><<<grid, cw::kThreads, lds, st>>>(a);
   return hipGetLastError();
@@ -670,8 +746,8 @@ static hipError_t launch_cw(const GemvArgs& a, hipStream_t st) {
 
 // The direct-gather kernel covers k <= 4 and d_in <= 16384 (the code words of a thread's
 // groups stay in registers); other shapes take the lookup-table path.
-static bool cw_fits(int K, int batch, int S) {
-  return K <= 4 && cw_blocks(S) <= kCwMaxBlocks && cw_nrep(K, cw_nb(batch), S) > 0;
+static bool cw_fits(int K, int batch, int S, bool bf16) {
+  return K <= 4 && cw_blocks(S) <= kCwMaxBlocks && cw_nrep(K, cw_nb(batch), S, bf16) > 0;
 }
 
 template <int K, int XDT>
@@ -743,7 +819,7 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   a.y_dtype = (int)y_dtype;
   const dim3 grid((L.d.d_out + kRowsPerWG - 1) / kRowsPerWG, L.S);
   const bool b16 = L.d.code_bits == 16;
-  if (!b16 && gemv_variant() == 1 && cw_fits(k, batch, L.S)) {   // direct gather: one kernel
+  if (!b16 && gemv_variant() == 1 && cw_fits(k, batch, L.S, x_dtype == AQMB_BF16)) {   // direct gather: one kernel
     return x_dtype == AQMB_F16 ? launch_cw_any<AQMB_F16>(a, st) : launch_cw_any<AQMB_BF16>(a, st);
   }
   if (x_dtype == AQMB_F16) launch_x<AQMB_F16>(a, b16, grid, st);
@@ -758,9 +834,9 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
 
 template <int K, int NB, int XDT>
 static hipError_t launch_multi_nb(GemvMultiArgs a, int grid, hipStream_t st) {
-  a.nrep = cw_nrep(K, NB, a.S);
+  a.nrep = cw_nrep(K, NB, a.S, XDT == AQMB_BF16);
   a.cb_shift = a.nrep == 8 ? 7 : 6;
-  const size_t lds = cw_lds(K, NB, a.S, a.nrep);
+  const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
   if (cw_blocks(a.S) == 1) gemv_cw_multi_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
   else gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks><<<grid, cw::kThreads, lds, st>>>(a);
   return hipGetLastError();
@@ -788,7 +864,7 @@ hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x
   // One launch when every layer takes the direct-gather path in a single batch tile (8-bit codes,
   // k <= 4, batch <= 4); otherwise the layers are launched one after another.
   const Layer& L0 = *Ls[0];
-  bool one = batch <= 4 && gemv_variant() == 1 && cw_fits(k, batch, L0.S);
+  bool one = batch <= 4 && gemv_variant() == 1 && cw_fits(k, batch, L0.S, x_dtype == AQMB_BF16);
   for (int i = 0; i < n && one; ++i) one = Ls[i]->d.code_bits == 8;
   if (!one) {
     for (int i = 0; i < n; ++i) {

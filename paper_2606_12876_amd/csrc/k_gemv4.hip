@@ -52,15 +52,30 @@ __device__ __forceinline__ float dot8(uint4 xw, uint4 cw) {
   }
 }
 
+// <x group, codeword> of fp16 values added to s.
+__device__ __forceinline__ float dot8_acc_f16(uint4 xw, uint4 cw, float s) {
+  s = dot2_f16(xw.x, cw.x, s);
+  s = dot2_f16(xw.y, cw.y, s);
+  s = dot2_f16(xw.z, cw.z, s);
+  return dot2_f16(xw.w, cw.w, s);
+}
+
 // UB = 512-group blocks per x stage: 1 when a row has at most 512 groups (no load is issued for
 // blocks past the row), else 4.
+// bf16 x at batch 1: every staged 16-byte group is converted in place to fp16 by the thread that
+// loaded it, with a power-of-two scale per group (largest magnitude put in [2^14, 2^15), where
+// bf16's 8 significant bits are exact in fp16; values below 2^-29 of the group maximum are
+// rounded to a multiple of 2^-39 of it), so the fp16 dot products apply; a group's sums over the
+// planes are multiplied by its scale.
 template <int K, int NB, int XDT, int UB>
 __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
   constexpr int kTiles = NB == 1 ? 1 : 4;    // batch <= 16
   constexpr int kChunk = UB * 512;
+  constexpr bool kXS = XDT == AQMB_BF16 && NB == 1;
   extern __shared__ uint4 smem_b4[];
   uint4* cb = smem_b4;                                       // [K][16] codewords
   char* xs = (char*)(smem_b4 + K * 16);                      // [NB][kChunk][16 bytes]
+  float* scl = (float*)(xs + (size_t)NB * kChunk * 16);      // kXS: [kChunk] group scales
   __shared__ float red[b4::kWaves][b4::kRows][NB];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -106,6 +121,26 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
           load_lds16(src, xs_base + (uint32_t)(b * kChunk * 16 + ch * 1024));
         }
         wait_vmcnt<0>();
+        if constexpr (kXS) {                                 // the groups this thread loaded
+          for (int q = wave; q < n_ch; q += b4::kWaves) {
+            const int gq = q * 64 + lane;
+            char* p = xs + (size_t)gq * 16;
+            const uint4 v = *(const uint4*)p;
+            uint32_t w[4] = {v.x, v.y, v.z, v.w};
+            uint32_t e = 0;
+#pragma unroll
+            for (int h = 0; h < 4; ++h) e = max(e, max((w[h] >> 7) & 0xFFu, (w[h] >> 23) & 0xFFu));
+            const int sh = (int)e - 141;                     // (e - 127) - 14
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+              const _Float16 lo = (_Float16)ldexpf(bf16lo(w[h]), -sh);
+              const _Float16 hi = (_Float16)ldexpf(bf16hi(w[h]), -sh);
+              w[h] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+            }
+            *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
+            scl[gq] = ldexpf(1.0f, sh);
+          }
+        }
         __syncthreads();
 #pragma unroll
         for (int u = 0; u < UB; ++u) {
@@ -115,12 +150,18 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
               uint4 xg[NB];
 #pragma unroll
               for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xs + (size_t)b * kChunk * 16 + (size_t)(j0 + jj) * 16);
+              float gs = 0.f;                                // kXS: the group's sum over the planes
 #pragma unroll
               for (int m = 0; m < K; ++m) {
                 const uint4 cwv = cb[m * 16 + ((code[u][m] >> (4 * jj)) & 15u)];
+                if constexpr (kXS) {
+                  gs = dot8_acc_f16(xg[0], cwv, gs);
+                } else {
 #pragma unroll
-                for (int b = 0; b < NB; ++b) acc[t][b] += dot8<XDT>(xg[b], cwv);
+                  for (int b = 0; b < NB; ++b) acc[t][b] += dot8<XDT>(xg[b], cwv);
+                }
               }
+              if constexpr (kXS) acc[t][0] = __builtin_fmaf(gs, scl[j0 + jj], acc[t][0]);
             };
             if constexpr (NB == 1) {
 #pragma unroll
@@ -175,7 +216,8 @@ template <int K, int XDT, int UB>
 static hipError_t launch_b4_ub(const Gemv4Args& a, hipStream_t st) {
   const unsigned grid = (unsigned)((a.d_out + b4::kRows - 1) / b4::kRows);
   const size_t row_bytes = (size_t)UB * 512 * 16;
-  if (a.batch == 1) gemv_b4_kernel<K, 1, XDT, UB><<<grid, b4::kThreads, (size_t)K * 256 + row_bytes, st>>>(a);
+  const size_t scl_bytes = XDT == AQMB_BF16 ? (size_t)UB * 512 * 4 : 0;   // bf16 x: group scales
+  if (a.batch == 1) gemv_b4_kernel<K, 1, XDT, UB><<<grid, b4::kThreads, (size_t)K * 256 + row_bytes + scl_bytes, st>>>(a);
   else gemv_b4_kernel<K, 4, XDT, UB><<<grid, b4::kThreads, (size_t)K * 256 + 4 * row_bytes, st>>>(a);
   return hipGetLastError();
 }
