@@ -25,6 +25,12 @@ flops 2 (M + 1) d_out d_in n: W X and one product per code plane); `roofline_bea
 rate 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3 Tops/s). The CPU baseline is the fp64
 oracle timed on a bounded sample.
 
+After the timed steps, `secondary` holds measurements taken once: the decode GEMV on the other
+layer shapes (1024 x 1024; 11008 x 4096 and 4096 x 11008 at batch 1, 8, 16 with bf16 x/y; 14336
+x 4096 with two codebooks of 65536 codewords), the prefill GEMM with 4-bit codes, and two
+labelled reference points (the GEMV on one cache-resident layer; the platform BLAS bf16 GEMM of
+the prefill shape on dense weights).
+
 Prints one JSON line on stdout; progress goes to stderr.
 """
 from __future__ import annotations
@@ -82,6 +88,7 @@ def main():
     ap.add_argument("--copies", type=int, default=64, help="resident layer copies per GEMV step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true", help="skip the once-only measurements after the timed steps")
     ap.add_argument("--counters", action="store_true",
                     help="counter-collection run: eager GEMV launches (k = 4, batch 1) over the layer copies, "
                          "then one plain device copy of 256 MiB that calibrates the HBM byte counters")
@@ -392,7 +399,118 @@ def main():
     if not args.no_gemm:
         for h in glayers:
             A.destroy(h)
+    if not args.no_secondary:
+        out["secondary"] = secondary_measurements(A, torch, stream, to_dev, args.no_gemm)
     print(json.dumps(out), flush=True)
+
+
+def _time_burst(torch, stream, fn, reps=5):
+    """Microseconds per replay of a HIP graph of fn's launches (one warm replay first)."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def secondary_measurements(A, torch, stream, to_dev, no_gemm):
+    """Measured once after the timed steps (not part of a step): the decode GEMV on the other
+    layer shapes, each over enough resident copies to stream from HBM; the prefill GEMM with
+    4-bit codes; and two labelled ceilings: the GEMV on one cache-resident layer (warm), and the
+    platform BLAS bf16 GEMM of the prefill shape (dense bf16 weights; a reference point only)."""
+    import dataclasses
+    from workloads import config, make_layer, make_activations
+    res = {}
+    dt = {"f16": (torch.float16, A.DType.F16), "bf16": (torch.bfloat16, A.DType.BF16)}
+
+    def gemv_bytes(spec, k, b):
+        code_b = 2 if spec.B == 16 else 1
+        return (k * spec.d_out * (spec.d_in // 8) * code_b + k * (1 << spec.B) * 16 + 2 * spec.d_out
+                + 2 * b * (spec.d_in + spec.d_out))
+
+    shapes = {}
+    for name, copies in (("c1", 64), ("c3_up", 24), ("c3_down", 24), ("c4", 20)):
+        spec = config(name)
+        log(f"secondary: {spec.name}, {copies} copies")
+        L = make_layer(spec)
+        desc = A.make_desc(spec.d_out, spec.d_in, spec.M, spec.B)
+        hs = [A.create(desc, to_dev(L.codes if r == 0 else np.ascontiguousarray(np.roll(L.codes, r * 61, axis=1))),
+                       to_dev(L.codebooks), to_dev(L.scales)) for r in range(copies)]
+        tdt, adt = dt[spec.act_dtype]
+        e = {}
+        for b in spec.batches:
+            x = to_dev(make_activations(L, b)).view(tdt)
+            ys = [torch.empty((b, spec.d_out), dtype=tdt, device="cuda") for _ in range(copies)]
+            for k in spec.ks:
+                us = _time_burst(torch, stream, lambda: [A.gemv(h, k, x, adt, b, y, adt) for h, y in zip(hs, ys)]) / copies
+                gbps = gemv_bytes(spec, k, b) / (us * 1e-6) / 1e9
+                e[f"k{k}_b{b}"] = {"us": round(us, 3), "GBps": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
+        shapes[spec.name] = e
+        for h in hs:
+            A.destroy(h)
+    res["gemv_other_shapes"] = {"note": "per launch, graph replay over resident copies; algorithmic bytes "
+                                "k*plane + k*codebook + scales + x + y", "per_shape": shapes}
+
+    # warm: one layer of the 4096 x 4096 workload, launched repeatedly (codes cache-resident)
+    spec = config("c2")
+    L = make_layer(spec)
+    h = A.create(A.make_desc(4096, 4096, 4, 8), to_dev(L.codes), to_dev(L.codebooks), to_dev(L.scales))
+    x = to_dev(make_activations(L, 1, "f16")).view(torch.float16)
+    y = torch.empty((1, 4096), dtype=torch.float16, device="cuda")
+    warm = {}
+    for k in spec.ks:
+        us = _time_burst(torch, stream, lambda: [A.gemv(h, k, x, A.DType.F16, 1, y, A.DType.F16) for _ in range(64)]) / 64
+        warm[str(k)] = {"us": round(us, 3), "GBps": round(gemv_bytes(spec, k, 1) / (us * 1e-6) / 1e9, 1)}
+    A.destroy(h)
+    res["gemv_warm_cache_resident"] = {"note": "one 4096x4096 layer launched 64 times in a row, batch 1: its "
+                                       "codes stay in the caches (not an HBM figure)", "per_k": warm}
+
+    if not no_gemm:
+        gspec = config("c5")
+        n = gspec.n_tokens
+        fl = 2.0 * n * gspec.d_out * gspec.d_in
+        s4 = dataclasses.replace(gspec, B=4, seed=gspec.seed + 100)
+        L4 = make_layer(s4)
+        d4 = A.make_desc(s4.d_out, s4.d_in, s4.M, 4)
+        hs = [A.create(d4, to_dev(L4.codes if r == 0 else np.ascontiguousarray(np.roll(L4.codes, r * 61, axis=1))),
+                       to_dev(L4.codebooks), to_dev(L4.scales)) for r in range(4)]
+        X = to_dev(make_activations(L4, n, "bf16")).view(torch.bfloat16)
+        Ys = [torch.empty((n, s4.d_out), dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+        g4 = {}
+        for k in s4.ks:
+            us = _time_burst(torch, stream, lambda: [A.gemm(hh, k, X, n, Y, A.DType.BF16) for hh, Y in zip(hs, Ys)]) / 4
+            g4[str(k)] = {"us": round(us, 2), "TFLOPs": round(fl / (us * 1e-6) / 1e12, 1)}
+        for hh in hs:
+            A.destroy(hh)
+        res["gemm_4bit"] = {"note": f"{n}-token prefill GEMM on a {s4.d_out}x{s4.d_in} layer with 4 codebooks of 16 "
+                            "codewords (4-bit codes), bf16 out", "per_k": g4}
+        # platform BLAS on dense bf16 weights of the same shape: a reference point, not part of the path
+        Wt = torch.randn((gspec.d_in, gspec.d_out), dtype=torch.float32, device="cuda").mul_(0.02).to(torch.bfloat16)
+        Wts = [Wt.clone() for _ in range(4)]
+        Yb = torch.empty((n, gspec.d_out), dtype=torch.bfloat16, device="cuda")
+        note = ("torch.matmul of the same shape on dense bf16 weights (the platform BLAS); a measurement "
+                "reference, not part of the path")
+        # eager launches (the BLAS is not captured in a graph); the first call warms it up
+        for w in Wts:
+            torch.matmul(X, w, out=Yb)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(5):
+            for w in Wts:
+                torch.matmul(X, w, out=Yb)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / 20
+        res["gemm_platform_blas_bf16"] = {"note": note, "us": round(us, 2), "TFLOPs": round(fl / (us * 1e-6) / 1e12, 1)}
+    return res
 
 
 def cpu_baseline(layer, x1bits, x4bits, ks, gemv_bytes):
