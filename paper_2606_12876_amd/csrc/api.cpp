@@ -91,6 +91,8 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
   L->d = *desc;
   hipError_t e = hipGetDevice(&L->device);
   if (e != hipSuccess) { free_layer(L); return hip_fail(e, "create: hipGetDevice"); }
+  e = hipDeviceGetAttribute(&L->n_cu, hipDeviceAttributeMultiprocessorCount, L->device);
+  if (e != hipSuccess) { free_layer(L); return hip_fail(e, "create: hipDeviceGetAttribute"); }
   L->G = desc->d_in / desc->group_size;
   L->J = kSliceBytes * 8 / desc->code_bits;     // groups per 16-byte slice: 32, 16 or 8
   L->S = (L->G + L->J - 1) / L->J;

@@ -43,6 +43,7 @@ struct GemvArgs {
   int y_dtype;
   int nrep;            // codebook replicas in LDS (direct-gather kernel), a power of two
   int cb_shift;        // log2(nrep * 16): byte shift from a code to its codeword
+  int n_cu;            // compute units (host side: the persistent grid)
 };
 
 size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S) {
@@ -611,6 +612,71 @@ void gemv_cw_kernel(GemvArgs a) {
   }
 }
 
+// Layers with more 16-row blocks than compute units (e.g. 11008 rows): one persistent workgroup
+// per CU walks the row blocks blockIdx.x, blockIdx.x + gridDim.x, ... (rows of at most 512
+// groups, one batch tile). x is staged and the codebooks replicated once; the code words of the
+// next block are requested before the current block is gathered (two register sets in turn), so
+// a block costs its gathers, not a workgroup's start-up, load latency and replica writes. Same
+// arithmetic and reduction order as gemv_cw_kernel.
+template <int K, int NB, int XDT>
+__global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_cw_persist_kernel(GemvArgs a) {
+  constexpr int UB = 1;
+  extern __shared__ uint4 smem_cw[];
+  const int nrep = a.nrep;
+  uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords
+  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);    // [NB][row_stride] x tile
+  __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
+  constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int rw = lane & 15;
+  const int Gp = a.S * 16;
+  const size_t rstride = cw::row_stride(a.S);
+  const uint32_t xs_base = lds_addr(xs);
+  const uint32_t rep_off = (uint32_t)(lane % nrep) * 16;
+  const int n_rb = (a.d_out + cw::kRows - 1) / cw::kRows;
+  float* scl = (float*)((char*)xs + NB * rstride);         // bf16 x: [NB][rstride / 16] group scales
+
+  auto load_block = [&](int rb, uint32_t& sbits, uint2 (&code)[UB][K]) {
+    const int row = rb * cw::kRows + rw;
+    const int rowc = row < a.d_out ? row : a.d_out - 1;
+    sbits = a.scales[rowc];
+    cw_load_codes<K, UB>(code, a.codes, a.plane_bytes, a.d_out, rowc, Gp);
+  };
+  auto run_block = [&](int rb, uint32_t sbits, const uint2 (&code)[UB][K]) {
+    const int row = rb * cw::kRows + rw;
+    cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
+                            row < a.d_out, f16_to_f32((uint16_t)sbits), a.y, a.d_out, a.y_dtype, scl);
+  };
+
+  int rb = blockIdx.x;                                     // the grid never exceeds the block count
+  cw_stage_x<NB>(a.x, a.zero_page, 0, a.batch, a.d_in, rstride, xs_base);
+  asm volatile("" ::: "memory");
+  const uint4 cbv = ((const uint4*)a.codebooks)[tid % (K * 256)];   // K * 256 <= 1024 codewords
+  asm volatile("" ::: "memory");
+  uint32_t sa, sb;
+  uint2 ca[UB][K], cb[UB][K];
+  load_block(rb, sa, ca);
+  wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
+  if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
+  cw_replicate<K>(cb_rep, cbv, nrep, a.cb_shift);
+  __syncthreads();
+  for (;;) {
+    int nrb = rb + (int)gridDim.x;
+    load_block(nrb < n_rb ? nrb : rb, sb, cb);            // past the last block: a harmless reload
+    run_block(rb, sa, ca);
+    if (nrb >= n_rb) break;
+    rb = nrb;
+    __syncthreads();                                       // wave 0 has read the previous row sums
+    nrb = rb + (int)gridDim.x;
+    load_block(nrb < n_rb ? nrb : rb, sa, ca);
+    run_block(rb, sb, cb);
+    if (nrb >= n_rb) break;
+    rb = nrb;
+    __syncthreads();
+  }
+}
+
 // ------------------------------------------------------------------ several layers, one launch
 // Layers that share the input x (fused projections such as q/k/v or gate/up): one persistent
 // workgroup per 16-row block walks through the layers that have that block. x is staged once;
@@ -730,9 +796,12 @@ static hipError_t launch_cw_nb(GemvArgs a, hipStream_t st) {
   a.nrep = cw_nrep(K, NB, a.S, XDT == AQMB_BF16);
   if (a.nrep == 0) return hipErrorInvalidValue;  // x tile does not fit: caller uses another path
   a.cb_shift = a.nrep == 8 ? 7 : 6;
-  const dim3 grid((a.d_out + cw::kRows - 1) / cw::kRows);
+  const int n_rb = (a.d_out + cw::kRows - 1) / cw::kRows;
+  const dim3 grid(n_rb);
   const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
-  if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
+  if (cw_blocks(a.S) == 1 && a.batch <= NB && n_rb > a.n_cu && a.n_cu > 0)   // one workgroup per CU
+    gemv_cw_persist_kernel<K, NB, XDT><<<dim3(a.n_cu), cw::kThreads, lds, st>>>(a);
+  else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
   else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks><<<grid, cw::kThreads, lds, st>>>(a);
   return hipGetLastError();
 }
@@ -817,6 +886,7 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   a.k = k;
   a.batch = batch;
   a.y_dtype = (int)y_dtype;
+  a.n_cu = L.n_cu;
   const dim3 grid((L.d.d_out + kRowsPerWG - 1) / kRowsPerWG, L.S);
   const bool b16 = L.d.code_bits == 16;
   if (!b16 && gemv_variant() == 1 && cw_fits(k, batch, L.S, x_dtype == AQMB_BF16)) {   // direct gather: one kernel

@@ -18,6 +18,7 @@ struct Layer {
   uint32_t magic;
   aqmb_desc d;
   int device;
+  int n_cu;              // compute units of that device (persistent grids)
   int G;                 // groups per row = d_in / g
   int J;                 // groups per slice
   int S;                 // slices per row = ceil(G / J)

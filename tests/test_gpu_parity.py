@@ -175,6 +175,25 @@ def test_gemv_wide_rows(d_in):
                 check_close(got, ref, "f32", f"d_in={d_in} b={b} k={k}")
 
 
+@pytest.mark.parametrize("xdt", ["f16", "bf16"])
+def test_gemv_more_row_blocks_than_cus(xdt):
+    """5000 rows = 313 blocks of 16 (the last one ragged): more than one block per compute unit,
+    so each workgroup walks several blocks with the codebooks replicated once; batch 1 and 2,
+    every k, against the oracle."""
+    spec = LayerSpec("tall", 5000, 520, M=4, seed=39, act_dtype=xdt)
+    L = make_layer(spec)
+    C, s = _f64(L)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for b in (1, 2):
+            xbits = make_activations(L, b, xdt, heavy_tail=True)
+            x = act_values(xbits, xdt)
+            for k in range(1, 5):
+                ref = oracle.linear(x, L.codes, C, s, k)
+                for ydt in ("f32", xdt):
+                    got = run_gemv(gl, k, xbits, xdt, ydt)
+                    check_close(got, ref, ydt, f"5000 rows {xdt} b={b} k={k} y={ydt}")
+
+
 def test_gemv_plane_linearity():
     """gemv(k) - gemv(k-1) equals the GEMV of a one-codebook layer holding plane k-1 alone."""
     spec = LayerSpec("lin", 777, 1024, seed=36)
