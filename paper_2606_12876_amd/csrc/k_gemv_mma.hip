@@ -36,6 +36,7 @@ struct GemvMmaArgs {
   const void* zero_page;      // >= 16 zero bytes
   size_t plane_bytes;
   int d_out, d_in, G, batch, y_dtype, nrep, cb_shift;
+  int n_cu;                   // compute units (host side: the persistent grid)
 };
 
 
@@ -47,45 +48,31 @@ struct MgRun {
   uint4 c[K];
 };
 
+// Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of batch
+// row `col` at inputs 128 r + 32 j + 8 kc .. + 7 for steps j = 0..3 (zeros past d_in, past the
+// batch, and for dummy runs), and slice r of the row in every plane.
+template <int K>
+__device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K>& R) {
+  const int lane = threadIdx.x & 63, col = lane & 15, kc = lane >> 4;
+  const int n_runs = (a.G + 15) / 16;
+  const int rc = r < n_runs ? r : n_runs - 1;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = rc * 128 + j * 32 + kc * 8;
+    const void* src = (xok && col < a.batch && e < a.d_in) ? (const void*)(a.x + (size_t)col * a.d_in + e) : a.zero_page;
+    R.xa[j] = *(const uint4*)src;
+  }
+#pragma unroll
+  for (int m = 0; m < K; ++m) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+}
+
+// Codebook word q (q < K * 256) into its nrep replicas (bf16 x: a book of high and a book of low
+// parts, split exactly).
 template <int K, int XDT>
-__global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
-void gemv_mma_kernel(GemvMmaArgs a) {
+__device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep) {
   using namespace mg;
-  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;            // fp16 codewords, or bf16 high and low parts
-  extern __shared__ uint4 smem_mg[];
-  uint4* cb_rep = smem_mg;                                   // [kBooks][K][256][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * 256 * a.nrep);   // [kWaves][64] partial tiles
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int col = lane & 15, kc = lane >> 4;                 // weight row in the block, group in a step
-  const int row0 = blockIdx.x * kRows;
-  const int rowc = row0 + col < a.d_out ? row0 + col : a.d_out - 1;
-  const int n_runs = (a.G + 15) / 16;                        // code slices per row
-  const uint32_t rep_off = (uint32_t)(lane & (a.nrep - 1)) * 16;
-  const bool brow = col < a.batch;                           // this lane's x row exists
-
-  // Loads of run r (past the end: the last run again, never used): x of batch row `col` at
-  // inputs 128 r + 32 j + 8 kc .. + 7 for steps j = 0..3 (zeros past d_in and past the batch),
-  // and slice r of weight row `rowc` in every plane.
-  auto load_run = [&](int r, MgRun<K>& R) {
-    const int rc = r < n_runs ? r : n_runs - 1;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = rc * 128 + j * 32 + kc * 8;
-      const void* src = (brow && e < a.d_in) ? (const void*)(a.x + (size_t)col * a.d_in + e) : a.zero_page;
-      R.xa[j] = *(const uint4*)src;
-    }
-#pragma unroll
-    for (int m = 0; m < K; ++m) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
-  };
-
-  // The wave's runs are wave, wave + 16, ...; the first two are requested before the codebooks are
-  // replicated into LDS (a 4096-wide row has 32 runs: two per wave).
-  MgRun<K> ra, rb;
-  int r = wave;
-  load_run(r, ra);
-  load_run(r + kWaves, rb);
-  for (int q = tid; q < K * 256; q += kThreads) {
+  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;
+  for (int q = threadIdx.x; q < K * 256; q += kThreads) {
     const uint4 v = ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - a.cb_shift);
     if constexpr (kBooks == 1) {
@@ -106,43 +93,45 @@ void gemv_mma_kernel(GemvMmaArgs a) {
       }
     }
   }
-  __syncthreads();
+}
 
-  f32x4_t acc[4];
+// The MFMAs of one run. Step j of a run: group 4 j + kc of the slice, code byte 4 j + kc of each
+// plane's word.
+template <int K, int XDT>
+__device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb_rep, uint32_t rep_off,
+                                           const MgRun<K>& R, mg::f32x4_t (&acc)[4]) {
+  using namespace mg;
+  const int kc = (threadIdx.x & 63) >> 4;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  // Step j of a run: group 4 j + kc of the slice, code byte 4 j + kc of each plane's word.
-  auto compute = [&](const MgRun<K>& R) {
+  for (int m = 0; m < K; ++m) {
 #pragma unroll
-    for (int m = 0; m < K; ++m) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
-        const uint32_t code = (word >> (8 * kc)) & 0xFFu;
-        const uint32_t off = (((uint32_t)(m * 256) + code) << a.cb_shift) + rep_off;
-        const uint4 cw = *(const uint4*)((const char*)cb_rep + off);
-        if constexpr (XDT == AQMB_F16) {
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, R.xa[j]),
-                                                          __builtin_bit_cast(f16x8_t, cw), acc[j], 0, 0, 0);
-        } else {
-          const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * 256) << a.cb_shift) + off);
-          const b16x8_t xb = __builtin_bit_cast(b16x8_t, R.xa[j]);
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cw), acc[j], 0, 0, 0);
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cl), acc[j], 0, 0, 0);
-        }
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
+      const uint32_t code = (word >> (8 * kc)) & 0xFFu;
+      const uint32_t off = (((uint32_t)(m * 256) + code) << a.cb_shift) + rep_off;
+      const uint4 cw = *(const uint4*)((const char*)cb_rep + off);
+      if constexpr (XDT == AQMB_F16) {
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, R.xa[j]),
+                                                        __builtin_bit_cast(f16x8_t, cw), acc[j], 0, 0, 0);
+      } else {
+        const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * 256) << a.cb_shift) + off);
+        const b16x8_t xb = __builtin_bit_cast(b16x8_t, R.xa[j]);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cw), acc[j], 0, 0, 0);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cl), acc[j], 0, 0, 0);
       }
     }
-  };
-  // Two register sets in turn: the loads of the wave's run after next are requested while it
-  // computes one.
-  for (; r < n_runs; r += 2 * kWaves) {
-    compute(ra);
-    if (r + kWaves >= n_runs) break;
-    if (r + 2 * kWaves < n_runs) load_run(r + 2 * kWaves, ra);
-    compute(rb);
-    if (r + 3 * kWaves < n_runs) load_run(r + 3 * kWaves, rb);
   }
-  // Partial tiles in wave order; element e of lane l is batch row 4 (l / 16) + e, weight row l % 16.
+}
+
+// Partial tiles of the 16 waves added in wave order by wave 0, scaled once and rounded once, for
+// the 16 weight rows from row0; element e of lane l is batch row 4 (l / 16) + e, weight row l % 16.
+// Ends with the block's partial tiles read (a barrier before and none after: the caller separates
+// two calls with a barrier).
+__device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_t* red, const mg::f32x4_t (&acc)[4],
+                                                int row0) {
+  using namespace mg;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int col = lane & 15, kc = lane >> 4;
   red[wave * 64 + lane] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   __syncthreads();
   if (wave == 0) {
@@ -168,14 +157,113 @@ void gemv_mma_kernel(GemvMmaArgs a) {
 }
 
 template <int K, int XDT>
+__global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_mma_kernel(GemvMmaArgs a) {
+  using namespace mg;
+  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;            // fp16 codewords, or bf16 high and low parts
+  extern __shared__ uint4 smem_mg[];
+  uint4* cb_rep = smem_mg;                                   // [kBooks][K][256][nrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * 256 * a.nrep);   // [kWaves][64] partial tiles
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15;                                 // weight row in the block
+  const int row0 = blockIdx.x * kRows;
+  const int rowc = row0 + col < a.d_out ? row0 + col : a.d_out - 1;
+  const int n_runs = (a.G + 15) / 16;                        // code slices per row
+  const uint32_t rep_off = (uint32_t)(lane & (a.nrep - 1)) * 16;
+
+  // The wave's runs are wave, wave + 16, ...; the first two are requested before the codebooks are
+  // replicated into LDS (a 4096-wide row has 32 runs: two per wave).
+  MgRun<K> ra, rb;
+  int r = wave;
+  mg_load_run<K>(a, r, rowc, true, ra);
+  mg_load_run<K>(a, r + kWaves, rowc, true, rb);
+  mg_replicate<K, XDT>(a, cb_rep);
+  __syncthreads();
+
+  f32x4_t acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // Two register sets in turn: the loads of the wave's run after next are requested while it
+  // computes one.
+  for (; r < n_runs; r += 2 * kWaves) {
+    mg_compute<K, XDT>(a, cb_rep, rep_off, ra, acc);
+    if (r + kWaves >= n_runs) break;
+    if (r + 2 * kWaves < n_runs) mg_load_run<K>(a, r + 2 * kWaves, rowc, true, ra);
+    mg_compute<K, XDT>(a, cb_rep, rep_off, rb, acc);
+    if (r + 3 * kWaves < n_runs) mg_load_run<K>(a, r + 3 * kWaves, rowc, true, rb);
+  }
+  mg_reduce_store(a, red, acc, row0);
+}
+
+// Layers with more 16-row blocks than compute units: one persistent workgroup per CU walks the
+// row blocks blockIdx.x, blockIdx.x + gridDim.x, ... with the codebooks replicated once. Each
+// wave takes the same per = ceil(n_runs / 16) runs of every block (wave, wave + 16, ...; runs past
+// the row are dummies: x reads zeros) as one flat sequence of items over its blocks, two items
+// ahead in two register sets, so the next block's first runs are in flight while a block ends
+// (partial tiles added in wave order, as in gemv_mma_kernel; same arithmetic and order).
+template <int K, int XDT>
+__global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_mma_persist_kernel(GemvMmaArgs a) {
+  using namespace mg;
+  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;
+  extern __shared__ uint4 smem_mg[];
+  uint4* cb_rep = smem_mg;                                   // [kBooks][K][256][nrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * 256 * a.nrep);   // [kWaves][64] partial tiles
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15;
+  const int n_runs = (a.G + 15) / 16;
+  const int n_rb = (a.d_out + kRows - 1) / kRows;
+  const int per = (n_runs + kWaves - 1) / kWaves;            // items per block, the same for every wave
+  const int nb = (n_rb - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;   // this workgroup's blocks
+  const int n_items = per * nb;
+  const uint32_t rep_off = (uint32_t)(lane & (a.nrep - 1)) * 16;
+
+  // item i: block blockIdx.x + (i / per) gridDim.x, run wave + (i % per) 16 (items past the end:
+  // the last item again, never used)
+  auto load_item = [&](int i, MgRun<K>& R) {
+    const int ic = i < n_items ? i : n_items - 1;
+    const int row = ((int)blockIdx.x + (ic / per) * (int)gridDim.x) * kRows + col;
+    const int r = wave + (ic % per) * kWaves;
+    mg_load_run<K>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R);
+  };
+  f32x4_t acc[4];
+  auto end_block = [&](int i) {                              // item i closed its block
+    mg_reduce_store(a, red, acc, ((int)blockIdx.x + (i / per) * (int)gridDim.x) * kRows);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    __syncthreads();                                         // wave 0 has read the partial tiles
+  };
+
+  MgRun<K> ra, rb;
+  load_item(0, ra);
+  load_item(1, rb);
+  mg_replicate<K, XDT>(a, cb_rep);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < n_items; i += 2) {
+    mg_compute<K, XDT>(a, cb_rep, rep_off, ra, acc);
+    load_item(i + 2, ra);
+    if ((i + 1) % per == 0) end_block(i);
+    if (i + 1 >= n_items) break;
+    mg_compute<K, XDT>(a, cb_rep, rep_off, rb, acc);
+    load_item(i + 3, rb);
+    if ((i + 2) % per == 0) end_block(i + 1);
+  }
+}
+
+template <int K, int XDT>
 static hipError_t launch_mma_k(GemvMmaArgs a, hipStream_t st) {
   const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * 256 * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
   a.nrep = book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
   a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : 5;
   const size_t lds = book * a.nrep + red;
-  const unsigned grid = (unsigned)((a.d_out + mg::kRows - 1) / mg::kRows);
-  gemv_mma_kernel<K, XDT><<<grid, mg::kThreads, lds, st>>>(a);
+  const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
+  if (n_rb > a.n_cu && a.n_cu > 0) gemv_mma_persist_kernel<K, XDT><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
+  else gemv_mma_kernel<K, XDT><<<dim3(n_rb), mg::kThreads, lds, st>>>(a);
   return hipGetLastError();
 }
 
@@ -208,6 +296,7 @@ hipError_t launch_gemv_mma(const Layer& L, int k, const void* x, aqmb_dtype x_dt
   a.G = L.G;
   a.batch = batch;
   a.y_dtype = (int)y_dtype;
+  a.n_cu = L.n_cu;
   return x_dtype == AQMB_F16 ? launch_mma_x<AQMB_F16>(a, k, st) : launch_mma_x<AQMB_BF16>(a, k, st);
 }
 

@@ -178,13 +178,14 @@ def test_gemv_wide_rows(d_in):
 @pytest.mark.parametrize("xdt", ["f16", "bf16"])
 def test_gemv_more_row_blocks_than_cus(xdt):
     """5000 rows = 313 blocks of 16 (the last one ragged): more than one block per compute unit,
-    so each workgroup walks several blocks with the codebooks replicated once; batch 1 and 2,
-    every k, against the oracle."""
+    so each workgroup walks several blocks with the codebooks replicated once. Batch 1 and 2
+    (direct gathers) and 3, 8, 16 (matrix cores; 65 groups = 5 runs of 16, so 11 of the 16 waves
+    run a dummy item per block), every k, against the oracle."""
     spec = LayerSpec("tall", 5000, 520, M=4, seed=39, act_dtype=xdt)
     L = make_layer(spec)
     C, s = _f64(L)
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
-        for b in (1, 2):
+        for b in (1, 2, 3, 8, 16):
             xbits = make_activations(L, b, xdt, heavy_tail=True)
             x = act_values(xbits, xdt)
             for k in range(1, 5):
