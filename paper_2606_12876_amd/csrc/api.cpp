@@ -153,8 +153,11 @@ static int gemv_mode() {
   return v;
 }
 
+// Matrix cores from batch 3 on, and at batch 2 for rows of more than 512 groups (where the
+// direct-gather kernel would hold two batch rows for four 512-group blocks of code words).
 static bool gemv_uses_mma(const Layer& L, int batch) {
-  return L.d.code_bits == 8 && (gemv_mode() == 3 || (gemv_mode() == 0 && batch >= 3));
+  const bool wide = L.S * L.J > 512;
+  return L.d.code_bits == 8 && (gemv_mode() == 3 || (gemv_mode() == 0 && (batch >= 3 || (batch == 2 && wide))));
 }
 
 static hipError_t launch_gemv_any(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,

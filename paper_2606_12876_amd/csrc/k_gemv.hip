@@ -932,9 +932,12 @@ static hipError_t launch_multi_x(const GemvMultiArgs& a, int k, int grid, hipStr
 hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x, aqmb_dtype x_dtype, int batch,
                              void* const* ys, aqmb_dtype y_dtype, hipStream_t st) {
   // One launch when every layer takes the direct-gather path in a single batch tile (8-bit codes,
-  // k <= 4, batch <= 4); otherwise the layers are launched one after another.
+  // k <= 4, batch <= 4) and, for rows of more than 512 groups, k = 1 (two layers' code words for
+  // several blocks do not fit in registers beyond one plane); otherwise the layers are launched
+  // one after another.
   const Layer& L0 = *Ls[0];
-  bool one = batch <= 4 && gemv_variant() == 1 && cw_fits(k, batch, L0.S, x_dtype == AQMB_BF16);
+  bool one = batch <= 4 && gemv_variant() == 1 && cw_fits(k, batch, L0.S, x_dtype == AQMB_BF16) &&
+             (cw_blocks(L0.S) == 1 || k == 1);
   for (int i = 0; i < n && one; ++i) one = Ls[i]->d.code_bits == 8;
   if (!one) {
     for (int i = 0; i < n; ++i) {

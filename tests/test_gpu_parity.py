@@ -161,12 +161,13 @@ def test_gemv_workloads(name):
 @pytest.mark.parametrize("d_in", [16384, 16392])
 def test_gemv_wide_rows(d_in):
     """Rows of 2048 groups (the widest the direct-gather kernel keeps in registers) and of 2049
-    groups (taken by the lookup-table kernel), batch 1 and 4, every k."""
+    groups (taken by the lookup-table kernel at batch 1), batch 1, 2 (matrix cores for rows of
+    more than 512 groups) and 4, every k."""
     spec = LayerSpec(f"wide{d_in}", 130, d_in, M=4, seed=38)
     L = make_layer(spec)
     C, s = _f64(L)
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
-        for b in (1, 4):
+        for b in (1, 2, 4):
             xbits = make_activations(L, b, "f16", heavy_tail=True)
             x = act_values(xbits, "f16")
             for k in range(1, 5):
