@@ -23,6 +23,8 @@
 //     one group of one row, i.e. C_m[code], gathered from codebooks replicated in LDS.
 // Each lane keeps fp64 sums of R_k^2 over its outputs; each workgroup writes its sums and a
 // second kernel adds them in a fixed order, so the result does not depend on scheduling.
+#include <type_traits>
+
 #include "device.h"
 #include "launch.h"
 
@@ -39,7 +41,9 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 // CB = code bits: 8 (256 codewords, replicated) or 4 (16 codewords: they fill the LDS banks once,
 // so one copy is read without conflicts).
 template <int M, int CB> struct Cfg {
-  static constexpr int NA = M <= 6 ? 2 : 1;  // 32-sample blocks per wave (accumulators: 16 NA (M+1))
+  // 32-sample blocks per wave (accumulators: 16 NA (M+1)); M = 6 with 4-bit codes takes one (with
+  // two, its registers overflow)
+  static constexpr int NA = M <= 5 || (M == 6 && CB == 8) ? 2 : 1;
   static constexpr int kTok = 32 * NA;
   static constexpr int NCW = 1 << CB;
   static constexpr int kNrep = CB == 4 ? 1 : M <= 4 ? 8 : 4;   // codebook replicas in LDS
@@ -50,7 +54,11 @@ template <int M, int CB> struct Cfg {
   static constexpr int kLoads = NA + 4 + M;                    // loads per wave per step
 };
 // One step's operands in registers: the W pieces of the four K-blocks and 8 code bytes per plane.
-template <int M> struct Frag { f16x8_t w[4]; uint2 c[M]; };
+// (8-bit codes: 8 code bytes per plane; 4-bit codes: one 4-byte word of 8 nibbles per plane.)
+template <int M, int CB> struct Frag {
+  f16x8_t w[4];
+  typename std::conditional<CB == 8, uint2, uint32_t>::type c[M];
+};
 }  // namespace dist
 
 size_t distortion_workspace_floats() { return (size_t)dist::kMaxGrid * 8 * 2; }
@@ -121,23 +129,25 @@ void distortion_kernel(DistArgs a) {
     // W pieces (K-block kb: values 16 kb + 8 h .. + 7 of the step) and the code bytes of groups
     // 8 st .. 8 st + 7 of this lane's row (one 8-byte half of a 16-group slice). Past the last
     // step the last one is loaded again (never used), so every step issues the same loads.
-    auto load_w = [&](int st, Frag<M>& f, int kb) {
+    auto load_w = [&](int st, Frag<M, CB>& f, int kb) {
       const int stc = st < nsteps ? st : nsteps - 1;
       int k = stc * kStep + kb * 16 + h * 8;
       k = k < a.d_in ? k : 0;                                  // only meets zero X
       f.w[kb] = *(const f16x8_t*)(a.W + (size_t)rowc * a.d_in + k);
     };
-    auto load_codes = [&](int st, Frag<M>& f) {
+    auto load_codes = [&](int st, Frag<M, CB>& f) {
       const int g0 = (st < nsteps ? st : nsteps - 1) * 8;
 #pragma unroll
-      for (int m = 0; m < M; ++m)
-        f.c[m] = CB == 8 ? *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 8))
-                         : make_uint2(*(const uint32_t*)(a.codes + m * a.plane_bytes +
-                                                         ((size_t)(g0 >> 5) * a.d_out + rowc) * 16 + ((g0 & 31) >> 1)), 0u);
+      for (int m = 0; m < M; ++m) {
+        if constexpr (CB == 8)
+          f.c[m] = *(const uint2*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 4) * a.d_out + rowc) * 16 + (g0 & 8));
+        else
+          f.c[m] = *(const uint32_t*)(a.codes + m * a.plane_bytes + ((size_t)(g0 >> 5) * a.d_out + rowc) * 16 + ((g0 & 31) >> 1));
+      }
     };
     // The loads of one step, issued in three parts (with the MFMAs of K-blocks 0, 1, 2 of the step
     // kPre earlier), kLoads in all.
-    auto issue_part = [&](int st, int buf, Frag<M>& f, int part) {
+    auto issue_part = [&](int st, int buf, Frag<M, CB>& f, int part) {
       if (part == 0) { stage_x(st, buf); load_w(st, f, 0); load_w(st, f, 1); }
       if (part == 1) { load_w(st, f, 2); load_w(st, f, 3); }
       if (part == 2) load_codes(st, f);
@@ -155,7 +165,7 @@ void distortion_kernel(DistArgs a) {
     // codebooks. No lane is masked: past d_in the staged X is zero, so whatever W piece or
     // codeword sits in the B operand there contributes nothing (W and the codebooks are finite).
     struct Ops { f16x8_t xa[NA]; f16x8_t bq[M]; };
-    auto read_ops = [&](int buf, const Frag<M>& f, int kb, Ops& o) {
+    auto read_ops = [&](int buf, const Frag<M, CB>& f, int kb, Ops& o) {
       const char* xst = xs + buf * C::kXBytes;
       const int piece = kb * 2 + h;                            // = group of the step
 #pragma unroll
@@ -170,7 +180,7 @@ void distortion_kernel(DistArgs a) {
           const uint32_t word = kb < 2 ? f.c[m].x : f.c[m].y;
           code = (word >> (16 * (kb & 1) + 8 * h)) & 0xFFu;
         } else {                                               // nibble `piece` of the step's word
-          code = (f.c[m].x >> (4 * piece)) & 15u;
+          code = (f.c[m] >> (4 * piece)) & 15u;
         }
         o.bq[m] = *(const f16x8_t*)(cbase + ((uint32_t)(m * NCW + code) << kShift));
       }
@@ -183,7 +193,7 @@ void distortion_kernel(DistArgs a) {
     //   are in; every wave has read step st's operands, whose buffer the loads issued during step
     //   st + 1 overwrite), and K-block 0 of step st + 1 is read: the MFMA stream never waits for
     //   the first reads of a step.
-    Frag<M> f[kBufs];
+    Frag<M, CB> f[kBufs];
     Ops o[2];
 #pragma unroll
     for (int j = 0; j < kPre; ++j)

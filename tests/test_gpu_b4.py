@@ -116,15 +116,18 @@ def test_gemm_full_size_sampled():
             check_close(out_values(Y)[rows], ref, "bf16", f"gemm 2048x4096x4096 B=4 k={k}")
 
 
-def test_prefix_distortion_matches_oracle():
+@pytest.mark.parametrize("M", [4, 6, 8])
+def test_prefix_distortion_matches_oracle(M):
+    """4-bit codes through the distortion kernel's layouts (two sample blocks per wave up to M = 5,
+    one beyond)."""
     from workloads import make_weights
-    L = make_layer(LayerSpec("d4", 257, 520, M=4, B=4, seed=350))
+    L = make_layer(LayerSpec("d4", 257, 520, M=M, B=4, seed=350 + M))
     Wb = make_weights(L)
     Xb = make_activations(L, 150, "f16")
     C, s = _vals(L)
     ref = oracle.prefix_distortions(formats.f16_bits_to_f64(Wb), L.codes, C, s, formats.f16_bits_to_f64(Xb))
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
-        D = torch.empty(4, dtype=torch.float64, device="cuda")
+        D = torch.empty(M, dtype=torch.float64, device="cuda")
         A.prefix_distortion(gl.handle, to_dev(Wb).view(torch.float16), A.DType.F16, to_dev(Xb).view(torch.float16),
                             A.DType.F16, 150, D)
         torch.cuda.synchronize()
