@@ -138,10 +138,12 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
   return AQMB_OK;
 }
 
-// GEMV kernel choice. Default: 4-bit codes -> their kernel; 8-bit codes at batch >= 3 -> the
-// matrix-core kernel (measured faster from batch 3 or 4 on, equal at 2); otherwise the direct-gather
-// kernel (k <= 4, rows <= 16384) or the lookup table kernel, as k_gemv.hip decides. AQMB_GEMV=mma uses the matrix-core kernel at batch 1 too,
-// AQMB_GEMV=cw or =lut keep 8-bit layers on k_gemv.hip's kernels (read once).
+// GEMV kernel choice. Default: 4-bit codes -> their kernel; 8-bit codes at batch >= 3, and at
+// batch 2 on rows of more than 512 groups -> the matrix-core kernel (measured faster there; at
+// batch 2 on shorter rows the two are within a few percent); otherwise the direct-gather kernel
+// (k <= 4, rows <= 16384) or the lookup table kernel, as k_gemv.hip decides. AQMB_GEMV=mma uses
+// the matrix-core kernel at every batch, AQMB_GEMV=cw or =lut keep 8-bit layers on k_gemv.hip's
+// kernels (read once).
 static int gemv_mode() {
   static const int v = [] {
     const char* e = getenv("AQMB_GEMV");
@@ -153,8 +155,8 @@ static int gemv_mode() {
   return v;
 }
 
-// Matrix cores from batch 3 on, and at batch 2 for rows of more than 512 groups (where the
-// direct-gather kernel would hold two batch rows for four 512-group blocks of code words).
+// (At batch 2 on rows of more than 512 groups the direct-gather kernel would hold the code words of
+// four 512-group blocks next to two batch rows: more than its registers.)
 static bool gemv_uses_mma(const Layer& L, int batch) {
   const bool wide = L.S * L.J > 512;
   return L.d.code_bits == 8 && (gemv_mode() == 3 || (gemv_mode() == 0 && (batch >= 3 || (batch == 2 && wide))));
