@@ -549,6 +549,17 @@ __device__ __forceinline__ void cw_convert_own_bf16(uint16_t* xs, float* scl, si
   }
 }
 
+// An execution barrier between the workgroup's small loads (x, codebook words, row scales) and its
+// code words: a CU's vector memory requests leave in order, so without it the waves that start
+// last queue their codebook word behind the other waves' code words, which stream from HBM, and
+// the codebook replication (which every gather waits for) waits for them. Measured on the
+// 4096 x 4096 layer, batch 1: 6.2 to 5.5 us at k = 4.
+__device__ __forceinline__ void cw_small_loads_first() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // This thread's code words (UB blocks x K planes) of row `rowc`: 8 groups per (block, plane),
 // streaming loads, addresses clamped so that every thread issues the same loads.
 template <int K, int UB>
@@ -589,6 +600,7 @@ void gemv_cw_kernel(GemvArgs a) {
   const uint4 cbv = ((const uint4*)a.codebooks)[tid % (K * 256)];   // K * 256 <= 1024 codewords
   asm volatile("" ::: "memory");
   const uint16_t sbits = a.scales[rowc];                   // the row scale, needed only at the end
+  cw_small_loads_first();
   uint2 code[UB][K];
   cw_load_codes<K, UB>(code, a.codes, a.plane_bytes, a.d_out, rowc, Gp);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in (older than the scale and codes)
@@ -656,6 +668,7 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   asm volatile("" ::: "memory");
   uint32_t sa, sb;
   uint2 ca[UB][K], cb[UB][K];
+  cw_small_loads_first();
   load_block(rb, sa, ca);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
@@ -725,14 +738,21 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
       if ((int)blockIdx.x < a.L[j].row_blocks) return j;
     return -1;
   };
-  // the layer's codebook word (first), row scale and code words
-  auto load_layer = [&](int l, uint4& cbv, uint32_t& sbits, uint2 (&code)[UB][K]) {
+  // the layer's codebook word (first) and row scale; its code words
+  auto load_small = [&](int l, uint4& cbv, uint32_t& sbits) {
     cbv = ((const uint4*)a.L[l].codebooks)[tid % (K * 256)];
     asm volatile("" ::: "memory");                        // the codebook word goes out first
     const int d_out = a.L[l].d_out;
-    const int rowc = row < d_out ? row : d_out - 1;
-    sbits = a.L[l].scales[rowc];
-    cw_load_codes<K, UB>(code, a.L[l].codes, a.L[l].plane_bytes, d_out, rowc, Gp);
+    sbits = a.L[l].scales[row < d_out ? row : d_out - 1];
+  };
+  auto load_codes = [&](int l, uint2 (&code)[UB][K]) {
+    const int d_out = a.L[l].d_out;
+    cw_load_codes<K, UB>(code, a.L[l].codes, a.L[l].plane_bytes, d_out, row < d_out ? row : d_out - 1, Gp);
+  };
+  // the layer's codebook word (first), row scale and code words
+  auto load_layer = [&](int l, uint4& cbv, uint32_t& sbits, uint2 (&code)[UB][K]) {
+    load_small(l, cbv, sbits);
+    load_codes(l, code);
   };
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group, once
   float* scl = (float*)((char*)xs + NB * rstride);         // [NB][rstride / 16] group scales
@@ -748,7 +768,9 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   uint4 cba, cbb;
   uint32_t sa, sb;
   uint2 ca[UB][K], cb[UB][K];
-  load_layer(cur, cba, sa, ca);
+  load_small(cur, cba, sa);
+  cw_small_loads_first();
+  load_codes(cur, ca);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
   cw_replicate<K>(cb_rep, cba, nrep, a.cb_shift);
