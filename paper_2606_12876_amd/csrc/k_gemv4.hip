@@ -96,18 +96,23 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
     for (int b = 0; b < NB; ++b) acc[t][b] = 0.f;
 
   for (int g0 = 0; g0 < Gp; g0 += kChunk) {
-    // code words of this chunk: block u, plane m -> 8 groups g0 + 512 u + 8 part .. + 7
+    // code words of this chunk: block u, plane m -> 8 groups g0 + 512 u + 8 part .. + 7. At batch 1
+    // they are requested after x (the small, cache-resident loads go first: a CU's requests leave in
+    // order) and awaited where each is used; with tiles of 4 batch rows, before the tiles.
     uint32_t code[UB][K];
+    auto load_codes = [&]() {
 #pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      int j0 = g0 + u * 512 + part * 8;
-      j0 = j0 < Gp ? j0 : Gp - 8;                            // unused blocks reload a valid word
+      for (int u = 0; u < UB; ++u) {
+        int j0 = g0 + u * 512 + part * 8;
+        j0 = j0 < Gp ? j0 : Gp - 8;                          // unused blocks reload a valid word
 #pragma unroll
-      for (int m = 0; m < K; ++m)
-        code[u][m] = __builtin_nontemporal_load(
-            (const uint32_t*)(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 5) * a.d_out + rowc) * 16 + ((j0 & 31) >> 1)));
-    }
+        for (int m = 0; m < K; ++m)
+          code[u][m] = __builtin_nontemporal_load(
+              (const uint32_t*)(a.codes + m * a.plane_bytes + ((size_t)(j0 >> 5) * a.d_out + rowc) * 16 + ((j0 & 31) >> 1)));
+      }
+    };
     const int n_ch = ((Gp - g0 < kChunk ? Gp - g0 : kChunk) + 63) / 64;   // 1 KiB pieces per x row
+    if constexpr (NB > 1) load_codes();
 #pragma unroll
     for (int t = 0; t < kTiles; ++t) {
       if (t < n_tiles) {
@@ -120,7 +125,15 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
                                                          : a.zero_page;
           load_lds16(src, xs_base + (uint32_t)(b * kChunk * 16 + ch * 1024));
         }
-        wait_vmcnt<0>();
+        if constexpr (NB == 1) {
+          asm volatile("" ::: "memory");
+          __builtin_amdgcn_s_barrier();                      // every wave's x requests before any code words
+          asm volatile("" ::: "memory");
+          load_codes();
+          wait_vmcnt<UB * K>();                              // this thread's x pieces are in
+        } else {
+          wait_vmcnt<0>();
+        }
         if constexpr (kXS) {                                 // the groups this thread loaded
           for (int q = wave; q < n_ch; q += b4::kWaves) {
             const int gq = q * 64 + lane;
