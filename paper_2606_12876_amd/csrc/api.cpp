@@ -138,7 +138,8 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
   return AQMB_OK;
 }
 
-// GEMV kernel choice. Default: 4-bit codes -> their kernel; 8-bit codes at batch >= 3, and at
+// GEMV kernel choice. Default: 4-bit codes -> the matrix-core kernel at batch >= 2, their own
+// kernel at batch 1; 8-bit codes at batch >= 3, and at
 // batch 2 on rows of more than 512 groups -> the matrix-core kernel (measured faster there; at
 // batch 2 on shorter rows the two are within a few percent); otherwise the direct-gather kernel
 // (k <= 4, rows <= 16384) or the lookup table kernel, as k_gemv.hip decides. AQMB_GEMV=mma uses
@@ -158,14 +159,15 @@ static int gemv_mode() {
 // (At batch 2 on rows of more than 512 groups the direct-gather kernel would hold the code words of
 // four 512-group blocks next to two batch rows: more than its registers.)
 static bool gemv_uses_mma(const Layer& L, int batch) {
+  if (L.d.code_bits == 4) return gemv_mode() == 3 || (gemv_mode() == 0 && batch >= 2);   // its own kernel tiles 4 rows from 2 on
   const bool wide = L.S * L.J > 512;
   return L.d.code_bits == 8 && (gemv_mode() == 3 || (gemv_mode() == 0 && (batch >= 3 || (batch == 2 && wide))));
 }
 
 static hipError_t launch_gemv_any(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                                   aqmb_dtype y_dtype, hipStream_t st) {
-  if (L.d.code_bits == 4) return launch_gemv_b4(L, k, x, x_dtype, batch, y, y_dtype, st);
   if (gemv_uses_mma(L, batch)) return launch_gemv_mma(L, k, x, x_dtype, batch, y, y_dtype, st);
+  if (L.d.code_bits == 4) return launch_gemv_b4(L, k, x, x_dtype, batch, y, y_dtype, st);
   return launch_gemv(L, k, x, x_dtype, batch, y, y_dtype, st);
 }
 

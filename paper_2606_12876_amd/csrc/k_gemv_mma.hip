@@ -1,9 +1,9 @@
-// Decode GEMV on the matrix cores (8-bit codes, any batch up to 16; used from batch 3 on): y[b][i] = s_i sum_j sum_{m<k}
+// Decode GEMV on the matrix cores (8- and 4-bit codes, any batch up to 16; used from batch 3 on): y[b][i] = s_i sum_j sum_{m<k}
 // <x[b, group j], C_m[b_{ijm}]>, the per-plane products computed by v_mfma_f32_16x16x32 with the
 // batch in the 16 rows of the A operand and 16 weight rows in the columns of the B operand.
 //
 // A workgroup of 16 waves owns 16 weight rows; the waves take interleaved runs of 4 K-steps of 32
-// inputs (a run is the 16 groups of one code slice, one 16-byte load per plane). In a K-step lane l
+// inputs (a run is 16 groups: one 16-byte code slice per plane, or half of a 4-bit slice). In a K-step lane l
 // of a wave stands for weight row l % 16 and group l / 16 of the step: it gathers that group's
 // codeword of every plane from the codebooks replicated in LDS, which is the B fragment of that
 // plane's MFMA as it is (8 fp16 values of one row and group). The A fragment is x itself: lane l
@@ -15,6 +15,8 @@
 // of high parts and a book of low parts), so a code costs two gathers and two MFMAs.
 // Sums are fp32. The 16 waves' partial tiles are added in wave order, scaled once and rounded
 // once, so results are reproducible.
+#include <type_traits>
+
 #include "device.h"
 #include "launch.h"
 
@@ -40,19 +42,20 @@ struct GemvMmaArgs {
 };
 
 
-// A run: 4 consecutive K-steps = the 16 groups of one code slice. Per lane: x of its batch row
-// for the 4 steps (8 values each) and one 16-byte slice word per plane (groups of its weight row).
-template <int K>
+// A run: 4 consecutive K-steps = 16 groups (8-bit codes: one 16-byte code slice; 4-bit codes:
+// half of a 32-group slice, 8 bytes). Per lane: x of its batch row for the 4 steps (8 values each)
+// and the run's code bytes of its weight row, per plane.
+template <int K, int CB>
 struct MgRun {
   uint4 xa[4];
-  uint4 c[K];
+  typename std::conditional<CB == 8, uint4, uint2>::type c[K];
 };
 
 // Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of batch
 // row `col` at inputs 128 r + 32 j + 8 kc .. + 7 for steps j = 0..3 (zeros past d_in, past the
 // batch, and for dummy runs), and slice r of the row in every plane.
-template <int K>
-__device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K>& R) {
+template <int K, int CB>
+__device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K, CB>& R) {
   const int lane = threadIdx.x & 63, col = lane & 15, kc = lane >> 4;
   const int n_runs = (a.G + 15) / 16;
   const int rc = r < n_runs ? r : n_runs - 1;
@@ -63,16 +66,19 @@ __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int row
     R.xa[j] = *(const uint4*)src;
   }
 #pragma unroll
-  for (int m = 0; m < K; ++m) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+  for (int m = 0; m < K; ++m) {
+    if constexpr (CB == 8) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+    else R.c[m] = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(rc >> 1) * a.d_out + rowc) * 16 + (rc & 1) * 8);
+  }
 }
 
-// Codebook word q (q < K * 256) into its nrep replicas (bf16 x: a book of high and a book of low
+// Codebook word q (q < K * NCW) into its nrep replicas (bf16 x: a book of high and a book of low
 // parts, split exactly).
-template <int K, int XDT>
+template <int K, int XDT, int CB>
 __device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep) {
   using namespace mg;
-  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;
-  for (int q = threadIdx.x; q < K * 256; q += kThreads) {
+  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2, NCW = 1 << CB;
+  for (int q = threadIdx.x; q < K * NCW; q += kThreads) {
     const uint4 v = ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - a.cb_shift);
     if constexpr (kBooks == 1) {
@@ -89,32 +95,39 @@ __device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep
       const uint4 vh = __builtin_bit_cast(uint4, hi), vl = __builtin_bit_cast(uint4, lo);
       for (int i = 0; i < a.nrep; ++i) {
         cb_rep[q * a.nrep + ((i + rot) & (a.nrep - 1))] = vh;
-        cb_rep[(K * 256 + q) * a.nrep + ((i + rot) & (a.nrep - 1))] = vl;
+        cb_rep[(K * NCW + q) * a.nrep + ((i + rot) & (a.nrep - 1))] = vl;
       }
     }
   }
 }
 
-// The MFMAs of one run. Step j of a run: group 4 j + kc of the slice, code byte 4 j + kc of each
-// plane's word.
-template <int K, int XDT>
+// The MFMAs of one run. Step j of a run: group 4 j + kc of the run (8-bit codes: byte 4 j + kc of
+// the plane's slice word; 4-bit codes: nibble 4 j + kc of its 8 bytes).
+template <int K, int XDT, int CB>
 __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb_rep, uint32_t rep_off,
-                                           const MgRun<K>& R, mg::f32x4_t (&acc)[4]) {
+                                           const MgRun<K, CB>& R, mg::f32x4_t (&acc)[4]) {
   using namespace mg;
+  constexpr int NCW = 1 << CB;
   const int kc = (threadIdx.x & 63) >> 4;
 #pragma unroll
   for (int m = 0; m < K; ++m) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
-      const uint32_t code = (word >> (8 * kc)) & 0xFFu;
-      const uint32_t off = (((uint32_t)(m * 256) + code) << a.cb_shift) + rep_off;
+      uint32_t code;
+      if constexpr (CB == 8) {
+        const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
+        code = (word >> (8 * kc)) & 0xFFu;
+      } else {
+        const uint32_t word = j < 2 ? R.c[m].x : R.c[m].y;
+        code = (word >> (4 * (4 * (j & 1) + kc))) & 15u;
+      }
+      const uint32_t off = (((uint32_t)(m * NCW) + code) << a.cb_shift) + rep_off;
       const uint4 cw = *(const uint4*)((const char*)cb_rep + off);
       if constexpr (XDT == AQMB_F16) {
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, R.xa[j]),
                                                         __builtin_bit_cast(f16x8_t, cw), acc[j], 0, 0, 0);
       } else {
-        const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * 256) << a.cb_shift) + off);
+        const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * NCW) << a.cb_shift) + off);
         const b16x8_t xb = __builtin_bit_cast(b16x8_t, R.xa[j]);
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cw), acc[j], 0, 0, 0);
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cl), acc[j], 0, 0, 0);
@@ -156,14 +169,14 @@ __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_
   }
 }
 
-template <int K, int XDT>
+template <int K, int XDT, int CB>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_kernel(GemvMmaArgs a) {
   using namespace mg;
   constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;            // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
-  uint4* cb_rep = smem_mg;                                   // [kBooks][K][256][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * 256 * a.nrep);   // [kWaves][64] partial tiles
+  uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;                                 // weight row in the block
@@ -174,11 +187,11 @@ void gemv_mma_kernel(GemvMmaArgs a) {
 
   // The wave's runs are wave, wave + 16, ...; the first two are requested before the codebooks are
   // replicated into LDS (a 4096-wide row has 32 runs: two per wave).
-  MgRun<K> ra, rb;
+  MgRun<K, CB> ra, rb;
   int r = wave;
-  mg_load_run<K>(a, r, rowc, true, ra);
-  mg_load_run<K>(a, r + kWaves, rowc, true, rb);
-  mg_replicate<K, XDT>(a, cb_rep);
+  mg_load_run<K, CB>(a, r, rowc, true, ra);
+  mg_load_run<K, CB>(a, r + kWaves, rowc, true, rb);
+  mg_replicate<K, XDT, CB>(a, cb_rep);
   __syncthreads();
 
   f32x4_t acc[4];
@@ -187,11 +200,11 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   // Two register sets in turn: the loads of the wave's run after next are requested while it
   // computes one.
   for (; r < n_runs; r += 2 * kWaves) {
-    mg_compute<K, XDT>(a, cb_rep, rep_off, ra, acc);
+    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, ra, acc);
     if (r + kWaves >= n_runs) break;
-    if (r + 2 * kWaves < n_runs) mg_load_run<K>(a, r + 2 * kWaves, rowc, true, ra);
-    mg_compute<K, XDT>(a, cb_rep, rep_off, rb, acc);
-    if (r + 3 * kWaves < n_runs) mg_load_run<K>(a, r + 3 * kWaves, rowc, true, rb);
+    if (r + 2 * kWaves < n_runs) mg_load_run<K, CB>(a, r + 2 * kWaves, rowc, true, ra);
+    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, rb, acc);
+    if (r + 3 * kWaves < n_runs) mg_load_run<K, CB>(a, r + 3 * kWaves, rowc, true, rb);
   }
   mg_reduce_store(a, red, acc, row0);
 }
@@ -202,14 +215,14 @@ void gemv_mma_kernel(GemvMmaArgs a) {
 // the row are dummies: x reads zeros) as one flat sequence of items over its blocks, two items
 // ahead in two register sets, so the next block's first runs are in flight while a block ends
 // (partial tiles added in wave order, as in gemv_mma_kernel; same arithmetic and order).
-template <int K, int XDT>
+template <int K, int XDT, int CB>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_persist_kernel(GemvMmaArgs a) {
   using namespace mg;
   constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;
   extern __shared__ uint4 smem_mg[];
-  uint4* cb_rep = smem_mg;                                   // [kBooks][K][256][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * 256 * a.nrep);   // [kWaves][64] partial tiles
+  uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;
@@ -222,11 +235,11 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 
   // item i: block blockIdx.x + (i / per) gridDim.x, run wave + (i % per) 16 (items past the end:
   // the last item again, never used)
-  auto load_item = [&](int i, MgRun<K>& R) {
+  auto load_item = [&](int i, MgRun<K, CB>& R) {
     const int ic = i < n_items ? i : n_items - 1;
     const int row = ((int)blockIdx.x + (ic / per) * (int)gridDim.x) * kRows + col;
     const int r = wave + (ic % per) * kWaves;
-    mg_load_run<K>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R);
+    mg_load_run<K, CB>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R);
   };
   f32x4_t acc[4];
   auto end_block = [&](int i) {                              // item i closed its block
@@ -236,48 +249,54 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
     __syncthreads();                                         // wave 0 has read the partial tiles
   };
 
-  MgRun<K> ra, rb;
+  MgRun<K, CB> ra, rb;
   load_item(0, ra);
   load_item(1, rb);
-  mg_replicate<K, XDT>(a, cb_rep);
+  mg_replicate<K, XDT, CB>(a, cb_rep);
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < n_items; i += 2) {
-    mg_compute<K, XDT>(a, cb_rep, rep_off, ra, acc);
+    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, ra, acc);
     load_item(i + 2, ra);
     if ((i + 1) % per == 0) end_block(i);
     if (i + 1 >= n_items) break;
-    mg_compute<K, XDT>(a, cb_rep, rep_off, rb, acc);
+    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, rb, acc);
     load_item(i + 3, rb);
     if ((i + 2) % per == 0) end_block(i + 1);
   }
 }
 
-template <int K, int XDT>
-static hipError_t launch_mma_k(GemvMmaArgs a, hipStream_t st) {
-  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * 256 * 16;
+// 16-codeword codebooks (4-bit codes) fill the LDS banks once: one copy reads without conflicts.
+template <int K, int XDT, int CB>
+static hipError_t launch_mma_kc(GemvMmaArgs a, hipStream_t st) {
+  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
-  a.nrep = book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
-  a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : 5;
+  a.nrep = CB == 4 ? 1 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
+  a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
   const size_t lds = book * a.nrep + red;
   const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
-  if (n_rb > a.n_cu && a.n_cu > 0) gemv_mma_persist_kernel<K, XDT><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
-  else gemv_mma_kernel<K, XDT><<<dim3(n_rb), mg::kThreads, lds, st>>>(a);
+  if (n_rb > a.n_cu && a.n_cu > 0) gemv_mma_persist_kernel<K, XDT, CB><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
+  else gemv_mma_kernel<K, XDT, CB><<<dim3(n_rb), mg::kThreads, lds, st>>>(a);
   return hipGetLastError();
 }
 
+template <int K, int XDT>
+static hipError_t launch_mma_k(const GemvMmaArgs& a, int code_bits, hipStream_t st) {
+  return code_bits == 4 ? launch_mma_kc<K, XDT, 4>(a, st) : launch_mma_kc<K, XDT, 8>(a, st);
+}
+
 template <int XDT>
-static hipError_t launch_mma_x(const GemvMmaArgs& a, int k, hipStream_t st) {
+static hipError_t launch_mma_x(const GemvMmaArgs& a, int k, int cb, hipStream_t st) {
   switch (k) {
-    case 1: return launch_mma_k<1, XDT>(a, st);
-    case 2: return launch_mma_k<2, XDT>(a, st);
-    case 3: return launch_mma_k<3, XDT>(a, st);
-    case 4: return launch_mma_k<4, XDT>(a, st);
-    case 5: return launch_mma_k<5, XDT>(a, st);
-    case 6: return launch_mma_k<6, XDT>(a, st);
-    case 7: return launch_mma_k<7, XDT>(a, st);
-    default: return launch_mma_k<8, XDT>(a, st);
+    case 1: return launch_mma_k<1, XDT>(a, cb, st);
+    case 2: return launch_mma_k<2, XDT>(a, cb, st);
+    case 3: return launch_mma_k<3, XDT>(a, cb, st);
+    case 4: return launch_mma_k<4, XDT>(a, cb, st);
+    case 5: return launch_mma_k<5, XDT>(a, cb, st);
+    case 6: return launch_mma_k<6, XDT>(a, cb, st);
+    case 7: return launch_mma_k<7, XDT>(a, cb, st);
+    default: return launch_mma_k<8, XDT>(a, cb, st);
   }
 }
 
@@ -297,7 +316,8 @@ hipError_t launch_gemv_mma(const Layer& L, int k, const void* x, aqmb_dtype x_dt
   a.batch = batch;
   a.y_dtype = (int)y_dtype;
   a.n_cu = L.n_cu;
-  return x_dtype == AQMB_F16 ? launch_mma_x<AQMB_F16>(a, k, st) : launch_mma_x<AQMB_BF16>(a, k, st);
+  const int cb = L.d.code_bits;
+  return x_dtype == AQMB_F16 ? launch_mma_x<AQMB_F16>(a, k, cb, st) : launch_mma_x<AQMB_BF16>(a, k, cb, st);
 }
 
 }  // namespace aqmb

@@ -48,10 +48,13 @@ def test_dequant_bit_exact(shape):
 
 
 @pytest.mark.parametrize("shape,batches", [((77, 360, 4), (1, 3, 16)), ((4096, 4096, 4), (1, 4)),
-                                           ((130, 20000, 3), (1, 5)), ((64, 512, 8), (1, 8))])
+                                           ((130, 20000, 3), (1, 5)), ((64, 512, 8), (1, 8)),
+                                           ((5000, 520, 4), (1, 2, 8))])
 def test_gemv_matches_oracle(shape, batches):
     """Ragged rows and groups (360 = 45 groups: one partial 32-group slice), the benchmarked shape,
-    a row longer than one 2048-group stage of x (20000 = 2500 groups), and M = 8."""
+    a row longer than one 2048-group stage of x (20000 = 2500 groups), M = 8, and 313 blocks of 16
+    rows (more than one per compute unit). Batch 1 on the 4-bit kernel, 2 and more on the matrix
+    cores."""
     d_out, d_in, M = shape
     L = make_layer(LayerSpec("b4g", d_out, d_in, M=M, B=4, seed=310 + d_in))
     C, s = _vals(L)
