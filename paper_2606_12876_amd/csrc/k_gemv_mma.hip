@@ -72,14 +72,34 @@ __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int row
   }
 }
 
+// When every thread replicates at most one codeword (K * NCW <= 1024), that word is requested
+// ahead of the code words: a CU's requests leave in order, and the replication waits for it.
+// (With more codewords per thread the runs' registers leave no room to hold it.)
+template <int K, int CB> constexpr bool mg_preload() { return K * (1 << CB) <= mg::kThreads; }
+template <int K, int CB>
+__device__ __forceinline__ uint4 mg_first_word(const GemvMmaArgs& a) {
+  if constexpr (!mg_preload<K, CB>()) return make_uint4(0, 0, 0, 0);
+  const int q = (int)threadIdx.x < K * (1 << CB) ? (int)threadIdx.x : 0;
+  return ((const uint4*)a.codebooks)[q];
+}
+
+// An execution barrier between every wave's small loads and the code words (see mg_first_word).
+template <int K, int CB>
+__device__ __forceinline__ void mg_small_loads_first() {
+  if constexpr (!mg_preload<K, CB>()) return;
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Codebook word q (q < K * NCW) into its nrep replicas (bf16 x: a book of high and a book of low
-// parts, split exactly).
+// parts, split exactly); v0 is word threadIdx.x, already loaded.
 template <int K, int XDT, int CB>
-__device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep) {
+__device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep, uint4 v0) {
   using namespace mg;
   constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2, NCW = 1 << CB;
   for (int q = threadIdx.x; q < K * NCW; q += kThreads) {
-    const uint4 v = ((const uint4*)a.codebooks)[q];
+    const uint4 v = mg_preload<K, CB>() ? v0 : ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - a.cb_shift);
     if constexpr (kBooks == 1) {
       for (int i = 0; i < a.nrep; ++i) cb_rep[q * a.nrep + ((i + rot) & (a.nrep - 1))] = v;
@@ -189,9 +209,11 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   // replicated into LDS (a 4096-wide row has 32 runs: two per wave).
   MgRun<K, CB> ra, rb;
   int r = wave;
+  const uint4 w0 = mg_first_word<K, CB>(a);
+  mg_small_loads_first<K, CB>();
   mg_load_run<K, CB>(a, r, rowc, true, ra);
   mg_load_run<K, CB>(a, r + kWaves, rowc, true, rb);
-  mg_replicate<K, XDT, CB>(a, cb_rep);
+  mg_replicate<K, XDT, CB>(a, cb_rep, w0);
   __syncthreads();
 
   f32x4_t acc[4];
@@ -250,9 +272,11 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   };
 
   MgRun<K, CB> ra, rb;
+  const uint4 w0 = mg_first_word<K, CB>(a);
+  mg_small_loads_first<K, CB>();
   load_item(0, ra);
   load_item(1, rb);
-  mg_replicate<K, XDT, CB>(a, cb_rep);
+  mg_replicate<K, XDT, CB>(a, cb_rep, w0);
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
