@@ -85,12 +85,23 @@ void gemm_small_kernel(GemmSmallArgs a) {
     }
   };
 
+  // When each thread replicates at most one codeword, that word is requested ahead of the runs
+  // (a CU's requests leave in order and the replication waits for it), with an execution barrier
+  // between every wave's codebook request and the code words.
+  constexpr bool kPre = K * NCW <= kThreads;
+  uint4 v0 = make_uint4(0, 0, 0, 0);
+  if constexpr (kPre) {
+    v0 = ((const uint4*)a.codebooks)[tid < K * NCW ? tid : 0];
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  }
   GsRun<K, NA> ra, rb;
   int r = wave;
   load_run(r, ra);
   load_run(r + kWaves, rb);
   for (int q = tid; q < K * NCW; q += kThreads) {
-    const uint4 v = ((const uint4*)a.codebooks)[q];
+    const uint4 v = kPre ? v0 : ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - kShift);
 #pragma unroll
     for (int i = 0; i < kNrep; ++i) cb_rep[q * kNrep + ((i + rot) & (kNrep - 1))] = v;
