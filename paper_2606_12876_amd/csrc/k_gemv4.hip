@@ -163,11 +163,14 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
               uint4 xg[NB];
 #pragma unroll
               for (int b = 0; b < NB; ++b) xg[b] = *(const uint4*)(xs + (size_t)b * kChunk * 16 + (size_t)(j0 + jj) * 16);
-              float gs = 0.f;                                // kXS: the group's sum over the planes
+              // batch 1 with fp16 values (fp16 x, or bf16 x converted): the group's products are
+              // chained over the planes into one sum (one v_dot2 per code word pair)
+              constexpr bool kChain = NB == 1 && (kXS || XDT == AQMB_F16);
+              float gs = 0.f;
 #pragma unroll
               for (int m = 0; m < K; ++m) {
                 const uint4 cwv = cb[m * 16 + ((code[u][m] >> (4 * jj)) & 15u)];
-                if constexpr (kXS) {
+                if constexpr (kChain) {
                   gs = dot8_acc_f16(xg[0], cwv, gs);
                 } else {
 #pragma unroll
@@ -175,6 +178,7 @@ __global__ __launch_bounds__(b4::kThreads) void gemv_b4_kernel(Gemv4Args a) {
                 }
               }
               if constexpr (kXS) acc[t][0] = __builtin_fmaf(gs, scl[j0 + jj], acc[t][0]);
+              else if constexpr (kChain) acc[t][0] += gs;
             };
             if constexpr (NB == 1) {
 #pragma unroll
