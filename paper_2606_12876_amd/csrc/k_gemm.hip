@@ -2,11 +2,12 @@
 // reconstruction from the first k codebooks (binary32 left fold over planes), rounded to bf16,
 // and the products run on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16, fp32 accumulate).
 //
-// A workgroup computes a BM x BN tile of Y (BM = 256 tokens, BN = 128 output rows), walking
+// A workgroup computes a BM x BN tile of Y (BM = 256 tokens, or 128 when 256-token tiles would
+// leave compute units idle; BN = 128 output rows), walking
 // d_in in steps of BK = 64 (four MFMA K-blocks of 16). Eight waves share the four SIMDs in two
 // roles, handing data over through LDS with one barrier per step:
-//   - four consumer waves each own a 128 x 64 block of the tile (4 x 2 MFMA blocks of 32 x 32,
-//     fp32 accumulators in registers). They also stream X: direct global->LDS loads (16 bytes
+//   - four consumer waves each own a BM/2 x 64 block of the tile (BM/64 x 2 MFMA blocks of
+//     32 x 32, fp32 accumulators in registers). They also stream X: direct global->LDS loads (16 bytes
 //     per lane, eight lanes per 128-byte row segment) fill a ring of X stages several steps
 //     ahead, so X reaches LDS without passing through registers. Within a step the fragments
 //     of K-block i + 1 are read from LDS while the MFMAs of block i run;
@@ -38,7 +39,7 @@ namespace gemm {
 constexpr int BM = 256, BN = 128, BK = 64;
 constexpr int kThreads = 512;                        // waves 0-3 consume, waves 4-7 produce
 template <int K> constexpr int x_depth() { return K <= 4 ? 3 : 2; }   // X stages (LDS budget)
-constexpr int kXStage = BM * BK;                     // bf16 elements: 256 rows x 128 bytes
+template <int BMT> constexpr int x_stage() { return BMT * BK; }   // bf16 elements: BMT rows x 128 bytes
 constexpr int kChunk = 512;                          // one weight fragment: 64 lanes x 8 bf16
 constexpr int kSlab = (BN / 32) * (BK / 16) * kChunk;  // 4 column blocks x 4 K-blocks
 constexpr int kCodeDepth = 4;                        // steps of code words in flight per producer wave
@@ -96,7 +97,7 @@ __device__ __forceinline__ uint4 dequant_group_bf16(const uint4* __restrict__ cb
 }
 
 // CB = code bits: 8 (256 codewords per codebook) or 4 (16 codewords).
-template <int K, int YDT, int CB>
+template <int K, int YDT, int CB, int BMT>
 __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned char* __restrict__ codes,
                                                               const uint16_t* __restrict__ codebooks,
                                                               const uint16_t* __restrict__ scales,
@@ -106,6 +107,9 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   using namespace gemm;
   constexpr int kDepth = x_depth<K>();
   constexpr int NCW = 1 << CB;
+  constexpr int kXStage = x_stage<BMT>();
+  constexpr int MA = BMT / 64;                     // 32-row MFMA blocks per consumer wave
+  constexpr int kXLoads = BMT / 32;                // direct X loads per consumer wave and step
   extern __shared__ uint4 smem[];
   uint16_t* Xs = (uint16_t*)smem;                  // [kDepth][256 rows][8 swizzled 16-byte pieces]
   uint16_t* Bs = Xs + kDepth * kXStage;            // [2][4 col blocks][4 K-blocks][64 lanes][8]
@@ -116,7 +120,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform across the wave
   const int half = lane >> 5, r32 = lane & 31;
   const int tb = blockIdx.x % n_tb, cb = blockIdx.x / n_tb;
-  const int n0 = tb * BM, i0 = cb * BN;
+  const int n0 = tb * BMT, i0 = cb * BN;
   const int nsteps = (d_in + BK - 1) / BK;
   const int s0 = (int)(((long long)cb * nsteps) / n_cb);
   auto step_of = [&](int seq) { int st = s0 + seq; return st >= nsteps ? st - nsteps : st; };
@@ -201,7 +205,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   }
 
   // -------------------------------------------------------------------- consumers
-  const int wm = wave >> 1, wn = wave & 1;          // 128 x 64 block of the tile
+  const int wm = wave >> 1, wn = wave & 1;          // BMT/2 x 64 block of the tile
   // X stage layout: row r's 16-byte piece kc (8 bf16 of K) sits at r * 128 + ((kc ^ ((r >> 1) & 7)) * 16)
   // bytes. A direct load covers 8 rows x 128 bytes (8 lanes per row, full cache lines); the
   // XOR keeps fragment reads (32 rows, one piece each) on distinct banks.
@@ -211,48 +215,48 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
     const int pos = lane & 7, rsub = lane >> 3;
     if (k0 + BK <= d_in) {
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {                 // this wave's rows 64 * wave .. + 63
-        const int r = wave * 64 + t * 8 + rsub;
+      for (int t = 0; t < kXLoads; ++t) {           // this wave's rows (BMT/4) wave .. + BMT/4 - 1
+        const int r = wave * (BMT / 4) + t * 8 + rsub;
         const int kc = pos ^ ((r >> 1) & 7);
         const int row = n0 + r < n_tokens ? n0 + r : n_tokens - 1;
-        uint16_t* base = stage + (wave * 64 + t * 8) * BK;   // 1 KiB: 8 rows, written lane-ordered
+        uint16_t* base = stage + (wave * (BMT / 4) + t * 8) * BK;   // 1 KiB: 8 rows, written lane-ordered
         load_lds16(X + (size_t)row * d_in + k0 + kc * 8, (uint32_t)(uintptr_t)(lds_ptr)base);
       }
     } else {                                         // the ragged last step: zero past d_in
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const int r = wave * 64 + t * 8 + rsub;
+      for (int t = 0; t < kXLoads; ++t) {
+        const int r = wave * (BMT / 4) + t * 8 + rsub;
         const int kc = pos ^ ((r >> 1) & 7);
         const int row = n0 + r;
-        uint16_t* base = stage + (wave * 64 + t * 8) * BK;
+        uint16_t* base = stage + (wave * (BMT / 4) + t * 8) * BK;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (row < n_tokens && k0 + kc * 8 < d_in) v = *(const uint4*)(X + (size_t)row * d_in + k0 + kc * 8);
         *(uint4*)(base + lane * 8) = v;
       }
     }
   };
-  f32x16_t acc[4][2];
+  f32x16_t acc[MA][2];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < MA; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
 
-  struct Frags { bf16x8_t a[4], b[2]; };
+  struct Frags { bf16x8_t a[MA], b[2]; };
   auto read_frags = [&](const uint16_t* xst, const uint16_t* bsl, int i, Frags& f) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) f.b[b] = *(const bf16x8_t*)(bsl + ((wn * 2 + b) * 4 + i) * kChunk + lane * 8);
     const int kc = 2 * i + half;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const int r = wm * 128 + a * 32 + r32;
+    for (int a = 0; a < MA; ++a) {
+      const int r = wm * (BMT / 2) + a * 32 + r32;
       f.a[a] = *(const bf16x8_t*)(xst + r * BK + ((kc ^ ((r >> 1) & 7)) * 8));
     }
   };
   auto mfmas = [&](const Frags& f) {
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < MA; ++a)
 #pragma unroll
       for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
   };
@@ -262,7 +266,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   for (int seq = 0; seq < nsteps; ++seq) {
     {                                                // own X loads of step seq done
       const int after = min(kDepth - 2, nsteps - 1 - seq);   // later steps already issued
-      if (after >= 1) AQMB_WAIT_VMCNT(8); else AQMB_WAIT_VMCNT(0);
+      if (after >= 1) AQMB_WAIT_VMCNT(kXLoads); else AQMB_WAIT_VMCNT(0);
     }
     __syncthreads();                                 // X stage seq and slab seq published
     if (seq + kDepth - 1 < nsteps) load_x(seq + kDepth - 1);
@@ -281,8 +285,8 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
       if (i < 3) read_frags(xst, bsl, i + 1, nxt);
       mfmas(cur);
       if (i < 3) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, MA + 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * MA, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -293,29 +297,44 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
     if (col >= d_out) continue;
     const float scale = f16_to_f32(scales[col]);
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
+    for (int a = 0; a < MA; ++a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int row = n0 + wm * 128 + a * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+        const int row = n0 + wm * (BMT / 2) + a * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
         if (row < n_tokens) OutT<YDT>::store(Y, (size_t)row * d_out + col, acc[a][b][e] * scale);
       }
     }
   }
 }
 
-template <int K, int CB>
-static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
+template <int K, int CB, int BMT>
+static void launch_kcm(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
   using namespace gemm;
   constexpr int kDepth = x_depth<K>();
-  const int n_tb = (n_tokens + BM - 1) / BM, n_cb = (L.d.d_out + BN - 1) / BN;
-  const size_t lds = ((size_t)kDepth * kXStage + 2 * kSlab) * 2 + (size_t)K * (1 << CB) * 16 + (size_t)kCodeDepth * 4 * K * 64 * 4;
+  const int n_tb = (n_tokens + BMT - 1) / BMT, n_cb = (L.d.d_out + BN - 1) / BN;
+  const size_t lds = ((size_t)kDepth * x_stage<BMT>() + 2 * kSlab) * 2 + (size_t)K * (1 << CB) * 16 +
+                     (size_t)kCodeDepth * 4 * K * 64 * 4;
   const dim3 grid(n_tb * n_cb);
   if (y_dtype == AQMB_BF16)
-    gemm_kernel<K, AQMB_BF16, CB><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                                n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+    gemm_kernel<K, AQMB_BF16, CB, BMT><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
+                                                                     n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
   else
-    gemm_kernel<K, AQMB_F32, CB><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                               n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+    gemm_kernel<K, AQMB_F32, CB, BMT><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
+                                                                    n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+}
+
+// 128-token tiles when 256-token tiles would leave compute units idle and the 128-token tiles still
+// fit in one wave of workgroups (e.g. 4096 rows: 257..1024 tokens); 256-token tiles otherwise.
+static bool gemm_use_bm128(const Layer& L, int n_tokens) {
+  const int n_cb = (L.d.d_out + gemm::BN - 1) / gemm::BN;
+  const long long wg256 = (long long)((n_tokens + 255) / 256) * n_cb, wg128 = (long long)((n_tokens + 127) / 128) * n_cb;
+  return wg256 < L.n_cu && wg128 <= L.n_cu;
+}
+
+template <int K, int CB>
+static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
+  if (gemm_use_bm128(L, n_tokens)) launch_kcm<K, CB, 128>(L, X, n_tokens, Y, y_dtype, st);
+  else launch_kcm<K, CB, 256>(L, X, n_tokens, Y, y_dtype, st);
 }
 
 template <int K>
