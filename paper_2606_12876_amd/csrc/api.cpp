@@ -183,7 +183,7 @@ static int gemm_mode() {
   }();
   return v;
 }
-constexpr int kGemmSmallMax = 192;   // tokens: the 16-row tiling re-gathers per 64 tokens; measured break-even near 256
+constexpr int kGemmSmallMax = 144;   // tokens: the 16-row tiling re-gathers per 64 tokens; measured break-even with 128 x 64 tiles near 150
 
 // k must name resident planes.
 static aqmb_status check_resident(const Layer* L, int k, const char* where) {

@@ -2,8 +2,8 @@
 // reconstruction from the first k codebooks (binary32 left fold over planes), rounded to bf16,
 // and the products run on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16, fp32 accumulate).
 //
-// A workgroup computes a BM x BN tile of Y (BM = 256 tokens, or 128 when 256-token tiles would
-// leave compute units idle; BN = 128 output rows), walking
+// A workgroup computes a BM x BN tile of Y (256 tokens x 128 output rows; 128 x 128 or 128 x 64
+// when larger tiles would leave compute units idle), walking
 // d_in in steps of BK = 64 (four MFMA K-blocks of 16). Eight waves share the four SIMDs in two
 // roles, handing data over through LDS with one barrier per step:
 //   - four consumer waves each own a BM/2 x 64 block of the tile (BM/64 x 2 MFMA blocks of
@@ -30,6 +30,8 @@
 // compiler cannot see that their destinations are disjoint and would otherwise serialise them.
 // Every such load instruction is issued unconditionally (out-of-range rows and groups read a
 // valid address and are masked later), so each wait counts a fixed number of loads.
+#include <cstdlib>
+
 #include "device.h"
 #include "launch.h"
 
@@ -41,7 +43,7 @@ constexpr int kThreads = 512;                        // waves 0-3 consume, waves
 template <int K> constexpr int x_depth() { return K <= 4 ? 3 : 2; }   // X stages (LDS budget)
 template <int BMT> constexpr int x_stage() { return BMT * BK; }   // bf16 elements: BMT rows x 128 bytes
 constexpr int kChunk = 512;                          // one weight fragment: 64 lanes x 8 bf16
-constexpr int kSlab = (BN / 32) * (BK / 16) * kChunk;  // 4 column blocks x 4 K-blocks
+template <int BNT> constexpr int slab_elems() { return (BNT / 32) * (BK / 16) * kChunk; }   // column blocks x 4 K-blocks
 constexpr int kCodeDepth = 4;                        // steps of code words in flight per producer wave
 typedef __attribute__((address_space(3))) void* lds_ptr;
 }  // namespace gemm
@@ -97,7 +99,7 @@ __device__ __forceinline__ uint4 dequant_group_bf16(const uint4* __restrict__ cb
 }
 
 // CB = code bits: 8 (256 codewords per codebook) or 4 (16 codewords).
-template <int K, int YDT, int CB, int BMT>
+template <int K, int YDT, int CB, int BMT, int BNT>
 __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned char* __restrict__ codes,
                                                               const uint16_t* __restrict__ codebooks,
                                                               const uint16_t* __restrict__ scales,
@@ -109,7 +111,10 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   constexpr int NCW = 1 << CB;
   constexpr int kXStage = x_stage<BMT>();
   constexpr int MA = BMT / 64;                     // 32-row MFMA blocks per consumer wave
+  constexpr int NBB = BNT / 64;                    // 32-column MFMA blocks per consumer wave
   constexpr int kXLoads = BMT / 32;                // direct X loads per consumer wave and step
+  constexpr int kSlab = slab_elems<BNT>();
+  constexpr int QG = BNT / 32;                     // groups per producer thread and step
   extern __shared__ uint4 smem[];
   uint16_t* Xs = (uint16_t*)smem;                  // [kDepth][256 rows][8 swizzled 16-byte pieces]
   uint16_t* Bs = Xs + kDepth * kXStage;            // [2][4 col blocks][4 K-blocks][64 lanes][8]
@@ -120,7 +125,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform across the wave
   const int half = lane >> 5, r32 = lane & 31;
   const int tb = blockIdx.x % n_tb, cb = blockIdx.x / n_tb;
-  const int n0 = tb * BMT, i0 = cb * BN;
+  const int n0 = tb * BMT, i0 = cb * BNT;
   const int nsteps = (d_in + BK - 1) / BK;
   const int s0 = (int)(((long long)cb * nsteps) / n_cb);
   auto step_of = [&](int seq) { int st = s0 + seq; return st >= nsteps ? st - nsteps : st; };
@@ -130,10 +135,10 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   if (wave >= 4) {
     // ------------------------------------------------------------------ producers
     const int p = tid - 256;
-    const int col = p & (BN - 1), gq = p >> 7;     // weight row; groups 4 gq .. 4 gq + 3 of a step
+    const int col = p & (BNT - 1), gq = p / BNT;   // weight row; groups QG gq .. QG gq + QG - 1 of a step
     const bool col_ok = i0 + col < d_out;
     // Code words: each producer wave streams exactly the words its own lanes need (one 4-byte
-    // word per plane: the 4 groups of this thread's column in the step) straight into its own
+    // word per plane holding this thread's groups of its column in the step) straight into its own
     // LDS ring, kCodeDepth steps ahead, and waits only for its own loads (no other wave reads
     // them). Exactly K loads per step per wave, so "step q's words are in" is a fixed vmcnt.
     const int pw = wave - 4;
@@ -144,7 +149,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
     auto load_codes = [&](int seq) {
       const uint32_t base = ring_base(seq);
       if constexpr (CB == 8) {
-        int j0 = step_of(seq) * (BK / 8) + 4 * gq;   // 4-aligned: one code word per plane
+        int j0 = step_of(seq) * (BK / 8) + ((QG * gq) & ~3);   // 4-aligned: one code word per plane
         if (j0 >= G) j0 = 0;                          // padding groups: any valid word, zeroed later
 #pragma unroll
         for (int m = 0; m < K; ++m)
@@ -165,24 +170,25 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
       else AQMB_WAIT_VMCNT(0);
     };
     auto produce = [&](int seq) {
-      const int j0 = step_of(seq) * (BK / 8) + 4 * gq;
+      const int j0 = step_of(seq) * (BK / 8) + QG * gq;
       uint16_t* slab = Bs + (seq & 1) * kSlab;
       const uint32_t* words = cring + ((seq % kCodeDepth) * 4 + pw) * K * 64 + lane;
       uint32_t word[K];
 #pragma unroll
       for (int m = 0; m < K; ++m) word[m] = words[m * 64];
-      // all 4K codeword gathers first, then the folds
-      uint4 cw[4][K];
+      // all QG K codeword gathers first, then the folds
+      uint4 cw[QG][K];
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < QG; ++q)
 #pragma unroll
         for (int m = 0; m < K; ++m) {
-          const uint32_t code = CB == 8 ? (word[m] >> (8 * q)) & 0xFFu : (word[m] >> (4 * (4 * gq + q))) & 15u;
+          const uint32_t code = CB == 8 ? (word[m] >> (8 * (((QG * gq) & 3) + q))) & 0xFFu
+                                        : (word[m] >> (4 * (QG * gq + q))) & 15u;
           cw[q][m] = cbs[m * NCW + code];
         }
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int g = 4 * gq + q;                   // group within the step: K-block g / 2, half g % 2
+      for (int q = 0; q < QG; ++q) {
+        const int g = QG * gq + q;                  // group within the step: K-block g / 2, half g % 2
         uint4 v = fold_bf16<K>(cw[q]);
         if (!col_ok || j0 + q >= G) v = make_uint4(0, 0, 0, 0);
         *(uint4*)(slab + ((col >> 5) * 4 + (g >> 1)) * kChunk + ((col & 31) + 32 * (g & 1)) * 8) = v;
@@ -235,18 +241,18 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
       }
     }
   };
-  f32x16_t acc[MA][2];
+  f32x16_t acc[MA][NBB];
 #pragma unroll
   for (int a = 0; a < MA; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NBB; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
 
-  struct Frags { bf16x8_t a[MA], b[2]; };
+  struct Frags { bf16x8_t a[MA], b[NBB]; };
   auto read_frags = [&](const uint16_t* xst, const uint16_t* bsl, int i, Frags& f) {
 #pragma unroll
-    for (int b = 0; b < 2; ++b) f.b[b] = *(const bf16x8_t*)(bsl + ((wn * 2 + b) * 4 + i) * kChunk + lane * 8);
+    for (int b = 0; b < NBB; ++b) f.b[b] = *(const bf16x8_t*)(bsl + ((wn * NBB + b) * 4 + i) * kChunk + lane * 8);
     const int kc = 2 * i + half;
 #pragma unroll
     for (int a = 0; a < MA; ++a) {
@@ -258,7 +264,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 #pragma unroll
     for (int a = 0; a < MA; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
+      for (int b = 0; b < NBB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
   };
 
   for (int seq = 0; seq < kDepth - 1 && seq < nsteps; ++seq) load_x(seq);
@@ -285,15 +291,15 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
       if (i < 3) read_frags(xst, bsl, i + 1, nxt);
       mfmas(cur);
       if (i < 3) {
-        __builtin_amdgcn_sched_group_barrier(0x100, MA + 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2 * MA, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, MA + NBB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NBB * MA, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
   }
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int col = i0 + wn * 64 + b * 32 + r32;
+  for (int b = 0; b < NBB; ++b) {
+    const int col = i0 + wn * (BNT / 2) + b * 32 + r32;
     if (col >= d_out) continue;
     const float scale = f16_to_f32(scales[col]);
 #pragma unroll
@@ -307,34 +313,54 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   }
 }
 
-template <int K, int CB, int BMT>
+template <int K, int CB, int BMT, int BNT>
 static void launch_kcm(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
   using namespace gemm;
   constexpr int kDepth = x_depth<K>();
-  const int n_tb = (n_tokens + BMT - 1) / BMT, n_cb = (L.d.d_out + BN - 1) / BN;
-  const size_t lds = ((size_t)kDepth * x_stage<BMT>() + 2 * kSlab) * 2 + (size_t)K * (1 << CB) * 16 +
+  const int n_tb = (n_tokens + BMT - 1) / BMT, n_cb = (L.d.d_out + BNT - 1) / BNT;
+  const size_t lds = ((size_t)kDepth * x_stage<BMT>() + 2 * slab_elems<BNT>()) * 2 + (size_t)K * (1 << CB) * 16 +
                      (size_t)kCodeDepth * 4 * K * 64 * 4;
   const dim3 grid(n_tb * n_cb);
   if (y_dtype == AQMB_BF16)
-    gemm_kernel<K, AQMB_BF16, CB, BMT><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                                     n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+    gemm_kernel<K, AQMB_BF16, CB, BMT, BNT><<<grid, kThreads, lds, st>>>(
+        L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y, n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
   else
-    gemm_kernel<K, AQMB_F32, CB, BMT><<<grid, kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y,
-                                                                    n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
+    gemm_kernel<K, AQMB_F32, CB, BMT, BNT><<<grid, kThreads, lds, st>>>(
+        L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y, n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
 }
 
-// 128-token tiles when 256-token tiles would leave compute units idle and the 128-token tiles still
-// fit in one wave of workgroups (e.g. 4096 rows: 257..1024 tokens); 256-token tiles otherwise.
-static bool gemm_use_bm128(const Layer& L, int n_tokens) {
-  const int n_cb = (L.d.d_out + gemm::BN - 1) / gemm::BN;
-  const long long wg256 = (long long)((n_tokens + 255) / 256) * n_cb, wg128 = (long long)((n_tokens + 127) / 128) * n_cb;
-  return wg256 < L.n_cu && wg128 <= L.n_cu;
+// Tile shape: 0 = 256 tokens x 128 rows, 1 = 128 x 128, 2 = 128 x 64. AQMB_GEMM_TILE=256|128|64
+// forces one (read once). Otherwise the shape with the least estimated time: rounds of workgroups
+// (one workgroup per CU) times the shape's measured cost per workgroup relative to the largest
+// tile (4096 x 4096 layer, one round: 1, 0.9, 0.6).
+static int gemm_tile(const Layer& L, int n_tokens) {
+  static const int forced = [] {
+    const char* e = getenv("AQMB_GEMM_TILE");
+    if (!e) return -1;
+    const int v = atoi(e);
+    return v == 256 ? 0 : v == 128 ? 1 : v == 64 ? 2 : -1;
+  }();
+  if (forced >= 0) return forced;
+  const int bm[3] = {256, 128, 128}, bn[3] = {128, 128, 64};
+  const double rel[3] = {1.0, 0.9, 0.6};
+  const long long ncu = L.n_cu > 0 ? L.n_cu : 256;
+  int best = 0;
+  double best_t = 0;
+  for (int c = 0; c < 3; ++c) {
+    const long long wg = (long long)((n_tokens + bm[c] - 1) / bm[c]) * ((L.d.d_out + bn[c] - 1) / bn[c]);
+    const double t = (double)((wg + ncu - 1) / ncu) * rel[c];
+    if (c == 0 || t < best_t) { best = c; best_t = t; }
+  }
+  return best;
 }
 
 template <int K, int CB>
 static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
-  if (gemm_use_bm128(L, n_tokens)) launch_kcm<K, CB, 128>(L, X, n_tokens, Y, y_dtype, st);
-  else launch_kcm<K, CB, 256>(L, X, n_tokens, Y, y_dtype, st);
+  switch (gemm_tile(L, n_tokens)) {
+    case 0: launch_kcm<K, CB, 256, 128>(L, X, n_tokens, Y, y_dtype, st); break;
+    case 1: launch_kcm<K, CB, 128, 128>(L, X, n_tokens, Y, y_dtype, st); break;
+    default: launch_kcm<K, CB, 128, 64>(L, X, n_tokens, Y, y_dtype, st); break;
+  }
 }
 
 template <int K>

@@ -81,10 +81,14 @@ print("variant ok", flush=True)
 """
 
 
-@pytest.mark.parametrize("variant", ["small", "big"])
+@pytest.mark.parametrize("variant", ["small", "big", "big:256", "big:128", "big:64"])
 def test_forced_gemm_tiling_matches_oracle(variant):
-    """Both GEMM tilings at token counts the default dispatch sends to the other one."""
-    env = dict(os.environ, AQMB_GEMM=variant)
+    """Both GEMM tilings at token counts the default dispatch sends to the other one, and each tile
+    shape of the large-tile kernel (256 x 128, 128 x 128, 128 x 64) at every test shape."""
+    tiling, _, tile = variant.partition(":")
+    env = dict(os.environ, AQMB_GEMM=tiling)
+    if tile:
+        env["AQMB_GEMM_TILE"] = tile
     code = GEMM_CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"))
     r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
-    assert r.returncode == 0 and "variant ok" in r.stdout, f"AQMB_GEMM={variant}:\n{r.stdout[-2000:]}\n{r.stderr[-3000:]}"
+    assert r.returncode == 0 and "variant ok" in r.stdout, f"AQMB_GEMM {variant}:\n{r.stdout[-2000:]}\n{r.stderr[-3000:]}"
