@@ -13,8 +13,8 @@
 // into two bf16 parts (an fp16 value has 11 significant bits: hi = RNE_bf16(c) and lo = c - hi has
 // at most 3, both exact), split once per codeword when the codebooks are copied into LDS (a book
 // of high parts and a book of low parts), so a code costs two gathers and two MFMAs.
-// Sums are fp32. The 16 waves' partial tiles are added in wave order, scaled once and rounded
-// once, so results are reproducible.
+// Sums are fp32. The 16 waves' partial tiles are added in a fixed order (four quarters of four
+// waves each, then the quarters), scaled once and rounded once, so results are reproducible.
 #include <type_traits>
 
 #include "device.h"
@@ -156,36 +156,35 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
   }
 }
 
-// Partial tiles of the 16 waves added in wave order by wave 0, scaled once and rounded once, for
-// the 16 weight rows from row0; element e of lane l is batch row 4 (l / 16) + e, weight row l % 16.
-// Ends with the block's partial tiles read (a barrier before and none after: the caller separates
-// two calls with a barrier).
+// Partial tiles of the 16 waves summed in a fixed order, scaled once and rounded once, for the 16
+// weight rows from row0. Element e of lane l of a tile is batch row 4 (l / 16) + e, weight row
+// l % 16; read as floats, a tile holds 256 outputs, output o = 4 l + e. Thread t adds tiles
+// 4 q .. 4 q + 3 of output t % 256 (q = t / 256) from left to right; threads t < 256 then add the
+// four quarter sums of output t in order, scale and store. sbits is the scale of weight row
+// row0 + (t / 4) % 16, used by threads t < 256. Ends with the quarter sums read (the caller
+// separates two calls with a barrier).
+__device__ __forceinline__ int mg_out_row(int t) { return (t >> 2) & 15; }
 __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_t* red, const mg::f32x4_t (&acc)[4],
-                                                int row0) {
+                                                int row0, uint16_t sbits) {
   using namespace mg;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
-  const int col = lane & 15, kc = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   red[wave * 64 + lane] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   __syncthreads();
-  if (wave == 0) {
-    f32x4_t sum = red[lane];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) sum += red[w * 64 + lane];
-    const int row = row0 + col;
-    if (row < a.d_out) {
-      const float scale = f16_to_f32(a.scales[row]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int b = 4 * kc + e;
-        if (b < a.batch) {
-          const size_t o = (size_t)b * a.d_out + row;
-          const float v = sum[e] * scale;
-          if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, o, v);
-          else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, o, v);
-          else OutT<AQMB_F32>::store(a.y, o, v);
-        }
-      }
-    }
+  const float* rf = (const float*)red;
+  float* qs = (float*)(red + kWaves * 64);                   // [4][256] quarter sums
+  const int o = tid & 255, q = tid >> 8;
+  const int b = 4 * (o >> 6) + (o & 3);                      // batch row of output o
+  if (b < a.batch)
+    qs[q * 256 + o] = ((rf[(4 * q) * 256 + o] + rf[(4 * q + 1) * 256 + o]) + rf[(4 * q + 2) * 256 + o]) +
+                      rf[(4 * q + 3) * 256 + o];
+  __syncthreads();
+  const int row = row0 + mg_out_row(tid);
+  if (tid < 256 && b < a.batch && row < a.d_out) {
+    const float v = (((qs[o] + qs[256 + o]) + qs[512 + o]) + qs[768 + o]) * f16_to_f32(sbits);
+    const size_t off = (size_t)b * a.d_out + row;
+    if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, off, v);
+    else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, off, v);
+    else OutT<AQMB_F32>::store(a.y, off, v);
   }
 }
 
@@ -196,7 +195,7 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;            // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
   uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles, quarter sums
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;                                 // weight row in the block
@@ -210,6 +209,8 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   MgRun<K, CB> ra, rb;
   int r = wave;
   const uint4 w0 = mg_first_word<K, CB>(a);
+  const int srow = row0 + mg_out_row(tid);                   // the row this thread stores, if any
+  const uint16_t sbits = tid < 256 ? a.scales[srow < a.d_out ? srow : a.d_out - 1] : 0;
   mg_small_loads_first<K, CB>();
   mg_load_run<K, CB>(a, r, rowc, true, ra);
   mg_load_run<K, CB>(a, r + kWaves, rowc, true, rb);
@@ -228,7 +229,7 @@ void gemv_mma_kernel(GemvMmaArgs a) {
     mg_compute<K, XDT, CB>(a, cb_rep, rep_off, rb, acc);
     if (r + 3 * kWaves < n_runs) mg_load_run<K, CB>(a, r + 3 * kWaves, rowc, true, rb);
   }
-  mg_reduce_store(a, red, acc, row0);
+  mg_reduce_store(a, red, acc, row0, sbits);
 }
 
 // Layers with more 16-row blocks than compute units: one persistent workgroup per CU walks the
@@ -236,7 +237,7 @@ void gemv_mma_kernel(GemvMmaArgs a) {
 // wave takes the same per = ceil(n_runs / 16) runs of every block (wave, wave + 16, ...; runs past
 // the row are dummies: x reads zeros) as one flat sequence of items over its blocks, two items
 // ahead in two register sets, so the next block's first runs are in flight while a block ends
-// (partial tiles added in wave order, as in gemv_mma_kernel; same arithmetic and order).
+// (partial tiles reduced as in gemv_mma_kernel; same arithmetic and order).
 template <int K, int XDT, int CB>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_persist_kernel(GemvMmaArgs a) {
@@ -244,7 +245,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;
   extern __shared__ uint4 smem_mg[];
   uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles, quarter sums
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;
@@ -263,16 +264,27 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
     const int r = wave + (ic % per) * kWaves;
     mg_load_run<K, CB>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R);
   };
+  auto block_row0 = [&](int i) {                             // first row of the block of item i
+    return ((int)blockIdx.x + ((i < n_items ? i : n_items - 1) / per) * (int)gridDim.x) * kRows;
+  };
+  // The scale of the row this thread stores (threads < 256), requested a block ahead.
+  auto scale_of = [&](int i) -> uint16_t {
+    const int row = block_row0(i) + mg_out_row(tid);
+    return tid < 256 ? a.scales[row < a.d_out ? row : a.d_out - 1] : 0;
+  };
+  uint16_t sbits;
   f32x4_t acc[4];
   auto end_block = [&](int i) {                              // item i closed its block
-    mg_reduce_store(a, red, acc, ((int)blockIdx.x + (i / per) * (int)gridDim.x) * kRows);
+    mg_reduce_store(a, red, acc, block_row0(i), sbits);
+    sbits = scale_of(i + 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();                                         // wave 0 has read the partial tiles
+    __syncthreads();                                         // the quarter sums have been read
   };
 
   MgRun<K, CB> ra, rb;
   const uint4 w0 = mg_first_word<K, CB>(a);
+  sbits = scale_of(0);
   mg_small_loads_first<K, CB>();
   load_item(0, ra);
   load_item(1, rb);
@@ -294,7 +306,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 // 16-codeword codebooks (4-bit codes) fill the LDS banks once: one copy reads without conflicts.
 template <int K, int XDT, int CB>
 static hipError_t launch_mma_kc(GemvMmaArgs a, hipStream_t st) {
-  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * (1 << CB) * 16;
+  const size_t red = (size_t)mg::kWaves * 64 * 16 + 4 * 256 * 4, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
   a.nrep = CB == 4 ? 1 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
   a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
