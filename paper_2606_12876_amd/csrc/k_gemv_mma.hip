@@ -43,27 +43,36 @@ struct GemvMmaArgs {
 
 
 // A run: 4 consecutive K-steps = 16 groups (8-bit codes: one 16-byte code slice; 4-bit codes:
-// half of a 32-group slice, 8 bytes). Per lane: x of its batch row for the 4 steps (8 values each)
-// and the run's code bytes of its weight row, per plane.
-template <int K, int CB>
+// half of a 32-group slice, 8 bytes). Per lane: NX 16-byte pieces of x (below) and the run's code
+// bytes of its weight row, per plane.
+//
+// x of a run is NX loads. Load t puts in lane L = 16 kc + R u + b (R = 4 NX rows per load,
+// u < 4 / NX) the 8 values of batch row b at inputs 32 j + 8 kc of the run, j = t (4 / NX) + u.
+// The A fragment of step j (lane 16 kc + b: row b, inputs 32 j + 8 kc) is then load j / (4 / NX)
+// shifted down by R (j % (4 / NX)) lanes within each row of 16 lanes (a DPP row shift). Lanes of
+// rows R and up take other rows' values: those rows of the product are never stored. One load per
+// run for batch <= 4, two for batch <= 8, four (no shift) above.
+template <int K, int CB, int NX>
 struct MgRun {
-  uint4 xa[4];
+  uint4 xa[NX];
   typename std::conditional<CB == 8, uint4, uint2>::type c[K];
 };
 
-// Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of batch
-// row `col` at inputs 128 r + 32 j + 8 kc .. + 7 for steps j = 0..3 (zeros past d_in, past the
-// batch, and for dummy runs), and slice r of the row in every plane.
-template <int K, int CB>
-__device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K, CB>& R) {
-  const int lane = threadIdx.x & 63, col = lane & 15, kc = lane >> 4;
+// Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of the
+// run in the layout above (zeros past d_in, past the batch, and for dummy runs), and slice r of
+// the row in every plane.
+template <int K, int CB, int NX>
+__device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K, CB, NX>& R) {
+  constexpr int kRowsX = 4 * NX, kPer = 4 / NX;              // batch rows per load, steps per load
+  const int lane = threadIdx.x & 63, kc = lane >> 4;
+  const int b = lane & (kRowsX - 1), u = (lane & 15) / kRowsX;
   const int n_runs = (a.G + 15) / 16;
   const int rc = r < n_runs ? r : n_runs - 1;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = rc * 128 + j * 32 + kc * 8;
-    const void* src = (xok && col < a.batch && e < a.d_in) ? (const void*)(a.x + (size_t)col * a.d_in + e) : a.zero_page;
-    R.xa[j] = *(const uint4*)src;
+  for (int t = 0; t < NX; ++t) {
+    const int e = rc * 128 + (t * kPer + u) * 32 + kc * 8;
+    const void* src = (xok && b < a.batch && e < a.d_in) ? (const void*)(a.x + (size_t)b * a.d_in + e) : a.zero_page;
+    R.xa[t] = *(const uint4*)src;
   }
 #pragma unroll
   for (int m = 0; m < K; ++m) {
@@ -121,14 +130,35 @@ __device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep
   }
 }
 
+// Lane i of each row of 16 lanes takes lane i + S of the row (S = 0: the value itself).
+template <int S>
+__device__ __forceinline__ uint4 mg_row_shift(uint4 v) {
+  if constexpr (S == 0) {
+    return v;
+  } else {
+    return make_uint4((uint32_t)__builtin_amdgcn_mov_dpp((int)v.x, 0x100 + S, 0xF, 0xF, false),
+                      (uint32_t)__builtin_amdgcn_mov_dpp((int)v.y, 0x100 + S, 0xF, 0xF, false),
+                      (uint32_t)__builtin_amdgcn_mov_dpp((int)v.z, 0x100 + S, 0xF, 0xF, false),
+                      (uint32_t)__builtin_amdgcn_mov_dpp((int)v.w, 0x100 + S, 0xF, 0xF, false));
+  }
+}
+
+// The A fragment of step J (layout above MgRun).
+template <int NX, int J>
+__device__ __forceinline__ uint4 mg_x_step(const uint4 (&xa)[NX]) {
+  constexpr int kPer = 4 / NX;
+  return mg_row_shift<4 * NX * (J % kPer)>(xa[J / kPer]);
+}
+
 // The MFMAs of one run. Step j of a run: group 4 j + kc of the run (8-bit codes: byte 4 j + kc of
 // the plane's slice word; 4-bit codes: nibble 4 j + kc of its 8 bytes).
-template <int K, int XDT, int CB>
+template <int K, int XDT, int CB, int NX>
 __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb_rep, uint32_t rep_off,
-                                           const MgRun<K, CB>& R, mg::f32x4_t (&acc)[4]) {
+                                           const MgRun<K, CB, NX>& R, mg::f32x4_t (&acc)[4]) {
   using namespace mg;
   constexpr int NCW = 1 << CB;
   const int kc = (threadIdx.x & 63) >> 4;
+  const uint4 xs[4] = {mg_x_step<NX, 0>(R.xa), mg_x_step<NX, 1>(R.xa), mg_x_step<NX, 2>(R.xa), mg_x_step<NX, 3>(R.xa)};
 #pragma unroll
   for (int m = 0; m < K; ++m) {
 #pragma unroll
@@ -144,11 +174,11 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
       const uint32_t off = (((uint32_t)(m * NCW) + code) << a.cb_shift) + rep_off;
       const uint4 cw = *(const uint4*)((const char*)cb_rep + off);
       if constexpr (XDT == AQMB_F16) {
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, R.xa[j]),
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
                                                         __builtin_bit_cast(f16x8_t, cw), acc[j], 0, 0, 0);
       } else {
         const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * NCW) << a.cb_shift) + off);
-        const b16x8_t xb = __builtin_bit_cast(b16x8_t, R.xa[j]);
+        const b16x8_t xb = __builtin_bit_cast(b16x8_t, xs[j]);
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cw), acc[j], 0, 0, 0);
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cl), acc[j], 0, 0, 0);
       }
@@ -188,7 +218,7 @@ __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_
   }
 }
 
-template <int K, int XDT, int CB>
+template <int K, int XDT, int CB, int NX>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_kernel(GemvMmaArgs a) {
   using namespace mg;
@@ -206,14 +236,14 @@ void gemv_mma_kernel(GemvMmaArgs a) {
 
   // The wave's runs are wave, wave + 16, ...; the first two are requested before the codebooks are
   // replicated into LDS (a 4096-wide row has 32 runs: two per wave).
-  MgRun<K, CB> ra, rb;
+  MgRun<K, CB, NX> ra, rb;
   int r = wave;
   const uint4 w0 = mg_first_word<K, CB>(a);
   const int srow = row0 + mg_out_row(tid);                   // the row this thread stores, if any
   const uint16_t sbits = tid < 256 ? a.scales[srow < a.d_out ? srow : a.d_out - 1] : 0;
   mg_small_loads_first<K, CB>();
-  mg_load_run<K, CB>(a, r, rowc, true, ra);
-  mg_load_run<K, CB>(a, r + kWaves, rowc, true, rb);
+  mg_load_run<K, CB, NX>(a, r, rowc, true, ra);
+  mg_load_run<K, CB, NX>(a, r + kWaves, rowc, true, rb);
   mg_replicate<K, XDT, CB>(a, cb_rep, w0);
   __syncthreads();
 
@@ -223,11 +253,11 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   // Two register sets in turn: the loads of the wave's run after next are requested while it
   // computes one.
   for (; r < n_runs; r += 2 * kWaves) {
-    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, ra, acc);
+    mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, ra, acc);
     if (r + kWaves >= n_runs) break;
-    if (r + 2 * kWaves < n_runs) mg_load_run<K, CB>(a, r + 2 * kWaves, rowc, true, ra);
-    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, rb, acc);
-    if (r + 3 * kWaves < n_runs) mg_load_run<K, CB>(a, r + 3 * kWaves, rowc, true, rb);
+    if (r + 2 * kWaves < n_runs) mg_load_run<K, CB, NX>(a, r + 2 * kWaves, rowc, true, ra);
+    mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, rb, acc);
+    if (r + 3 * kWaves < n_runs) mg_load_run<K, CB, NX>(a, r + 3 * kWaves, rowc, true, rb);
   }
   mg_reduce_store(a, red, acc, row0, sbits);
 }
@@ -238,7 +268,7 @@ void gemv_mma_kernel(GemvMmaArgs a) {
 // the row are dummies: x reads zeros) as one flat sequence of items over its blocks, two items
 // ahead in two register sets, so the next block's first runs are in flight while a block ends
 // (partial tiles reduced as in gemv_mma_kernel; same arithmetic and order).
-template <int K, int XDT, int CB>
+template <int K, int XDT, int CB, int NX>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_persist_kernel(GemvMmaArgs a) {
   using namespace mg;
@@ -258,11 +288,11 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 
   // item i: block blockIdx.x + (i / per) gridDim.x, run wave + (i % per) 16 (items past the end:
   // the last item again, never used)
-  auto load_item = [&](int i, MgRun<K, CB>& R) {
+  auto load_item = [&](int i, MgRun<K, CB, NX>& R) {
     const int ic = i < n_items ? i : n_items - 1;
     const int row = ((int)blockIdx.x + (ic / per) * (int)gridDim.x) * kRows + col;
     const int r = wave + (ic % per) * kWaves;
-    mg_load_run<K, CB>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R);
+    mg_load_run<K, CB, NX>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R);
   };
   auto block_row0 = [&](int i) {                             // first row of the block of item i
     return ((int)blockIdx.x + ((i < n_items ? i : n_items - 1) / per) * (int)gridDim.x) * kRows;
@@ -282,7 +312,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
     __syncthreads();                                         // the quarter sums have been read
   };
 
-  MgRun<K, CB> ra, rb;
+  MgRun<K, CB, NX> ra, rb;
   const uint4 w0 = mg_first_word<K, CB>(a);
   sbits = scale_of(0);
   mg_small_loads_first<K, CB>();
@@ -293,11 +323,11 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < n_items; i += 2) {
-    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, ra, acc);
+    mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, ra, acc);
     load_item(i + 2, ra);
     if ((i + 1) % per == 0) end_block(i);
     if (i + 1 >= n_items) break;
-    mg_compute<K, XDT, CB>(a, cb_rep, rep_off, rb, acc);
+    mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, rb, acc);
     load_item(i + 3, rb);
     if ((i + 2) % per == 0) end_block(i + 1);
   }
@@ -312,8 +342,19 @@ static hipError_t launch_mma_kc(GemvMmaArgs a, hipStream_t st) {
   a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
   const size_t lds = book * a.nrep + red;
   const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
-  if (n_rb > a.n_cu && a.n_cu > 0) gemv_mma_persist_kernel<K, XDT, CB><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
-  else gemv_mma_kernel<K, XDT, CB><<<dim3(n_rb), mg::kThreads, lds, st>>>(a);
+  // x loads per run: batch rows in groups of 4 per 16-lane row (see MgRun)
+  const bool persist = n_rb > a.n_cu && a.n_cu > 0;
+  const dim3 grid(persist ? a.n_cu : n_rb);
+  if (a.batch <= 4) {
+    if (persist) gemv_mma_persist_kernel<K, XDT, CB, 1><<<grid, mg::kThreads, lds, st>>>(a);
+    else gemv_mma_kernel<K, XDT, CB, 1><<<grid, mg::kThreads, lds, st>>>(a);
+  } else if (a.batch <= 8) {
+    if (persist) gemv_mma_persist_kernel<K, XDT, CB, 2><<<grid, mg::kThreads, lds, st>>>(a);
+    else gemv_mma_kernel<K, XDT, CB, 2><<<grid, mg::kThreads, lds, st>>>(a);
+  } else {
+    if (persist) gemv_mma_persist_kernel<K, XDT, CB, 4><<<grid, mg::kThreads, lds, st>>>(a);
+    else gemv_mma_kernel<K, XDT, CB, 4><<<grid, mg::kThreads, lds, st>>>(a);
+  }
   return hipGetLastError();
 }
 
