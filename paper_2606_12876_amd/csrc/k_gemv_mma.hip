@@ -52,10 +52,19 @@ struct GemvMmaArgs {
 // shifted down by R (j % (4 / NX)) lanes within each row of 16 lanes (a DPP row shift). Lanes of
 // rows R and up take other rows' values: those rows of the product are never stored. One load per
 // run for batch <= 4, two for batch <= 8, four (no shift) above.
+//
+// 8-bit codes at k >= 2 are loaded four planes at a time: lane 16 m + r of load t holds the run's
+// slice of plane 4 t + m for weight row r (16 bytes). Before use, each lane packs the code bytes
+// of group 4 j + q (j = 0..3) into dword q, and a transpose across the rows of 16 lanes (swaps of
+// lane halves and of row pairs) leaves in lane 16 kc + r, dword m, the codes that lane uses from
+// plane 4 t + m. So a run costs ceil(k / 4) code loads instead of k.
+template <int K, int CB> constexpr bool mg_codes_t() { return CB == 8 && K >= 2; }
+template <int K, int CB> constexpr int mg_code_loads() { return mg_codes_t<K, CB>() ? (K + 3) / 4 : K; }
+
 template <int K, int CB, int NX>
 struct MgRun {
   uint4 xa[NX];
-  typename std::conditional<CB == 8, uint4, uint2>::type c[K];
+  typename std::conditional<CB == 8, uint4, uint2>::type c[mg_code_loads<K, CB>()];
 };
 
 // Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of the
@@ -74,10 +83,18 @@ __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int row
     const void* src = (xok && b < a.batch && e < a.d_in) ? (const void*)(a.x + (size_t)b * a.d_in + e) : a.zero_page;
     R.xa[t] = *(const uint4*)src;
   }
+  if constexpr (mg_codes_t<K, CB>()) {
 #pragma unroll
-  for (int m = 0; m < K; ++m) {
-    if constexpr (CB == 8) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
-    else R.c[m] = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(rc >> 1) * a.d_out + rowc) * 16 + (rc & 1) * 8);
+    for (int t = 0; t < mg_code_loads<K, CB>(); ++t) {
+      const int m = 4 * t + kc < K ? 4 * t + kc : K - 1;     // rows past the last plane reload it (unused)
+      R.c[t] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+    }
+  } else {
+#pragma unroll
+    for (int m = 0; m < K; ++m) {
+      if constexpr (CB == 8) R.c[m] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+      else R.c[m] = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(rc >> 1) * a.d_out + rowc) * 16 + (rc & 1) * 8);
+    }
   }
 }
 
@@ -143,6 +160,23 @@ __device__ __forceinline__ uint4 mg_row_shift(uint4 v) {
   }
 }
 
+// Code dwords of a four-plane load (layout above MgRun): dword m of the result holds the lane's
+// codes of plane 4 t + m, the code of step j in byte j.
+__device__ __forceinline__ void mg_codes_transpose(uint4 v, uint32_t (&d)[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {                              // byte q of each slice word: group 4 j + q
+    const uint32_t lo = __builtin_amdgcn_perm(v.y, v.x, 0x0C0C0000u | ((4u + q) << 8) | q);
+    const uint32_t hi = __builtin_amdgcn_perm(v.w, v.z, (((4u + q) << 24) | (q << 16)) | 0x0C0Cu);
+    d[q] = lo | hi;
+  }
+  // rows 2, 3 of d0 / d1 <-> rows 0, 1 of d2 / d3, then rows 1, 3 of d0 / d2 <-> rows 0, 2 of d1 / d3
+  auto s02 = __builtin_amdgcn_permlane32_swap(d[0], d[2], false, false);
+  auto s13 = __builtin_amdgcn_permlane32_swap(d[1], d[3], false, false);
+  auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+  auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+  d[0] = s01[0]; d[1] = s01[1]; d[2] = s23[0]; d[3] = s23[1];
+}
+
 // The A fragment of step J (layout above MgRun).
 template <int NX, int J>
 __device__ __forceinline__ uint4 mg_x_step(const uint4 (&xa)[NX]) {
@@ -159,12 +193,25 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
   constexpr int NCW = 1 << CB;
   const int kc = (threadIdx.x & 63) >> 4;
   const uint4 xs[4] = {mg_x_step<NX, 0>(R.xa), mg_x_step<NX, 1>(R.xa), mg_x_step<NX, 2>(R.xa), mg_x_step<NX, 3>(R.xa)};
+  constexpr int kCT = mg_codes_t<K, CB>() ? 4 * mg_code_loads<K, CB>() : 1;
+  uint32_t cd[kCT];
+  if constexpr (mg_codes_t<K, CB>()) {
+#pragma unroll
+    for (int t = 0; t < mg_code_loads<K, CB>(); ++t) {
+      uint32_t d[4];
+      mg_codes_transpose(R.c[t], d);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cd[4 * t + q] = d[q];
+    }
+  }
 #pragma unroll
   for (int m = 0; m < K; ++m) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       uint32_t code;
-      if constexpr (CB == 8) {
+      if constexpr (mg_codes_t<K, CB>()) {
+        code = (cd[m] >> (8 * j)) & 0xFFu;
+      } else if constexpr (CB == 8) {
         const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
         code = (word >> (8 * kc)) & 0xFFu;
       } else {
