@@ -1,4 +1,4 @@
-// Decode GEMV on the matrix cores (8- and 4-bit codes, any batch up to 16; used from batch 3 on): y[b][i] = s_i sum_j sum_{m<k}
+// Decode GEMV on the matrix cores (8- and 4-bit codes, any batch up to 16): y[b][i] = s_i sum_j sum_{m<k}
 // <x[b, group j], C_m[b_{ijm}]>, the per-plane products computed by v_mfma_f32_16x16x32 with the
 // batch in the 16 rows of the A operand and 16 weight rows in the columns of the B operand.
 //
