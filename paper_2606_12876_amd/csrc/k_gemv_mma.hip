@@ -13,8 +13,8 @@
 // into two bf16 parts (an fp16 value has 11 significant bits: hi = RNE_bf16(c) and lo = c - hi has
 // at most 3, both exact), split once per codeword when the codebooks are copied into LDS (a book
 // of high parts and a book of low parts), so a code costs two gathers and two MFMAs.
-// Sums are fp32. The 16 waves' partial tiles are added in a fixed order (four quarters of four
-// waves each, then the quarters), scaled once and rounded once, so results are reproducible.
+// Sums are fp32. The 16 waves' partial tiles are added in a fixed order (a tree over the waves),
+// scaled once and rounded once, so results are reproducible.
 #include <type_traits>
 
 #include "device.h"
@@ -235,11 +235,10 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
 
 // Partial tiles of the 16 waves summed in a fixed order, scaled once and rounded once, for the 16
 // weight rows from row0. Element e of lane l of a tile is batch row 4 (l / 16) + e, weight row
-// l % 16; read as floats, a tile holds 256 outputs, output o = 4 l + e. Thread t adds tiles
-// 4 q .. 4 q + 3 of output t % 256 (q = t / 256) from left to right; threads t < 256 then add the
-// four quarter sums of output t in order, scale and store. sbits is the scale of weight row
-// row0 + (t / 4) % 16, used by threads t < 256. Ends with the quarter sums read (the caller
-// separates two calls with a barrier).
+// l % 16; read as floats, a tile holds 256 outputs, output o = 4 l + e. Thread t < 256 reads the
+// 16 partials of output t (all requested at once) and adds them in a fixed tree, scales and
+// stores. sbits is the scale of weight row row0 + (t / 4) % 16. Ends with the partial tiles read
+// by threads < 256 (the caller separates two calls with a barrier).
 __device__ __forceinline__ int mg_out_row(int t) { return (t >> 2) & 15; }
 __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_t* red, const mg::f32x4_t (&acc)[4],
                                                 int row0, uint16_t sbits) {
@@ -247,17 +246,18 @@ __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   red[wave * 64 + lane] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   __syncthreads();
-  const float* rf = (const float*)red;
-  float* qs = (float*)(red + kWaves * 64);                   // [4][256] quarter sums
-  const int o = tid & 255, q = tid >> 8;
-  const int b = 4 * (o >> 6) + (o & 3);                      // batch row of output o
-  if (b < a.batch)
-    qs[q * 256 + o] = ((rf[(4 * q) * 256 + o] + rf[(4 * q + 1) * 256 + o]) + rf[(4 * q + 2) * 256 + o]) +
-                      rf[(4 * q + 3) * 256 + o];
-  __syncthreads();
+  const int b = 4 * (tid >> 6) + (tid & 3);                  // batch row of output tid (tid < 256)
   const int row = row0 + mg_out_row(tid);
   if (tid < 256 && b < a.batch && row < a.d_out) {
-    const float v = (((qs[o] + qs[256 + o]) + qs[512 + o]) + qs[768 + o]) * f16_to_f32(sbits);
+    const float* rf = (const float*)red + tid;
+    float p[kWaves];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) p[w] = rf[w * 256];
+#pragma unroll
+    for (int h = 1; h < kWaves; h *= 2)                      // pairs, then pairs of pairs, ...
+#pragma unroll
+      for (int w = 0; w < kWaves; w += 2 * h) p[w] += p[w + h];
+    const float v = p[0] * f16_to_f32(sbits);
     const size_t off = (size_t)b * a.d_out + row;
     if (a.y_dtype == AQMB_F16) OutT<AQMB_F16>::store(a.y, off, v);
     else if (a.y_dtype == AQMB_BF16) OutT<AQMB_BF16>::store(a.y, off, v);
@@ -272,7 +272,7 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;            // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
   uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles, quarter sums
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;                                 // weight row in the block
@@ -322,7 +322,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;
   extern __shared__ uint4 smem_mg[];
   uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles, quarter sums
+  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;
@@ -356,7 +356,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
     sbits = scale_of(i + 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();                                         // the quarter sums have been read
+    __syncthreads();                                         // the partial tiles have been read
   };
 
   MgRun<K, CB, NX> ra, rb;
@@ -383,7 +383,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 // 16-codeword codebooks (4-bit codes) fill the LDS banks once: one copy reads without conflicts.
 template <int K, int XDT, int CB>
 static hipError_t launch_mma_kc(GemvMmaArgs a, hipStream_t st) {
-  const size_t red = (size_t)mg::kWaves * 64 * 16 + 4 * 256 * 4, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * (1 << CB) * 16;
+  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
   a.nrep = CB == 4 ? 1 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
   a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
