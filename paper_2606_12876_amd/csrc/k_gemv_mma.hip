@@ -53,12 +53,14 @@ struct GemvMmaArgs {
 // rows R and up take other rows' values: those rows of the product are never stored. One load per
 // run for batch <= 4, two for batch <= 8, four (no shift) above.
 //
-// 8-bit codes at k >= 2 are loaded four planes at a time: lane 16 m + r of load t holds the run's
-// slice of plane 4 t + m for weight row r (16 bytes). Before use, each lane packs the code bytes
-// of group 4 j + q (j = 0..3) into dword q, and a transpose across the rows of 16 lanes (swaps of
-// lane halves and of row pairs) leaves in lane 16 kc + r, dword m, the codes that lane uses from
-// plane 4 t + m. So a run costs ceil(k / 4) code loads instead of k.
-template <int K, int CB> constexpr bool mg_codes_t() { return CB == 8 && K >= 2; }
+// At k >= 2 (4-bit codes: k >= 3; at k = 2 the nibble packing costs more than the load it saves)
+// the codes are loaded four planes at a time: lane 16 m + r of load t holds the run's
+// codes of plane 4 t + m for weight row r (8-bit: the 16-byte slice; 4-bit: its 8-byte half).
+// Before use, each lane packs the codes of group 4 j + q (j = 0..3) into dword q (8-bit: byte j;
+// 4-bit: nibble j), and a transpose across the rows of 16 lanes (swaps of lane halves and of row
+// pairs) leaves in lane 16 kc + r, dword m, the codes that lane uses from plane 4 t + m. So a run
+// costs ceil(k / 4) code loads instead of k.
+template <int K, int CB> constexpr bool mg_codes_t() { return CB == 8 ? K >= 2 : K >= 3; }
 template <int K, int CB> constexpr int mg_code_loads() { return mg_codes_t<K, CB>() ? (K + 3) / 4 : K; }
 
 template <int K, int CB, int NX>
@@ -87,7 +89,8 @@ __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int row
 #pragma unroll
     for (int t = 0; t < mg_code_loads<K, CB>(); ++t) {
       const int m = 4 * t + kc < K ? 4 * t + kc : K - 1;     // rows past the last plane reload it (unused)
-      R.c[t] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+      if constexpr (CB == 8) R.c[t] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
+      else R.c[t] = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(rc >> 1) * a.d_out + rowc) * 16 + (rc & 1) * 8);
     }
   } else {
 #pragma unroll
@@ -161,7 +164,8 @@ __device__ __forceinline__ uint4 mg_row_shift(uint4 v) {
 }
 
 // Code dwords of a four-plane load (layout above MgRun): dword m of the result holds the lane's
-// codes of plane 4 t + m, the code of step j in byte j.
+// codes of plane 4 t + m, the code of step j in byte j (8-bit) or nibble j (4-bit).
+__device__ __forceinline__ void mg_rows_transpose(uint32_t (&d)[4]);
 __device__ __forceinline__ void mg_codes_transpose(uint4 v, uint32_t (&d)[4]) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) {                              // byte q of each slice word: group 4 j + q
@@ -169,6 +173,19 @@ __device__ __forceinline__ void mg_codes_transpose(uint4 v, uint32_t (&d)[4]) {
     const uint32_t hi = __builtin_amdgcn_perm(v.w, v.z, (((4u + q) << 24) | (q << 16)) | 0x0C0Cu);
     d[q] = lo | hi;
   }
+  mg_rows_transpose(d);
+}
+__device__ __forceinline__ void mg_codes_transpose(uint2 v, uint32_t (&d)[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {                              // nibble 4 j + q of the 8 bytes: dword j / 2, bits 16 (j % 2) + 4 q
+    const uint32_t a = (v.x >> (4 * q)) & 0x000F000Fu, b = (v.y >> (4 * q)) & 0x000F000Fu;
+    d[q] = (a & 0xFu) | ((a >> 12) & 0xF0u) | ((b & 0xFu) << 8) | ((b >> 4) & 0xF000u);
+  }
+  mg_rows_transpose(d);
+}
+
+// d[q] of lane 16 m + r -> d[m] of lane 16 q + r (a 4 x 4 transpose of dwords and rows of 16 lanes).
+__device__ __forceinline__ void mg_rows_transpose(uint32_t (&d)[4]) {
   // rows 2, 3 of d0 / d1 <-> rows 0, 1 of d2 / d3, then rows 1, 3 of d0 / d2 <-> rows 0, 2 of d1 / d3
   auto s02 = __builtin_amdgcn_permlane32_swap(d[0], d[2], false, false);
   auto s13 = __builtin_amdgcn_permlane32_swap(d[1], d[3], false, false);
@@ -210,7 +227,7 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
     for (int j = 0; j < 4; ++j) {
       uint32_t code;
       if constexpr (mg_codes_t<K, CB>()) {
-        code = (cd[m] >> (8 * j)) & 0xFFu;
+        code = CB == 8 ? (cd[m] >> (8 * j)) & 0xFFu : (cd[m] >> (4 * j)) & 15u;
       } else if constexpr (CB == 8) {
         const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
         code = (word >> (8 * kc)) & 0xFFu;

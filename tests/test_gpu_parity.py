@@ -158,30 +158,33 @@ def test_gemv_workloads(name):
             del W
 
 
+@pytest.mark.parametrize("xdt", ["f16", "bf16"])
 @pytest.mark.parametrize("d_in", [16384, 16392])
-def test_gemv_wide_rows(d_in):
+def test_gemv_wide_rows(d_in, xdt):
     """Rows of 2048 groups (the widest the direct-gather kernel keeps in registers) and of 2049
-    groups (taken by the lookup-table kernel at batch 1), batch 1, 2 (matrix cores for rows of
-    more than 512 groups) and 4, every k."""
-    spec = LayerSpec(f"wide{d_in}", 130, d_in, M=4, seed=38)
+    groups (beyond it: the lookup-table kernel), batch 1, 2 and 4, every k. Rows of more than 512
+    groups go to the matrix cores except at batch 1 with bf16 x, which takes the direct-gather
+    kernel (2048 groups) or the lookup-table kernel (2049)."""
+    spec = LayerSpec(f"wide{d_in}", 130, d_in, M=4, seed=38, act_dtype=xdt)
     L = make_layer(spec)
     C, s = _f64(L)
+    ydt = "f32" if xdt == "f16" else "bf16"
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
         for b in (1, 2, 4):
-            xbits = make_activations(L, b, "f16", heavy_tail=True)
-            x = act_values(xbits, "f16")
+            xbits = make_activations(L, b, xdt, heavy_tail=True)
+            x = act_values(xbits, xdt)
             for k in range(1, 5):
                 ref = oracle.linear(x, L.codes, C, s, k)
-                got = run_gemv(gl, k, xbits, "f16", "f32")
-                check_close(got, ref, "f32", f"d_in={d_in} b={b} k={k}")
+                got = run_gemv(gl, k, xbits, xdt, ydt)
+                check_close(got, ref, ydt, f"d_in={d_in} b={b} k={k} {xdt}")
 
 
 @pytest.mark.parametrize("xdt", ["f16", "bf16"])
 def test_gemv_more_row_blocks_than_cus(xdt):
     """5000 rows = 313 blocks of 16 (the last one ragged): more than one block per compute unit,
-    so each workgroup walks several blocks with the codebooks replicated once. Batch 1 and 2
-    (direct gathers) and 3, 8, 16 (matrix cores; 65 groups = 5 runs of 16, so 11 of the 16 waves
-    run a dummy item per block), every k, against the oracle."""
+    so each workgroup walks several blocks with the codebooks replicated once. Batch 1 (direct
+    gathers; with bf16 x also batch 2) and 2, 3, 8, 16 (matrix cores; 65 groups = 5 runs of 16, so
+    11 of the 16 waves run a dummy item per block), every k, against the oracle."""
     spec = LayerSpec("tall", 5000, 520, M=4, seed=39, act_dtype=xdt)
     L = make_layer(spec)
     C, s = _f64(L)
