@@ -138,14 +138,14 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
   return AQMB_OK;
 }
 
-// GEMV kernel choice. Default: 4-bit codes -> the matrix-core kernel at batch >= 2, their own
-// kernel at batch 1; 8-bit codes -> the matrix-core kernel for fp16 x at batch >= 2 and at
-// batch 1 on rows of more than 512 groups, for bf16 x (two products per code there) at batch
-// >= 3 and at batch 2 on rows of more than 512 groups (measured faster in those cases);
-// otherwise the direct-gather kernel (k <= 4, rows <= 16384) or the lookup table kernel, as
-// k_gemv.hip decides. AQMB_GEMV=mma uses
+// GEMV kernel choice (measured faster in each case). Default: 4-bit codes -> the matrix-core
+// kernel at batch >= 2 and, for fp16 x at k >= 2, at batch 1 on rows of more than 512 groups;
+// their own kernel otherwise. 8-bit codes -> the matrix-core kernel for fp16 x at batch >= 2 and
+// at batch 1 on rows of more than 512 groups, for bf16 x (two products per code there) at batch
+// >= 3 and at batch 2 on rows of more than 512 groups; otherwise the direct-gather kernel
+// (k <= 4, rows <= 16384) or the lookup table kernel, as k_gemv.hip decides. AQMB_GEMV=mma uses
 // the matrix-core kernel at every batch, AQMB_GEMV=cw or =lut keep 8-bit layers on k_gemv.hip's
-// kernels (read once).
+// kernels and 4-bit layers on theirs (read once).
 static int gemv_mode() {
   static const int v = [] {
     const char* e = getenv("AQMB_GEMV");
@@ -159,18 +159,18 @@ static int gemv_mode() {
 
 // (At batch 2 on rows of more than 512 groups the direct-gather kernel would hold the code words of
 // four 512-group blocks next to two batch rows: more than its registers.)
-static bool gemv_uses_mma(const Layer& L, int batch, aqmb_dtype x_dtype) {
-  if (L.d.code_bits == 4) return gemv_mode() == 3 || (gemv_mode() == 0 && batch >= 2);   // its own kernel tiles 4 rows from 2 on
-  if (L.d.code_bits != 8) return false;
+static bool gemv_uses_mma(const Layer& L, int k, int batch, aqmb_dtype x_dtype) {
+  if (L.d.code_bits != 8 && L.d.code_bits != 4) return false;
   if (gemv_mode() != 0) return gemv_mode() == 3;
   const bool wide = L.S * L.J > 512;
+  if (L.d.code_bits == 4) return batch >= 2 || (x_dtype == AQMB_F16 && wide && k >= 2);
   if (x_dtype == AQMB_F16) return batch >= 2 || wide;
   return batch >= 3 || (batch == 2 && wide);
 }
 
 static hipError_t launch_gemv_any(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                                   aqmb_dtype y_dtype, hipStream_t st) {
-  if (gemv_uses_mma(L, batch, x_dtype)) return launch_gemv_mma(L, k, x, x_dtype, batch, y, y_dtype, st);
+  if (gemv_uses_mma(L, k, batch, x_dtype)) return launch_gemv_mma(L, k, x, x_dtype, batch, y, y_dtype, st);
   if (L.d.code_bits == 4) return launch_gemv_b4(L, k, x, x_dtype, batch, y, y_dtype, st);
   return launch_gemv(L, k, x, x_dtype, batch, y, y_dtype, st);
 }
@@ -342,7 +342,7 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
   // would send to another kernel (4-bit codes, the matrix-core kernel) run one launch each, so the
   // results are always those of aqmb_gemv.
   bool per_layer = false;
-  for (int i = 0; i < n_layers; ++i) per_layer = per_layer || Ls[i]->d.code_bits == 4 || gemv_uses_mma(*Ls[i], batch, x_dtype);
+  for (int i = 0; i < n_layers; ++i) per_layer = per_layer || Ls[i]->d.code_bits == 4 || gemv_uses_mma(*Ls[i], k, batch, x_dtype);
   hipError_t e = hipSuccess;
   if (per_layer) {
     for (int i = 0; i < n_layers && e == hipSuccess; ++i)
