@@ -6,13 +6,12 @@
 // inputs (a run is 16 groups: one 16-byte code slice per plane, or half of a 4-bit slice). In a K-step lane l
 // of a wave stands for weight row l % 16 and group l / 16 of the step: it gathers that group's
 // codeword of every plane from the codebooks replicated in LDS, which is the B fragment of that
-// plane's MFMA as it is (8 fp16 values of one row and group). The A fragment is x itself: lane l
-// holds 8 values of batch row l % 16 (rows past the batch read zeros). So every code costs one
+// plane's MFMA as it is (8 fp16 values of one row and group). The A fragment is x: lane l holds 8
+// values of batch row l % 16 (rows past the batch are never stored). So every code costs one
 // codeword gather, as at batch 1, and the dot products run on the matrix cores whatever the batch.
-// Products are exact: fp16 x by the fp16 codeword directly; bf16 x by the codeword split exactly
-// into two bf16 parts (an fp16 value has 11 significant bits: hi = RNE_bf16(c) and lo = c - hi has
-// at most 3, both exact), split once per codeword when the codebooks are copied into LDS (a book
-// of high parts and a book of low parts), so a code costs two gathers and two MFMAs.
+// Products are exact: fp16 x by the fp16 codeword directly; bf16 x either converted to fp16 times
+// a power of two per batch row and run, or multiplied by the codeword split exactly into two bf16
+// parts (see mg_split).
 // Sums are fp32. The 16 waves' partial tiles are added in a fixed order (a tree over the waves),
 // scaled once and rounded once, so results are reproducible.
 #include <type_traits>
@@ -121,16 +120,25 @@ __device__ __forceinline__ void mg_small_loads_first() {
   asm volatile("" ::: "memory");
 }
 
-// Codebook word q (q < K * NCW) into its nrep replicas (bf16 x: a book of high and a book of low
-// parts, split exactly); v0 is word threadIdx.x, already loaded.
-template <int K, int XDT, int CB>
+// bf16 x takes one of two exact forms. Converted (mg_bf16_to_f16): x becomes fp16 times a power
+// of two per batch row and run, one gather and one fp16 MFMA per code, at the price of the
+// conversion (NX registers per lane and run). Split: every codeword is split once, when copied
+// into LDS, into a bf16 high part (RNE) and a bf16 low part (the remainder, at most 3
+// significant bits, exact): two gathers and two bf16 MFMAs per code, no conversion. The split
+// form is kept where the planes are too few to repay the conversion (measured crossovers).
+template <int K, int XDT, int NX>
+constexpr bool mg_split() { return XDT == AQMB_BF16 && K < (NX == 1 ? 2 : NX == 2 ? 3 : 4); }
+
+// Codebook word q (q < K * NCW) into its nrep replicas (split form: a book of high and a book of
+// low parts); v0 is word threadIdx.x, already loaded.
+template <int K, int CB, bool kSplit>
 __device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep, uint4 v0) {
   using namespace mg;
-  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2, NCW = 1 << CB;
+  constexpr int NCW = 1 << CB;
   for (int q = threadIdx.x; q < K * NCW; q += kThreads) {
     const uint4 v = mg_preload<K, CB>() ? v0 : ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - a.cb_shift);
-    if constexpr (kBooks == 1) {
+    if constexpr (!kSplit) {
       for (int i = 0; i < a.nrep; ++i) cb_rep[q * a.nrep + ((i + rot) & (a.nrep - 1))] = v;
     } else {
       const f16x8_t c = __builtin_bit_cast(f16x8_t, v);
@@ -194,6 +202,43 @@ __device__ __forceinline__ void mg_rows_transpose(uint32_t (&d)[4]) {
   d[0] = s01[0]; d[1] = s01[1]; d[2] = s23[0]; d[3] = s23[1];
 }
 
+// bf16 x of a run as fp16 times a power of two per batch row: the exponent shift that puts the
+// row's largest magnitude over the run's 128 inputs in [2^14, 2^15) (the same rule as the
+// direct-gather kernel's per-group conversion). Every lane computes the shift of the batch row it
+// loaded (its largest exponent field, then the maximum over the lanes that hold the same row:
+// the same position in the other rows of 16 lanes and, for NX < 4, positions R apart within the
+// row) and converts its own values; a bf16 value is then exact in fp16 unless it lies below 2^-29
+// of that maximum. Returns the lane's shift: its values were multiplied by 2^-sh.
+template <int NX>
+__device__ __forceinline__ int mg_bf16_to_f16(uint4 (&xa)[NX]) {
+  uint32_t e = 0;
+#pragma unroll
+  for (int t = 0; t < NX; ++t) {
+    const uint32_t w[4] = {xa[t].x, xa[t].y, xa[t].z, xa[t].w};
+#pragma unroll
+    for (int h = 0; h < 4; ++h) e = max(e, max((w[h] >> 7) & 0xFFu, (w[h] >> 23) & 0xFFu));
+  }
+  const auto r32 = __builtin_amdgcn_permlane32_swap(e, e, false, false);   // rows 0, 1 <-> rows 2, 3
+  e = max(r32[0], r32[1]);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(e, e, false, false);   // rows 0, 2 <-> rows 1, 3
+  e = max(r16[0], r16[1]);
+  if constexpr (NX == 1) e = max(e, (uint32_t)__builtin_amdgcn_mov_dpp((int)e, 0x124, 0xF, 0xF, false));  // row_ror:4
+  if constexpr (NX <= 2) e = max(e, (uint32_t)__builtin_amdgcn_mov_dpp((int)e, 0x128, 0xF, 0xF, false));  // row_ror:8
+  const int sh = (int)e - 141;                               // (e - 127) - 14
+#pragma unroll
+  for (int t = 0; t < NX; ++t) {
+    uint32_t w[4] = {xa[t].x, xa[t].y, xa[t].z, xa[t].w};
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const _Float16 lo = (_Float16)ldexpf(bf16lo(w[h]), -sh);
+      const _Float16 hi = (_Float16)ldexpf(bf16hi(w[h]), -sh);
+      w[h] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+    }
+    xa[t] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  return sh;
+}
+
 // The A fragment of step J (layout above MgRun).
 template <int NX, int J>
 __device__ __forceinline__ uint4 mg_x_step(const uint4 (&xa)[NX]) {
@@ -208,8 +253,19 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
                                            const MgRun<K, CB, NX>& R, mg::f32x4_t (&acc)[4]) {
   using namespace mg;
   constexpr int NCW = 1 << CB;
-  const int kc = (threadIdx.x & 63) >> 4;
-  const uint4 xs[4] = {mg_x_step<NX, 0>(R.xa), mg_x_step<NX, 1>(R.xa), mg_x_step<NX, 2>(R.xa), mg_x_step<NX, 3>(R.xa)};
+  const int lane = threadIdx.x & 63, kc = lane >> 4;
+  uint4 xa[NX];
+#pragma unroll
+  for (int t = 0; t < NX; ++t) xa[t] = R.xa[t];
+  constexpr bool kSplit = mg_split<K, XDT, NX>(), kConv = XDT == AQMB_BF16 && !kSplit;
+  int sh = 0;
+  if constexpr (kConv) sh = mg_bf16_to_f16<NX>(xa);
+  const uint4 xs[4] = {mg_x_step<NX, 0>(xa), mg_x_step<NX, 1>(xa), mg_x_step<NX, 2>(xa), mg_x_step<NX, 3>(xa)};
+  // bf16 x: the run's products go to fresh sums, scaled by each batch row's 2^sh at the end
+  f32x4_t run[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) run[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  f32x4_t (&dst)[4] = kConv ? run : acc;
   constexpr int kCT = mg_codes_t<K, CB>() ? 4 * mg_code_loads<K, CB>() : 1;
   uint32_t cd[kCT];
   if constexpr (mg_codes_t<K, CB>()) {
@@ -237,15 +293,24 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
       }
       const uint32_t off = (((uint32_t)(m * NCW) + code) << a.cb_shift) + rep_off;
       const uint4 cw = *(const uint4*)((const char*)cb_rep + off);
-      if constexpr (XDT == AQMB_F16) {
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
-                                                        __builtin_bit_cast(f16x8_t, cw), acc[j], 0, 0, 0);
+      if constexpr (!kSplit) {
+        dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
+                                                        __builtin_bit_cast(f16x8_t, cw), dst[j], 0, 0, 0);
       } else {
         const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * NCW) << a.cb_shift) + off);
         const b16x8_t xb = __builtin_bit_cast(b16x8_t, xs[j]);
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cw), acc[j], 0, 0, 0);
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cl), acc[j], 0, 0, 0);
       }
+    }
+  }
+  if constexpr (kConv) {
+    // element e of this lane is batch row 4 kc + e, whose shift lane 4 kc + e computed
+    const f32x4_t t = (run[0] + run[1]) + (run[2] + run[3]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int she = __builtin_amdgcn_ds_bpermute((4 * kc + e) * 4, sh);
+      acc[0][e] += ldexpf(t[e], she);
     }
   }
 }
@@ -286,7 +351,7 @@ template <int K, int XDT, int CB, int NX>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_kernel(GemvMmaArgs a) {
   using namespace mg;
-  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;            // fp16 codewords, or bf16 high and low parts
+  constexpr int kBooks = mg_split<K, XDT, NX>() ? 2 : 1;    // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
   uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
   f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
@@ -308,7 +373,7 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   mg_small_loads_first<K, CB>();
   mg_load_run<K, CB, NX>(a, r, rowc, true, ra);
   mg_load_run<K, CB, NX>(a, r + kWaves, rowc, true, rb);
-  mg_replicate<K, XDT, CB>(a, cb_rep, w0);
+  mg_replicate<K, CB, mg_split<K, XDT, NX>()>(a, cb_rep, w0);
   __syncthreads();
 
   f32x4_t acc[4];
@@ -336,7 +401,7 @@ template <int K, int XDT, int CB, int NX>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_persist_kernel(GemvMmaArgs a) {
   using namespace mg;
-  constexpr int kBooks = XDT == AQMB_F16 ? 1 : 2;
+  constexpr int kBooks = mg_split<K, XDT, NX>() ? 2 : 1;    // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
   uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
   f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
@@ -382,7 +447,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   mg_small_loads_first<K, CB>();
   load_item(0, ra);
   load_item(1, rb);
-  mg_replicate<K, XDT, CB>(a, cb_rep, w0);
+  mg_replicate<K, CB, mg_split<K, XDT, NX>()>(a, cb_rep, w0);
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -398,28 +463,25 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 }
 
 // 16-codeword codebooks (4-bit codes) fill the LDS banks once: one copy reads without conflicts.
-template <int K, int XDT, int CB>
-static hipError_t launch_mma_kc(GemvMmaArgs a, hipStream_t st) {
-  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(XDT == AQMB_F16 ? 1 : 2) * K * (1 << CB) * 16;
+template <int K, int XDT, int CB, int NX>
+static hipError_t launch_mma_knx(GemvMmaArgs a, hipStream_t st) {
+  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(mg_split<K, XDT, NX>() ? 2 : 1) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
   a.nrep = CB == 4 ? 1 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
   a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
   const size_t lds = book * a.nrep + red;
   const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
-  // x loads per run: batch rows in groups of 4 per 16-lane row (see MgRun)
-  const bool persist = n_rb > a.n_cu && a.n_cu > 0;
-  const dim3 grid(persist ? a.n_cu : n_rb);
-  if (a.batch <= 4) {
-    if (persist) gemv_mma_persist_kernel<K, XDT, CB, 1><<<grid, mg::kThreads, lds, st>>>(a);
-    else gemv_mma_kernel<K, XDT, CB, 1><<<grid, mg::kThreads, lds, st>>>(a);
-  } else if (a.batch <= 8) {
-    if (persist) gemv_mma_persist_kernel<K, XDT, CB, 2><<<grid, mg::kThreads, lds, st>>>(a);
-    else gemv_mma_kernel<K, XDT, CB, 2><<<grid, mg::kThreads, lds, st>>>(a);
-  } else {
-    if (persist) gemv_mma_persist_kernel<K, XDT, CB, 4><<<grid, mg::kThreads, lds, st>>>(a);
-    else gemv_mma_kernel<K, XDT, CB, 4><<<grid, mg::kThreads, lds, st>>>(a);
-  }
+  if (n_rb > a.n_cu && a.n_cu > 0) gemv_mma_persist_kernel<K, XDT, CB, NX><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
+  else gemv_mma_kernel<K, XDT, CB, NX><<<dim3(n_rb), mg::kThreads, lds, st>>>(a);
   return hipGetLastError();
+}
+
+// x loads per run: batch rows in groups of 4 per 16-lane row (see MgRun).
+template <int K, int XDT, int CB>
+static hipError_t launch_mma_kc(const GemvMmaArgs& a, hipStream_t st) {
+  if (a.batch <= 4) return launch_mma_knx<K, XDT, CB, 1>(a, st);
+  if (a.batch <= 8) return launch_mma_knx<K, XDT, CB, 2>(a, st);
+  return launch_mma_knx<K, XDT, CB, 4>(a, st);
 }
 
 template <int K, int XDT>
