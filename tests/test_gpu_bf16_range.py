@@ -1,11 +1,12 @@
 """bf16 activations far outside fp16's range and 8-value groups with a wide dynamic range: the
-decode GEMV (direct-gather kernel at batch 1 and 2, 4-bit kernel at batch 1, matrix-core kernel
-at batch 4) against the fp64 oracle, fp32 output.
+decode GEMV (direct-gather and 4-bit kernels at batch 1, matrix-core kernel from batch 2, in
+both its bf16 forms: the exact codeword split at low k, the per-run conversion above) against
+the fp64 oracle, fp32 output.
 
 The direct-gather and 4-bit kernels represent each bf16 group as fp16 values times a power of two
-that puts the group maximum in [2^14, 2^15); values more than 2^29 below the group maximum are
-rounded. The outputs must stay within the usual tolerance and, at fp32 output, close to fp32
-summation accuracy.
+that puts the group maximum in [2^14, 2^15), the matrix-core kernel each batch row's 128 inputs of
+a run; values more than 2^29 below that maximum are rounded. The outputs must stay within the
+usual tolerance and, at fp32 output, close to fp32 summation accuracy.
 """
 from __future__ import annotations
 
@@ -46,11 +47,11 @@ def test_bf16_range(kind, B):
     L = make_layer(LayerSpec("rng", 96, 1032, M=4, B=B, seed=400 + B, act_dtype="bf16"))
     C, s = formats.f16_bits_to_f64(L.codebooks), formats.f16_bits_to_f64(L.scales)
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
-        for b in (1, 2, 4):
+        for b in (1, 2, 4, 8, 16):
             xbits = _x(kind, b, 1032, seed=410 + b)
             xv = act_values(xbits, "bf16")
             x = to_dev(xbits).view(torch.bfloat16)
-            for k in (1, 4):
+            for k in (1, 2, 3, 4):
                 ref = oracle.linear(xv, L.codes, C, s, k)
                 y = torch.empty((b, 96), dtype=torch.float32, device="cuda")
                 A.gemv(gl.handle, k, x, A.DType.BF16, b, y, A.DType.F32)

@@ -1,7 +1,7 @@
 """Every GEMV kernel for 8-bit codes and both GEMM tilings (8- and 4-bit codes), whatever the default dispatch picks.
 
-By default batch 1 (and batch 2 with bf16 x) runs the direct-gather kernel and larger batches the
-matrix-core kernel; the AQMB_GEMV variable (read once per process) forces one of them for every
+By default batch 1 runs the direct-gather kernel (fp16 x: on rows of at most 512 groups) and
+larger batches the matrix-core kernel; the AQMB_GEMV variable (read once per process) forces one of them for every
 batch. A child process
 with the variable set runs the small GEMV cases against the oracle, so both kernels stay
 parity-tested at every batch. Oracle and tolerance as in the other GEMV tests.

@@ -183,7 +183,7 @@ def test_gemv_wide_rows(d_in, xdt):
 def test_gemv_more_row_blocks_than_cus(xdt):
     """5000 rows = 313 blocks of 16 (the last one ragged): more than one block per compute unit,
     so each workgroup walks several blocks with the codebooks replicated once. Batch 1 (direct
-    gathers; with bf16 x also batch 2) and 2, 3, 8, 16 (matrix cores; 65 groups = 5 runs of 16, so
+    gathers) and 2, 3, 8, 16 (matrix cores; 65 groups = 5 runs of 16, so
     11 of the 16 waves run a dummy item per block), every k, against the oracle."""
     spec = LayerSpec("tall", 5000, 520, M=4, seed=39, act_dtype=xdt)
     L = make_layer(spec)
