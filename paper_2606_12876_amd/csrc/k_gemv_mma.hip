@@ -10,8 +10,8 @@
 // values of batch row l % 16 (rows past the batch are never stored). So every code costs one
 // codeword gather, as at batch 1, and the dot products run on the matrix cores whatever the batch.
 // Products are exact: fp16 x by the fp16 codeword directly; bf16 x either converted to fp16 times
-// a power of two per batch row and run, or multiplied by the codeword split exactly into two bf16
-// parts (see mg_split).
+// a power of two per batch row and run (values far below the row's maximum truncated), or
+// multiplied by the codeword split exactly into two bf16 parts (see mg_split).
 // Sums are fp32. The 16 waves' partial tiles are added in a fixed order (a tree over the waves),
 // scaled once and rounded once, so results are reproducible.
 #include <type_traits>
@@ -120,14 +120,15 @@ __device__ __forceinline__ void mg_small_loads_first() {
   asm volatile("" ::: "memory");
 }
 
-// bf16 x takes one of two exact forms. Converted (mg_bf16_to_f16): x becomes fp16 times a power
-// of two per batch row and run, one gather and one fp16 MFMA per code, at the price of the
-// conversion (NX registers per lane and run). Split: every codeword is split once, when copied
+// bf16 x takes one of two forms. Converted (mg_bf16_to_f16): x becomes fp16 times a power of two
+// per batch row and run (exact but for values far below the row's maximum), one gather and one
+// fp16 MFMA per code, at the price of the conversion (NX registers per lane and run). Split
+// (exact): every codeword is split once, when copied
 // into LDS, into a bf16 high part (RNE) and a bf16 low part (the remainder, at most 3
 // significant bits, exact): two gathers and two bf16 MFMAs per code, no conversion. The split
 // form is kept where the planes are too few to repay the conversion (measured crossovers).
 template <int K, int XDT, int NX>
-constexpr bool mg_split() { return XDT == AQMB_BF16 && K < (NX == 1 ? 2 : NX == 2 ? 3 : 4); }
+constexpr bool mg_split() { return XDT == AQMB_BF16 && K < (NX == 1 ? 2 : 3); }
 
 // Codebook word q (q < K * NCW) into its nrep replicas (split form: a book of high and a book of
 // low parts); v0 is word threadIdx.x, already loaded.
@@ -203,21 +204,28 @@ __device__ __forceinline__ void mg_rows_transpose(uint32_t (&d)[4]) {
 }
 
 // bf16 x of a run as fp16 times a power of two per batch row: the exponent shift that puts the
-// row's largest magnitude over the run's 128 inputs in [2^14, 2^15) (the same rule as the
+// row's largest magnitude over the run's 128 inputs in [2^14, 2^15) (the rule of the
 // direct-gather kernel's per-group conversion). Every lane computes the shift of the batch row it
-// loaded (its largest exponent field, then the maximum over the lanes that hold the same row:
-// the same position in the other rows of 16 lanes and, for NX < 4, positions R apart within the
-// row) and converts its own values; a bf16 value is then exact in fp16 unless it lies below 2^-29
-// of that maximum. Returns the lane's shift: its values were multiplied by 2^-sh.
+// loaded (its largest exponent field e, then the maximum over the lanes that hold the same row:
+// the same position in the other rows of 16 lanes and, for NX < 4, positions 4 NX apart within
+// the row) and converts its own values. For 30 <= e <= 254 the conversion is integer arithmetic
+// on the bit patterns (two values per 32-bit word): the exponent field lowered by e - 29 with the
+// mantissa's 7 bits moved to fp16's 10, so a value is exact unless it lies below 2^-28 of the
+// row maximum, where it is truncated (error below 2^-29 of the maximum); rows past the batch (never
+// stored) take it too. Other rows (a maximum below 2^-97, Inf or NaN) are converted by ldexp and
+// round-to-nearest-even, as in the direct-gather kernel. Returns the lane's shift: its values were
+// multiplied by 2^-sh.
+typedef unsigned short mg_u16x2 __attribute__((ext_vector_type(2)));
 template <int NX>
-__device__ __forceinline__ int mg_bf16_to_f16(uint4 (&xa)[NX]) {
-  uint32_t e = 0;
+__device__ __forceinline__ int mg_bf16_to_f16(uint4 (&xa)[NX], int batch) {
+  mg_u16x2 ex = {0, 0};
 #pragma unroll
   for (int t = 0; t < NX; ++t) {
     const uint32_t w[4] = {xa[t].x, xa[t].y, xa[t].z, xa[t].w};
 #pragma unroll
-    for (int h = 0; h < 4; ++h) e = max(e, max((w[h] >> 7) & 0xFFu, (w[h] >> 23) & 0xFFu));
+    for (int h = 0; h < 4; ++h) ex = __builtin_elementwise_max(ex, __builtin_bit_cast(mg_u16x2, w[h] & 0x7F807F80u));
   }
+  uint32_t e = (uint32_t)max(ex.x, ex.y) >> 7;
   const auto r32 = __builtin_amdgcn_permlane32_swap(e, e, false, false);   // rows 0, 1 <-> rows 2, 3
   e = max(r32[0], r32[1]);
   const auto r16 = __builtin_amdgcn_permlane16_swap(e, e, false, false);   // rows 0, 2 <-> rows 1, 3
@@ -225,6 +233,23 @@ __device__ __forceinline__ int mg_bf16_to_f16(uint4 (&xa)[NX]) {
   if constexpr (NX == 1) e = max(e, (uint32_t)__builtin_amdgcn_mov_dpp((int)e, 0x124, 0xF, 0xF, false));  // row_ror:4
   if constexpr (NX <= 2) e = max(e, (uint32_t)__builtin_amdgcn_mov_dpp((int)e, 0x128, 0xF, 0xF, false));  // row_ror:8
   const int sh = (int)e - 141;                               // (e - 127) - 14
+  const int row = (int)(threadIdx.x & 63) & (4 * NX - 1);   // the batch row this lane loaded
+  if ((e >= 30 && e <= 254) || row >= batch) {
+    const uint32_t d = (uint32_t)max((int)e - 29, 1) << 7;
+    const mg_u16x2 dd = {(unsigned short)d, (unsigned short)d};
+#pragma unroll
+    for (int t = 0; t < NX; ++t) {
+      uint32_t w[4] = {xa[t].x, xa[t].y, xa[t].z, xa[t].w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        mg_u16x2 v = __builtin_elementwise_sub_sat(__builtin_bit_cast(mg_u16x2, w[h] & 0x7FFF7FFFu), dd);
+        v = v << (unsigned short)3;
+        w[h] = __builtin_bit_cast(uint32_t, v) | (w[h] & 0x80008000u);
+      }
+      xa[t] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    return sh;
+  }
 #pragma unroll
   for (int t = 0; t < NX; ++t) {
     uint32_t w[4] = {xa[t].x, xa[t].y, xa[t].z, xa[t].w};
@@ -259,7 +284,7 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
   for (int t = 0; t < NX; ++t) xa[t] = R.xa[t];
   constexpr bool kSplit = mg_split<K, XDT, NX>(), kConv = XDT == AQMB_BF16 && !kSplit;
   int sh = 0;
-  if constexpr (kConv) sh = mg_bf16_to_f16<NX>(xa);
+  if constexpr (kConv) sh = mg_bf16_to_f16<NX>(xa, a.batch);
   const uint4 xs[4] = {mg_x_step<NX, 0>(xa), mg_x_step<NX, 1>(xa), mg_x_step<NX, 2>(xa), mg_x_step<NX, 3>(xa)};
   // bf16 x: the run's products go to fresh sums, scaled by each batch row's 2^sh at the end
   f32x4_t run[4];
