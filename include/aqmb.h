@@ -129,7 +129,7 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
  * gate/up): for each l < n_layers, ys[l][b][i] = sum_t x[b][t] * W_k^(l)[i][t], exactly what
  * aqmb_gemv(layers[l], k, x, x_dtype, batch, ys[l], y_dtype, stream) computes (same arithmetic,
  * same rounding), in one launch when every layer has 8-bit codes, k <= 4, aqmb_gemv would use
- * the direct-gather kernel (batch 1; with fp16 x only on rows of at most 512 groups) and, for
+ * the direct-gather kernel (batch 1; on rows of more than 512 groups only bf16 x at k < 4) and, for
  * rows of more than 512 groups, k = 1 (one workgroup per row block walks through the layers,
  * loading the next layer's codes while it works on the current one); otherwise the layers are
  * launched one after another.

@@ -140,8 +140,8 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
 
 // GEMV kernel choice (measured faster in each case). Default: 4-bit codes -> the matrix-core
 // kernel at batch >= 2 and, for fp16 x at k >= 2, at batch 1 on rows of more than 512 groups;
-// their own kernel otherwise. 8-bit codes -> the matrix-core kernel at batch >= 2 and, for fp16
-// x, at batch 1 on rows of more than 512 groups; otherwise the direct-gather kernel (k <= 4,
+// their own kernel otherwise. 8-bit codes -> the matrix-core kernel at batch >= 2 and at batch 1
+// on rows of more than 512 groups (bf16 x: only at k >= 4); otherwise the direct-gather kernel (k <= 4,
 // rows <= 16384) or the lookup table kernel, as k_gemv.hip decides. AQMB_GEMV=mma uses
 // the matrix-core kernel at every batch, AQMB_GEMV=cw or =lut keep 8-bit layers on k_gemv.hip's
 // kernels and 4-bit layers on theirs (read once).
@@ -161,8 +161,7 @@ static bool gemv_uses_mma(const Layer& L, int k, int batch, aqmb_dtype x_dtype) 
   if (gemv_mode() != 0) return gemv_mode() == 3;
   const bool wide = L.S * L.J > 512;
   if (L.d.code_bits == 4) return batch >= 2 || (x_dtype == AQMB_F16 && wide && k >= 2);
-  if (x_dtype == AQMB_F16) return batch >= 2 || wide;
-  return batch >= 2;
+  return batch >= 2 || (wide && (x_dtype == AQMB_F16 || k >= 4));
 }
 
 static hipError_t launch_gemv_any(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,

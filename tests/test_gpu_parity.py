@@ -163,8 +163,8 @@ def test_gemv_workloads(name):
 def test_gemv_wide_rows(d_in, xdt):
     """Rows of 2048 groups (the widest the direct-gather kernel keeps in registers) and of 2049
     groups (beyond it: the lookup-table kernel), batch 1, 2 and 4, every k. Rows of more than 512
-    groups go to the matrix cores except at batch 1 with bf16 x, which takes the direct-gather
-    kernel (2048 groups) or the lookup-table kernel (2049)."""
+    groups go to the matrix cores except at batch 1 with bf16 x and k < 4, which takes the
+    direct-gather kernel (2048 groups) or the lookup-table kernel (2049)."""
     spec = LayerSpec(f"wide{d_in}", 130, d_in, M=4, seed=38, act_dtype=xdt)
     L = make_layer(spec)
     C, s = _f64(L)
