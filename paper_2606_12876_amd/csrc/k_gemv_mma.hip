@@ -123,10 +123,10 @@ __device__ __forceinline__ void mg_small_loads_first() {
 // bf16 x takes one of two forms. Converted (mg_bf16_to_f16): x becomes fp16 times a power of two
 // per batch row and run (exact but for values far below the row's maximum), one gather and one
 // fp16 MFMA per code, at the price of the conversion (NX registers per lane and run). Split
-// (exact): every codeword is split once, when copied
-// into LDS, into a bf16 high part (RNE) and a bf16 low part (the remainder, at most 3
-// significant bits, exact): two gathers and two bf16 MFMAs per code, no conversion. The split
-// form is kept where the planes are too few to repay the conversion (measured crossovers).
+// (exact): every codeword is split once, when copied into LDS, into a bf16 high part (RNE) and a
+// bf16 low part (the remainder, at most 3 significant bits): two gathers and two bf16 MFMAs per
+// code, no conversion. The split form is kept where the planes are too few to repay the
+// conversion (measured crossovers: k = 1 at batch <= 4, k <= 2 above).
 template <int K, int XDT, int NX>
 constexpr bool mg_split() { return XDT == AQMB_BF16 && K < (NX == 1 ? 2 : 3); }
 
