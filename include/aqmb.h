@@ -128,11 +128,16 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
  * Decode GEMV of several layers that read the same input (fused projections such as q/k/v or
  * gate/up): for each l < n_layers, ys[l][b][i] = sum_t x[b][t] * W_k^(l)[i][t], exactly what
  * aqmb_gemv(layers[l], k, x, x_dtype, batch, ys[l], y_dtype, stream) computes (same arithmetic,
- * same rounding), in one launch when every layer has 8-bit codes, k <= 4, aqmb_gemv would use
- * the direct-gather kernel (batch 1; on rows of more than 512 groups only bf16 x at k < 4) and, for
- * rows of more than 512 groups, k = 1 (one workgroup per row block walks through the layers,
- * loading the next layer's codes while it works on the current one); otherwise the layers are
- * launched one after another.
+ * same rounding), in one launch when either
+ *   - every layer has 8-bit codes, k <= 4, aqmb_gemv would use the direct-gather kernel (batch 1;
+ *     on rows of more than 512 groups only bf16 x at k < 4) and, for rows of more than 512
+ *     groups, k = 1 (one workgroup per row block walks through the layers, loading the next
+ *     layer's codes while it works on the current one), or
+ *   - n_layers >= 2, every layer would take the matrix-core kernel (batch >= 2, and batch 1 on
+ *     rows of more than 512 groups: see aqmb_gemv's kernel choice in the library source), all
+ *     have the same code width and none has more 16-row blocks than the device has compute units
+ *     (one grid over all the layers' row blocks);
+ * otherwise the layers are launched one after another.
  *   layers  n_layers live handles, all with the same d_in and on the same device
  *   x       [batch][d_in], dtype x_dtype in {F16, BF16}
  *   ys      n_layers device pointers, ys[l] is [batch][d_out of layer l], dtype y_dtype

@@ -334,13 +334,22 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
   }
   aqmb_status s = check_device((Layer*)Ls[0]);
   if (s != AQMB_OK) return s;
-  // The one-launch kernel shares the direct-gather kernel's arithmetic; layers that a single call
-  // would send to another kernel (4-bit codes, the matrix-core kernel) run one launch each, so the
-  // results are always those of aqmb_gemv.
-  bool per_layer = false;
-  for (int i = 0; i < n_layers; ++i) per_layer = per_layer || Ls[i]->d.code_bits == 4 || gemv_uses_mma(*Ls[i], k, batch, x_dtype);
+  // The one-launch kernels share the single-layer kernels' arithmetic, so the results are always
+  // those of aqmb_gemv: the direct-gather multi-layer kernel when every layer would take the
+  // direct-gather kernel; the matrix-core grid over all layers' row blocks when every layer would
+  // take the one-block matrix-core kernel (same code width, at most one block per compute unit:
+  // taller layers run their persistent kernel, one launch each); otherwise one launch per layer.
+  bool per_layer = false, all_mma = true;
+  for (int i = 0; i < n_layers; ++i) {
+    const bool mma = gemv_uses_mma(*Ls[i], k, batch, x_dtype);
+    per_layer = per_layer || Ls[i]->d.code_bits == 4 || mma;
+    all_mma = all_mma && mma && Ls[i]->d.code_bits == Ls[0]->d.code_bits &&
+              (Ls[i]->d.d_out + 15) / 16 <= Ls[i]->n_cu;
+  }
   hipError_t e = hipSuccess;
-  if (per_layer) {
+  if (all_mma && n_layers >= 2) {
+    e = launch_gemv_mma_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
+  } else if (per_layer) {
     for (int i = 0; i < n_layers && e == hipSuccess; ++i)
       e = launch_gemv_any(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, (hipStream_t)stream);
   } else {

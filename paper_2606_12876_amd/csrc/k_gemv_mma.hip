@@ -372,9 +372,9 @@ __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_
   }
 }
 
+// 16-row block blk of a layer (the body of a one-block workgroup).
 template <int K, int XDT, int CB, int NX>
-__global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
-void gemv_mma_kernel(GemvMmaArgs a) {
+__device__ __forceinline__ void mg_one_block(const GemvMmaArgs& a, int blk) {
   using namespace mg;
   constexpr int kBooks = mg_split<K, XDT, NX>() ? 2 : 1;    // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
@@ -383,7 +383,7 @@ void gemv_mma_kernel(GemvMmaArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;                                 // weight row in the block
-  const int row0 = blockIdx.x * kRows;
+  const int row0 = blk * kRows;
   const int rowc = row0 + col < a.d_out ? row0 + col : a.d_out - 1;
   const int n_runs = (a.G + 15) / 16;                        // code slices per row
   const uint32_t rep_off = (uint32_t)(lane & (a.nrep - 1)) * 16;
@@ -414,6 +414,29 @@ void gemv_mma_kernel(GemvMmaArgs a) {
     if (r + 3 * kWaves < n_runs) mg_load_run<K, CB, NX>(a, r + 3 * kWaves, rowc, true, rb);
   }
   mg_reduce_store(a, red, acc, row0, sbits);
+}
+
+template <int K, int XDT, int CB, int NX>
+__global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_mma_kernel(GemvMmaArgs a) {
+  mg_one_block<K, XDT, CB, NX>(a, (int)blockIdx.x);
+}
+
+// Several layers on one input (same d_in, code width and k): one launch over the row blocks of
+// all of them, workgroup w running block w - first[l] of the layer l with first[l] <= w <
+// first[l + 1], exactly as a one-block workgroup of that layer's own launch.
+struct GemvMmaMultiArgs {
+  GemvMmaArgs L[AQMB_MAX_MULTI];
+  int first[AQMB_MAX_MULTI + 1];
+  int n;
+};
+
+template <int K, int XDT, int CB, int NX>
+__global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void gemv_mma_multi_kernel(GemvMmaMultiArgs m) {
+  int l = 0;
+  while (l + 1 < m.n && (int)blockIdx.x >= m.first[l + 1]) ++l;
+  mg_one_block<K, XDT, CB, NX>(m.L[l], (int)blockIdx.x - m.first[l]);
 }
 
 // Layers with more 16-row blocks than compute units: one persistent workgroup per CU walks the
@@ -488,13 +511,22 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 }
 
 // 16-codeword codebooks (4-bit codes) fill the LDS banks once: one copy reads without conflicts.
+// (mm: several layers in one launch; a is then mm->L[0].)
 template <int K, int XDT, int CB, int NX>
-static hipError_t launch_mma_knx(GemvMmaArgs a, hipStream_t st) {
+static hipError_t launch_mma_knx(GemvMmaArgs a, GemvMmaMultiArgs* mm, hipStream_t st) {
   const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(mg_split<K, XDT, NX>() ? 2 : 1) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
   a.nrep = CB == 4 ? 1 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
   a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
   const size_t lds = book * a.nrep + red;
+  if (mm) {
+    for (int l = 0; l < mm->n; ++l) {
+      mm->L[l].nrep = a.nrep;
+      mm->L[l].cb_shift = a.cb_shift;
+    }
+    gemv_mma_multi_kernel<K, XDT, CB, NX><<<dim3(mm->first[mm->n]), mg::kThreads, lds, st>>>(*mm);
+    return hipGetLastError();
+  }
   const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
   if (n_rb > a.n_cu && a.n_cu > 0) gemv_mma_persist_kernel<K, XDT, CB, NX><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
   else gemv_mma_kernel<K, XDT, CB, NX><<<dim3(n_rb), mg::kThreads, lds, st>>>(a);
@@ -503,33 +535,32 @@ static hipError_t launch_mma_knx(GemvMmaArgs a, hipStream_t st) {
 
 // x loads per run: batch rows in groups of 4 per 16-lane row (see MgRun).
 template <int K, int XDT, int CB>
-static hipError_t launch_mma_kc(const GemvMmaArgs& a, hipStream_t st) {
-  if (a.batch <= 4) return launch_mma_knx<K, XDT, CB, 1>(a, st);
-  if (a.batch <= 8) return launch_mma_knx<K, XDT, CB, 2>(a, st);
-  return launch_mma_knx<K, XDT, CB, 4>(a, st);
+static hipError_t launch_mma_kc(const GemvMmaArgs& a, GemvMmaMultiArgs* mm, hipStream_t st) {
+  if (a.batch <= 4) return launch_mma_knx<K, XDT, CB, 1>(a, mm, st);
+  if (a.batch <= 8) return launch_mma_knx<K, XDT, CB, 2>(a, mm, st);
+  return launch_mma_knx<K, XDT, CB, 4>(a, mm, st);
 }
 
 template <int K, int XDT>
-static hipError_t launch_mma_k(const GemvMmaArgs& a, int code_bits, hipStream_t st) {
-  return code_bits == 4 ? launch_mma_kc<K, XDT, 4>(a, st) : launch_mma_kc<K, XDT, 8>(a, st);
+static hipError_t launch_mma_k(const GemvMmaArgs& a, GemvMmaMultiArgs* mm, int code_bits, hipStream_t st) {
+  return code_bits == 4 ? launch_mma_kc<K, XDT, 4>(a, mm, st) : launch_mma_kc<K, XDT, 8>(a, mm, st);
 }
 
 template <int XDT>
-static hipError_t launch_mma_x(const GemvMmaArgs& a, int k, int cb, hipStream_t st) {
+static hipError_t launch_mma_x(const GemvMmaArgs& a, GemvMmaMultiArgs* mm, int k, int cb, hipStream_t st) {
   switch (k) {
-    case 1: return launch_mma_k<1, XDT>(a, cb, st);
-    case 2: return launch_mma_k<2, XDT>(a, cb, st);
-    case 3: return launch_mma_k<3, XDT>(a, cb, st);
-    case 4: return launch_mma_k<4, XDT>(a, cb, st);
-    case 5: return launch_mma_k<5, XDT>(a, cb, st);
-    case 6: return launch_mma_k<6, XDT>(a, cb, st);
-    case 7: return launch_mma_k<7, XDT>(a, cb, st);
-    default: return launch_mma_k<8, XDT>(a, cb, st);
+    case 1: return launch_mma_k<1, XDT>(a, mm, cb, st);
+    case 2: return launch_mma_k<2, XDT>(a, mm, cb, st);
+    case 3: return launch_mma_k<3, XDT>(a, mm, cb, st);
+    case 4: return launch_mma_k<4, XDT>(a, mm, cb, st);
+    case 5: return launch_mma_k<5, XDT>(a, mm, cb, st);
+    case 6: return launch_mma_k<6, XDT>(a, mm, cb, st);
+    case 7: return launch_mma_k<7, XDT>(a, mm, cb, st);
+    default: return launch_mma_k<8, XDT>(a, mm, cb, st);
   }
 }
 
-hipError_t launch_gemv_mma(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
-                           aqmb_dtype y_dtype, hipStream_t st) {
+static GemvMmaArgs mma_args(const Layer& L, const void* x, int batch, void* y, aqmb_dtype y_dtype) {
   GemvMmaArgs a{};
   a.codes = L.codes;
   a.codebooks = L.codebooks;
@@ -544,8 +575,28 @@ hipError_t launch_gemv_mma(const Layer& L, int k, const void* x, aqmb_dtype x_dt
   a.batch = batch;
   a.y_dtype = (int)y_dtype;
   a.n_cu = L.n_cu;
+  return a;
+}
+
+hipError_t launch_gemv_mma(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                           aqmb_dtype y_dtype, hipStream_t st) {
+  const GemvMmaArgs a = mma_args(L, x, batch, y, y_dtype);
   const int cb = L.d.code_bits;
-  return x_dtype == AQMB_F16 ? launch_mma_x<AQMB_F16>(a, k, cb, st) : launch_mma_x<AQMB_BF16>(a, k, cb, st);
+  return x_dtype == AQMB_F16 ? launch_mma_x<AQMB_F16>(a, nullptr, k, cb, st) : launch_mma_x<AQMB_BF16>(a, nullptr, k, cb, st);
+}
+
+hipError_t launch_gemv_mma_multi(const Layer* const* Ls, int n, int k, const void* x, aqmb_dtype x_dtype, int batch,
+                                 void* const* ys, aqmb_dtype y_dtype, hipStream_t st) {
+  GemvMmaMultiArgs m{};
+  m.n = n;
+  m.first[0] = 0;
+  for (int l = 0; l < n; ++l) {
+    m.L[l] = mma_args(*Ls[l], x, batch, ys[l], y_dtype);
+    m.first[l + 1] = m.first[l] + (Ls[l]->d.d_out + mg::kRows - 1) / mg::kRows;
+  }
+  const int cb = Ls[0]->d.code_bits;
+  return x_dtype == AQMB_F16 ? launch_mma_x<AQMB_F16>(m.L[0], &m, k, cb, st)
+                             : launch_mma_x<AQMB_BF16>(m.L[0], &m, k, cb, st);
 }
 
 }  // namespace aqmb

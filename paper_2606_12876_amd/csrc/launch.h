@@ -14,9 +14,13 @@ hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hi
 hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                        aqmb_dtype y_dtype, hipStream_t st);
 size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S);
-// Decode GEMV of an 8-bit-code layer on the matrix cores (batch 1..16; used for batch >= 2).
+// Decode GEMV of a layer with 8- or 4-bit codes on the matrix cores (batch 1..16).
 hipError_t launch_gemv_mma(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                            aqmb_dtype y_dtype, hipStream_t st);
+// The same for n layers with the same d_in, code width and device, in one launch (results equal to
+// launch_gemv_mma's for each layer); n <= AQMB_MAX_MULTI.
+hipError_t launch_gemv_mma_multi(const Layer* const* Ls, int n, int k, const void* x, aqmb_dtype x_dtype, int batch,
+                                 void* const* ys, aqmb_dtype y_dtype, hipStream_t st);
 // Decode GEMV of a layer with 4-bit codes (16-codeword codebooks).
 hipError_t launch_gemv_b4(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                           aqmb_dtype y_dtype, hipStream_t st);

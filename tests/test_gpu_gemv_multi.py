@@ -1,9 +1,10 @@
 """aqmb_gemv_multi: several layers on one input in one call (GPU).
 
 Each output must equal, bit for bit, the output of aqmb_gemv on that layer alone (the one-launch
-kernel runs the same per-row arithmetic in the same order), and the fp64 oracle within the GEMV
-tolerance. Covers the one-launch path (8-bit codes, k <= 4, batch <= 4), layers of different
-heights, and the paths that fall back to one launch per layer.
+kernels run the same per-row arithmetic in the same order), and the fp64 oracle within the GEMV
+tolerance. Covers both one-launch paths (the direct-gather multi-layer kernel at batch 1; the
+matrix-core grid over all layers' row blocks from batch 2, also with 4-bit codes), layers of
+different heights, and the paths that fall back to one launch per layer.
 """
 from __future__ import annotations
 
@@ -82,7 +83,8 @@ def test_single_layer_and_wide_rows():
 
 
 def test_fallback_paths():
-    """k > 4, batch > 4 and 16-bit codes take one launch per layer; results are the same."""
+    """k > 4 at batch 1 and 16-bit codes take one launch per layer; k > 4 at batch 8 the
+    matrix-core grid; results are the same."""
     _check([LayerSpec("m6a", 130, 136, M=6, seed=71), LayerSpec("m6b", 77, 136, M=6, seed=72)], (1, 8), (5, 6))
     _check([LayerSpec("b16a", 90, 64, M=2, B=16, seed=73), LayerSpec("b16b", 33, 64, M=2, B=16, seed=74)], (1, 2),
            (1, 2))
@@ -100,3 +102,13 @@ def test_mismatched_inputs_rejected_and_nothing_written():
             A.gemv_multi([ga.handle, ga.handle], 3, x, A.DType.F16, 1, ys, A.DType.F32)   # k > M
         torch.cuda.synchronize()
         assert all(torch.all(y == 7.0) for y in ys)
+
+
+def test_matrix_core_grid_4bit_and_tall_layers():
+    """4-bit layers from batch 2 share one matrix-core launch; a layer with more 16-row blocks than
+    compute units (5000 rows: 313 blocks) next to a small one makes the call fall back to one
+    launch per layer (the tall one on its persistent kernel)."""
+    _check([LayerSpec("f4a", 300, 520, M=4, B=4, seed=77), LayerSpec("f4b", 64, 520, M=4, B=4, seed=78)],
+           (2, 5), (1, 3, 4))
+    _check([LayerSpec("tall", 5000, 520, M=4, seed=79), LayerSpec("small", 100, 520, M=4, seed=80)], (3, 16),
+           (1, 4), xdt="bf16", ydts=("bf16",))
