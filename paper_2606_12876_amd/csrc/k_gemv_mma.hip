@@ -430,6 +430,7 @@ struct GemvMmaMultiArgs {
   int first[AQMB_MAX_MULTI + 1];
   int n;
 };
+static_assert(sizeof(GemvMmaMultiArgs) <= 4096, "kernel arguments are limited to 4 KiB");
 
 template <int K, int XDT, int CB, int NX>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
