@@ -69,20 +69,23 @@ struct MgRun {
 };
 
 // Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of the
-// run in the layout above (zeros past d_in, past the batch, and for dummy runs), and slice r of
-// the row in every plane.
+// run in the layout above (zeros past d_in, past the batch, and for dummy runs; skipped when
+// with_x is false and R already holds it), and slice r of the row in every plane.
 template <int K, int CB, int NX>
-__device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K, CB, NX>& R) {
+__device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K, CB, NX>& R,
+                                            bool with_x = true) {
   constexpr int kRowsX = 4 * NX, kPer = 4 / NX;              // batch rows per load, steps per load
   const int lane = threadIdx.x & 63, kc = lane >> 4;
   const int b = lane & (kRowsX - 1), u = (lane & 15) / kRowsX;
   const int n_runs = (a.G + 15) / 16;
   const int rc = r < n_runs ? r : n_runs - 1;
+  if (with_x) {
 #pragma unroll
-  for (int t = 0; t < NX; ++t) {
-    const int e = rc * 128 + (t * kPer + u) * 32 + kc * 8;
-    const void* src = (xok && b < a.batch && e < a.d_in) ? (const void*)(a.x + (size_t)b * a.d_in + e) : a.zero_page;
-    R.xa[t] = *(const uint4*)src;
+    for (int t = 0; t < NX; ++t) {
+      const int e = rc * 128 + (t * kPer + u) * 32 + kc * 8;
+      const void* src = (xok && b < a.batch && e < a.d_in) ? (const void*)(a.x + (size_t)b * a.d_in + e) : a.zero_page;
+      R.xa[t] = *(const uint4*)src;
+    }
   }
   if constexpr (mg_codes_t<K, CB>()) {
 #pragma unroll
@@ -465,12 +468,14 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   const uint32_t rep_off = (uint32_t)(lane & (a.nrep - 1)) * 16;
 
   // item i: block blockIdx.x + (i / per) gridDim.x, run wave + (i % per) 16 (items past the end:
-  // the last item again, never used)
+  // the last item again, never used). Even items go to register set ra, odd ones to rb; with at
+  // most two runs per wave and block (rows of at most 32 runs) a set always holds the same run, so
+  // its x is loaded once, with the first block.
   auto load_item = [&](int i, MgRun<K, CB, NX>& R) {
     const int ic = i < n_items ? i : n_items - 1;
     const int row = ((int)blockIdx.x + (ic / per) * (int)gridDim.x) * kRows + col;
     const int r = wave + (ic % per) * kWaves;
-    mg_load_run<K, CB, NX>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R);
+    mg_load_run<K, CB, NX>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R, i < 2 || per > 2);
   };
   auto block_row0 = [&](int i) {                             // first row of the block of item i
     return ((int)blockIdx.x + ((i < n_items ? i : n_items - 1) / per) * (int)gridDim.x) * kRows;
