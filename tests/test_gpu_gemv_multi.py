@@ -112,3 +112,11 @@ def test_matrix_core_grid_4bit_and_tall_layers():
            (2, 5), (1, 3, 4))
     _check([LayerSpec("tall", 5000, 520, M=4, seed=79), LayerSpec("small", 100, 520, M=4, seed=80)], (3, 16),
            (1, 4), xdt="bf16", ydts=("bf16",))
+
+
+def test_matrix_core_grid_sixteen_layers():
+    """AQMB_MAX_MULTI layers of ragged heights (1 to 481 rows) in one matrix-core launch: every
+    slot of the launch's layer table in use, blocks of different layers interleaved in the grid."""
+    assert A.MAX_MULTI == 16
+    specs = [LayerSpec(f"s{i}", 1 + 32 * i, 264, M=3, seed=90 + i) for i in range(16)]
+    _check(specs, (2, 9), (1, 3), ydts=("f32",))
