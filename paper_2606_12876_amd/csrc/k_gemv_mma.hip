@@ -104,23 +104,15 @@ __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int row
 }
 
 // When every thread replicates at most one codeword (K * NCW <= 1024), that word is requested
-// ahead of the code words: a CU's requests leave in order, and the replication waits for it.
-// (With more codewords per thread the runs' registers leave no room to hold it.)
+// ahead of the wave's run loads, so the replication waits for it only. (With more codewords per
+// thread the runs' registers leave no room to hold it.) No barrier orders these small loads ahead
+// of the other waves' run loads: with one or two loads per run it cost more than it saved.
 template <int K, int CB> constexpr bool mg_preload() { return K * (1 << CB) <= mg::kThreads; }
 template <int K, int CB>
 __device__ __forceinline__ uint4 mg_first_word(const GemvMmaArgs& a) {
   if constexpr (!mg_preload<K, CB>()) return make_uint4(0, 0, 0, 0);
   const int q = (int)threadIdx.x < K * (1 << CB) ? (int)threadIdx.x : 0;
   return ((const uint4*)a.codebooks)[q];
-}
-
-// An execution barrier between every wave's small loads and the code words (see mg_first_word).
-template <int K, int CB>
-__device__ __forceinline__ void mg_small_loads_first() {
-  if constexpr (!mg_preload<K, CB>()) return;
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 // bf16 x takes one of two forms. Converted (mg_bf16_to_f16): x becomes fp16 times a power of two
@@ -398,7 +390,6 @@ __device__ __forceinline__ void mg_one_block(const GemvMmaArgs& a, int blk) {
   const uint4 w0 = mg_first_word<K, CB>(a);
   const int srow = row0 + mg_out_row(tid);                   // the row this thread stores, if any
   const uint16_t sbits = tid < 256 ? a.scales[srow < a.d_out ? srow : a.d_out - 1] : 0;
-  mg_small_loads_first<K, CB>();
   mg_load_run<K, CB, NX>(a, r, rowc, true, ra);
   mg_load_run<K, CB, NX>(a, r + kWaves, rowc, true, rb);
   mg_replicate<K, CB, mg_split<K, XDT, NX>()>(a, cb_rep, w0);
@@ -498,7 +489,6 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   MgRun<K, CB, NX> ra, rb;
   const uint4 w0 = mg_first_word<K, CB>(a);
   sbits = scale_of(0);
-  mg_small_loads_first<K, CB>();
   load_item(0, ra);
   load_item(1, rb);
   mg_replicate<K, CB, mg_split<K, XDT, NX>()>(a, cb_rep, w0);
