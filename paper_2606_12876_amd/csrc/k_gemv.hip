@@ -379,12 +379,17 @@ __device__ __forceinline__ float group_dot_acc(uint4 xw, uint4 cw, float s) {
 // cw_convert_own_bf16 to x / scl[group] (scl rows of rstride / 16 floats). A group's dot products
 // are chained over the planes into one partial sum (independent chains, one v_dot2 per code word
 // pair), which is then added to the row's accumulator (XS: multiplied by the group's scale).
-template <int K, int NB, int UB, bool XS>
+// `after_gathers` runs in each wave once its own gathers are done, before the row reduction's
+// barrier (the multi-layer kernel writes the next layer's replicas there).
+struct CwNothing {
+  __device__ void operator()() const {}
+};
+template <int K, int NB, int UB, bool XS, typename After = CwNothing>
 __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4* cb_rep, const uint16_t* xs,
                                         size_t rstride, int Gp, int cb_shift, uint32_t rep_off,
                                         float (&red)[cw::kWaves][cw::kRows][NB], int b0, int batch, int row,
                                         bool row_ok, float scale, void* y, int d_out, int y_dtype,
-                                        const float* scl) {
+                                        const float* scl, const After& after_gathers = After()) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rw = lane & 15, part = tid >> 4;
@@ -459,6 +464,7 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
       }
     }
   }
+  after_gathers();
   // row sum: lanes rw, rw + 16, rw + 32, rw + 48 of the wave, then the 16 waves in order
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -717,14 +723,19 @@ struct GemvMultiArgs {
   int n_layers, d_in, S, batch, y_dtype, nrep, cb_shift;
 };
 
-template <int K, int NB, int XDT, int UB>
+template <int K, int NB, int XDT, int UB, bool DB>
 __global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_cw_multi_kernel(GemvMultiArgs a) {
   extern __shared__ uint4 smem_cw[];
   const int nrep = a.nrep;
-  uint4* cb_rep = smem_cw;
-  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);
-  __shared__ float red[cw::kWaves][cw::kRows][NB];
+  // DB: two replica sets (and two row-sum buffers) in turn. Each wave writes the next layer's
+  // replicas into the idle set as soon as its own gathers of the current layer are done; the
+  // row reduction's barrier then separates those writes from the next layer's gathers, and no
+  // barrier of its own is needed. A set (or buffer) is written again two layers later, after a
+  // barrier that every wave reaches only once it has finished reading it.
+  uint4* rep[2] = {smem_cw, smem_cw + (DB ? K * 256 * nrep : 0)};
+  uint16_t* xs = (uint16_t*)(smem_cw + (DB ? 2 : 1) * K * 256 * nrep);
+  __shared__ float red[DB ? 2 : 1][cw::kWaves][cw::kRows][NB];
   const int tid = threadIdx.x, lane = tid & 63;
   const int rw = lane & 15;
   const int row = blockIdx.x * cw::kRows + rw;
@@ -756,10 +767,31 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   };
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group, once
   float* scl = (float*)((char*)xs + NB * rstride);         // [NB][rstride / 16] group scales
-  auto run_layer = [&](int l, uint32_t sbits, const uint2 (&code)[UB][K]) {
+  int buf = 0;                                             // the replica set and row-sum buffer in use
+  // layer l from replica set `buf`; with DB and a next layer, its replicas (word cbn) go to the
+  // other set once this wave's gathers are done
+  auto run_layer = [&](int l, uint32_t sbits, const uint2 (&code)[UB][K], bool next, const uint4& cbn) {
     const int d_out = a.L[l].d_out;
-    cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
-                            row < d_out, f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype, scl);
+    auto after = [&]() {
+      if constexpr (DB) {
+        if (next) {
+          wait_vmcnt<UB * K + 1>();                        // the next codebook word is in
+          cw_replicate<K>(rep[buf ^ 1], cbn, nrep, a.cb_shift);
+        }
+      }
+    };
+    cw_tile<K, NB, UB, kXS>(code, rep[buf], xs, rstride, Gp, a.cb_shift, rep_off, red[DB ? buf : 0], 0, a.batch,
+                            row, row < d_out, f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype, scl, after);
+  };
+  // after layer `cur` (its reduction barrier passed): make `nxt` current
+  auto switch_to = [&](const uint4& cbn) {
+    if constexpr (DB) {
+      buf ^= 1;
+    } else {
+      wait_vmcnt<UB * K + 1>();                            // the next codebook word is in
+      cw_replicate<K>(rep[0], cbn, nrep, a.cb_shift);
+      __syncthreads();
+    }
   };
 
   int cur = next_layer(-1);                                // the grid never exceeds the largest layer
@@ -773,24 +805,20 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   load_codes(cur, ca);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
-  cw_replicate<K>(cb_rep, cba, nrep, a.cb_shift);
+  cw_replicate<K>(rep[0], cba, nrep, a.cb_shift);
   __syncthreads();
   for (;;) {
     int nxt = next_layer(cur);
     load_layer(nxt >= 0 ? nxt : cur, cbb, sb, cb);         // without a next layer: a harmless reload
-    run_layer(cur, sa, ca);                                // its reduction barrier: all gathers done
+    run_layer(cur, sa, ca, nxt >= 0, cbb);                 // its reduction barrier: all gathers done
     if (nxt < 0) break;
-    wait_vmcnt<UB * K + 1>();                              // the next codebook word is in
-    cw_replicate<K>(cb_rep, cbb, nrep, a.cb_shift);
-    __syncthreads();
+    switch_to(cbb);
     cur = nxt;
     nxt = next_layer(cur);
     load_layer(nxt >= 0 ? nxt : cur, cba, sa, ca);
-    run_layer(cur, sb, cb);
+    run_layer(cur, sb, cb, nxt >= 0, cba);
     if (nxt < 0) break;
-    wait_vmcnt<UB * K + 1>();
-    cw_replicate<K>(cb_rep, cba, nrep, a.cb_shift);
-    __syncthreads();
+    switch_to(cba);
     cur = nxt;
   }
 }
@@ -929,8 +957,20 @@ static hipError_t launch_multi_nb(GemvMultiArgs a, int grid, hipStream_t st) {
   a.nrep = cw_nrep(K, NB, a.S, XDT == AQMB_BF16);
   a.cb_shift = a.nrep == 8 ? 7 : 6;
   const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
-  if (cw_blocks(a.S) == 1) gemv_cw_multi_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
-  else gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks><<<grid, cw::kThreads, lds, st>>>(a);
+  // two replica sets when they fit (k <= 2, one 512-group block, rows of at most 512 groups)
+  const size_t lds2 = lds + (size_t)K * 256 * a.nrep * 16;
+  const size_t budget = 160 * 1024 - (size_t)2 * cw::kWaves * cw::kRows * 4 * NB - 512;
+  if constexpr (K <= 2) {
+    if (cw_blocks(a.S) == 1 && lds2 <= budget) {
+      gemv_cw_multi_kernel<K, NB, XDT, 1, true><<<grid, cw::kThreads, lds2, st>>>(a);
+      return hipGetLastError();
+    }
+  }
+  if (cw_blocks(a.S) == 1) {
+    gemv_cw_multi_kernel<K, NB, XDT, 1, false><<<grid, cw::kThreads, lds, st>>>(a);
+  } else {
+    gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false><<<grid, cw::kThreads, lds, st>>>(a);
+  }
   return hipGetLastError();
 }
 
