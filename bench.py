@@ -320,8 +320,7 @@ def main():
 
     t_dom = per_launch_us[("gemv", 4, 1)]
     ach = gemv_bytes(4, 1) / (t_dom * 1e-6) / 1e9
-    gemv_kernel = ("gemv_lut_kernel<K=4,BT=1> + gemv_reduce_kernel" if os.environ.get("AQMB_GEMV") == "lut"
-                   else "gemv_cw_kernel<K=4,NB=1>")
+    gemv_kernel = "gemv_cw_kernel<K=4,NB=1>"
     roofline = {"bound": "hbm", "kernel": f"{gemv_kernel} (k=4, batch 1)", "achieved": round(ach, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic(), "bytes_per_launch": gemv_bytes(4, 1), "us_per_launch": round(t_dom, 3)}

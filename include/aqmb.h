@@ -23,9 +23,17 @@
  *     error nothing is launched and no output byte is written; the status says
  *     why and aqmb_last_error() gives a message for the calling thread.
  *   - No exception or abort crosses this interface.
- *   - A layer is read-only for gemm and dequant, which may run concurrently on
- *     different streams. aqmb_gemv uses a per-layer workspace: gemv calls on one
- *     layer must be ordered (one stream, or synchronised by the caller).
+ *   - A layer is read-only after creation (it is the stored format (C, b, s) that
+ *     Alg. 1 returns): every compute call reads the layer and writes only the
+ *     caller's outputs, so calls on one layer may run concurrently on different
+ *     streams. Only aqmb_load_planes, aqmb_drop_planes and aqmb_destroy change a
+ *     layer, and they must not overlap other calls on it.
+ *   - Device scratch memory that a kernel needs for partial results (the lookup-
+ *     table GEMV, the prefix distortion) is taken per call from the device's
+ *     stream-ordered pool (hipMallocAsync / hipFreeAsync on `stream`), so two
+ *     calls never share it. Every other call needs no scratch. Kernel choice does
+ *     not depend on environment variables: aqmb_gemv_select and aqmb_gemm_select
+ *     choose a kernel explicitly.
  */
 #ifndef AQMB_H
 #define AQMB_H
@@ -102,6 +110,7 @@ aqmb_status aqmb_drop_planes(aqmb_layer_t layer, int keep);
 aqmb_status aqmb_resident_planes(aqmb_layer_t layer, int* resident);
 
 /* Free a layer and its device memory (waits for the device first). NULL is a no-op.
+ * (The counterpart of aqmb_create: the stored format (C, b, s) of Alg. 1 is released.)
  * EINVAL for a handle that is not a live layer. */
 aqmb_status aqmb_destroy(aqmb_layer_t layer);
 
@@ -120,6 +129,35 @@ aqmb_status aqmb_get_desc(aqmb_layer_t layer, aqmb_desc* out);
  */
 aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch,
                       void* y, aqmb_dtype y_dtype, aqmb_stream_t stream);
+
+/*
+ * The GEMV kernels. Each computes the quantity aqmb_gemv defines, to the same contract (fp32
+ * products and sums, one rounding to y_dtype); they differ in speed only.
+ *   AQMB_GEMV_AUTO    the library's choice for the layer, k, batch and x dtype (what aqmb_gemv runs)
+ *   AQMB_GEMV_DIRECT  the direct-gather kernel of the layer's code width: codewords gathered per
+ *                     code and dotted with x on the vector ALUs. 8-bit codes: k <= 4 and rows of
+ *                     at most 2048 groups (16384 inputs); 4- and 16-bit codes: every k and row
+ *   AQMB_GEMV_MMA     the matrix-core kernel (8- and 4-bit codes; every k, batch and row length)
+ *   AQMB_GEMV_LUT     per-group lookup tables LUT_m[j][c] = <x_j, C_m[c]> in LDS, one read per
+ *                     code (8-bit codes); its split-K partial sums take per-call scratch from the
+ *                     stream-ordered pool (ENOMEM if that fails)
+ */
+typedef enum {
+  AQMB_GEMV_AUTO = 0,
+  AQMB_GEMV_DIRECT = 1,
+  AQMB_GEMV_MMA = 2,
+  AQMB_GEMV_LUT = 3
+} aqmb_gemv_kernel;
+
+/*
+ * aqmb_gemv with the kernel named by `kernel` (section 5 reconstruction, as aqmb_gemv). For
+ * tests and tuning: every kernel can be checked against the same reference whatever the default
+ * choice is. Arguments as aqmb_gemv.
+ * Errors: those of aqmb_gemv; EUNSUPPORTED when the kernel cannot serve this layer, k, batch
+ * or row length (see aqmb_gemv_kernel); EINVAL for an unknown kernel; ENOMEM (LUT scratch).
+ */
+aqmb_status aqmb_gemv_select(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch,
+                             void* y, aqmb_dtype y_dtype, aqmb_gemv_kernel kernel, aqmb_stream_t stream);
 
 /* Most layers accepted by one aqmb_gemv_multi call. */
 #define AQMB_MAX_MULTI 16
@@ -141,8 +179,8 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
  *   layers  n_layers live handles, all with the same d_in and on the same device
  *   x       [batch][d_in], dtype x_dtype in {F16, BF16}
  *   ys      n_layers device pointers, ys[l] is [batch][d_out of layer l], dtype y_dtype
- * 1 <= n_layers <= AQMB_MAX_MULTI; k must be valid for every layer. Calls on a layer must be
- * ordered as for aqmb_gemv. Nothing is launched when validation fails.
+ * 1 <= n_layers <= AQMB_MAX_MULTI; k must be valid for every layer. Nothing is launched when
+ * validation fails.
  * Errors: EINVAL (null pointer, bad handle, n_layers < 1, d_in or device differ, k outside
  * [1, M] of some layer, batch < 1), EUNSUPPORTED (n_layers > AQMB_MAX_MULTI, batch >
  * AQMB_MAX_BATCH, dtype), EHIP.
@@ -151,10 +189,12 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
                             int batch, void* const* ys, aqmb_dtype y_dtype, aqmb_stream_t stream);
 
 /*
- * Prefill GEMM: Y[n][i] = s_i * sum_t X[n][t] * Wb_k[i][t] for n < n_tokens, where Wb_k is the
+ * Prefill GEMM (the section 5 partial reconstruction applied to n_tokens inputs at once, the
+ * product Y = W X of section 2.2 in row-major form): Y[n][i] = s_i * sum_t X[n][t] * Wb_k[i][t]
+ * for n < n_tokens, where Wb_k is the
  * unscaled reconstruction sum_{m<k} C_m[b_{ijm}] formed as a binary32 left fold over m and
  * rounded to nearest-even bf16 (the operand fed to bf16 matrix cores); accumulation is fp32.
- *   X  [n_tokens][d_in]  bf16
+ *   X  [n_tokens][d_in]  bf16 (no other activation dtype: convert before the call)
  *   Y  [n_tokens][d_out] dtype y_dtype in {BF16, F32}
  * Requires B = 8 or B = 4. Errors: EINVAL (bad handle, null pointer, k outside [1, M],
  * n_tokens < 1), EUNSUPPORTED (B = 16, dtype), EHIP.
@@ -163,7 +203,29 @@ aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, vo
                       aqmb_dtype y_dtype, aqmb_stream_t stream);
 
 /*
- * Dequantize: W[i][t] = W_k[i][t] in w_dtype in {F16, BF16, F32}, bit-exact to this evaluation
+ * The prefill GEMM's tilings (the same arithmetic and rounding; they differ in speed only).
+ *   AQMB_GEMM_AUTO     the library's choice (what aqmb_gemm runs): 16-row tiles up to 144 tokens,
+ *                      else the large tile that needs the fewest rounds of workgroups
+ *   AQMB_GEMM_ROWS16   16 weight rows per workgroup, all tokens in tiles of 16 (made for few tokens)
+ *   AQMB_GEMM_256x128, AQMB_GEMM_128x128, AQMB_GEMM_128x64
+ *                      tokens x weight rows per workgroup of the large-tile kernel
+ */
+typedef enum {
+  AQMB_GEMM_AUTO = 0,
+  AQMB_GEMM_ROWS16 = 1,
+  AQMB_GEMM_256x128 = 2,
+  AQMB_GEMM_128x128 = 3,
+  AQMB_GEMM_128x64 = 4
+} aqmb_gemm_tiling;
+
+/* aqmb_gemm with the tiling named by `tiling` (tests and tuning). Errors: those of aqmb_gemm;
+ * EINVAL for an unknown tiling. */
+aqmb_status aqmb_gemm_select(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y,
+                             aqmb_dtype y_dtype, aqmb_gemm_tiling tiling, aqmb_stream_t stream);
+
+/*
+ * Dequantize (the section 5 partial reconstruction W_k written out as a dense matrix):
+ * W[i][t] = W_k[i][t] in w_dtype in {F16, BF16, F32}, bit-exact to this evaluation
  * order: each fp16 codebook entry is taken exactly to binary32; the entries of planes
  * 0..k-1 are summed as a binary32 left fold (C_0 + C_1, then + C_2, ...), each sum rounded
  * to nearest even; the fold is multiplied by s_i in binary32 (one rounding, no fused
@@ -188,10 +250,10 @@ aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype,
  * The Hessian form of the same quantity, tr[(W - W_k) H (W - W_k)^T] / d_out with H = X X^T / n,
  * is obtained by passing any factor F with F F^T = H (e.g. a Cholesky factor) as Xt = F^T,
  * n = d_in, and multiplying D by d_in.
- * Requires B = 8 or B = 4. Uses the layer's workspace: calls on a layer must be ordered with each
- * other and with aqmb_gemv / aqmb_gemv_multi calls on that layer.
+ * Requires B = 8 or B = 4. The per-workgroup sums (at most 256 x 8 doubles) take per-call scratch
+ * from the stream-ordered pool, freed on `stream` after the final sum.
  * Errors: EINVAL (bad handle, null pointer, n < 1, misaligned pointer), EUNSUPPORTED (B = 16,
- * dtype other than F16, n > 2^30), EHIP.
+ * dtype other than F16, n > 2^30), ENOMEM (scratch), EHIP.
  */
 aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* Xt,
                                    aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream);

@@ -16,8 +16,9 @@ import enum
 import os
 from typing import Optional
 
-__all__ = ["Status", "DType", "Desc", "AqmbError", "lib", "create", "destroy", "get_desc", "gemv", "gemm",
-           "dequant", "bits_per_weight", "strerror", "last_error", "validate", "QuantLinear", "LIB_PATH"]
+__all__ = ["Status", "DType", "Desc", "AqmbError", "GemvKernel", "GemmTiling", "lib", "create", "destroy", "get_desc",
+           "gemv", "gemv_select", "gemm", "gemm_select", "dequant", "bits_per_weight", "strerror", "last_error",
+           "validate", "QuantLinear", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libaqmb.so")
 
@@ -34,6 +35,23 @@ class DType(enum.IntEnum):
     F16 = 0
     BF16 = 1
     F32 = 2
+
+
+class GemvKernel(enum.IntEnum):
+    """aqmb_gemv_kernel: which GEMV kernel aqmb_gemv_select runs."""
+    AUTO = 0
+    DIRECT = 1
+    MMA = 2
+    LUT = 3
+
+
+class GemmTiling(enum.IntEnum):
+    """aqmb_gemm_tiling: which tiling aqmb_gemm_select runs."""
+    AUTO = 0
+    ROWS16 = 1
+    T256x128 = 2
+    T128x128 = 3
+    T128x64 = 4
 
 
 class Desc(ctypes.Structure):
@@ -65,6 +83,8 @@ def _load() -> ctypes.CDLL:
     L.aqmb_resident_planes.argtypes = [vp, ctypes.POINTER(i32)]
     L.aqmb_get_desc.argtypes = [vp, ctypes.POINTER(Desc)]
     L.aqmb_gemv.argtypes = [vp, i32, vp, i32, i32, vp, i32, vp]
+    L.aqmb_gemv_select.argtypes = [vp, i32, vp, i32, i32, vp, i32, i32, vp]
+    L.aqmb_gemm_select.argtypes = [vp, i32, vp, i32, vp, i32, i32, vp]
     L.aqmb_gemv_multi.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, i32, ctypes.POINTER(vp), i32, vp]
     L.aqmb_gemm.argtypes = [vp, i32, vp, i32, vp, i32, vp]
     L.aqmb_dequant.argtypes = [vp, i32, vp, i32, vp]
@@ -78,7 +98,8 @@ def _load() -> ctypes.CDLL:
     L.aqmb_last_error.argtypes = []
     L.aqmb_last_error.restype = ctypes.c_char_p
     for f in ("aqmb_create", "aqmb_create_prefix", "aqmb_load_planes", "aqmb_drop_planes", "aqmb_resident_planes",
-              "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_multi", "aqmb_gemm",
+              "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_select", "aqmb_gemv_multi", "aqmb_gemm",
+              "aqmb_gemm_select",
               "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_beam_search", "aqmb_validate"):
         getattr(L, f).restype = st
     return L
@@ -220,6 +241,16 @@ def gemv(layer: int, k: int, x, x_dtype, batch: int, y, y_dtype, stream=None) ->
            "aqmb_gemv")
 
 
+def gemv_select(layer: int, k: int, x, x_dtype, batch: int, y, y_dtype, kernel, stream=None) -> None:
+    """aqmb_gemv_select: aqmb_gemv with the kernel named by ``kernel`` (a GemvKernel)."""
+    d = get_desc(layer)
+    if 1 <= batch <= 16:
+        _need(x, batch * d.d_in, x_dtype, "x", "aqmb_gemv_select")
+        _need(y, batch * d.d_out, y_dtype, "y", "aqmb_gemv_select")
+    _check(lib.aqmb_gemv_select(layer, k, _ptr(x), int(x_dtype), batch, _ptr(y), int(y_dtype), int(kernel),
+                                _stream(stream)), "aqmb_gemv_select")
+
+
 MAX_MULTI = 16
 
 
@@ -246,6 +277,16 @@ def gemm(layer: int, k: int, X, n_tokens: int, Y, y_dtype, stream=None) -> None:
         _need(X, n_tokens * d.d_in, DType.BF16, "X", "aqmb_gemm")
         _need(Y, n_tokens * d.d_out, y_dtype, "Y", "aqmb_gemm")
     _check(lib.aqmb_gemm(layer, k, _ptr(X), n_tokens, _ptr(Y), int(y_dtype), _stream(stream)), "aqmb_gemm")
+
+
+def gemm_select(layer: int, k: int, X, n_tokens: int, Y, y_dtype, tiling, stream=None) -> None:
+    """aqmb_gemm_select: aqmb_gemm with the tiling named by ``tiling`` (a GemmTiling)."""
+    d = get_desc(layer)
+    if n_tokens >= 1:
+        _need(X, n_tokens * d.d_in, DType.BF16, "X", "aqmb_gemm_select")
+        _need(Y, n_tokens * d.d_out, y_dtype, "Y", "aqmb_gemm_select")
+    _check(lib.aqmb_gemm_select(layer, k, _ptr(X), n_tokens, _ptr(Y), int(y_dtype), int(tiling), _stream(stream)),
+           "aqmb_gemm_select")
 
 
 def dequant(layer: int, k: int, W, w_dtype, stream=None) -> None:
@@ -299,18 +340,29 @@ def validate(desc: Desc, op: int, k: int, n: int, in_dtype, out_dtype, inp, out)
 class QuantLinear:
     """A quantized linear layer y = x . W_k^T served at any precision level k <= M.
 
-    Holds the library's layer handle; ``forward`` allocates the output with PyTorch and calls
-    the library on the current stream.
+    Holds the library's layer handle. ``forward`` allocates the output with PyTorch and calls the
+    library on the current stream: up to 16 input rows go to aqmb_gemv (fp16 or bf16 x), more
+    rows to aqmb_gemm, which takes bf16 x only (other dtypes are refused, not converted: the
+    binding only marshals arguments). The code width B follows from the codebooks: 16, 256 or
+    65536 codewords give 4-, 8- or 16-bit codes (4-bit codes are passed one per byte, 0..15).
     """
+
+    _BITS = {16: 4, 256: 8, 65536: 16}
 
     def __init__(self, codes, codebooks, scales, group_size: int = 8):
         import torch
         M, d_out, n_groups = codes.shape
-        code_bits = 8 if codes.dtype == torch.uint8 else 16
+        n_cw = int(codebooks.shape[1])
+        if n_cw not in self._BITS:
+            raise AqmbError(Status.EUNSUPPORTED, "QuantLinear", f"codebooks of {n_cw} codewords (16, 256 or 65536)")
+        code_bits = self._BITS[n_cw]
+        want = torch.int16 if code_bits == 16 else torch.uint8
+        if codes.dtype not in ((torch.int16, torch.uint16) if code_bits == 16 else (torch.uint8,)):
+            raise AqmbError(Status.EINVAL, "QuantLinear", f"codes of dtype {codes.dtype} for {code_bits}-bit codes")
         self.desc = make_desc(d_out, n_groups * group_size, M, code_bits, group_size)
-        self.handle = create(self.desc, codes.contiguous(), codebooks.contiguous().view(torch.int16),
+        self.handle = create(self.desc, codes.contiguous().view(want), codebooks.contiguous().view(torch.int16),
                              scales.contiguous().view(torch.int16))
-        self.M, self.d_out, self.d_in = M, d_out, n_groups * group_size
+        self.M, self.d_out, self.d_in, self.code_bits = M, d_out, n_groups * group_size, code_bits
 
     def forward(self, x, k: int, out_dtype=None):
         import torch
@@ -318,6 +370,9 @@ class QuantLinear:
         lead = x.shape[:-1]
         x2 = x.reshape(-1, self.d_in).contiguous()
         n = x2.shape[0]
+        if n > 16 and x2.dtype != torch.bfloat16:
+            raise AqmbError(Status.EUNSUPPORTED, "QuantLinear",
+                            f"{n} rows go to aqmb_gemm, which takes bf16 x only (got {x2.dtype})")
         y = torch.empty((n, self.d_out), dtype=out_dtype, device=x.device)
         if n <= 16:
             gemv(self.handle, k, x2, _dtype(x2), n, y, _dtype(y))

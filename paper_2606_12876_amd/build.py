@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libaqmb.so")
 
-SOURCES = ["validate.cpp", "api.cpp", "k_dequant.hip", "k_gemv.hip", "k_gemv4.hip", "k_gemv_mma.hip", "k_gemm.hip", "k_gemm_small.hip", "k_distortion.hip", "k_beam.hip"]
+SOURCES = ["validate.cpp", "api.cpp", "k_dequant.hip", "k_gemv.hip", "k_gemv16.hip", "k_gemv4.hip", "k_gemv_mma.hip", "k_gemm.hip", "k_gemm_small.hip", "k_distortion.hip", "k_beam.hip"]
 ARCH = "gfx950"
 
 

@@ -1,7 +1,6 @@
 // The C-ABI entry points: layer registry, creation (copy + re-tile), dispatch.
 #include <hip/hip_runtime.h>
 
-#include <cstdlib>
 #include <mutex>
 #include <new>
 #include <unordered_set>
@@ -32,7 +31,7 @@ static void free_layer(Layer* L) {
   if (L->codes) (void)hipFree(L->codes);
   if (L->codebooks) (void)hipFree(L->codebooks);
   if (L->scales) (void)hipFree(L->scales);
-  if (L->ws) (void)hipFree(L->ws);
+  if (L->aux) (void)hipFree(L->aux);
   L->magic = 0;
   delete L;
 }
@@ -60,7 +59,7 @@ namespace aqmb {
 // above 15 (the re-tiling flags them in the workspace). Synchronous.
 static aqmb_status upload_planes(Layer* L, const void* codes, int n, unsigned char* dst, hipStream_t st,
                                  const char* where) {
-  int* flag = (int*)(L->ws + 256);
+  int* flag = L->upload_flag();
   hipError_t e;
   if ((e = hipMemsetAsync(flag, 0, sizeof(int), st)) != hipSuccess ||
       (e = launch_retile(*L, codes, n, dst, flag, st)) != hipSuccess || (e = hipStreamSynchronize(st)) != hipSuccess)
@@ -100,14 +99,12 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
   L->resident = resident;
   const size_t n_codewords = (size_t)1 << desc->code_bits;
   const size_t cb_bytes = (size_t)desc->num_codebooks * n_codewords * desc->group_size * 2;
-  L->ws_floats = gemv_workspace_floats(*desc, L->G, L->S);
-  if (L->ws_floats < 256 + distortion_workspace_floats()) L->ws_floats = 256 + distortion_workspace_floats();
 
   struct { void** p; size_t n; const char* what; } allocs[] = {
       {(void**)&L->codes, (size_t)resident * L->plane_bytes, "codes"},
       {(void**)&L->codebooks, cb_bytes, "codebooks"},
       {(void**)&L->scales, (size_t)desc->d_out * 2, "scales"},
-      {(void**)&L->ws, L->ws_floats * sizeof(float), "workspace"},
+      {(void**)&L->aux, kAuxBytes, "zero page"},
   };
   for (auto& a : allocs) {
     e = hipMalloc(a.p, a.n);
@@ -118,9 +115,8 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
       return fail(AQMB_ENOMEM, "create: hipMalloc(%zu) for %s failed: %s", a.n, a.what, hipGetErrorString(e));
     }
   }
-  // The workspace's first KiB is a zero page that kernels read in place of out-of-range
-  // inputs (never written); the rest holds per-call partial sums (gemv, prefix distortion).
-  if ((e = hipMemsetAsync(L->ws, 0, L->ws_floats * sizeof(float), st)) != hipSuccess ||
+  // The zero page that kernels read in place of out-of-range inputs (never written afterwards).
+  if ((e = hipMemsetAsync(L->aux, 0, kAuxBytes, st)) != hipSuccess ||
       (e = hipMemcpyAsync(L->codebooks, codebooks, cb_bytes, hipMemcpyDeviceToDevice, st)) != hipSuccess ||
       (e = hipMemcpyAsync(L->scales, scales, (size_t)desc->d_out * 2, hipMemcpyDeviceToDevice, st)) != hipSuccess) {
     free_layer(L);
@@ -138,51 +134,77 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
   return AQMB_OK;
 }
 
-// GEMV kernel choice (measured faster in each case). Default: 4-bit codes -> the matrix-core
-// kernel at batch >= 2 and, for fp16 x at k >= 2, at batch 1 on rows of more than 512 groups;
-// their own kernel otherwise. 8-bit codes -> the matrix-core kernel at batch >= 2 and at batch 1
-// on rows of more than 512 groups (bf16 x: only at k >= 4); otherwise the direct-gather kernel (k <= 4,
-// rows <= 16384) or the lookup table kernel, as k_gemv.hip decides. AQMB_GEMV=mma uses
-// the matrix-core kernel at every batch, AQMB_GEMV=cw or =lut keep 8-bit layers on k_gemv.hip's
-// kernels and 4-bit layers on theirs (read once).
-static int gemv_mode() {
-  static const int v = [] {
-    const char* e = getenv("AQMB_GEMV");
-    if (!e) return 0;
-    if (e[0] == 'm' || e[0] == 'M') return 3;
-    if (e[0] == 'c' || e[0] == 'C' || e[0] == 'l' || e[0] == 'L') return 2;
-    return 0;
-  }();
-  return v;
-}
-
-static bool gemv_uses_mma(const Layer& L, int k, int batch, aqmb_dtype x_dtype) {
-  if (L.d.code_bits != 8 && L.d.code_bits != 4) return false;
-  if (gemv_mode() != 0) return gemv_mode() == 3;
+// GEMV kernel choice (AQMB_GEMV_AUTO), measured faster in each case: 4-bit codes -> the
+// matrix-core kernel at batch >= 2 and, for fp16 x at k >= 2, at batch 1 on rows of more than 512
+// groups; their direct-gather kernel otherwise. 8-bit codes -> the matrix-core kernel at batch >= 2
+// and at batch 1 on rows of more than 512 groups (bf16 x: only at k >= 4); otherwise the
+// direct-gather kernel when it fits (k <= 4, rows of at most 16384 inputs), else the matrix-core
+// kernel. 16-bit codes -> their direct-gather kernel.
+static aqmb_gemv_kernel gemv_auto(const Layer& L, int k, int batch, aqmb_dtype x_dtype) {
+  if (L.d.code_bits == 16) return AQMB_GEMV_DIRECT;
   const bool wide = L.S * L.J > 512;
-  if (L.d.code_bits == 4) return batch >= 2 || (x_dtype == AQMB_F16 && wide && k >= 2);
-  return batch >= 2 || (wide && (x_dtype == AQMB_F16 || k >= 4));
+  if (L.d.code_bits == 4)
+    return batch >= 2 || (x_dtype == AQMB_F16 && wide && k >= 2) ? AQMB_GEMV_MMA : AQMB_GEMV_DIRECT;
+  if (batch >= 2 || (wide && (x_dtype == AQMB_F16 || k >= 4))) return AQMB_GEMV_MMA;
+  return gemv_cw_fits(L, k, batch, x_dtype) ? AQMB_GEMV_DIRECT : AQMB_GEMV_MMA;
 }
 
-static hipError_t launch_gemv_any(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
-                                  aqmb_dtype y_dtype, hipStream_t st) {
-  if (gemv_uses_mma(L, k, batch, x_dtype)) return launch_gemv_mma(L, k, x, x_dtype, batch, y, y_dtype, st);
-  if (L.d.code_bits == 4) return launch_gemv_b4(L, k, x, x_dtype, batch, y, y_dtype, st);
-  return launch_gemv(L, k, x, x_dtype, batch, y, y_dtype, st);
+// Whether `kernel` can serve this call (AUTO always can).
+static bool gemv_kernel_serves(const Layer& L, int k, int batch, aqmb_dtype x_dtype, aqmb_gemv_kernel kernel) {
+  switch (kernel) {
+    case AQMB_GEMV_AUTO: return true;
+    case AQMB_GEMV_DIRECT: return L.d.code_bits != 8 || gemv_cw_fits(L, k, batch, x_dtype);
+    case AQMB_GEMV_MMA: return L.d.code_bits != 16;
+    case AQMB_GEMV_LUT: return L.d.code_bits == 8;
+  }
+  return false;
+}
+
+// Stream-ordered scratch for one call: allocated from the device's default pool on st and freed on
+// st after the kernels that use it, so calls on different streams never share it.
+struct CallScratch {
+  void* p = nullptr;
+  hipStream_t st = nullptr;
+  hipError_t alloc(size_t bytes, hipStream_t s) {
+    st = s;
+    return hipMallocAsync(&p, bytes, s);
+  }
+  hipError_t release() {
+    if (!p) return hipSuccess;
+    hipError_t e = hipFreeAsync(p, st);
+    p = nullptr;
+    return e;
+  }
+};
+
+static aqmb_status launch_gemv_kernel(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                                      aqmb_dtype y_dtype, aqmb_gemv_kernel kernel, hipStream_t st,
+                                      const char* where) {
+  if (kernel == AQMB_GEMV_AUTO) kernel = gemv_auto(L, k, batch, x_dtype);
+  hipError_t e = hipSuccess;
+  switch (kernel) {
+    case AQMB_GEMV_MMA: e = launch_gemv_mma(L, k, x, x_dtype, batch, y, y_dtype, st); break;
+    case AQMB_GEMV_DIRECT:
+      e = L.d.code_bits == 4    ? launch_gemv_b4(L, k, x, x_dtype, batch, y, y_dtype, st)
+          : L.d.code_bits == 16 ? launch_gemv_b16(L, k, x, x_dtype, batch, y, y_dtype, st)
+                                : launch_gemv_cw(L, k, x, x_dtype, batch, y, y_dtype, st);
+      break;
+    default: {  // AQMB_GEMV_LUT
+      CallScratch sc;
+      if ((e = sc.alloc(gemv_lut_scratch_bytes(L, batch), st)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(AQMB_ENOMEM, "%s: scratch for the lookup-table kernel: %s", where, hipGetErrorString(e));
+      }
+      e = launch_gemv_lut(L, k, x, x_dtype, batch, y, y_dtype, (float*)sc.p, st);
+      const hipError_t e2 = sc.release();
+      if (e == hipSuccess) e = e2;
+    }
+  }
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, where);
 }
 
 // GEMM tiling: small token counts take the 16-row tiling (every CU busy), larger ones the
-// 256 x 128 tiles. AQMB_GEMM=small or =big forces one (read once).
-static int gemm_mode() {
-  static const int v = [] {
-    const char* e = getenv("AQMB_GEMM");
-    if (!e) return 0;
-    if (e[0] == 's' || e[0] == 'S') return 1;
-    if (e[0] == 'b' || e[0] == 'B') return 2;
-    return 0;
-  }();
-  return v;
-}
+// large-tile kernel with the tile shape that needs the fewest rounds of workgroups.
 constexpr int kGemmSmallMax = 144;   // tokens: the 16-row tiling re-gathers per 64 tokens; measured break-even with 128 x 64 tiles near 150
 
 // k must name resident planes.
@@ -302,17 +324,32 @@ aqmb_status aqmb_get_desc(aqmb_layer_t layer, aqmb_desc* out) {
   return AQMB_OK;
 }
 
+static aqmb_status gemv_impl(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                             aqmb_dtype y_dtype, aqmb_gemv_kernel kernel, aqmb_stream_t stream, const char* where) {
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "%s: not a live layer", where);
+  aqmb_status s = validate_call(&L->d, 0, k, batch, x_dtype, y_dtype, x, y);
+  if (s != AQMB_OK) return s;
+  if ((int)kernel < AQMB_GEMV_AUTO || (int)kernel > AQMB_GEMV_LUT)
+    return fail(AQMB_EINVAL, "%s: unknown kernel %d", where, (int)kernel);
+  if (!gemv_kernel_serves(*L, k, batch, x_dtype, kernel))
+    return fail(AQMB_EUNSUPPORTED, "%s: kernel %d cannot serve B = %d, k = %d, batch = %d, d_in = %d", where,
+                (int)kernel, L->d.code_bits, k, batch, L->d.d_in);
+  if ((s = check_resident(L, k, where)) != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  return launch_gemv_kernel(*L, k, x, x_dtype, batch, y, y_dtype, kernel, (hipStream_t)stream, where);
+}
+
 aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
                       aqmb_dtype y_dtype, aqmb_stream_t stream) {
   clear_error();
-  Layer* L = (Layer*)layer;
-  if (!is_live(L)) return fail(AQMB_EINVAL, "gemv: not a live layer");
-  aqmb_status s = validate_call(&L->d, 0, k, batch, x_dtype, y_dtype, x, y);
-  if (s != AQMB_OK) return s;
-  if ((s = check_resident(L, k, "gemv")) != AQMB_OK) return s;
-  if ((s = check_device(L)) != AQMB_OK) return s;
-  hipError_t e = launch_gemv_any(*L, k, x, x_dtype, batch, y, y_dtype, (hipStream_t)stream);
-  return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv: launch");
+  return gemv_impl(layer, k, x, x_dtype, batch, y, y_dtype, AQMB_GEMV_AUTO, stream, "gemv");
+}
+
+aqmb_status aqmb_gemv_select(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                             aqmb_dtype y_dtype, aqmb_gemv_kernel kernel, aqmb_stream_t stream) {
+  clear_error();
+  return gemv_impl(layer, k, x, x_dtype, batch, y, y_dtype, kernel, stream, "gemv_select");
 }
 
 aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, const void* x, aqmb_dtype x_dtype,
@@ -341,36 +378,55 @@ aqmb_status aqmb_gemv_multi(const aqmb_layer_t* layers, int n_layers, int k, con
   // taller layers run their persistent kernel, one launch each); otherwise one launch per layer.
   bool per_layer = false, all_mma = true;
   for (int i = 0; i < n_layers; ++i) {
-    const bool mma = gemv_uses_mma(*Ls[i], k, batch, x_dtype);
-    per_layer = per_layer || Ls[i]->d.code_bits == 4 || mma;
+    const aqmb_gemv_kernel kern = gemv_auto(*Ls[i], k, batch, x_dtype);
+    const bool mma = kern == AQMB_GEMV_MMA;
+    per_layer = per_layer || Ls[i]->d.code_bits != 8 || kern != AQMB_GEMV_DIRECT;
     all_mma = all_mma && mma && Ls[i]->d.code_bits == Ls[0]->d.code_bits &&
               (Ls[i]->d.d_out + 15) / 16 <= Ls[i]->n_cu;
   }
-  hipError_t e = hipSuccess;
   if (all_mma && n_layers >= 2) {
-    e = launch_gemv_mma_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
-  } else if (per_layer) {
-    for (int i = 0; i < n_layers && e == hipSuccess; ++i)
-      e = launch_gemv_any(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, (hipStream_t)stream);
-  } else {
-    e = launch_gemv_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
+    hipError_t e = launch_gemv_mma_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
+    return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv_multi: launch");
   }
+  if (per_layer) {
+    for (int i = 0; i < n_layers; ++i) {
+      s = launch_gemv_kernel(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, AQMB_GEMV_AUTO, (hipStream_t)stream,
+                             "gemv_multi: launch");
+      if (s != AQMB_OK) return s;
+    }
+    return AQMB_OK;
+  }
+  hipError_t e = launch_gemv_multi(Ls, n_layers, k, x, x_dtype, batch, ys, y_dtype, (hipStream_t)stream);
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemv_multi: launch");
+}
+
+static aqmb_status gemm_impl(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
+                             aqmb_gemm_tiling tiling, aqmb_stream_t stream, const char* where) {
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "%s: not a live layer", where);
+  aqmb_status s = validate_call(&L->d, 1, k, n_tokens, AQMB_BF16, y_dtype, X, Y);
+  if (s != AQMB_OK) return s;
+  if ((int)tiling < AQMB_GEMM_AUTO || (int)tiling > AQMB_GEMM_128x64)
+    return fail(AQMB_EINVAL, "%s: unknown tiling %d", where, (int)tiling);
+  if ((s = check_resident(L, k, where)) != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  const bool small = tiling == AQMB_GEMM_ROWS16 || (tiling == AQMB_GEMM_AUTO && n_tokens <= kGemmSmallMax);
+  const int tile = tiling == AQMB_GEMM_256x128 ? 0 : tiling == AQMB_GEMM_128x128 ? 1 : tiling == AQMB_GEMM_128x64 ? 2 : -1;
+  hipError_t e = small ? launch_gemm_small(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream)
+                       : launch_gemm(*L, k, X, n_tokens, Y, y_dtype, tile, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, where);
 }
 
 aqmb_status aqmb_gemm(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
                       aqmb_stream_t stream) {
   clear_error();
-  Layer* L = (Layer*)layer;
-  if (!is_live(L)) return fail(AQMB_EINVAL, "gemm: not a live layer");
-  aqmb_status s = validate_call(&L->d, 1, k, n_tokens, AQMB_BF16, y_dtype, X, Y);
-  if (s != AQMB_OK) return s;
-  if ((s = check_resident(L, k, "gemm")) != AQMB_OK) return s;
-  if ((s = check_device(L)) != AQMB_OK) return s;
-  const bool small = gemm_mode() == 1 || (gemm_mode() == 0 && n_tokens <= kGemmSmallMax);
-  hipError_t e = small ? launch_gemm_small(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream)
-                       : launch_gemm(*L, k, X, n_tokens, Y, y_dtype, (hipStream_t)stream);
-  return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemm: launch");
+  return gemm_impl(layer, k, X, n_tokens, Y, y_dtype, AQMB_GEMM_AUTO, stream, "gemm");
+}
+
+aqmb_status aqmb_gemm_select(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
+                             aqmb_gemm_tiling tiling, aqmb_stream_t stream) {
+  clear_error();
+  return gemm_impl(layer, k, X, n_tokens, Y, y_dtype, tiling, stream, "gemm_select");
 }
 
 aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* X,
@@ -383,7 +439,16 @@ aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype
   aqmb_status s = validate_call(&L->d, 3, 0, n, x_dtype, w_dtype, X, D);
   if (s != AQMB_OK) return s;
   if ((s = check_device(L)) != AQMB_OK) return s;
-  hipError_t e = launch_distortion(*L, W, X, n, D, (hipStream_t)stream);
+  const hipStream_t st = (hipStream_t)stream;
+  CallScratch sc;
+  hipError_t e = sc.alloc(distortion_scratch_bytes(), st);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AQMB_ENOMEM, "prefix_distortion: scratch: %s", hipGetErrorString(e));
+  }
+  e = launch_distortion(*L, W, X, n, D, (double*)sc.p, st);
+  const hipError_t e2 = sc.release();
+  if (e == hipSuccess) e = e2;
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "prefix_distortion: launch");
 }
 

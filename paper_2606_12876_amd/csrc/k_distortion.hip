@@ -61,7 +61,7 @@ template <int M, int CB> struct Frag {
 };
 }  // namespace dist
 
-size_t distortion_workspace_floats() { return (size_t)dist::kMaxGrid * 8 * 2; }
+size_t distortion_scratch_bytes() { return (size_t)dist::kMaxGrid * 8 * sizeof(double); }
 
 struct DistArgs {
   const unsigned char* codes;
@@ -306,15 +306,16 @@ static hipError_t launch_dist_m(DistArgs& a, int code_bits, hipStream_t st, int*
   return code_bits == 4 ? launch_dist_mc<M, 4>(a, st, grid_out) : launch_dist_mc<M, 8>(a, st, grid_out);
 }
 
-hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n, double* D, hipStream_t st) {
+hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n, double* D, double* scratch,
+                             hipStream_t st) {
   DistArgs a{};
   a.codes = L.codes;
   a.codebooks = L.codebooks;
   a.scales = L.scales;
   a.W = (const uint16_t*)W;
   a.X = (const uint16_t*)X;
-  a.partials = (double*)(L.ws + 256);
-  a.zero_page = L.ws;
+  a.partials = scratch;                            // [grid][8], every slot written before it is read
+  a.zero_page = L.zero_page();
   a.plane_bytes = L.plane_bytes;
   a.d_out = L.d.d_out;
   a.d_in = L.d.d_in;

@@ -329,18 +329,12 @@ static void launch_kcm(const Layer& L, const void* X, int n_tokens, void* Y, aqm
         L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y, n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
 }
 
-// Tile shape: 0 = 256 tokens x 128 rows, 1 = 128 x 128, 2 = 128 x 64. AQMB_GEMM_TILE=256|128|64
-// forces one (read once). Otherwise the shape with the least estimated time: rounds of workgroups
-// (one workgroup per CU) times the shape's measured cost per workgroup relative to the largest
-// tile (4096 x 4096 layer, one round: 1, 0.9, 0.6).
-static int gemm_tile(const Layer& L, int n_tokens) {
-  static const int forced = [] {
-    const char* e = getenv("AQMB_GEMM_TILE");
-    if (!e) return -1;
-    const int v = atoi(e);
-    return v == 256 ? 0 : v == 128 ? 1 : v == 64 ? 2 : -1;
-  }();
-  if (forced >= 0) return forced;
+// Tile shape: 0 = 256 tokens x 128 rows, 1 = 128 x 128, 2 = 128 x 64. Unless the caller names one,
+// the shape with the least estimated time: rounds of workgroups (one workgroup per CU) times the
+// shape's measured cost per workgroup relative to the largest tile (4096 x 4096 layer, one round:
+// 1, 0.9, 0.6).
+static int gemm_tile(const Layer& L, int n_tokens, int forced) {
+  if (forced >= 0 && forced <= 2) return forced;
   const int bm[3] = {256, 128, 128}, bn[3] = {128, 128, 64};
   const double rel[3] = {1.0, 0.9, 0.6};
   const long long ncu = L.n_cu > 0 ? L.n_cu : 256;
@@ -355,8 +349,9 @@ static int gemm_tile(const Layer& L, int n_tokens) {
 }
 
 template <int K, int CB>
-static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
-  switch (gemm_tile(L, n_tokens)) {
+static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, int tile,
+                      hipStream_t st) {
+  switch (gemm_tile(L, n_tokens, tile)) {
     case 0: launch_kcm<K, CB, 256, 128>(L, X, n_tokens, Y, y_dtype, st); break;
     case 1: launch_kcm<K, CB, 128, 128>(L, X, n_tokens, Y, y_dtype, st); break;
     default: launch_kcm<K, CB, 128, 64>(L, X, n_tokens, Y, y_dtype, st); break;
@@ -364,22 +359,23 @@ static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb
 }
 
 template <int K>
-static void launch_k(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
-  if (L.d.code_bits == 4) launch_kc<K, 4>(L, X, n_tokens, Y, y_dtype, st);
-  else launch_kc<K, 8>(L, X, n_tokens, Y, y_dtype, st);
+static void launch_k(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, int tile,
+                     hipStream_t st) {
+  if (L.d.code_bits == 4) launch_kc<K, 4>(L, X, n_tokens, Y, y_dtype, tile, st);
+  else launch_kc<K, 8>(L, X, n_tokens, Y, y_dtype, tile, st);
 }
 
-hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
+hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, int tile,
                        hipStream_t st) {
   switch (k) {
-    case 1: launch_k<1>(L, X, n_tokens, Y, y_dtype, st); break;
-    case 2: launch_k<2>(L, X, n_tokens, Y, y_dtype, st); break;
-    case 3: launch_k<3>(L, X, n_tokens, Y, y_dtype, st); break;
-    case 4: launch_k<4>(L, X, n_tokens, Y, y_dtype, st); break;
-    case 5: launch_k<5>(L, X, n_tokens, Y, y_dtype, st); break;
-    case 6: launch_k<6>(L, X, n_tokens, Y, y_dtype, st); break;
-    case 7: launch_k<7>(L, X, n_tokens, Y, y_dtype, st); break;
-    default: launch_k<8>(L, X, n_tokens, Y, y_dtype, st); break;
+    case 1: launch_k<1>(L, X, n_tokens, Y, y_dtype, tile, st); break;
+    case 2: launch_k<2>(L, X, n_tokens, Y, y_dtype, tile, st); break;
+    case 3: launch_k<3>(L, X, n_tokens, Y, y_dtype, tile, st); break;
+    case 4: launch_k<4>(L, X, n_tokens, Y, y_dtype, tile, st); break;
+    case 5: launch_k<5>(L, X, n_tokens, Y, y_dtype, tile, st); break;
+    case 6: launch_k<6>(L, X, n_tokens, Y, y_dtype, tile, st); break;
+    case 7: launch_k<7>(L, X, n_tokens, Y, y_dtype, tile, st); break;
+    default: launch_k<8>(L, X, n_tokens, Y, y_dtype, tile, st); break;
   }
   return hipGetLastError();
 }

@@ -208,7 +208,7 @@ hipError_t launch_gemm_small(const Layer& L, int k, const void* X, int n_tokens,
   a.scales = L.scales;
   a.X = (const uint16_t*)X;
   a.Y = Y;
-  a.zero_page = L.ws;                                       // the first KiB of the workspace stays zero
+  a.zero_page = L.zero_page();
   a.plane_bytes = L.plane_bytes;
   a.d_out = L.d.d_out;
   a.d_in = L.d.d_in;

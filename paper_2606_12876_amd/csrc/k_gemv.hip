@@ -1,22 +1,22 @@
-// Decode GEMV: y[b][i] = s_i * sum_j sum_{m<k} <x[b, group j], C_m[code(m,i,j)]>.
+// Decode GEMV of layers with 8-bit codes (256-codeword codebooks):
+//   y[b][i] = s_i * sum_j sum_{m<k} <x[b, group j], C_m[code(m,i,j)]>
+// (section 5: the partial reconstruction from the first k codebooks, applied as a product).
 //
-// Work split: a workgroup owns a chunk of rows and one slice (16 consecutive groups for
-// 8-bit codes, 8 for 16-bit codes); every row's sum over slices is a split-K reduction.
-// Each workgroup writes fp32 partial sums for its rows to the layer's workspace; a second,
-// small kernel adds the partials of all slices in slice order, applies the row scale and
-// rounds once to the output dtype. The kernel boundary orders the two phases (no
-// device-wide fences inside the main kernel), and the result does not depend on scheduling.
+// Direct gathers (gemv_cw_kernel and its persistent and multi-layer forms, the default at batch 1):
+// the codebooks are replicated in LDS and every code costs one 16-byte codeword read and its dot
+// product with x, accumulated per row; no partial sums leave the workgroup.
 //
-// 8-bit codes (256 codewords): lookup tables in LDS. For the slice's groups and every used
-// plane m, LUT_m[j][c] = <x[b, group j], C_m[c]> is built once per workgroup (one codeword per
-// thread, fp32 dot products of exact fp16 products), then every code byte costs one LDS read
-// and one fp32 add. Rows map to threads, so each thread's accumulators need no cross-lane
-// reduction. Code planes m >= k are never read.
+// Lookup tables (gemv_lut_kernel + gemv_reduce_kernel, chosen explicitly): a workgroup owns a
+// chunk of rows and one slice (16 consecutive groups); for the slice's groups and every used plane
+// m, LUT_m[j][c] = <x[b, group j], C_m[c]> is built once per workgroup (one codeword per thread,
+// fp32 dot products of exact fp16 products), then every code byte costs one LDS read and one fp32
+// add. Rows map to threads, so each thread's accumulators need no cross-lane reduction. Every
+// row's sum over slices is a split-K reduction: each workgroup writes fp32 partial sums for its
+// rows to caller-provided scratch and a second, small kernel adds the partials of all slices in
+// slice order, applies the row scale and rounds once to the output dtype. The kernel boundary
+// orders the two phases, and the result does not depend on scheduling.
 //
-// 16-bit codes (65536 codewords, 1 MiB per codebook): codewords are gathered from global
-// memory (resident in L2), summed over planes, and dotted with x staged in LDS.
-#include <cstdlib>
-
+// Code planes m >= k are never read.
 #include "device.h"
 #include "launch.h"
 
@@ -36,7 +36,7 @@ struct GemvArgs {
   const uint16_t* scales;
   const void* x;
   void* y;
-  float* partials;     // [S][batch][d_out]
+  float* partials;     // [S][batch][d_out] (lookup-table kernel: caller's scratch)
   const void* zero_page;  // 1 KiB of zeros, never written
   size_t plane_bytes;
   int d_out, d_in, G, S, k, batch;
@@ -46,9 +46,8 @@ struct GemvArgs {
   int n_cu;            // compute units (host side: the persistent grid)
 };
 
-size_t gemv_workspace_floats(const aqmb_desc& d, int G, int S) {
-  (void)G;
-  return 256 + (size_t)S * AQMB_MAX_BATCH * d.d_out + 64;   // zero page, then partial sums
+size_t gemv_lut_scratch_bytes(const Layer& L, int batch) {
+  return (size_t)L.S * batch * L.d.d_out * sizeof(float);   // [S][batch][d_out] partial sums
 }
 
 // Partial sums of one batch tile of this workgroup's rows.
@@ -263,77 +262,6 @@ __global__ __launch_bounds__(kThreads) void gemv_lut_kernel(GemvArgs a) {
   }
 }
 
-// 16-bit codes: codewords from global memory. One slice = 8 groups per row.
-template <int XDT, int NB>
-__global__ __launch_bounds__(kThreads) void gemv_b16_kernel(GemvArgs a) {
-  __shared__ float xs[AQMB_MAX_BATCH][64];  // x of the slice's 8 groups, fp32
-  const int tid = threadIdx.x;
-  const int slice = blockIdx.y;
-  const int row0 = blockIdx.x * kRowsPerWG;
-  const int k = a.k;
-  for (int q = tid; q < a.batch * 64; q += kThreads) {
-    const int b = q / 64, e = q % 64;
-    const int col = slice * 64 + e;
-    float v = 0.f;
-    if (col < a.d_in) {
-      const uint16_t bits = ((const uint16_t*)a.x)[(size_t)b * a.d_in + col];
-      v = XDT == AQMB_F16 ? f16_to_f32(bits) : __builtin_bit_cast(float, (uint32_t)bits << 16);
-    }
-    xs[b][e] = v;
-  }
-  uint4 v[kRowsPerThread][8];
-#pragma unroll
-  for (int r = 0; r < kRowsPerThread; ++r) {
-    const int row = row0 + tid + r * kThreads;
-#pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      v[r][m] = make_uint4(0, 0, 0, 0);
-      if (m < k && row < a.d_out)
-        v[r][m] = load_stream16(
-            (a.codes + m * a.plane_bytes + ((size_t)slice * a.d_out + row) * 16));
-    }
-  }
-  __syncthreads();
-  float acc[kRowsPerThread][NB];
-#pragma unroll
-  for (int r = 0; r < kRowsPerThread; ++r)
-#pragma unroll
-    for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
-  const uint4* cb = (const uint4*)a.codebooks;
-#pragma unroll
-  for (int r = 0; r < kRowsPerThread; ++r) {
-    if (row0 + tid + r * kThreads >= a.d_out) continue;
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-      const int j = slice * 8 + jj;
-      if (j >= a.G) continue;
-      float w[8];
-#pragma unroll
-      for (int m = 0; m < 8; ++m) {
-        if (m < k) {
-          const uint32_t word = (&v[r][m].x)[jj >> 1];
-          const uint32_t c = (word >> (16 * (jj & 1))) & 0xFFFFu;
-          const uint4 cwv = cb[((size_t)m << 16) + c];
-          const float f[8] = {f16lo(cwv.x), f16hi(cwv.x), f16lo(cwv.y), f16hi(cwv.y),
-                              f16lo(cwv.z), f16hi(cwv.z), f16lo(cwv.w), f16hi(cwv.w)};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) w[e] = m == 0 ? f[e] : w[e] + f[e];
-        }
-      }
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        if (b < a.batch) {
-          float s = acc[r][b];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) s = __builtin_fmaf(xs[b][jj * 8 + e], w[e], s);
-          acc[r][b] = s;
-        }
-      }
-    }
-  }
-  store_partials<NB>(a, 0, acc);
-}
-
 // Direct-gather GEMV for 8-bit codes: one kernel, no partial sums. A workgroup of 1024 threads
 // owns 16 rows; the 64 threads of a row split its groups (thread `part` takes groups
 // 512 u + 8 part .. + 7 for u = 0 .. UB - 1), gather each code's codeword from the codebooks held
@@ -344,7 +272,7 @@ __global__ __launch_bounds__(kThreads) void gemv_b16_kernel(GemvArgs a) {
 // at (c * nrep + r) * 16 bytes: lane l reads replica l % nrep, which spreads the random 16-byte
 // reads of a wave over nrep bank groups instead of colliding at random.
 // x is staged in LDS once per batch tile of NB rows by direct global->LDS loads, each row padded
-// with zeros (read from the zero page at the head of the layer workspace) up to the padded group
+// with zeros (read from the layer's zero page) up to the padded group
 // count, so the group loops need no bounds tests: padding groups have code 0 and x = 0.
 // Issue order: x, then the codebooks, then every code word the thread needs (all planes, all
 // blocks, addresses clamped into the layer so that each thread issues the same loads). Code
@@ -864,9 +792,13 @@ static hipError_t launch_cw(const GemvArgs& a, hipStream_t st) {
 }
 
 // The direct-gather kernel covers k <= 4 and d_in <= 16384 (the code words of a thread's
-// groups stay in registers); other shapes take the lookup-table path.
+// groups stay in registers); the matrix-core and lookup-table kernels take the other shapes.
 static bool cw_fits(int K, int batch, int S, bool bf16) {
   return K <= 4 && cw_blocks(S) <= kCwMaxBlocks && cw_nrep(K, cw_nb(batch), S, bf16) > 0;
+}
+
+bool gemv_cw_fits(const Layer& L, int k, int batch, aqmb_dtype x_dtype) {
+  return L.d.code_bits == 8 && cw_fits(k, batch, L.S, x_dtype == AQMB_BF16);
 }
 
 template <int K, int XDT>
@@ -889,12 +821,7 @@ static hipError_t launch_cw_any(const GemvArgs& a, hipStream_t st) {
 }
 
 template <int XDT>
-static void launch_x(const GemvArgs& a, bool b16, dim3 grid, hipStream_t st) {
-  if (b16) {
-    if (a.batch <= 4) gemv_b16_kernel<XDT, 4><<<grid, kThreads, 0, st>>>(a);
-    else gemv_b16_kernel<XDT, AQMB_MAX_BATCH><<<grid, kThreads, 0, st>>>(a);
-    return;
-  }
+static void launch_lut_k(const GemvArgs& a, dim3 grid, hipStream_t st) {
   switch (a.k) {
     case 1: launch_lut<1, XDT>(a, grid, st); break;
     case 2: launch_lut<2, XDT>(a, grid, st); break;
@@ -907,27 +834,15 @@ static void launch_x(const GemvArgs& a, bool b16, dim3 grid, hipStream_t st) {
   }
 }
 
-// 8-bit GEMV variant: 1 = direct codeword gather (default), 0 = split-K lookup tables.
-// AQMB_GEMV=lut|cw overrides (read once).
-static int gemv_variant() {
-  static const int v = [] {
-    const char* e = getenv("AQMB_GEMV");
-    if (e && (e[0] == 'l' || e[0] == 'L')) return 0;
-    return 1;
-  }();
-  return v;
-}
-
-hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
-                       aqmb_dtype y_dtype, hipStream_t st) {
-  GemvArgs a;
+static GemvArgs gemv_args(const Layer& L, int k, const void* x, int batch, void* y, aqmb_dtype y_dtype) {
+  GemvArgs a{};
   a.codes = L.codes;
   a.codebooks = L.codebooks;
   a.scales = L.scales;
   a.x = x;
   a.y = y;
-  a.zero_page = L.ws;                    // the first KiB of the workspace stays zero
-  a.partials = L.ws + 256;
+  a.zero_page = L.zero_page();
+  a.partials = nullptr;
   a.plane_bytes = L.plane_bytes;
   a.d_out = L.d.d_out;
   a.d_in = L.d.d_in;
@@ -937,20 +852,29 @@ hipError_t launch_gemv(const Layer& L, int k, const void* x, aqmb_dtype x_dtype,
   a.batch = batch;
   a.y_dtype = (int)y_dtype;
   a.n_cu = L.n_cu;
+  return a;
+}
+
+hipError_t launch_gemv_cw(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                          aqmb_dtype y_dtype, hipStream_t st) {
+  if (!gemv_cw_fits(L, k, batch, x_dtype)) return hipErrorInvalidValue;   // the caller checks first
+  const GemvArgs a = gemv_args(L, k, x, batch, y, y_dtype);
+  return x_dtype == AQMB_F16 ? launch_cw_any<AQMB_F16>(a, st) : launch_cw_any<AQMB_BF16>(a, st);
+}
+
+hipError_t launch_gemv_lut(const Layer& L, int k, const void* x, aqmb_dtype x_dtype, int batch, void* y,
+                           aqmb_dtype y_dtype, float* scratch, hipStream_t st) {
+  GemvArgs a = gemv_args(L, k, x, batch, y, y_dtype);
+  a.partials = scratch;
   const dim3 grid((L.d.d_out + kRowsPerWG - 1) / kRowsPerWG, L.S);
-  const bool b16 = L.d.code_bits == 16;
-  if (!b16 && gemv_variant() == 1 && cw_fits(k, batch, L.S, x_dtype == AQMB_BF16)) {   // direct gather: one kernel
-    return x_dtype == AQMB_F16 ? launch_cw_any<AQMB_F16>(a, st) : launch_cw_any<AQMB_BF16>(a, st);
-  }
-  if (x_dtype == AQMB_F16) launch_x<AQMB_F16>(a, b16, grid, st);
-  else launch_x<AQMB_BF16>(a, b16, grid, st);
+  if (x_dtype == AQMB_F16) launch_lut_k<AQMB_F16>(a, grid, st);
+  else launch_lut_k<AQMB_BF16>(a, grid, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int items = batch * ((L.d.d_out + 3) / 4);
   gemv_reduce_kernel<<<(items + 63) / 64, kReduceThreads, 0, st>>>(a);
   return hipGetLastError();
 }
-
 
 template <int K, int NB, int XDT>
 static hipError_t launch_multi_nb(GemvMultiArgs a, int grid, hipStream_t st) {
@@ -998,12 +922,11 @@ hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x
   // several blocks do not fit in registers beyond one plane); otherwise the layers are launched
   // one after another.
   const Layer& L0 = *Ls[0];
-  bool one = batch <= 4 && gemv_variant() == 1 && cw_fits(k, batch, L0.S, x_dtype == AQMB_BF16) &&
-             (cw_blocks(L0.S) == 1 || k == 1);
+  bool one = batch <= 4 && cw_fits(k, batch, L0.S, x_dtype == AQMB_BF16) && (cw_blocks(L0.S) == 1 || k == 1);
   for (int i = 0; i < n && one; ++i) one = Ls[i]->d.code_bits == 8;
   if (!one) {
     for (int i = 0; i < n; ++i) {
-      hipError_t e = launch_gemv(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, st);
+      hipError_t e = launch_gemv_cw(*Ls[i], k, x, x_dtype, batch, ys[i], y_dtype, st);
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -1022,7 +945,7 @@ hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x
     grid = a.L[i].row_blocks > grid ? a.L[i].row_blocks : grid;
   }
   a.x = x;
-  a.zero_page = L0.ws;
+  a.zero_page = L0.zero_page();
   a.n_layers = n;
   a.d_in = L0.d.d_in;
   a.S = L0.S;

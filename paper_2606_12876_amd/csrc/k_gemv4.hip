@@ -266,7 +266,7 @@ hipError_t launch_gemv_b4(const Layer& L, int k, const void* x, aqmb_dtype x_dty
   a.scales = L.scales;
   a.x = x;
   a.y = y;
-  a.zero_page = L.ws;                                       // the first KiB of the workspace stays zero
+  a.zero_page = L.zero_page();
   a.plane_bytes = L.plane_bytes;
   a.d_out = L.d.d_out;
   a.d_in = L.d.d_in;

@@ -563,7 +563,7 @@ static GemvMmaArgs mma_args(const Layer& L, const void* x, int batch, void* y, a
   a.scales = L.scales;
   a.x = (const uint16_t*)x;
   a.y = y;
-  a.zero_page = L.ws;                                       // the first KiB of the workspace stays zero
+  a.zero_page = L.zero_page();
   a.plane_bytes = L.plane_bytes;
   a.d_out = L.d.d_out;
   a.d_in = L.d.d_in;

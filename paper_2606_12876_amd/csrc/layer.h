@@ -13,6 +13,8 @@ namespace aqmb {
 // are padding (code 0) and contribute nothing. Planes stay outermost: level k
 // reads the first k * plane_bytes bytes only.
 constexpr int kSliceBytes = 16;
+constexpr size_t kZeroPageBytes = 1024;
+constexpr size_t kAuxBytes = kZeroPageBytes + 256;
 
 struct Layer {
   uint32_t magic;
@@ -27,8 +29,12 @@ struct Layer {
   unsigned char* codes;  // [resident][S][d_out][16 bytes]
   uint16_t* codebooks;   // [M][2^B][g] fp16
   uint16_t* scales;      // [d_out] fp16
-  float* ws;             // gemv split-K partial sums
-  size_t ws_floats;
+  // 1 KiB of zeros that kernels read in place of inputs past their end (never written after
+  // create), followed by one int that the code upload of create / load_planes uses to flag 4-bit
+  // codes above 15. Compute calls never write layer memory, so they may overlap on any streams.
+  unsigned char* aux;
+  const void* zero_page() const { return aux; }
+  int* upload_flag() const { return (int*)(aux + kZeroPageBytes); }
 };
 
 constexpr uint32_t kMagic = 0x41514D42u;  // "AQMB"

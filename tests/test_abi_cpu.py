@@ -124,6 +124,8 @@ def test_bad_handles_rejected_without_gpu():
     assert A.lib.aqmb_gemv(bogus, 1, 16, 0, 1, 32, 0, None) == A.Status.EINVAL
     assert A.lib.aqmb_gemm(bogus, 1, 16, 1, 32, 1, None) == A.Status.EINVAL
     assert A.lib.aqmb_dequant(bogus, 1, 32, 0, None) == A.Status.EINVAL
+    assert A.lib.aqmb_gemv_select(bogus, 1, 16, 0, 1, 32, 0, 0, None) == A.Status.EINVAL
+    assert A.lib.aqmb_gemm_select(bogus, 1, 16, 1, 32, 1, 0, None) == A.Status.EINVAL
     assert A.lib.aqmb_prefix_distortion(bogus, 16, 0, 32, 0, 8, 64, None) == A.Status.EINVAL
     assert "live" in A.last_error()
     assert A.lib.aqmb_beam_search(None, 1, 1, 16, 16, 16, 16, None, None) == A.Status.EINVAL   # null desc

@@ -101,14 +101,13 @@ def test_gemm_matches_oracle(n):
                 check_close(out_values(Y), ref, ydt, f"gemm n={n} k={k} {ydt}")
 
 
-def test_gemm_full_size_sampled():
+def test_gemm_full_size():
     """The prefill shape (2048 tokens x 4096 x 4096, 4 codebooks of 16 codewords): every output
-    of 24 sampled token rows against the reference, at k = 1 and 4."""
+    against the reference, at k = 1 and 4."""
     L = make_layer(LayerSpec("g4full", 4096, 4096, M=4, B=4, seed=345, act_dtype="bf16"))
     n = 2048
     Xbits = make_activations(L, n, "bf16")
-    rows = np.sort(np.random.default_rng(9).choice(n, 24, replace=False))
-    X = act_values(Xbits[rows], "bf16")
+    X = act_values(Xbits, "bf16")
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
         Xd = to_dev(Xbits).view(torch.bfloat16)
         for k in (1, 4):
@@ -116,7 +115,7 @@ def test_gemm_full_size_sampled():
             A.gemm(gl.handle, k, Xd, n, Y, A.DType.BF16)
             torch.cuda.synchronize()
             ref = oracle.gemm_reference(X, L.codes, L.codebooks, L.scales, k)
-            check_close(out_values(Y)[rows], ref, "bf16", f"gemm 2048x4096x4096 B=4 k={k}")
+            check_close(out_values(Y), ref, "bf16", f"gemm 2048x4096x4096 B=4 k={k}")
 
 
 @pytest.mark.parametrize("M", [4, 6, 8])

@@ -19,7 +19,7 @@ if not torch.cuda.is_available():  # collected on CPU hosts too; every test here
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_2606_12876_amd as A  # noqa: E402
-from gpu_helpers import GpuLayer, out_values, check_close, to_dev, TORCH_DT, A_DT, act_values  # noqa: E402
+from gpu_helpers import GpuLayer, abs_terms, out_values, check_close, to_dev, TORCH_DT, A_DT, act_values  # noqa: E402
 
 
 def _f64(L):
@@ -71,16 +71,17 @@ def test_dequant_bit_exact(spec, dt):
                                   ref.view(np.uint32) if dt == "f32" else ref), (spec.name, k, dt)
 
 
-def test_dequant_workload_layers_bit_exact():
-    for name in ("c1", "c2", "c4"):
-        spec = config(name)
-        L = make_layer(spec)
-        with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
-            for k in spec.ks:
-                for dt in ("bf16", "f16"):
-                    got = run_dequant(gl, k, dt)
-                    ref = oracle.dequant_canonical(L.codes, L.codebooks, L.scales, k, dt)
-                    assert np.array_equal(got, ref), (name, k, dt)
+@pytest.mark.parametrize("name", ["c1", "c2", "c3_up", "c3_down", "c4"])
+def test_dequant_workload_layers_bit_exact(name):
+    spec = config(name)
+    L = make_layer(spec)
+    dts = ("bf16", "f16") if not name.startswith("c3") else ("bf16",)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for k in spec.ks:
+            for dt in dts:
+                got = run_dequant(gl, k, dt)
+                ref = oracle.dequant_canonical(L.codes, L.codebooks, L.scales, k, dt)
+                assert np.array_equal(got, ref), (name, k, dt)
 
 
 def test_dequant_index_revealing():
@@ -136,9 +137,10 @@ def test_gemv_small_shapes(spec, batches, xdt):
             x = act_values(xbits, xdt)
             for k in range(1, spec.M + 1):
                 ref = oracle.linear(x, L.codes, C, s, k)
+                T = abs_terms(x, L.codes, C, s, k)
                 for ydt in ("f32", "f16", "bf16"):
                     got = run_gemv(gl, k, xbits, xdt, ydt)
-                    check_close(got, ref, ydt, f"{spec.name} b={b} k={k} {xdt}->{ydt}")
+                    check_close(got, ref, ydt, f"{spec.name} b={b} k={k} {xdt}->{ydt}", terms=T, n_terms=k * spec.d_in)
 
 
 @pytest.mark.parametrize("name", ["c1", "c2", "c3_up", "c3_down", "c4"])
@@ -176,7 +178,8 @@ def test_gemv_wide_rows(d_in, xdt):
             for k in range(1, 5):
                 ref = oracle.linear(x, L.codes, C, s, k)
                 got = run_gemv(gl, k, xbits, xdt, ydt)
-                check_close(got, ref, ydt, f"d_in={d_in} b={b} k={k} {xdt}")
+                check_close(got, ref, ydt, f"d_in={d_in} b={b} k={k} {xdt}",
+                            terms=abs_terms(x, L.codes, C, s, k), n_terms=k * d_in)
 
 
 @pytest.mark.parametrize("xdt", ["f16", "bf16"])
@@ -194,9 +197,10 @@ def test_gemv_more_row_blocks_than_cus(xdt):
             x = act_values(xbits, xdt)
             for k in range(1, 5):
                 ref = oracle.linear(x, L.codes, C, s, k)
+                T = abs_terms(x, L.codes, C, s, k)
                 for ydt in ("f32", xdt):
                     got = run_gemv(gl, k, xbits, xdt, ydt)
-                    check_close(got, ref, ydt, f"5000 rows {xdt} b={b} k={k} y={ydt}")
+                    check_close(got, ref, ydt, f"5000 rows {xdt} b={b} k={k} y={ydt}", terms=T, n_terms=k * 520)
 
 
 def test_gemv_plane_linearity():

@@ -1,8 +1,10 @@
 """Run-time loading and dropping of code planes (GPU).
 
-A layer created with only its first r planes, then grown and shrunk, must give bit-identical
-results to a layer created with all planes at every resident level, and refuse levels that need
-planes it does not hold (the multi-bitwidth property: level k reads planes 0..k-1 only).
+A layer created with only its first r planes, then grown and shrunk, must at every resident level
+match the oracle (dequant bit-exact to the canonical rounding, GEMV and GEMM within the parity
+tolerance) and give bit-identical results to a layer created with all planes, and it must refuse
+levels that need planes it does not hold (the multi-bitwidth property: level k reads planes
+0..k-1 only).
 """
 from __future__ import annotations
 
@@ -20,7 +22,7 @@ if not torch.cuda.is_available():  # collected on CPU hosts too; every test here
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_2606_12876_amd as A  # noqa: E402
-from gpu_helpers import GpuLayer, to_dev  # noqa: E402
+from gpu_helpers import GpuLayer, abs_terms, check_close, out_values, to_dev  # noqa: E402
 
 
 def _outputs(h, k, x, d_out, d_in, X):
@@ -45,7 +47,21 @@ def test_grow_and_shrink_match_full_layer(B):
     desc = A.make_desc(spec.d_out, spec.d_in, M, B)
     xb = make_activations(L, 3, "f16")
     x = to_dev(xb).view(torch.float16)
-    X = to_dev(make_activations(L, 70, "bf16")).view(torch.bfloat16) if B == 8 else None
+    Xbits = make_activations(L, 70, "bf16") if B != 16 else None
+    X = to_dev(Xbits).view(torch.bfloat16) if B != 16 else None
+    C, s = formats.f16_bits_to_f64(L.codebooks), formats.f16_bits_to_f64(L.scales)
+    x64 = formats.f16_bits_to_f64(xb)
+
+    def oracle_check(got, k):
+        """The prefix layer's outputs at level k against the oracle."""
+        ref = oracle.linear(x64, L.codes, C, s, k)
+        check_close(out_values(got[0]), ref, "f32", f"prefix B={B} gemv k={k}",
+                    terms=abs_terms(x64, L.codes, C, s, k), n_terms=k * spec.d_in)
+        wref = oracle.dequant_canonical(L.codes, L.codebooks, L.scales, k, "bf16")
+        assert np.array_equal(got[1].cpu().view(torch.int16).numpy().view(np.uint16), wref), f"prefix B={B} dequant k={k}"
+        if X is not None:
+            gref = oracle.gemm_reference(formats.bf16_bits_to_f64(Xbits), L.codes, L.codebooks, L.scales, k)
+            check_close(out_values(got[2]), gref, "f32", f"prefix B={B} gemm k={k}")
     cb, sc = to_dev(L.codebooks), to_dev(L.scales)
     with GpuLayer(L.codes, L.codebooks, L.scales) as full:
         ref = {k: _outputs(full.handle, k, x, spec.d_out, spec.d_in, X) for k in range(1, M + 1)}
@@ -54,6 +70,7 @@ def test_grow_and_shrink_match_full_layer(B):
             assert A.resident_planes(h) == 1
             def same(k):
                 got = _outputs(h, k, x, spec.d_out, spec.d_in, X)
+                oracle_check(got, k)
                 for a, b in zip(got, ref[k]):
                     assert torch.equal(a, b), f"B={B} k={k}"
             def refused(k):
