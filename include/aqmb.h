@@ -258,6 +258,20 @@ aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype,
 aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* Xt,
                                    aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream);
 
+/*
+ * aqmb_prefix_distortion without any device allocation, for callers that cannot allocate (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same arguments,
+ * kernels, arithmetic and result as aqmb_prefix_distortion. Its per-workgroup sums live in a
+ * fixed array of the library, 16 KiB per device (256 workgroups x 8 levels of doubles; the need is
+ * the same for every layer and n), held until the process ends; the call allocates and frees
+ * nothing. Every call on one device shares that device's array, so calls that overlap on one
+ * device (different streams, or other threads) race and give wrong results: order them.
+ * Errors: those of aqmb_prefix_distortion except ENOMEM; EUNSUPPORTED if the kernels ever need
+ * more scratch than the array holds.
+ */
+aqmb_status aqmb_prefix_distortion_noalloc(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* Xt,
+                                           aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream);
+
 /* Widest beam accepted by aqmb_beam_search. */
 #define AQMB_MAX_BEAM 16
 

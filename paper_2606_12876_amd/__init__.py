@@ -89,6 +89,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_gemm.argtypes = [vp, i32, vp, i32, vp, i32, vp]
     L.aqmb_dequant.argtypes = [vp, i32, vp, i32, vp]
     L.aqmb_prefix_distortion.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
+    L.aqmb_prefix_distortion_noalloc.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
     L.aqmb_beam_search.argtypes = [ctypes.POINTER(Desc), i32, i32, vp, vp, vp, vp, vp, vp]
     L.aqmb_validate.argtypes = [ctypes.POINTER(Desc), i32, i32, i32, i32, i32, vp, vp]
     L.aqmb_bits_per_weight.argtypes = [ctypes.POINTER(Desc), i32]
@@ -100,7 +101,8 @@ def _load() -> ctypes.CDLL:
     for f in ("aqmb_create", "aqmb_create_prefix", "aqmb_load_planes", "aqmb_drop_planes", "aqmb_resident_planes",
               "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_select", "aqmb_gemv_multi", "aqmb_gemm",
               "aqmb_gemm_select",
-              "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_beam_search", "aqmb_validate"):
+              "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_prefix_distortion_noalloc", "aqmb_beam_search",
+              "aqmb_validate"):
         getattr(L, f).restype = st
     return L
 
@@ -309,6 +311,21 @@ def prefix_distortion(layer: int, W, w_dtype, Xt, x_dtype, n: int, D, stream=Non
         raise AqmbError(Status.EINVAL, "aqmb_prefix_distortion", f"D holds {nd} bytes, needs {need}")
     _check(lib.aqmb_prefix_distortion(layer, _ptr(W), int(w_dtype), _ptr(Xt), int(x_dtype), n, _ptr(D),
                                       _stream(stream)), "aqmb_prefix_distortion")
+
+
+def prefix_distortion_noalloc(layer: int, W, w_dtype, Xt, x_dtype, n: int, D, stream=None) -> None:
+    """aqmb_prefix_distortion_noalloc: prefix_distortion with the library's fixed scratch (no device
+    allocation; calls that overlap on one device race)."""
+    d = get_desc(layer)
+    _need(W, d.d_out * d.d_in, w_dtype, "W", "aqmb_prefix_distortion_noalloc")
+    if n >= 1:
+        _need(Xt, n * d.d_in, x_dtype, "Xt", "aqmb_prefix_distortion_noalloc")
+    nd = _nbytes(D)
+    need = 8 * resident_planes(layer)
+    if nd is not None and nd < need:
+        raise AqmbError(Status.EINVAL, "aqmb_prefix_distortion_noalloc", f"D holds {nd} bytes, needs {need}")
+    _check(lib.aqmb_prefix_distortion_noalloc(layer, _ptr(W), int(w_dtype), _ptr(Xt), int(x_dtype), n, _ptr(D),
+                                              _stream(stream)), "aqmb_prefix_distortion_noalloc")
 
 
 MAX_BEAM = 16

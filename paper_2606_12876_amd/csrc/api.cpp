@@ -452,6 +452,27 @@ aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "prefix_distortion: launch");
 }
 
+aqmb_status aqmb_prefix_distortion_noalloc(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* X,
+                                           aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "prefix_distortion_noalloc: not a live layer");
+  if (!W) return fail(AQMB_EINVAL, "prefix_distortion_noalloc: W is NULL");
+  if ((uintptr_t)W % 16) return fail(AQMB_EINVAL, "prefix_distortion_noalloc: W must be 16-byte aligned");
+  aqmb_status s = validate_call(&L->d, 3, 0, n, x_dtype, w_dtype, X, D);
+  if (s != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  double* sc = nullptr;
+  size_t have = 0;
+  hipError_t e = distortion_static_scratch(L->device, &sc, &have);
+  if (e != hipSuccess) return hip_fail(e, "prefix_distortion_noalloc: scratch address");
+  if (distortion_scratch_bytes() > have)
+    return fail(AQMB_EUNSUPPORTED, "prefix_distortion_noalloc: needs %zu bytes of scratch, the library holds %zu",
+                distortion_scratch_bytes(), have);
+  e = launch_distortion(*L, W, X, n, D, sc, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "prefix_distortion_noalloc: launch");
+}
+
 aqmb_status aqmb_beam_search(const aqmb_desc* desc, int k, int beam, const void* W, const uint16_t* codebooks,
                              const uint16_t* scales, uint8_t* codes, float* errors, aqmb_stream_t stream) {
   clear_error();

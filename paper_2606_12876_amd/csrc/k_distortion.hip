@@ -23,6 +23,7 @@
 //     one group of one row, i.e. C_m[code], gathered from codebooks replicated in LDS.
 // Each lane keeps fp64 sums of R_k^2 over its outputs; each workgroup writes its sums and a
 // second kernel adds them in a fixed order, so the result does not depend on scheduling.
+#include <mutex>
 #include <type_traits>
 
 #include "device.h"
@@ -62,6 +63,32 @@ template <int M, int CB> struct Frag {
 }  // namespace dist
 
 size_t distortion_scratch_bytes() { return (size_t)dist::kMaxGrid * 8 * sizeof(double); }
+
+// Scratch of the allocation-free entry point: one per-workgroup sum slot for each of the at most
+// kMaxGrid workgroups and 8 levels (16 KiB per device, held until the process ends). Host code
+// never passes the array's name to a kernel: its device address, looked up once per device with
+// hipGetSymbolAddress while that device is current, is what the kernels receive. Every call on a
+// device shares that device's copy, so calls that overlap on one device race. Nothing in it needs
+// clearing: each workgroup writes its slots before the final sum reads them.
+static __device__ __align__(256) double scratch[dist::kMaxGrid * 8];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static double* g_scratch_ptr[kMaxDevices];
+
+hipError_t distortion_static_scratch(int device, double** out, size_t* bytes) {
+  *out = nullptr;
+  *bytes = sizeof(scratch);
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = (double*)p;
+  }
+  *out = g_scratch_ptr[device];
+  return hipSuccess;
+}
 
 struct DistArgs {
   const unsigned char* codes;

@@ -41,6 +41,9 @@ hipError_t launch_gemv_multi(const Layer* const* Ls, int n, int k, const void* x
 hipError_t launch_distortion(const Layer& L, const void* W, const void* X, int n, double* D, double* scratch,
                              hipStream_t st);
 size_t distortion_scratch_bytes();
+// The device address of the distortion's file-scope scratch array on `device` (which must be
+// current), looked up on the first call per device; *bytes is its size.
+hipError_t distortion_static_scratch(int device, double** out, size_t* bytes);
 // Beam search of codes for every group of W [d_out][d_in] fp16 over codebooks 0..k-1 (8-bit).
 hipError_t launch_beam_search(const aqmb_desc& d, int k, int beam_width, const void* W, const uint16_t* codebooks,
                               const uint16_t* scales, unsigned char* codes, float* errors, hipStream_t st);
