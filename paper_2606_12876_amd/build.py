@@ -2,7 +2,8 @@
 
 Objects go to ``_build/`` at the repository root; the shared library is written next to
 this file, where the binding loads it. Every HIP source is compiled with packed-fp32
-instruction generation turned off.
+instruction generation turned off. ``libaqmb_ceilings.so`` (the benchmark's measured-ceiling
+kernels, not part of the layer) is built beside it.
 """
 from __future__ import annotations
 
@@ -17,6 +18,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libaqmb.so")
+CEIL_SOURCES = ["ceilings.hip"]
+CEIL_LIB = os.path.join(HERE, "libaqmb_ceilings.so")
 
 SOURCES = ["validate.cpp", "api.cpp", "k_dequant.hip", "k_gemv.hip", "k_gemv16.hip", "k_gemv4.hip", "k_gemv_mma.hip", "k_gemm.hip", "k_gemm_small.hip", "k_distortion.hip", "k_beam.hip"]
 ARCH = "gfx950"
@@ -45,19 +48,25 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    jobs = min(len(SOURCES), max(1, min(16, os.cpu_count() or 1)))
-    with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib):
+    tmp = lib + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"linking failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + CEIL_SOURCES
+    jobs = min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
+    with cf.ThreadPoolExecutor(jobs) as ex:
+        objs = dict(zip(srcs, ex.map(_compile, srcs)))
+    _link([objs[s] for s in SOURCES], LIB)
+    _link([objs[s] for s in CEIL_SOURCES], CEIL_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {CEIL_LIB}")
     return LIB
 
 
