@@ -241,6 +241,118 @@ __global__ __launch_bounds__(256) void dequant8_kernel(const unsigned char* code
   }
 }
 
+// 8-bit codes, 16-bit output (f16 or bf16), K = k planes: tiles of 64 rows x 64 groups (4 slices),
+// 512 threads. Thread t takes row t % 64 of the tile and half (t / 64) % 2 of slice t / 128: one
+// 8-byte code load per plane brings its 8 groups, which it folds (same arithmetic and order as
+// dequant8_kernel) into a 64 KiB tile in LDS, row-major, its 16-byte chunks XOR-swizzled by row so
+// that both the column-wise writes and the row-wise reads hit every bank group. Then each wave
+// writes 8 whole rows of the tile, 1 KiB contiguous per store instruction (measured: 64 rows x
+// 256-byte pieces per instruction, the thread-per-group layout, is 20 % slower; rows written by
+// one lane each, 4x slower). Code words of the workgroup's next tile are requested before the
+// current one is folded. The launcher gives every tile its own workgroup (measured best for the
+// 4096 x 4096 layer: two workgroups per CU, one tile each).
+namespace dq {
+constexpr int kThreads = 512, kRows = 64, kSlices = 4, kWaves = kThreads / 64;
+}
+
+// LDS writes of this wave complete, then a workgroup barrier (global loads stay in flight).
+__device__ __forceinline__ void dq_lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);                  // lgkmcnt(0); vmcnt and expcnt at their maxima
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int OUT, int K>
+__global__ __launch_bounds__(dq::kThreads) void dequant8_tile_kernel(const unsigned char* codes, const uint16_t* codebooks,
+                                                                    const uint16_t* scales, void* W, int d_out, int d_in,
+                                                                    int G, int S, size_t plane_bytes) {
+  static_assert(OUT == AQMB_F16 || OUT == AQMB_BF16, "16-bit outputs");
+  using namespace dq;
+  extern __shared__ uint4 dq_smem[];
+  uint4* cb8 = dq_smem;                                // [K][256] codewords
+  uint4* tile = dq_smem + K * 256;                     // [64 rows][64 chunks of 16 bytes], swizzled
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  for (int q = tid; q < K * 256; q += kThreads) cb8[q] = ((const uint4*)codebooks)[q];
+  const int n_rt = (d_out + kRows - 1) / kRows, n_tiles = n_rt * ((S + kSlices - 1) / kSlices);
+  const int rl = lane, sl_t = wave >> 1, half = wave & 1;   // row in the tile, slice in the tile, half slice
+  uint2 c[K];
+  uint32_t sc = 0;
+  // code words (8 bytes per plane) and row scale of tile t for this thread; tiles past the end
+  // reload the last one, rows and slices past the layer reload its last row and slice (never stored)
+  auto load = [&](int t) {
+    const int tc = t < n_tiles ? t : n_tiles - 1;
+    int row = (tc % n_rt) * kRows + rl, sl = (tc / n_rt) * kSlices + sl_t;
+    row = row < d_out ? row : d_out - 1;
+    sl = sl < S ? sl : S - 1;
+    sc = scales[row];
+#pragma unroll
+    for (int m = 0; m < K; ++m) c[m] = load_stream8(codes + m * plane_bytes + ((size_t)sl * d_out + row) * 16 + half * 8);
+  };
+  int t = blockIdx.x;
+  load(t);
+  __syncthreads();
+  for (; t < n_tiles; t += gridDim.x) {
+    const int r0 = (t % n_rt) * kRows, s0 = (t / n_rt) * kSlices;
+    const float scale = f16_to_f32((uint16_t)sc);
+    uint2 w[K];
+#pragma unroll
+    for (int m = 0; m < K; ++m) w[m] = c[m];
+    load(t + gridDim.x);
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      float acc[8];
+#pragma unroll
+      for (int m = 0; m < K; ++m) {
+        const uint32_t word = jj < 4 ? w[m].x : w[m].y;
+        fold_codeword(acc, cb8[m * 256 + ((word >> (8 * (jj & 3))) & 0xFFu)], m == 0);
+      }
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[e] = acc[e] * scale;
+        asm volatile("" : "+v"(v[e]));  // keep the binary32 product (see dequant_kernel)
+      }
+      const uint4 o = OUT == AQMB_F16
+                          ? make_uint4(pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3]), pack_f16x2(v[4], v[5]), pack_f16x2(v[6], v[7]))
+                          : make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                                       pack_bf16x2(v[6], v[7]));
+      const int chunk = sl_t * 16 + half * 8 + jj;
+      tile[rl * 64 + (chunk ^ rl)] = o;
+    }
+    dq_lds_barrier();
+    const int grp = s0 * 16 + lane;                    // the group this lane writes in every row
+#pragma unroll
+    for (int i = 0; i < kRows / kWaves; ++i) {
+      const int r = wave * (kRows / kWaves) + i, row = r0 + r;
+      const uint4 o = tile[r * 64 + (lane ^ r)];
+      if (row < d_out && grp < G) store_stream16((uint16_t*)W + (size_t)row * d_in + (size_t)grp * 8, o.x, o.y, o.z, o.w);
+    }
+    dq_lds_barrier();                                   // the tile is read before the next one is written
+  }
+}
+
+template <int OUT>
+static void launch_dequant8_tile(const Layer& L, int k, void* W, hipStream_t st) {
+  const int n_tiles = ((L.d.d_out + dq::kRows - 1) / dq::kRows) * ((L.S + dq::kSlices - 1) / dq::kSlices);
+  const unsigned grid = (unsigned)std::min(n_tiles, 65535);
+  const size_t lds = (size_t)k * 256 * 16 + (size_t)dq::kRows * 64 * 16;
+  auto go = [&](auto kern) {
+    kern<<<grid, dq::kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, W, L.d.d_out, L.d.d_in, L.G, L.S, L.plane_bytes);
+  };
+  switch (k) {
+    case 1: go(dequant8_tile_kernel<OUT, 1>); break;
+    case 2: go(dequant8_tile_kernel<OUT, 2>); break;
+    case 3: go(dequant8_tile_kernel<OUT, 3>); break;
+    case 4: go(dequant8_tile_kernel<OUT, 4>); break;
+    case 5: go(dequant8_tile_kernel<OUT, 5>); break;
+    case 6: go(dequant8_tile_kernel<OUT, 6>); break;
+    case 7: go(dequant8_tile_kernel<OUT, 7>); break;
+    default: go(dequant8_tile_kernel<OUT, 8>); break;
+  }
+}
+
 template <int OUT>
 static void launch_dequant8(const Layer& L, int k, void* W, unsigned grid, hipStream_t st) {
   const size_t lds = (size_t)k * 256 * 16;
@@ -261,14 +373,17 @@ static void launch_dequant8(const Layer& L, int k, void* W, unsigned grid, hipSt
 
 hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hipStream_t st) {
   const size_t nslot = (size_t)L.S * L.d.d_out * 16;
+  if (L.d.code_bits == 8 && w_dtype != AQMB_F32 && nslot < ((size_t)1 << 30)) {
+    if (w_dtype == AQMB_F16) launch_dequant8_tile<AQMB_F16>(L, k, W, st);
+    else launch_dequant8_tile<AQMB_BF16>(L, k, W, st);
+    return hipGetLastError();
+  }
   if (L.d.code_bits == 8 && nslot < ((size_t)1 << 30)) {
-    // one thread per group slot and pass; at most 2048 workgroups (eight per CU), so large layers
-    // take several passes and the reads of one overlap the writes of another (t + 2 * stride
-    // stays below 2^31)
+    // fp32 output: one thread per group slot and pass; at most 2048 workgroups (eight per CU), so
+    // large layers take several passes and the reads of one overlap the writes of another
+    // (t + 2 * stride stays below 2^31)
     const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nslot + 255) / 256, 2048));
-    if (w_dtype == AQMB_F32) launch_dequant8<AQMB_F32>(L, k, W, grid, st);
-    else if (w_dtype == AQMB_F16) launch_dequant8<AQMB_F16>(L, k, W, grid, st);
-    else launch_dequant8<AQMB_BF16>(L, k, W, grid, st);
+    launch_dequant8<AQMB_F32>(L, k, W, grid, st);
     return hipGetLastError();
   }
   // 16- and 4-bit codes (and 8-bit layers too large for 32-bit thread indices): one thread per group
