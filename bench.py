@@ -66,6 +66,10 @@ def gemv_bytes(d_out, d_in, B, k, b):
     return int(k * d_out * (d_in // 8) * code_bytes) + k * (1 << B) * 16 + 2 * d_out + 2 * b * (d_in + d_out)
 
 
+# the sources the decode GEMV launches of the headline depend on (kernels and their dispatch)
+GEMV_SOURCES = ("api.cpp", "device.h", "k_gemv.hip", "k_gemv_mma.hip")
+
+
 def measured_traffic(kernel_key):
     """HBM bytes per launch of a kernel from the committed counter summary, if its sources still
     hash to what was measured (else None)."""
@@ -79,7 +83,7 @@ def measured_traffic(kernel_key):
             key, val = line.split(":", 1)
             fields[key.strip()] = val.strip()
     h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2606_12876_amd", "csrc"))):
+    for f in GEMV_SOURCES:
         h.update(open(os.path.join(ROOT, "paper_2606_12876_amd", "csrc", f), "rb").read())
     if fields.get("sources_sha256") != h.hexdigest() or f"traffic[{kernel_key}]" not in fields:
         return None

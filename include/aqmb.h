@@ -135,12 +135,15 @@ aqmb_status aqmb_gemv(aqmb_layer_t layer, int k, const void* x, aqmb_dtype x_dty
  * products and sums, one rounding to y_dtype); they differ in speed only.
  *   AQMB_GEMV_AUTO    the library's choice for the layer, k, batch and x dtype (what aqmb_gemv runs)
  *   AQMB_GEMV_DIRECT  the direct-gather kernel of the layer's code width: codewords gathered per
- *                     code and dotted with x on the vector ALUs. 8-bit codes: k <= 4 and rows of
- *                     at most 2048 groups (16384 inputs); 4- and 16-bit codes: every k and row
+ *                     code and dotted with x on the vector ALUs, 16 rows per workgroup. 8-bit
+ *                     codes: k <= 4 and rows of at most 2048 groups (16384 inputs); 4- and 16-bit
+ *                     codes: every k and row
  *   AQMB_GEMV_MMA     the matrix-core kernel (8- and 4-bit codes; every k, batch and row length)
  *   AQMB_GEMV_LUT     per-group lookup tables LUT_m[j][c] = <x_j, C_m[c]> in LDS, one read per
  *                     code (8-bit codes); its split-K partial sums take per-call scratch from the
  *                     stream-ordered pool (ENOMEM if that fails)
+ * DIRECT with 8-bit codes also refuses when its codebook replicas and x tile do not fit in LDS
+ * for the row length and batch (batch above 2 on rows of several thousand inputs).
  */
 typedef enum {
   AQMB_GEMV_AUTO = 0,
