@@ -79,9 +79,10 @@ def measured_traffic(kernel_key):
         return None
     fields = {}
     for line in open(path):
-        if ":" in line and line.split(":", 1)[0].strip() in (f"traffic[{kernel_key}]", "sources_sha256"):
-            key, val = line.split(":", 1)
-            fields[key.strip()] = val.strip()
+        if ":" in line:
+            key, val = line.rsplit(":", 1)                    # keys hold colons themselves
+            if key.strip() in (f"traffic[{kernel_key}]", "sources_sha256"):
+                fields[key.strip()] = val.strip()
     h = hashlib.sha256()
     for f in GEMV_SOURCES:
         h.update(open(os.path.join(ROOT, "paper_2606_12876_amd", "csrc", f), "rb").read())
