@@ -20,8 +20,8 @@ Each (operation, layer, k, batch) runs as a burst of R launches captured in a HI
 with HIP events on the launch stream; the per-launch time is burst time / R.
 
 `value` is the decode GEMV throughput of the headline workload in algorithmic GB/s: code planes
-0..k-1, their codebooks, scales, x and y of every config-3 launch in the timed steps, over their
-time. `roofline` is the config-3 GEMV kernel with the largest share of that time, against the
+0..k-1, their codebooks, scales, x and y of every MLP-pair launch in the timed steps, over their
+time. `roofline` is the MLP-pair GEMV kernel with the largest share of that time, against the
 published HBM peak and against the measured ceilings that bind it.
 
 Measured ceilings (`ceilings`, timed once after the steps with the kernels of
@@ -203,7 +203,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceilings", action="store_true")
     ap.add_argument("--counters", choices=["gemv", "gemm"], default=None,
-                    help="counter-collection run: eager launches (gemv: the config-3 GEMVs at every batch and k and "
+                    help="counter-collection run: eager launches (gemv: the MLP-pair GEMVs at every batch and k and "
                          "the 4096 x 4096 batch-1 GEMV at every k; gemm: the prefill GEMM at k = 1 and 4), then one "
                          "plain 256 MiB device copy that calibrates the HBM byte counters")
     args = ap.parse_args()
@@ -254,9 +254,9 @@ def main():
     # ---------------------------------------------------------------- workloads
     ops = []     # dicts: name, shape, k, b, fn, n, bytes, flops, kernel
 
-    # headline: config 3, both layers
+    # headline: the MLP pair, both layers
     gemv_layers = {}
-    for name in ("c3_up", "c3_down", "c4", "c2"):
+    for name in ("mlp_up", "mlp_down", "b16", "square"):
         spec = config(name)
         R = n_copies(spec)
         log(f"creating {R} copies of {spec.name}")
@@ -277,7 +277,7 @@ def main():
                                 kernel=gemv_kernel_name(spec, k, b, spec.act_dtype)))
 
     # 4096 x 4096 several layers per launch
-    spec2, L2, hs2, xs2, ys2, _ = gemv_layers["c2"]
+    spec2, L2, hs2, xs2, ys2, _ = gemv_layers["square"]
     for G in (4, 16):
         for k in KS:
             for b in (1, 4):
@@ -289,7 +289,7 @@ def main():
 
     # 4-bit codes, same shape
     import dataclasses
-    spec4 = dataclasses.replace(spec2, name="c2_4096x4096_B4", B=4, seed=spec2.seed + 100, batches=(1,))
+    spec4 = dataclasses.replace(spec2, name="square_4096x4096_B4", B=4, seed=spec2.seed + 100, batches=(1,))
     R4 = n_copies(spec4)
     log(f"creating {R4} copies of {spec4.name}")
     L4, hs4 = copies(spec4, R4)
@@ -312,7 +312,7 @@ def main():
                         bytes=k * 4096 * 512 + k * 4096 + 2 * 4096 + 2 * 4096 * 4096, kernel="dequant_kernel"))
 
     # prefill GEMM
-    gspec = config("c5")
+    gspec = config("prefill")
     n_tok = gspec.n_tokens
     G_COPIES = 4
     Lg, glayers = copies(gspec, G_COPIES)
@@ -351,10 +351,10 @@ def main():
     torch.cuda.synchronize()
 
     # eager reference of one headline burst, for the graph check below
-    ref_op = [o for o in ops if o["name"] == "gemv" and o["shape"].startswith("c3_up") and o["k"] == 4 and o["b"] == 1][0]
+    ref_op = [o for o in ops if o["name"] == "gemv" and o["shape"].startswith("mlp_up") and o["k"] == 4 and o["b"] == 1][0]
     ref_op["fn"]()
     torch.cuda.synchronize()
-    yref = gemv_layers["c3_up"][4][1][0].clone()
+    yref = gemv_layers["mlp_up"][4][1][0].clone()
 
     log(f"capturing {len(ops)} bursts")
     graphs = []
@@ -376,10 +376,10 @@ def main():
     for _ in range(args.warmup):
         run_step(None)
     torch.cuda.synchronize()
-    gemv_layers["c3_up"][4][1][0].zero_()
+    gemv_layers["mlp_up"][4][1][0].zero_()
     graphs[ops.index(ref_op)].replay()
     torch.cuda.synchronize()
-    assert torch.equal(gemv_layers["c3_up"][4][1][0], yref), "graph replay differs from the eager GEMV"
+    assert torch.equal(gemv_layers["mlp_up"][4][1][0], yref), "graph replay differs from the eager GEMV"
 
     log(f"timing {args.steps} steps")
     events = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
@@ -405,7 +405,7 @@ def main():
         ceil = measure_ceilings(torch, stream, n_cu, ops)
 
     # ---------------------------------------------------------------- report
-    head = [o for o in ops if o["name"] == "gemv" and o["shape"].startswith("c3")]
+    head = [o for o in ops if o["name"] == "gemv" and o["shape"].startswith("mlp_")]
     value = sum(o["bytes"] * o["n"] for o in head) / (sum(o["step_us"] for o in head) * 1e-6) / 1e9
     per_k = {}
     for k in KS:
@@ -471,7 +471,7 @@ def main():
                                            "frac": round(g4["tflops"] / ceil["mfma_bf16_random_TFLOPs"], 4)}
     out["gemm_TFLOPs"] = round(len(gemm) * gflop / (sum(o["us"] for o in gemm) * 1e-6) / 1e12, 1)
     dq = [o for o in ops if o["name"] == "dequant"]
-    out["roofline_dequant"] = {"bound": "hbm", "kernel": "dequant_kernel (bf16 out), 4096 x 4096", "unit": "GB/s",
+    out["roofline_dequant"] = {"bound": "hbm", "kernel": "dequant8_tile_kernel (bf16 out), 4096 x 4096", "unit": "GB/s",
                                "peak": HBM_PEAK_GBPS,
                                "per_k": {str(o["k"]): {"us": round(o["us"], 3), "GBps": round(gbps(o), 1),
                                                        "frac": round(gbps(o) / HBM_PEAK_GBPS, 4)} for o in dq}}
@@ -500,7 +500,7 @@ def main():
     tot = sum(o["step_us"] for o in ops)
     share = {}
     for o in ops:
-        key = "gemv_c3" if o in head else o["name"] if o["name"] != "gemv" else f"gemv_{o['shape'].split('_')[0]}"
+        key = "gemv_mlp" if o in head else o["name"] if o["name"] != "gemv" else f"gemv_{o['shape'].split('_')[0]}"
         share[key] = share.get(key, 0.0) + o["step_us"] / tot
     out["time_share"] = {k: round(v, 4) for k, v in share.items()}
 
@@ -582,7 +582,7 @@ def measure_ceilings(torch, stream, n_cu, ops):
 def other_gemv(ops, gbps, ceil):
     res = {}
     for o in ops:
-        if o["name"] == "gemv" and o["shape"].startswith("c3"):
+        if o["name"] == "gemv" and o["shape"].startswith("mlp_"):
             continue
         if not o["name"].startswith("gemv"):
             continue
@@ -602,7 +602,7 @@ def run_counters(mode, A, torch, dev, config, make_layer, make_activations, copi
     plain 256 MiB device copy that calibrates FETCH_SIZE and WRITE_SIZE."""
     meta = {"mode": f"counters-{mode}", "ops": []}
     if mode == "gemv":
-        for name in ("c3_up", "c3_down", "c2"):
+        for name in ("mlp_up", "mlp_down", "square"):
             spec = config(name)
             R = n_copies(spec)
             L, hs = copies(spec, R)
@@ -620,7 +620,7 @@ def run_counters(mode, A, torch, dev, config, make_layer, make_activations, copi
             for h in hs:
                 A.destroy(h)
     else:
-        spec = config("c5")
+        spec = config("prefill")
         L, hs = copies(spec, 4)
         X = to_dev(make_activations(L, spec.n_tokens, "bf16")).view(torch.bfloat16)
         Y = torch.empty((spec.n_tokens, spec.d_out), dtype=torch.bfloat16, device=dev)
@@ -642,7 +642,7 @@ def run_counters(mode, A, torch, dev, config, make_layer, make_activations, copi
 
 def cpu_baseline(gemv_layers, rows=4096):
     """The fp64 oracle on the host cores over a bounded sample of the headline workload: the first
-    `rows` output rows of both config-3 layers, every k, batch 1, 8 and 16, each call the oracle's
+    `rows` output rows of both MLP layers, every k, batch 1, 8 and 16, each call the oracle's
     reconstruction of W_k and its product with x (about 10-20 s), in the same algorithmic GB/s as
     the GPU figure (bytes of the sampled rows)."""
     import oracle
@@ -654,7 +654,7 @@ def cpu_baseline(gemv_layers, rows=4096):
         blas_threads = 1
     from workloads import make_activations
     total_bytes, t_total = 0, 0.0
-    for name in ("c3_up", "c3_down"):
+    for name in ("mlp_up", "mlp_down"):
         spec, L, _, _, _, _ = gemv_layers[name]
         C = formats.f16_bits_to_f64(L.codebooks)
         s = formats.f16_bits_to_f64(L.scales)[:rows]
@@ -668,7 +668,7 @@ def cpu_baseline(gemv_layers, rows=4096):
                 total_bytes += gemv_bytes(rows, spec.d_in, 8, k, b)
     return {"value": round(total_bytes / t_total / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
             "kind": "oracle",
-            "sample": f"the first {rows} output rows of both config-3 layers, k=1..4, batch 1, 8 and 16: 24 calls of "
+            "sample": f"the first {rows} output rows of both MLP layers, k=1..4, batch 1, 8 and 16: 24 calls of "
                       "the oracle's fp64 reconstruction of W_k and its product with x (reconstruction "
                       "single-threaded, product on the BLAS threads)",
             "seconds": round(t_total, 2), "host_cpus": len(os.sched_getaffinity(0))}

@@ -100,7 +100,7 @@ def test_eight_codebooks_and_one_row():
 def test_full_size_sampled_groups():
     """The benchmarked shape (4096 x 4096 weights, M = 4, k = 4, beam 8): the whole matrix on the
     GPU, 300 groups spread over it against the oracle."""
-    L = make_layer(LayerSpec("c2", 4096, 4096, M=4, seed=2))
+    L = make_layer(LayerSpec("square", 4096, 4096, M=4, seed=2))
     Wb = make_weights(L)
     c_gpu, e_gpu = _gpu(L, Wb, 4, 8)
     rng = np.random.default_rng(5)

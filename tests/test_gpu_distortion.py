@@ -181,7 +181,7 @@ def test_identity_inputs_give_weight_mse():
 
 
 def test_full_size_gaussian_within_bound():
-    L = make_layer(LayerSpec("c2", 4096, 4096, M=4, seed=2))
+    L = make_layer(LayerSpec("square", 4096, 4096, M=4, seed=2))
     Wb = make_weights(L)
     Xb = make_activations(L, 4096, "f16")
     _check_bound(L, Wb, Xb, "4096x4096 n=4096")

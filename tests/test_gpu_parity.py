@@ -71,11 +71,11 @@ def test_dequant_bit_exact(spec, dt):
                                   ref.view(np.uint32) if dt == "f32" else ref), (spec.name, k, dt)
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3_up", "c3_down", "c4"])
+@pytest.mark.parametrize("name", ["tiny", "square", "mlp_up", "mlp_down", "b16"])
 def test_dequant_workload_layers_bit_exact(name):
     spec = config(name)
     L = make_layer(spec)
-    dts = ("bf16", "f16") if not name.startswith("c3") else ("bf16",)
+    dts = ("bf16", "f16") if not name.startswith("mlp_") else ("bf16",)
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
         for k in spec.ks:
             for dt in dts:
@@ -143,7 +143,7 @@ def test_gemv_small_shapes(spec, batches, xdt):
                     check_close(got, ref, ydt, f"{spec.name} b={b} k={k} {xdt}->{ydt}", terms=T, n_terms=k * spec.d_in)
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3_up", "c3_down", "c4"])
+@pytest.mark.parametrize("name", ["tiny", "square", "mlp_up", "mlp_down", "b16"])
 def test_gemv_workloads(name):
     spec = config(name)
     L = make_layer(spec)
@@ -272,7 +272,7 @@ def test_gemm_subnormal_codebook_entries():
 
 
 def test_gemm_workload_full_size():
-    spec = config("c5")
+    spec = config("prefill")
     L = make_layer(spec)
     Xbits = make_activations(L, spec.n_tokens, "bf16")
     X = act_values(Xbits, "bf16")

@@ -151,14 +151,15 @@ def make_integer_rows(layer: Layer, rows: int, lim: int) -> np.ndarray:
     return float_to_f16_bits(layer.rng.integers(-lim, lim + 1, size=(rows, layer.spec.d_in)).astype(np.float64))
 
 
-# The five workloads. Config 3 is a pair of layers (up and down projection).
+# The workloads: a small and a square layer, the up and down projections of a Llama-7B MLP, a
+# layer with 2^16-entry codebooks, and a 2048-token prefill.
 CONFIGS: List[LayerSpec] = [
-    LayerSpec("c1_1024x1024", 1024, 1024, seed=1, act_dtype="f16", batches=(1,)),
-    LayerSpec("c2_4096x4096", 4096, 4096, seed=2, act_dtype="f16", batches=(1, 4)),
-    LayerSpec("c3_up_11008x4096", 11008, 4096, seed=31, act_dtype="bf16", batches=(1, 8, 16), heavy_tail=True),
-    LayerSpec("c3_down_4096x11008", 4096, 11008, seed=32, act_dtype="bf16", batches=(1, 8, 16), heavy_tail=True),
-    LayerSpec("c4_14336x4096_B16", 14336, 4096, M=2, B=16, seed=4, act_dtype="f16", batches=(1,), ks=(1, 2)),
-    LayerSpec("c5_gemm_2048x4096x4096", 4096, 4096, seed=5, act_dtype="bf16", n_tokens=2048),
+    LayerSpec("tiny_1024x1024", 1024, 1024, seed=1, act_dtype="f16", batches=(1,)),
+    LayerSpec("square_4096x4096", 4096, 4096, seed=2, act_dtype="f16", batches=(1, 4)),
+    LayerSpec("mlp_up_11008x4096", 11008, 4096, seed=31, act_dtype="bf16", batches=(1, 8, 16), heavy_tail=True),
+    LayerSpec("mlp_down_4096x11008", 4096, 11008, seed=32, act_dtype="bf16", batches=(1, 8, 16), heavy_tail=True),
+    LayerSpec("b16_14336x4096", 14336, 4096, M=2, B=16, seed=4, act_dtype="f16", batches=(1,), ks=(1, 2)),
+    LayerSpec("prefill_2048x4096x4096", 4096, 4096, seed=5, act_dtype="bf16", n_tokens=2048),
 ]
 
 
