@@ -66,6 +66,7 @@ template <int K, int CB, int NX>
 struct MgRun {
   uint4 xa[NX];
   typename std::conditional<CB == 8, uint4, uint2>::type c[mg_code_loads<K, CB>()];
+  int sh;                                                    // bf16 x converted in place: the lane's shift
 };
 
 // Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of the
@@ -121,9 +122,13 @@ __device__ __forceinline__ uint4 mg_first_word(const GemvMmaArgs& a) {
 // (exact): every codeword is split once, when copied into LDS, into a bf16 high part (RNE) and a
 // bf16 low part (the remainder, at most 3 significant bits): two gathers and two bf16 MFMAs per
 // code, no conversion. The split form is kept where the planes are too few to repay the
-// conversion (measured crossovers: k = 1 at batch <= 4, k <= 2 above).
+// conversion (measured crossovers: k = 1 at batch <= 4, k <= 2 above). The persistent kernel (P)
+// converts each run's x once for all its blocks, so there the conversion wins from k = 2 at every
+// batch (11008 x 4096, k = 2: batch 8 11.95 -> 11.37 us, batch 16 13.74 -> 12.73 us).
+template <int K, int XDT, int NX, bool P = false>
+constexpr bool mg_split_p() { return XDT == AQMB_BF16 && K < (P ? 2 : (NX == 1 ? 2 : 3)); }
 template <int K, int XDT, int NX>
-constexpr bool mg_split() { return XDT == AQMB_BF16 && K < (NX == 1 ? 2 : 3); }
+constexpr bool mg_split() { return mg_split_p<K, XDT, NX, false>(); }
 
 // Codebook word q (q < K * NCW) into its nrep replicas (split form: a book of high and a book of
 // low parts); v0 is word threadIdx.x, already loaded.
@@ -268,18 +273,24 @@ __device__ __forceinline__ uint4 mg_x_step(const uint4 (&xa)[NX]) {
 
 // The MFMAs of one run. Step j of a run: group 4 j + kc of the run (8-bit codes: byte 4 j + kc of
 // the plane's slice word; 4-bit codes: nibble 4 j + kc of its 8 bytes).
-template <int K, int XDT, int CB, int NX>
+// With bf16 x in the converted form, `convert` says whether R holds x as loaded: it is then
+// converted in place (R.xa, R.sh), so a register set that keeps its run's x for several blocks
+// (the persistent kernel) converts it once.
+template <int K, int XDT, int CB, int NX, bool P = false>
 __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb_rep, uint32_t rep_off,
-                                           const MgRun<K, CB, NX>& R, mg::f32x4_t (&acc)[4]) {
+                                           MgRun<K, CB, NX>& R, mg::f32x4_t (&acc)[4], bool convert = true) {
   using namespace mg;
   constexpr int NCW = 1 << CB;
   const int lane = threadIdx.x & 63, kc = lane >> 4;
+  constexpr bool kSplit = mg_split_p<K, XDT, NX, P>(), kConv = XDT == AQMB_BF16 && !kSplit;
+  int sh = 0;
+  if constexpr (kConv) {
+    if (convert) R.sh = mg_bf16_to_f16<NX>(R.xa, a.batch);
+    sh = R.sh;
+  }
   uint4 xa[NX];
 #pragma unroll
   for (int t = 0; t < NX; ++t) xa[t] = R.xa[t];
-  constexpr bool kSplit = mg_split<K, XDT, NX>(), kConv = XDT == AQMB_BF16 && !kSplit;
-  int sh = 0;
-  if constexpr (kConv) sh = mg_bf16_to_f16<NX>(xa, a.batch);
   const uint4 xs[4] = {mg_x_step<NX, 0>(xa), mg_x_step<NX, 1>(xa), mg_x_step<NX, 2>(xa), mg_x_step<NX, 3>(xa)};
   // bf16 x: the run's products go to fresh sums, scaled by each batch row's 2^sh at the end
   f32x4_t run[4];
@@ -444,7 +455,7 @@ template <int K, int XDT, int CB, int NX>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_persist_kernel(GemvMmaArgs a) {
   using namespace mg;
-  constexpr int kBooks = mg_split<K, XDT, NX>() ? 2 : 1;    // fp16 codewords, or bf16 high and low parts
+  constexpr int kBooks = mg_split_p<K, XDT, NX, true>() ? 2 : 1;    // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
   uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
   f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
@@ -491,16 +502,16 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   sbits = scale_of(0);
   load_item(0, ra);
   load_item(1, rb);
-  mg_replicate<K, CB, mg_split<K, XDT, NX>()>(a, cb_rep, w0);
+  mg_replicate<K, CB, mg_split_p<K, XDT, NX, true>()>(a, cb_rep, w0);
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < n_items; i += 2) {
-    mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, ra, acc);
+    mg_compute<K, XDT, CB, NX, true>(a, cb_rep, rep_off, ra, acc, i < 2 || per > 2);   // x loaded with the item
     load_item(i + 2, ra);
     if ((i + 1) % per == 0) end_block(i);
     if (i + 1 >= n_items) break;
-    mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, rb, acc);
+    mg_compute<K, XDT, CB, NX, true>(a, cb_rep, rep_off, rb, acc, i < 2 || per > 2);
     load_item(i + 3, rb);
     if ((i + 2) % per == 0) end_block(i + 1);
   }
@@ -510,7 +521,10 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
 // (mm: several layers in one launch; a is then mm->L[0].)
 template <int K, int XDT, int CB, int NX>
 static hipError_t launch_mma_knx(GemvMmaArgs a, GemvMmaMultiArgs* mm, hipStream_t st) {
-  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(mg_split<K, XDT, NX>() ? 2 : 1) * K * (1 << CB) * 16;
+  const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
+  const bool persist = !mm && n_rb > a.n_cu && a.n_cu > 0;   // one workgroup per CU walks the blocks
+  const bool split = persist ? mg_split_p<K, XDT, NX, true>() : mg_split<K, XDT, NX>();
+  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(split ? 2 : 1) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
   a.nrep = CB == 4 ? 1 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
   a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
@@ -523,8 +537,7 @@ static hipError_t launch_mma_knx(GemvMmaArgs a, GemvMmaMultiArgs* mm, hipStream_
     gemv_mma_multi_kernel<K, XDT, CB, NX><<<dim3(mm->first[mm->n]), mg::kThreads, lds, st>>>(*mm);
     return hipGetLastError();
   }
-  const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
-  if (n_rb > a.n_cu && a.n_cu > 0) gemv_mma_persist_kernel<K, XDT, CB, NX><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
+  if (persist) gemv_mma_persist_kernel<K, XDT, CB, NX><<<dim3(a.n_cu), mg::kThreads, lds, st>>>(a);
   else gemv_mma_kernel<K, XDT, CB, NX><<<dim3(n_rb), mg::kThreads, lds, st>>>(a);
   return hipGetLastError();
 }
