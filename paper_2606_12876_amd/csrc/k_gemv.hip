@@ -759,22 +759,32 @@ static size_t cw_lds(int K, int nb, int S, int nrep, bool bf16) {
 }
 
 // Replicas per codebook: as many as fit next to the x tile (LDS holds 160 KiB per workgroup).
-static int cw_nrep(int K, int nb, int S, bool bf16) {
+// Sixteen (allowed by the caller) let every 16 lanes of a wave gather without bank conflicts (a
+// codeword's 16 copies span the 64 banks): half the LDS cycles of eight copies per gather, for
+// twice the replica writes; they fit for k <= 2.
+static int cw_nrep(int K, int nb, int S, bool bf16, bool allow16 = false) {
   const size_t budget = 160 * 1024 - (size_t)cw::kWaves * cw::kRows * 4 * nb - 512;  // minus the row sums
+  if (allow16 && cw_lds(K, nb, S, 16, bf16) <= budget) return 16;
   for (int r : {8, 4})
     if (cw_lds(K, nb, S, r, bf16) <= budget) return r;
   return 0;
 }
+static int cw_shift(int nrep) { return nrep == 16 ? 8 : nrep == 8 ? 7 : 6; }
 
 static int cw_nb(int batch) { return batch == 1 ? 1 : batch == 2 ? 2 : 4; }
 static int cw_blocks(int S) { return (S * 16 + 511) / 512; }
 
 template <int K, int NB, int XDT>
 static hipError_t launch_cw_nb(GemvArgs a, hipStream_t st) {
-  a.nrep = cw_nrep(K, NB, a.S, XDT == AQMB_BF16);
-  if (a.nrep == 0) return hipErrorInvalidValue;  // x tile does not fit: caller uses another path
-  a.cb_shift = a.nrep == 8 ? 7 : 6;
   const int n_rb = (a.d_out + cw::kRows - 1) / cw::kRows;
+  // Sixteen replicas where a workgroup gathers at least two 512-group blocks (long rows, or a
+  // persistent workgroup with two or more row blocks): there the halved gather cost repays the
+  // extra replica writes (batch 1: 11008 x 4096, k = 1: 6.62 -> 5.95 us; 4096 x 11008, k = 2:
+  // 7.98 -> 7.47 us; one block of 4096 x 4096 gains nothing).
+  const bool many = cw_blocks(a.S) >= 2 || (a.n_cu > 0 && n_rb >= 2 * a.n_cu);
+  a.nrep = cw_nrep(K, NB, a.S, XDT == AQMB_BF16, many);
+  if (a.nrep == 0) return hipErrorInvalidValue;  // x tile does not fit: caller uses another path
+  a.cb_shift = cw_shift(a.nrep);
   const dim3 grid(n_rb);
   const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
   if (cw_blocks(a.S) == 1 && a.batch <= NB && n_rb > a.n_cu && a.n_cu > 0)   // one workgroup per CU
@@ -879,7 +889,7 @@ hipError_t launch_gemv_lut(const Layer& L, int k, const void* x, aqmb_dtype x_dt
 template <int K, int NB, int XDT>
 static hipError_t launch_multi_nb(GemvMultiArgs a, int grid, hipStream_t st) {
   a.nrep = cw_nrep(K, NB, a.S, XDT == AQMB_BF16);
-  a.cb_shift = a.nrep == 8 ? 7 : 6;
+  a.cb_shift = cw_shift(a.nrep);
   const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
   // two replica sets when they fit (k <= 2, one 512-group block, rows of at most 512 groups)
   const size_t lds2 = lds + (size_t)K * 256 * a.nrep * 16;

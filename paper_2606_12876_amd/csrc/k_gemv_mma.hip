@@ -218,12 +218,17 @@ __device__ __forceinline__ void mg_rows_transpose(uint32_t (&d)[4]) {
 typedef unsigned short mg_u16x2 __attribute__((ext_vector_type(2)));
 template <int NX>
 __device__ __forceinline__ int mg_bf16_to_f16(uint4 (&xa)[NX], int batch) {
+  // magnitudes (sign bits cleared): their largest 16-bit pattern holds the largest exponent field
+  uint32_t mag[NX][4];
   mg_u16x2 ex = {0, 0};
 #pragma unroll
   for (int t = 0; t < NX; ++t) {
     const uint32_t w[4] = {xa[t].x, xa[t].y, xa[t].z, xa[t].w};
 #pragma unroll
-    for (int h = 0; h < 4; ++h) ex = __builtin_elementwise_max(ex, __builtin_bit_cast(mg_u16x2, w[h] & 0x7F807F80u));
+    for (int h = 0; h < 4; ++h) {
+      mag[t][h] = w[h] & 0x7FFF7FFFu;
+      ex = __builtin_elementwise_max(ex, __builtin_bit_cast(mg_u16x2, mag[t][h]));
+    }
   }
   uint32_t e = (uint32_t)max(ex.x, ex.y) >> 7;
   const auto r32 = __builtin_amdgcn_permlane32_swap(e, e, false, false);   // rows 0, 1 <-> rows 2, 3
@@ -242,9 +247,9 @@ __device__ __forceinline__ int mg_bf16_to_f16(uint4 (&xa)[NX], int batch) {
       uint32_t w[4] = {xa[t].x, xa[t].y, xa[t].z, xa[t].w};
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
-        mg_u16x2 v = __builtin_elementwise_sub_sat(__builtin_bit_cast(mg_u16x2, w[h] & 0x7FFF7FFFu), dd);
+        mg_u16x2 v = __builtin_elementwise_sub_sat(__builtin_bit_cast(mg_u16x2, mag[t][h]), dd);
         v = v << (unsigned short)3;
-        w[h] = __builtin_bit_cast(uint32_t, v) | (w[h] & 0x80008000u);
+        w[h] = (w[h] & 0x80008000u) | __builtin_bit_cast(uint32_t, v);
       }
       xa[t] = make_uint4(w[0], w[1], w[2], w[3]);
     }
@@ -526,8 +531,11 @@ static hipError_t launch_mma_knx(GemvMmaArgs a, GemvMmaMultiArgs* mm, hipStream_
   const bool split = persist ? mg_split_p<K, XDT, NX, true>() : mg_split<K, XDT, NX>();
   const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(split ? 2 : 1) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
-  a.nrep = CB == 4 ? 1 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
-  a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
+  // Sixteen copies (conflict-free gathers, twice the replica writes) where a workgroup gathers at
+  // least two 512-group blocks' worth: long rows, or a persistent workgroup with two or more blocks.
+  const bool many = !mm && (a.G >= 1024 || (a.n_cu > 0 && n_rb >= 2 * a.n_cu));
+  a.nrep = CB == 4 ? 1 : many && book * 16 <= budget ? 16 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
+  a.cb_shift = a.nrep == 16 ? 8 : a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
   const size_t lds = book * a.nrep + red;
   if (mm) {
     for (int l = 0; l < mm->n; ++l) {
