@@ -30,7 +30,9 @@ the GEMV's grid), attainable write rate, random 16-byte LDS gathers from replica
 and without the batch-1 dot products), random 16-byte L2 gathers from 1 and 2 MiB tables, and the
 bf16 MFMA rate on random operands.
 
-`--counters MODE` runs eager launches for rocprofv3 counter passes instead.
+`--counters MODE` runs eager launches for rocprofv3 counter passes instead (gemv: every MLP-pair and
+4096 x 4096 GEMV; gemm: the prefill GEMM at k = 1 and 4; dequant: the 4096 x 4096 dequant to bf16 at
+k = 1..4), then one plain 256 MiB copy that calibrates the byte counters.
 Prints one JSON line on stdout; progress goes to stderr.
 """
 from __future__ import annotations
@@ -98,7 +100,7 @@ def gemv_kernel_name(spec, k, b, xdt):
         return f"gemv_b16_kernel<KC={min(k, 4)}>"
     wide = G > 512
     rb = (spec.d_out + 15) // 16
-    if b >= 2 or (wide and (xdt == "f16" or k >= 4)):
+    if b >= 2 or (wide and (xdt == "f16" or k >= 3)):
         return ("gemv_mma_persist_kernel" if rb > 256 else "gemv_mma_kernel") + f"<K={k}> (batch {b})"
     return ("gemv_cw_persist_kernel" if rb > 256 else "gemv_cw_kernel") + f"<K={k}> (batch {b})"
 
@@ -202,14 +204,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceilings", action="store_true")
-    ap.add_argument("--counters", choices=["gemv", "gemm"], default=None,
+    ap.add_argument("--counters", choices=["gemv", "gemm", "dequant"], default=None,
                     help="counter-collection run: eager launches (gemv: the MLP-pair GEMVs at every batch and k and "
-                         "the 4096 x 4096 batch-1 GEMV at every k; gemm: the prefill GEMM at k = 1 and 4), then one "
-                         "plain 256 MiB device copy that calibrates the HBM byte counters")
+                         "the 4096 x 4096 GEMV at batch 1 and 4, every k; gemm: the prefill GEMM at k = 1 and 4; "
+                         "dequant: the 4096 x 4096 dequant to bf16 at every k), then one plain 256 MiB device copy "
+                         "that calibrates the HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no multi-GPU "
-              f"path; DESIGN.md describes how the layer would shard", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU "
+              f"path (no collectives, no sharded layers)", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -273,7 +276,7 @@ def main():
                         A.gemv(h, k, xs[b], adt, b, y, adt)
                 ops.append(dict(name="gemv", shape=spec.name, k=k, b=b, fn=fn, n=R,
                                 bytes=gemv_bytes(spec.d_out, spec.d_in, spec.B, k, b),
-                                rows_groups=spec.d_out * (spec.d_in // 8),
+                                rows_groups=spec.d_out * (spec.d_in // 8), code_bits=spec.B,
                                 kernel=gemv_kernel_name(spec, k, b, spec.act_dtype)))
 
     # 4096 x 4096 several layers per launch
@@ -309,7 +312,7 @@ def main():
             for r in range(n_w):
                 A.dequant(hs2[r * 7], k, Ws[r], A.DType.BF16)
         ops.append(dict(name="dequant", shape=spec2.name, k=k, b=0, fn=fn, n=n_w,
-                        bytes=k * 4096 * 512 + k * 4096 + 2 * 4096 + 2 * 4096 * 4096, kernel="dequant_kernel"))
+                        bytes=k * 4096 * 512 + k * 4096 + 2 * 4096 + 2 * 4096 * 4096, kernel="dequant8_tile_kernel"))
 
     # prefill GEMM
     gspec = config("prefill")
@@ -530,7 +533,7 @@ def binding_fracs(o, ceil):
         # one codeword gather per code (the matrix-core kernel serves every batch row with it; the
         # direct-gather kernel at batch 1 also spends 4 fp16 dot products on it)
         gathers = spec_rows * o["k"]
-        kind = ("l2_gather_G_per_s" if "B16" in o["shape"] else
+        kind = ("l2_gather_G_per_s" if o.get("code_bits") == 16 else
                 "lds_gather_dot_G_per_s" if o["b"] == 1 else "lds_gather_G_per_s")
         rate = ceil.get(kind)
         if rate:
@@ -619,6 +622,21 @@ def run_counters(mode, A, torch, dev, config, make_layer, make_activations, copi
                                         "bytes": gemv_bytes(spec.d_out, spec.d_in, spec.B, k, b)})
             for h in hs:
                 A.destroy(h)
+    elif mode == "dequant":
+        spec = config("square")
+        R = n_copies(spec)
+        L, hs = copies(spec, R)
+        n_w = 16                                             # 512 MiB of outputs per burst
+        Ws = [torch.empty((spec.d_out, spec.d_in), dtype=torch.bfloat16, device=dev) for _ in range(n_w)]
+        for k in spec.ks:
+            for r in range(4 * n_w):
+                A.dequant(hs[(r * 7) % R], k, Ws[r % n_w], A.DType.BF16)
+            torch.cuda.synchronize()
+            meta["ops"].append({"shape": spec.name, "k": k, "launches": 4 * n_w,
+                                "bytes_read": k * spec.d_out * spec.d_in // 8 + k * 4096 + 2 * spec.d_out,
+                                "bytes_written": 2 * spec.d_out * spec.d_in})
+        for h in hs:
+            A.destroy(h)
     else:
         spec = config("prefill")
         L, hs = copies(spec, 4)
