@@ -13,8 +13,8 @@ checked against the paper by eye:
                   rounded dequantization, the GEMM reference, the weighted MSE,
                   the distortion of every prefix level and the average-bits formula;
 * ``search``    - residual k-means encoding, exhaustive / beam code search on tiny
-                  groups, and the beam search with decisions taken in binary32 (the
-                  reference of the GPU search).
+                  groups (plain or data-weighted error), and the beam searches with
+                  decisions taken in binary32 (the references of the GPU searches).
 
 Every function cites the passage of the paper it follows. Pins live in
 ``tests/test_oracle_*.py``; functions without a pin say "parity unpinned".
@@ -22,4 +22,5 @@ Every function cites the passage of the paper it follows. Pins live in
 from . import formats, aq, search  # noqa: F401
 from .aq import (reconstruct, linear, dequant_canonical, gemm_reference, wmse_frobenius,
                  wmse_trace, prefix_distortions, bits_per_weight, code_bits_per_weight)  # noqa: F401
-from .search import encode_residual_kmeans, brute_force_codes, beam_search_codes, beam_search_codes_f32  # noqa: F401
+from .search import (encode_residual_kmeans, brute_force_codes, beam_search_codes, beam_search_codes_f32,  # noqa: F401
+                     beam_search_codes_weighted_f32, group_hessian_blocks)
