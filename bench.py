@@ -14,7 +14,8 @@ streams at least 512 MiB of code planes, twice the 256 MB Infinity Cache:
     dequantization of the 4096 x 4096 layer to bf16, k = 1..4
     prefill GEMM, 2048 bf16 tokens x 4096 x 4096, bf16 out, k = 1..4
     prefix distortions D^(1..4) of the 4096 x 4096 layer against a dense fp16 W over 4096 fp16
-      calibration inputs; beam search (k = 4, beam 8) of codes for every group of that W
+      calibration inputs; beam search (k = 4, beam 8) of codes for every group of that W, with the
+      plain squared error and with the data-aware error d^T H_j d
 
 Each (operation, layer, k, batch) runs as a burst of R launches captured in a HIP graph and timed
 with HIP events on the launch stream; the per-launch time is burst time / R.
@@ -217,7 +218,7 @@ def main():
 
     import torch
     import paper_2606_12876_amd as A
-    from workloads import config, make_layer, make_activations, make_weights
+    from workloads import config, make_layer, make_activations, make_weights, make_calibration_inputs
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
@@ -351,6 +352,18 @@ def main():
     beam_cands = 4096 * 512 * 256 * (1 + (BEAM_K - 1) * BEAM_WIDTH)
     ops.append(dict(name="beam", shape=spec2.name, k=BEAM_K, b=BEAM_WIDTH, fn=beam_fn, n=1,
                     flops=beam_cands * 23.0, kernel=f"beam_kernel<{BEAM_WIDTH}>"))
+    # the data-aware search: the 8 x 8 diagonal blocks of X X^T / n of seeded calibration inputs
+    # (input preparation with torch, outside the timed region)
+    Xc = torch.from_numpy(make_calibration_inputs(L2, n_cal)).to(dev, torch.float32)     # [d_in][n]
+    Xg = Xc.view(512, 8, n_cal)
+    Hblk = (torch.bmm(Xg, Xg.transpose(1, 2).contiguous()) / n_cal).contiguous()        # [G][8][8] fp32
+    wbeam_codes = torch.empty_like(beam_codes)
+    wbeam_errs = torch.empty_like(beam_errs)
+
+    def wbeam_fn():
+        A.beam_search_weighted(desc2, BEAM_K, BEAM_WIDTH, Wd, cb2, sc2, Hblk, wbeam_codes, wbeam_errs)
+    ops.append(dict(name="beam_weighted", shape=spec2.name, k=BEAM_K, b=BEAM_WIDTH, fn=wbeam_fn, n=1,
+                    flops=beam_cands * 19.0, kernel=f"beam_weighted_kernel<{BEAM_WIDTH}>"))
     torch.cuda.synchronize()
 
     # eager reference of one headline burst, for the graph check below
@@ -453,7 +466,7 @@ def main():
                    "launch": "HIP graph per burst of copies", "accumulate": "fp32",
                    "per_step_also": "16-bit-code 14336x4096 GEMV (k=1,2); 4096x4096 GEMV (batch 1, 4; single "
                                     "and 4/16 layers per launch; 4-bit codes); dequant 4096x4096 to bf16; "
-                                    "2048-token prefill GEMM; prefix distortions; beam search"},
+                                    "2048-token prefill GEMM; prefix distortions; beam search (plain and data-aware)"},
         "per_k": per_k,
         "roofline": roofline,
     }
@@ -498,6 +511,15 @@ def main():
                             "us_per_launch": round(ob["us"], 1), "candidates_per_s": round(beam_cands / (ob["us"] * 1e-6), 1),
                             "workload": f"codes for the 2097152 groups of a 4096x4096 fp16 W, k={BEAM_K} "
                                         f"codebooks of 256, beam {BEAM_WIDTH}"}
+    ow = [o for o in ops if o["name"] == "beam_weighted"][0]
+    achw = ow["flops"] / (ow["us"] * 1e-6) / 1e12
+    out["roofline_beam_weighted"] = {
+        "bound": "alu", "kernel": ow["kernel"] + f" (k={BEAM_K})", "achieved": round(achw, 2),
+        "peak": round(FP32_PLAIN_PEAK_TOPS, 2), "unit": "TFLOP/s", "frac": round(achw / FP32_PLAIN_PEAK_TOPS, 4),
+        "traffic": None, "us_per_launch": round(ow["us"], 1),
+        "candidates_per_s": round(beam_cands / (ow["us"] * 1e-6), 1),
+        "workload": f"codes for the 2097152 groups of a 4096x4096 fp16 W minimising d^T H_j d (H_j: 8x8 blocks of "
+                    f"X X^T / n over {n_cal} calibration inputs), k={BEAM_K} codebooks of 256, beam {BEAM_WIDTH}"}
     if ceil:
         out["ceilings"] = {k: (round(v, 2) if isinstance(v, float) else v) for k, v in ceil.items()}
     tot = sum(o["step_us"] for o in ops)
@@ -509,9 +531,10 @@ def main():
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(gemv_layers)
-        dist_cpu, beam_cpu = cpu_oracle_widened(L2, make_weights, make_activations)
+        dist_cpu, beam_cpu, wbeam_cpu = cpu_oracle_widened(L2, make_weights, make_activations, Hblk.cpu().numpy())
         out["roofline_distortion"]["cpu_oracle"] = dist_cpu
         out["roofline_beam"]["cpu_oracle"] = beam_cpu
+        out["roofline_beam_weighted"]["cpu_oracle"] = wbeam_cpu
     print(json.dumps(out), flush=True)
     for v in gemv_layers.values():
         for h in v[2]:
@@ -692,7 +715,7 @@ def cpu_baseline(gemv_layers, rows=4096):
             "seconds": round(t_total, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
-def cpu_oracle_widened(layer, make_weights, make_activations):
+def cpu_oracle_widened(layer, make_weights, make_activations, H_blocks):
     """The oracle beside the distortion evaluator and the beam search, on bounded samples of the
     same workloads (a few seconds each): the fp64 prefix distortions of the first 2048 rows over 1024
     calibration inputs (in TFLOP/s of the same 2 (M + 1) d_out d_in n count), and the binary32
@@ -725,7 +748,14 @@ def cpu_oracle_widened(layer, make_weights, make_activations):
     beam = {"value": round(cands / tb, 1), "unit": "candidates/s", "cores": 1, "kind": "oracle",
             "seconds": round(tb, 2), "sample": f"binary32 beam search (k={BEAM_K}, beam {BEAM_WIDTH}) of "
                                                 f"{len(groups)} groups, one thread"}
-    return dist, beam
+    t0 = time.perf_counter()
+    oracle.beam_search_codes_weighted_f32(formats.f16_bits_to_f64(make_weights(layer)[:8]), C[:BEAM_K], s[:8],
+                                          H_blocks.astype("float64"), BEAM_K, BEAM_WIDTH, groups=groups)
+    tw = time.perf_counter() - t0
+    wbeam = {"value": round(cands / tw, 1), "unit": "candidates/s", "cores": 1, "kind": "oracle",
+             "seconds": round(tw, 2), "sample": f"binary32 data-aware beam search (k={BEAM_K}, beam {BEAM_WIDTH}) "
+                                                 f"of {len(groups)} groups, one thread"}
+    return dist, beam, wbeam
 
 
 if __name__ == "__main__":

@@ -306,6 +306,27 @@ aqmb_status aqmb_beam_search(const aqmb_desc* desc, int k, int beam, const void*
                              const uint16_t* scales, uint8_t* codes, float* errors, aqmb_stream_t stream);
 
 /*
+ * The same code search with the data-aware objective of §2.2 (Eq. wmse-task: the weighted MSE
+ * (1/n) ||(W - W_hat) X||_F^2 over calibration inputs X, which App. C's code optimisation
+ * minimises): the error of group (i, j) is d^T H_j d with d = w_ij - s_i sum_m C_m[c_m] and H_j
+ * the 8 x 8 diagonal block of H = X X^T / n for inputs 8 j .. 8 j + 7 (terms coupling different
+ * groups are left out, so groups stay independent; with every H_j = I this is aqmb_beam_search's
+ * objective). Every comparison is decided in binary32 in this order, with r the kept tuple's
+ * residual (as in aqmb_beam_search) and C the unscaled candidate codeword:
+ *   b_t = sum_u H_tu r_u and A = sum_t r_t b_t per kept tuple; Q = sum_t C_t (sum_u H_tu C_u) per
+ *   codeword; T = sum_t C_t b_t and e = (A - (2 s_i) T) + (s_i s_i) Q per candidate,
+ * every product and sum rounded, sums left to right over t, u = 0..7, no fused multiply-add;
+ * candidates ordered by e, equal e by the code tuple.
+ *   H       [d_in/8][8][8] fp32 (device, 4-byte aligned): the symmetric blocks H_j, row-major
+ *   others  as for aqmb_beam_search; errors receive e of the chosen tuple
+ * Work: 2^B (1 + (k - 1) beam) candidates per group, one workgroup per group j and 256 rows.
+ * Errors: those of aqmb_beam_search; EINVAL also for a NULL or misaligned H.
+ */
+aqmb_status aqmb_beam_search_weighted(const aqmb_desc* desc, int k, int beam, const void* W,
+                                      const uint16_t* codebooks, const uint16_t* scales, const float* H,
+                                      uint8_t* codes, float* errors, aqmb_stream_t stream);
+
+/*
  * Average storage bits per weight at level k (appendix C, Eq. avg_bits): codebooks
  * 16*g*k*2^B bits, codes d_out*(d_in/g)*B bits per used plane, scales 16*d_out bits,
  * over d_out*d_in weights. The printed codes term lacks the per-plane factor; the

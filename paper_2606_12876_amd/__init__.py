@@ -91,6 +91,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_prefix_distortion.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
     L.aqmb_prefix_distortion_noalloc.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
     L.aqmb_beam_search.argtypes = [ctypes.POINTER(Desc), i32, i32, vp, vp, vp, vp, vp, vp]
+    L.aqmb_beam_search_weighted.argtypes = [ctypes.POINTER(Desc), i32, i32, vp, vp, vp, vp, vp, vp, vp]
     L.aqmb_validate.argtypes = [ctypes.POINTER(Desc), i32, i32, i32, i32, i32, vp, vp]
     L.aqmb_bits_per_weight.argtypes = [ctypes.POINTER(Desc), i32]
     L.aqmb_bits_per_weight.restype = ctypes.c_double
@@ -102,6 +103,7 @@ def _load() -> ctypes.CDLL:
               "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_select", "aqmb_gemv_multi", "aqmb_gemm",
               "aqmb_gemm_select",
               "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_prefix_distortion_noalloc", "aqmb_beam_search",
+              "aqmb_beam_search_weighted",
               "aqmb_validate"):
         getattr(L, f).restype = st
     return L
@@ -344,6 +346,24 @@ def beam_search(desc: Desc, k: int, beam: int, W, codebooks, scales, codes, erro
         raise AqmbError(Status.EINVAL, "aqmb_beam_search", f"errors holds {ne} bytes, needs {4 * desc.d_out * G}")
     _check(lib.aqmb_beam_search(ctypes.byref(desc), k, beam, _ptr(W), _ptr(codebooks), _ptr(scales), _ptr(codes),
                                 _ptr(errors) if errors is not None else None, _stream(stream)), "aqmb_beam_search")
+
+
+def beam_search_weighted(desc: Desc, k: int, beam: int, W, codebooks, scales, H, codes, errors=None,
+                         stream=None) -> None:
+    """aqmb_beam_search_weighted: the code search with the data-aware error d^T H_j d; H is
+    [d_in/8][8][8] float32 (the symmetric diagonal blocks of X X^T / n)."""
+    G = desc.d_in // max(desc.group_size, 1)
+    _need(W, desc.d_out * desc.d_in, DType.F16, "W", "aqmb_beam_search_weighted")
+    _need(H, G * 64, DType.F32, "H", "aqmb_beam_search_weighted")
+    nc = _nbytes(codes)
+    if nc is not None and 1 <= k and nc < k * desc.d_out * G:
+        raise AqmbError(Status.EINVAL, "aqmb_beam_search_weighted", f"codes holds {nc} bytes, needs {k * desc.d_out * G}")
+    ne = _nbytes(errors) if errors is not None else None
+    if ne is not None and ne < 4 * desc.d_out * G:
+        raise AqmbError(Status.EINVAL, "aqmb_beam_search_weighted", f"errors holds {ne} bytes, needs {4 * desc.d_out * G}")
+    _check(lib.aqmb_beam_search_weighted(ctypes.byref(desc), k, beam, _ptr(W), _ptr(codebooks), _ptr(scales), _ptr(H),
+                                         _ptr(codes), _ptr(errors) if errors is not None else None, _stream(stream)),
+           "aqmb_beam_search_weighted")
 
 
 def bits_per_weight(desc: Desc, k: int) -> float:

@@ -489,6 +489,21 @@ aqmb_status aqmb_beam_search(const aqmb_desc* desc, int k, int beam, const void*
   return e == hipSuccess ? AQMB_OK : hip_fail(e, "beam_search: launch");
 }
 
+aqmb_status aqmb_beam_search_weighted(const aqmb_desc* desc, int k, int beam, const void* W,
+                                      const uint16_t* codebooks, const uint16_t* scales, const float* H,
+                                      uint8_t* codes, float* errors, aqmb_stream_t stream) {
+  clear_error();
+  aqmb_status s = validate_call(desc, 4, k, beam, AQMB_F16, AQMB_F16, W, codes);
+  if (s != AQMB_OK) return s;
+  if (!codebooks || !scales || !H) return fail(AQMB_EINVAL, "beam_search_weighted: codebooks, scales or H is NULL");
+  if ((uintptr_t)codebooks % 16) return fail(AQMB_EINVAL, "beam_search_weighted: codebooks must be 16-byte aligned");
+  if ((uintptr_t)scales % 2 || (uintptr_t)errors % 4 || (uintptr_t)H % 4)
+    return fail(AQMB_EINVAL, "beam_search_weighted: misaligned scales, H or errors");
+  hipError_t e = launch_beam_search_weighted(*desc, k, beam, W, codebooks, scales, H, codes, errors,
+                                             (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "beam_search_weighted: launch");
+}
+
 aqmb_status aqmb_dequant(aqmb_layer_t layer, int k, void* W, aqmb_dtype w_dtype, aqmb_stream_t stream) {
   clear_error();
   Layer* L = (Layer*)layer;

@@ -47,6 +47,10 @@ hipError_t distortion_static_scratch(int device, double** out, size_t* bytes);
 // Beam search of codes for every group of W [d_out][d_in] fp16 over codebooks 0..k-1 (8-bit).
 hipError_t launch_beam_search(const aqmb_desc& d, int k, int beam_width, const void* W, const uint16_t* codebooks,
                               const uint16_t* scales, unsigned char* codes, float* errors, hipStream_t st);
+// The same search for the data-aware objective d^T H_jj d (H: [G][8][8] fp32 symmetric blocks).
+hipError_t launch_beam_search_weighted(const aqmb_desc& d, int k, int beam_width, const void* W,
+                                       const uint16_t* codebooks, const uint16_t* scales, const float* H,
+                                       unsigned char* codes, float* errors, hipStream_t st);
 // Prefill GEMM tiled for small token counts (same arithmetic as launch_gemm).
 hipError_t launch_gemm_small(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
                              hipStream_t st);

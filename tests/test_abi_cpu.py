@@ -129,6 +129,10 @@ def test_bad_handles_rejected_without_gpu():
     assert A.lib.aqmb_prefix_distortion(bogus, 16, 0, 32, 0, 8, 64, None) == A.Status.EINVAL
     assert "live" in A.last_error()
     assert A.lib.aqmb_beam_search(None, 1, 1, 16, 16, 16, 16, None, None) == A.Status.EINVAL   # null desc
+    assert A.lib.aqmb_beam_search_weighted(None, 1, 1, 16, 16, 16, 16, 16, None, None) == A.Status.EINVAL
+    dw = A.make_desc(4, 64, 2)
+    assert A.lib.aqmb_beam_search_weighted(ctypes.byref(dw), 1, 1, 16, 16, 16, None, 16, None, None) == A.Status.EINVAL
+    assert "H" in A.last_error()
     d = A.Desc()
     assert A.lib.aqmb_get_desc(bogus, ctypes.byref(d)) == A.Status.EINVAL
     h = ctypes.c_void_p(0x1234)

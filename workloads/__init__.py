@@ -127,6 +127,18 @@ def make_activations(layer: Layer, rows: int, dtype: Optional[str] = None,
     raise ValueError(dtype)
 
 
+def make_calibration_inputs(layer: Layer, n: int) -> np.ndarray:
+    """Draw n calibration inputs as the columns of X [d_in][n] in fp64 (step 6 of the recipe):
+    normal(0, 1) scaled per input channel by exp(normal(0, 0.5)), with 0.5 % of the channels
+    (at least one) scaled by 10 more (the outlier channels of LLM activations), so that the
+    diagonal blocks of X X^T / n differ from group to group and are far from the identity."""
+    spec = layer.spec
+    sigma = np.exp(layer.rng.normal(0.0, 0.5, size=spec.d_in))
+    n_big = max(1, int(round(0.005 * spec.d_in)))
+    sigma[layer.rng.choice(spec.d_in, size=n_big, replace=False)] *= 10.0
+    return layer.rng.normal(0.0, 1.0, size=(spec.d_in, n)) * sigma[:, None]
+
+
 def make_weights(layer: Layer, std: float = 0.02) -> np.ndarray:
     """Draw a dense weight matrix [d_out][d_in], normal(0, std), as fp16 bits (step 5)."""
     spec = layer.spec
