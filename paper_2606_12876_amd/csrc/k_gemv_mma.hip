@@ -109,11 +109,42 @@ __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int row
 // thread the runs' registers leave no room to hold it.) No barrier orders these small loads ahead
 // of the other waves' run loads: with one or two loads per run it cost more than it saved.
 template <int K, int CB> constexpr bool mg_preload() { return K * (1 << CB) <= mg::kThreads; }
-template <int K, int CB>
+
+// Paired codebook layout (8-bit codes; the default wherever it fits). A random 16-byte gather by
+// 16 lanes is conflict-free only if the 16 lanes hit 16 different 16-byte units of the 64 banks;
+// with 8 interleaved copies of one codebook, lanes l and l + 8 use the same copy and collide when
+// their codewords have the same parity (half the time: 8 instead of 4 LDS cycles per gather).
+// Here the codebooks are stored in 64 KiB regions of 256 rows of 256 bytes, row c holding, for a
+// pair of planes (2p, 2p + 1), 8 copies of plane 2p's codeword c in its first 128 bytes and 8
+// copies of plane 2p + 1's codeword c in the second. A pair of planes is gathered in two
+// instructions: in the first, lanes with (l % 16) < 8 read their plane-2p codeword (bytes
+// 0..127 of its row, copy l % 8) and lanes with (l % 16) >= 8 their plane-(2p + 1) codeword (bytes
+// 128..255), in the second the other way round, so the 16 lanes always cover the 16 units: no
+// conflicts, whatever the codes, and no more LDS than 8 copies. A plane without a partner (odd k)
+// has a region of 16 copies. The split bf16 form pairs a plane's high and low parts. Each MFMA
+// then takes codewords of two planes in its two halves of weight rows (columns 0..7 and 8..15),
+// and the two MFMAs of a pair add both planes to every column (in a different order for the two
+// halves: fixed, so results are reproducible). Regions: ceil(k / 2), or k in the split form.
+template <int K, bool kSplit> constexpr int mg_regions() { return kSplit ? K : (K + 1) / 2; }
+template <int K, int CB, bool kSplit> constexpr bool mg_paired() { return CB == 8 && mg_regions<K, kSplit>() <= 2; }
+constexpr uint32_t kMgRegion = 256 * 256;                    // bytes per region
+
+// The codebook word (index m * NCW + c) that replication slot q copies: in the paired layout
+// slots of a pair region alternate between its two planes, so that the 16 lanes of a replica
+// write also cover the 16 units of a row.
+template <int K, int CB, bool kSplit>
+__device__ __forceinline__ int mg_rep_word(int q) {
+  if constexpr (mg_paired<K, CB, kSplit>() && !kSplit) {
+    if (q < (K / 2) * 512) return (2 * (q >> 9) + (q & 1)) * 256 + ((q & 511) >> 1);
+  }
+  return q;
+}
+
+template <int K, int CB, bool kSplit>
 __device__ __forceinline__ uint4 mg_first_word(const GemvMmaArgs& a) {
   if constexpr (!mg_preload<K, CB>()) return make_uint4(0, 0, 0, 0);
   const int q = (int)threadIdx.x < K * (1 << CB) ? (int)threadIdx.x : 0;
-  return ((const uint4*)a.codebooks)[q];
+  return ((const uint4*)a.codebooks)[mg_rep_word<K, CB, kSplit>(q)];
 }
 
 // bf16 x takes one of two forms. Converted (mg_bf16_to_f16): x becomes fp16 times a power of two
@@ -136,6 +167,45 @@ template <int K, int CB, bool kSplit>
 __device__ __forceinline__ void mg_replicate(const GemvMmaArgs& a, uint4* cb_rep, uint4 v0) {
   using namespace mg;
   constexpr int NCW = 1 << CB;
+  if constexpr (mg_paired<K, CB, kSplit>()) {
+    // write i of slot q goes to unit (i + c) % 8 of its half row (16 units for a lone plane), so
+    // the 16 lanes of a write cover a row's 16 units
+    char* base = (char*)cb_rep;
+    for (int q = threadIdx.x; q < K * NCW; q += kThreads) {
+      const uint4 v = mg_preload<K, CB>() ? v0 : ((const uint4*)a.codebooks)[mg_rep_word<K, CB, kSplit>(q)];
+      if constexpr (!kSplit) {
+        if (q < (K / 2) * 512) {                             // a pair region: 8 copies in its half
+          const int c = (q & 511) >> 1, half = q & 1;
+          char* row = base + (q >> 9) * kMgRegion + c * 256 + half * 128;
+          for (int i = 0; i < 8; ++i) *(uint4*)(row + ((i + c) & 7) * 16) = v;
+        } else {                                             // the plane without a partner: 16 copies
+          const int c = q - (K / 2) * 512;
+          char* row = base + (K / 2) * kMgRegion + c * 256;
+          for (int i = 0; i < 16; ++i) *(uint4*)(row + ((i + c) & 15) * 16) = v;
+        }
+      } else {                                               // region m: high parts, then low parts
+        const f16x8_t cv = __builtin_bit_cast(f16x8_t, v);
+        b16x8_t hi, lo;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const float cf = (float)cv[t];
+          hi[t] = (__bf16)cf;                                // round to nearest even
+          lo[t] = (__bf16)(cf - (float)hi[t]);               // exact: at most 3 significant bits
+        }
+        const uint4 vh = __builtin_bit_cast(uint4, hi), vl = __builtin_bit_cast(uint4, lo);
+        const int c = q & (NCW - 1);
+        // slots with c % 16 < 8 write their high part first, the others their low part, so the
+        // 16 lanes of each write cover both halves of a row
+        const bool sw = (c & 8) != 0;
+        const uint4 va = sw ? vl : vh, vb = sw ? vh : vl;
+        char* row = base + (q >> 8) * kMgRegion + c * 256;
+        const int ha = sw ? 128 : 0, hb = 128 - ha;
+        for (int i = 0; i < 8; ++i) *(uint4*)(row + ha + ((i + c) & 7) * 16) = va;
+        for (int i = 0; i < 8; ++i) *(uint4*)(row + hb + ((i + c) & 7) * 16) = vb;
+      }
+    }
+    return;
+  }
   for (int q = threadIdx.x; q < K * NCW; q += kThreads) {
     const uint4 v = mg_preload<K, CB>() ? v0 : ((const uint4*)a.codebooks)[q];
     const int rot = q >> (8 - a.cb_shift);
@@ -313,6 +383,60 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
       for (int q = 0; q < 4; ++q) cd[4 * t + q] = d[q];
     }
   }
+  if constexpr (mg_paired<K, CB, kSplit>()) {
+    const char* base = (const char*)cb_rep;
+    const bool upper = (lane & 8) != 0;                       // weight rows 8..15 of the tile
+    const uint32_t r8 = (uint32_t)(lane & 7) * 16 + (upper ? 128u : 0u);   // slot 0: own half
+    // the code of plane m for step j (this lane's weight row and group)
+    auto code_of = [&](int m, int j) -> uint32_t {
+      if constexpr (mg_codes_t<K, CB>()) {
+        return (cd[m] >> (8 * j)) & 0xFFu;
+      } else {
+        const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
+        return (word >> (8 * kc)) & 0xFFu;
+      }
+    };
+    if constexpr (!kSplit) {
+#pragma unroll
+      for (int pp = 0; pp < K / 2; ++pp) {
+        const char* reg = base + pp * kMgRegion;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t ca = code_of(2 * pp, j), cb2 = code_of(2 * pp + 1, j);
+          const uint32_t c0 = upper ? cb2 : ca, c1 = upper ? ca : cb2;    // slot 0: own half's plane
+          const uint4 w0 = *(const uint4*)(reg + (c0 << 8) + r8);
+          const uint4 w1 = *(const uint4*)(reg + (c1 << 8) + (r8 ^ 128u));
+          dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
+                                                          __builtin_bit_cast(f16x8_t, w0), dst[j], 0, 0, 0);
+          dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
+                                                          __builtin_bit_cast(f16x8_t, w1), dst[j], 0, 0, 0);
+        }
+      }
+      if constexpr (K & 1) {                                 // the plane without a partner: 16 copies
+        const char* reg = base + (K / 2) * kMgRegion + (uint32_t)(lane & 15) * 16;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint4 w = *(const uint4*)(reg + (code_of(K - 1, j) << 8));
+          dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
+                                                          __builtin_bit_cast(f16x8_t, w), dst[j], 0, 0, 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < K; ++m) {
+        const char* reg = base + m * kMgRegion;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t c = code_of(m, j) << 8;
+          const uint4 w0 = *(const uint4*)(reg + c + r8);            // high (rows 0..7) or low part
+          const uint4 w1 = *(const uint4*)(reg + c + (r8 ^ 128u));   // the other part
+          const b16x8_t xb = __builtin_bit_cast(b16x8_t, xs[j]);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, w0), acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, w1), acc[j], 0, 0, 0);
+        }
+      }
+    }
+  } else {
 #pragma unroll
   for (int m = 0; m < K; ++m) {
 #pragma unroll
@@ -339,6 +463,7 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, cl), acc[j], 0, 0, 0);
       }
     }
+  }
   }
   if constexpr (kConv) {
     // element e of this lane is batch row 4 kc + e, whose shift lane 4 kc + e computed
@@ -387,10 +512,12 @@ __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_
 template <int K, int XDT, int CB, int NX>
 __device__ __forceinline__ void mg_one_block(const GemvMmaArgs& a, int blk) {
   using namespace mg;
-  constexpr int kBooks = mg_split<K, XDT, NX>() ? 2 : 1;    // fp16 codewords, or bf16 high and low parts
+  constexpr bool kSpl = mg_split<K, XDT, NX>();
+  constexpr int kBooks = kSpl ? 2 : 1;                       // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
-  uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
+  uint4* cb_rep = smem_mg;                                   // paired regions, or [kBooks][K][NCW][nrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_mg + (mg_paired<K, CB, kSpl>() ? mg_regions<K, kSpl>() * (kMgRegion / 16)
+                                                                 : kBooks * K * (1 << CB) * a.nrep));   // [kWaves][64] partial tiles
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;                                 // weight row in the block
@@ -403,12 +530,12 @@ __device__ __forceinline__ void mg_one_block(const GemvMmaArgs& a, int blk) {
   // replicated into LDS (a 4096-wide row has 32 runs: two per wave).
   MgRun<K, CB, NX> ra, rb;
   int r = wave;
-  const uint4 w0 = mg_first_word<K, CB>(a);
+  const uint4 w0 = mg_first_word<K, CB, kSpl>(a);
   const int srow = row0 + mg_out_row(tid);                   // the row this thread stores, if any
   const uint16_t sbits = tid < 256 ? a.scales[srow < a.d_out ? srow : a.d_out - 1] : 0;
   mg_load_run<K, CB, NX>(a, r, rowc, true, ra);
   mg_load_run<K, CB, NX>(a, r + kWaves, rowc, true, rb);
-  mg_replicate<K, CB, mg_split<K, XDT, NX>()>(a, cb_rep, w0);
+  mg_replicate<K, CB, kSpl>(a, cb_rep, w0);
   __syncthreads();
 
   f32x4_t acc[4];
@@ -460,10 +587,12 @@ template <int K, int XDT, int CB, int NX>
 __global__ __launch_bounds__(mg::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_mma_persist_kernel(GemvMmaArgs a) {
   using namespace mg;
-  constexpr int kBooks = mg_split_p<K, XDT, NX, true>() ? 2 : 1;    // fp16 codewords, or bf16 high and low parts
+  constexpr bool kSpl = mg_split_p<K, XDT, NX, true>();
+  constexpr int kBooks = kSpl ? 2 : 1;                       // fp16 codewords, or bf16 high and low parts
   extern __shared__ uint4 smem_mg[];
-  uint4* cb_rep = smem_mg;                                   // [kBooks][K][NCW][nrep] codewords
-  f32x4_t* red = (f32x4_t*)(smem_mg + kBooks * K * (1 << CB) * a.nrep);   // [kWaves][64] partial tiles
+  uint4* cb_rep = smem_mg;                                   // paired regions, or [kBooks][K][NCW][nrep] codewords
+  f32x4_t* red = (f32x4_t*)(smem_mg + (mg_paired<K, CB, kSpl>() ? mg_regions<K, kSpl>() * (kMgRegion / 16)
+                                                                 : kBooks * K * (1 << CB) * a.nrep));   // [2][kWaves][64] partial tiles
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;
@@ -494,20 +623,22 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   };
   uint16_t sbits;
   f32x4_t acc[4];
+  // Two partial-tile buffers in turn: block b's tiles are read (by threads < 256) while the other
+  // waves go on to block b + 1; block b + 2 writes the buffer again only after block b + 1's
+  // barrier, which every thread reaches after its reads of block b.
   auto end_block = [&](int i) {                              // item i closed its block
-    mg_reduce_store(a, red, acc, block_row0(i), sbits);
+    mg_reduce_store(a, red + ((i / per) & 1) * (kWaves * 64), acc, block_row0(i), sbits);
     sbits = scale_of(i + 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();                                         // the partial tiles have been read
   };
 
   MgRun<K, CB, NX> ra, rb;
-  const uint4 w0 = mg_first_word<K, CB>(a);
+  const uint4 w0 = mg_first_word<K, CB, kSpl>(a);
   sbits = scale_of(0);
   load_item(0, ra);
   load_item(1, rb);
-  mg_replicate<K, CB, mg_split_p<K, XDT, NX, true>()>(a, cb_rep, w0);
+  mg_replicate<K, CB, kSpl>(a, cb_rep, w0);
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -529,14 +660,16 @@ static hipError_t launch_mma_knx(GemvMmaArgs a, GemvMmaMultiArgs* mm, hipStream_
   const int n_rb = (a.d_out + mg::kRows - 1) / mg::kRows;
   const bool persist = !mm && n_rb > a.n_cu && a.n_cu > 0;   // one workgroup per CU walks the blocks
   const bool split = persist ? mg_split_p<K, XDT, NX, true>() : mg_split<K, XDT, NX>();
-  const size_t red = (size_t)mg::kWaves * 64 * 16, book = (size_t)(split ? 2 : 1) * K * (1 << CB) * 16;
+  // partial tiles: one buffer, two in the persistent kernel
+  const size_t red = (size_t)(persist ? 2 : 1) * mg::kWaves * 64 * 16, book = (size_t)(split ? 2 : 1) * K * (1 << CB) * 16;
   const size_t budget = 160 * 1024 - 1024 - red;
-  // Sixteen copies (conflict-free gathers, twice the replica writes) where a workgroup gathers at
-  // least two 512-group blocks' worth: long rows, or a persistent workgroup with two or more blocks.
-  const bool many = !mm && (a.G >= 1024 || (a.n_cu > 0 && n_rb >= 2 * a.n_cu));
-  a.nrep = CB == 4 ? 1 : many && book * 16 <= budget ? 16 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
-  a.cb_shift = a.nrep == 16 ? 8 : a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
-  const size_t lds = book * a.nrep + red;
+  const bool paired = persist ? mg_paired<K, CB, mg_split_p<K, XDT, NX, true>()>()
+                              : mg_paired<K, CB, mg_split<K, XDT, NX>()>();
+  const int regions = persist ? mg_regions<K, mg_split_p<K, XDT, NX, true>()>() : mg_regions<K, mg_split<K, XDT, NX>()>();
+  // otherwise (k > 4; k > 2 split): as many interleaved copies per codebook as fit
+  a.nrep = CB == 4 ? 1 : paired ? 8 : book * 8 <= budget ? 8 : book * 4 <= budget ? 4 : 2;
+  a.cb_shift = a.nrep == 8 ? 7 : a.nrep == 4 ? 6 : a.nrep == 2 ? 5 : 4;
+  const size_t lds = (paired ? (size_t)regions * kMgRegion : book * a.nrep) + red;
   if (mm) {
     for (int l = 0; l < mm->n; ++l) {
       mm->L[l].nrep = a.nrep;
