@@ -118,6 +118,7 @@ class Ceilings:
         self.lib.aqmbc_hbm_read.argtypes = [vp, sz, i32, vp, vp]
         self.lib.aqmbc_hbm_write.argtypes = [vp, sz, i32, vp]
         self.lib.aqmbc_lds_gather.argtypes = [vp, i32, i32, i32, i32, vp, vp]
+        self.lib.aqmbc_lds_gather_paired.argtypes = [vp, i32, i32, vp, vp]
         self.lib.aqmbc_l2_gather.argtypes = [vp, i32, i32, i32, vp, vp]
         self.lib.aqmbc_mfma_bf16.argtypes = [vp, i32, i32, vp, vp]
         self.torch, self.stream = torch, stream
@@ -162,6 +163,15 @@ class Ceilings:
         n = self.n_cu
         us = self.time(lambda: self._check(self.lib.aqmbc_lds_gather(codes.data_ptr(), n, rounds, nrep, int(dot),
                                                                      self.sink.data_ptr(), self._st())))
+        return n * 1024 * 16 * rounds / (us * 1e-6) / 1e9
+
+    def lds_gather_paired(self, rounds=200):
+        """G gathers/s of random 16-byte LDS reads in the matrix-core GEMV's paired layout."""
+        torch = self.torch
+        codes = torch.randint(0, 2 ** 31 - 1, (4096,), dtype=torch.int32, device="cuda")
+        n = self.n_cu
+        us = self.time(lambda: self._check(self.lib.aqmbc_lds_gather_paired(codes.data_ptr(), n, rounds,
+                                                                            self.sink.data_ptr(), self._st())))
         return n * 1024 * 16 * rounds / (us * 1e-6) / 1e9
 
     def l2_gather(self, table_bytes, n_wg, rounds=64):
@@ -556,8 +566,10 @@ def binding_fracs(o, ceil):
         # one codeword gather per code (the matrix-core kernel serves every batch row with it; the
         # direct-gather kernel at batch 1 also spends 4 fp16 dot products on it)
         gathers = spec_rows * o["k"]
+        # the direct-gather kernel (batch 1) is bound by its gathers with their dot products; the
+        # matrix-core kernel gathers from the conflict-free paired layout
         kind = ("l2_gather_G_per_s" if o.get("code_bits") == 16 else
-                "lds_gather_dot_G_per_s" if o["b"] == 1 else "lds_gather_G_per_s")
+                "lds_gather_paired_G_per_s" if "gemv_mma" in o.get("kernel", "") else "lds_gather_dot_G_per_s")
         rate = ceil.get(kind)
         if rate:
             t = gathers / (rate * 1e9) * 1e6
@@ -590,9 +602,11 @@ def measure_ceilings(torch, stream, n_cu, ops):
     res["hbm_write_32MiB_GBps"] = (32 << 20) / (c.hbm_write(32 << 20, 16) * 1e-6) / 1e9
     res["lds_gather_G_per_s"] = c.lds_gather(8, False)
     res["lds_gather_dot_G_per_s"] = c.lds_gather(8, True)
+    res["lds_gather_paired_G_per_s"] = c.lds_gather_paired()
     res["lds_gather_note"] = ("random 16-byte LDS reads from 4 codebooks of 256 codewords stored 8 times interleaved "
                               "(the direct-gather GEMV's layout), one 1024-thread workgroup per CU; _dot adds the 4 "
-                              "fp16 dot products per codeword of the batch-1 GEMV")
+                              "fp16 dot products per codeword of the batch-1 GEMV; _paired: the matrix-core GEMV's conflict-free "
+                              "layout (two codebooks per 256-byte row, 8 copies each)")
     l2 = {}
     for tb in (1 << 20, 2 << 20):
         l2[f"{tb >> 20}MiB"] = max(c.l2_gather(tb, n_cu), c.l2_gather(tb, 2 * n_cu))

@@ -9,6 +9,7 @@
 //                 interleaved as the direct-gather GEMV stores them (codeword c of replica r at
 //                 (c nrep + r) 16 bytes, lane l reads replica l % nrep), with (dot = 1) or without
 //                 the four fp16 dot products the batch-1 GEMV spends on each codeword;
+//   - lds_gather_paired: the same reads from the matrix-core GEMV's conflict-free paired layout;
 //   - l2_gather:  random 16-byte global loads from a table that stays in the L2 caches (the
 //                 16-bit-code GEMV's codebooks);
 //   - mfma_bf16:  back-to-back v_mfma_f32_32x32x16_bf16 on operands taken from a buffer (random
@@ -94,6 +95,38 @@ __global__ __launch_bounds__(kThreads) void lds_gather_kernel(const uint32_t* __
   if (v == 0x9E3779B9u) sink[0] = v;
 }
 
+// The matrix-core GEMV's paired layout: two 64 KiB regions of 256 rows of 256 bytes, row c holding
+// 8 copies of codeword c of two codebooks (bytes 0..127 and 128..255); in gather j, lanes with
+// (lane % 16) < 8 read the first codebook's copy lane % 8 when j is even, the second when j is
+// odd, and the other lanes the reverse, so every 16 lanes hit the 64 banks once.
+__global__ __launch_bounds__(kThreads) void lds_gather_paired_kernel(const uint32_t* __restrict__ codes, int rounds,
+                                                                    unsigned* sink) {
+  extern __shared__ u32x4_t cb[];                          // [2][256][16]
+  const int tid = threadIdx.x, lane = tid & 63;
+  for (int q = tid; q < 2 * 256 * 16; q += kThreads) {
+    const u32x4_t v = {(uint32_t)q * 0x3C003C00u, (uint32_t)q, 0x3C00u, 0x3C003C00u};
+    cb[q] = v;
+  }
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = codes[tid * 4 + i];
+  const uint32_t rep = (uint32_t)(lane & 7) * 16, upper = (uint32_t)((lane >> 3) & 1);
+  __syncthreads();
+  u32x4_t acc = {0, 0, 0, 0};
+  for (int r = 0; r < rounds; ++r) {
+    const uint32_t pat = 0x01010101u * (uint32_t)(r * 37 + 11);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const uint32_t c = ((w[j >> 2] ^ pat) >> (8 * (j & 3))) & 0xFFu;
+      const uint32_t half = (uint32_t)(j & 1) ^ upper;
+      const uint32_t addr = (uint32_t)((j >> 1) & 1) * 65536 + (c << 8) + (half << 7) + rep;
+      acc ^= *(const u32x4_t*)((const char*)cb + addr);
+    }
+  }
+  const unsigned v = acc.x ^ acc.y ^ acc.z ^ acc.w;
+  if (v == 0x9E3779B9u) sink[0] = v;
+}
+
 // table: 2^log2n entries of 16 bytes. Each lane walks its own linear congruential sequence and
 // keeps 8 loads in flight.
 __global__ __launch_bounds__(kThreads) void l2_gather_kernel(const u32x4_t* __restrict__ table, int log2n, int rounds,
@@ -172,6 +205,12 @@ int aqmbc_lds_gather(const uint32_t* codes, int n_wg, int rounds, int nrep, int 
   } else {
     return (int)hipErrorInvalidValue;
   }
+  return (int)hipGetLastError();
+}
+
+// codes: at least 4096 words; 128 KiB of LDS per workgroup.
+int aqmbc_lds_gather_paired(const uint32_t* codes, int n_wg, int rounds, unsigned* sink, void* stream) {
+  lds_gather_paired_kernel<<<n_wg, kThreads, 2 * 65536, (hipStream_t)stream>>>(codes, rounds, sink);
   return (int)hipGetLastError();
 }
 
