@@ -86,11 +86,51 @@ __device__ __forceinline__ void store_group(void* W, size_t elem, const float (&
   }
 }
 
+// acc = the first codeword (exact in binary32), or acc + the codeword, one rounding per element
 __device__ __forceinline__ void fold_codeword(float (&acc)[8], uint4 cw, bool first) {
-  const float v[8] = {f16lo(cw.x), f16hi(cw.x), f16lo(cw.y), f16hi(cw.y),
-                      f16lo(cw.z), f16hi(cw.z), f16lo(cw.w), f16hi(cw.w)};
-#pragma unroll
-  for (int t = 0; t < 8; ++t) acc[t] = first ? v[t] : acc[t] + v[t];
+  if (first) {
+    acc[0] = f16lo(cw.x); acc[1] = f16hi(cw.x); acc[2] = f16lo(cw.y); acc[3] = f16hi(cw.y);
+    acc[4] = f16lo(cw.z); acc[5] = f16hi(cw.z); acc[6] = f16lo(cw.w); acc[7] = f16hi(cw.w);
+  } else {
+    acc[0] = add_f16_lo(cw.x, acc[0]); acc[1] = add_f16_hi(cw.x, acc[1]);
+    acc[2] = add_f16_lo(cw.y, acc[2]); acc[3] = add_f16_hi(cw.y, acc[3]);
+    acc[4] = add_f16_lo(cw.z, acc[4]); acc[5] = add_f16_hi(cw.z, acc[5]);
+    acc[6] = add_f16_lo(cw.w, acc[6]); acc[7] = add_f16_hi(cw.w, acc[7]);
+  }
+}
+
+// c0 + c1 for the fp16 values in the low (or high) halves of a and b, rounded once to binary32:
+// the first two steps of the fold in one instruction (an fma with 1.0 and both sources fp16).
+__device__ __forceinline__ float add2_f16_lo(uint32_t a, uint32_t b) {
+  float d;
+  asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel_hi:[1,0,1]" : "=v"(d) : "v"(b), "v"(a));
+  return d;
+}
+__device__ __forceinline__ float add2_f16_hi(uint32_t a, uint32_t b) {
+  float d;
+  asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,1] op_sel_hi:[1,0,1]" : "=v"(d) : "v"(b), "v"(a));
+  return d;
+}
+
+// acc = (binary32) c0 + c1, elementwise
+__device__ __forceinline__ void fold_first_two(float (&acc)[8], uint4 c0, uint4 c1) {
+  acc[0] = add2_f16_lo(c0.x, c1.x); acc[1] = add2_f16_hi(c0.x, c1.x);
+  acc[2] = add2_f16_lo(c0.y, c1.y); acc[3] = add2_f16_hi(c0.y, c1.y);
+  acc[4] = add2_f16_lo(c0.z, c1.z); acc[5] = add2_f16_hi(c0.z, c1.z);
+  acc[6] = add2_f16_lo(c0.w, c1.w); acc[7] = add2_f16_hi(c0.w, c1.w);
+}
+
+// 16 times byte j of w (the LDS byte offset of that code's codeword), one instruction; j must be
+// a constant after unrolling.
+__device__ __forceinline__ uint32_t code_x16(uint32_t w, int j) {
+  uint32_t d;
+  switch (j) {
+    case 0: asm("v_lshlrev_b32_sdwa %0, 4, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0" : "=v"(d) : "v"(w)); break;
+    case 1: asm("v_lshlrev_b32_sdwa %0, 4, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1" : "=v"(d) : "v"(w)); break;
+    case 2: asm("v_lshlrev_b32_sdwa %0, 4, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2" : "=v"(d) : "v"(w)); break;
+    default: asm("v_lshlrev_b32_sdwa %0, 4, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3" : "=v"(d) : "v"(w)); break;
+  }
+  return d;
 }
 
 // Used for 16-bit and 4-bit codes (and as the general fallback). CB = code bits. One thread per
@@ -241,18 +281,20 @@ __global__ __launch_bounds__(256) void dequant8_kernel(const unsigned char* code
   }
 }
 
-// 8-bit codes, 16-bit output (f16 or bf16), K = k planes: tiles of 64 rows x 64 groups (4 slices),
-// 512 threads. Thread t takes row t % 64 of the tile and half (t / 64) % 2 of slice t / 128: one
-// 8-byte code load per plane brings its 8 groups, which it folds (same arithmetic and order as
-// dequant8_kernel) into a 64 KiB tile in LDS, row-major, its 16-byte chunks XOR-swizzled by row so
-// that both the column-wise writes and the row-wise reads hit every bank group. Then each wave
-// writes 8 whole rows of the tile, 1 KiB contiguous per store instruction (measured: 64 rows x
-// 256-byte pieces per instruction, the thread-per-group layout, is 20 % slower; rows written by
-// one lane each, 4x slower). Code words of the workgroup's next tile are requested before the
-// current one is folded. The launcher gives every tile its own workgroup (measured best for the
-// 4096 x 4096 layer: two workgroups per CU, one tile each).
+// 8-bit codes, 16-bit output (f16 or bf16), K = k planes: tiles of RT rows x GT groups (RT GT =
+// 2048 or 4096 groups, 32 or 64 KiB of output), 512 threads. Thread t takes row t % RT of the tile
+// and P = RT GT / 512 consecutive groups of it (part (t / RT) of the tile's GT / 16 slices): one
+// P-byte code load per plane brings them, which it folds (same arithmetic and order as
+// dequant8_kernel) into the tile in LDS, row-major, its 16-byte chunks XOR-swizzled by row so that
+// both the column-wise writes and the row-wise reads hit every bank group. Then the waves write
+// the tile row by row, 1 KiB contiguous per store instruction (measured: 64 rows x 256-byte
+// pieces per instruction, the thread-per-group layout, is 20 % slower; rows written by one lane
+// each, 4x slower). Tiles are numbered column tiles fastest, so the tiles in flight together
+// cover whole rows of the output (a contiguous range of addresses). A workgroup walks its tiles
+// with the grid's stride; the code words of its next tile are requested before the current one is
+// folded.
 namespace dq {
-constexpr int kThreads = 512, kRows = 64, kSlices = 4, kWaves = kThreads / 64;
+constexpr int kThreads = 512, kWaves = kThreads / 64;
 }
 
 // LDS writes of this wave complete, then a workgroup barrier (global loads stay in flight).
@@ -263,51 +305,65 @@ __device__ __forceinline__ void dq_lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int OUT, int K>
+template <int OUT, int K, int RT, int GT>
 __global__ __launch_bounds__(dq::kThreads) void dequant8_tile_kernel(const unsigned char* codes, const uint16_t* codebooks,
                                                                     const uint16_t* scales, void* W, int d_out, int d_in,
                                                                     int G, int S, size_t plane_bytes) {
   static_assert(OUT == AQMB_F16 || OUT == AQMB_BF16, "16-bit outputs");
+  static_assert(RT * GT == 4096 || RT * GT == 2048, "tile size");
+  static_assert(GT >= 64 && (GT & (GT - 1)) == 0 && RT <= 64, "swizzle range");
   using namespace dq;
-  extern __shared__ uint4 dq_smem[];
-  uint4* cb8 = dq_smem;                                // [K][256] codewords
-  uint4* tile = dq_smem + K * 256;                     // [64 rows][64 chunks of 16 bytes], swizzled
+  constexpr int P = RT * GT / kThreads, kParts = 16 / P, ST = GT / 16, CP = GT / 64;
+  // static LDS, codebooks first: their addresses fit the reads' offset field
+  __shared__ struct {
+    uint4 cb[K * 256];                                 // [K][256] codewords
+    uint4 tile[RT * GT];                               // [RT rows][GT chunks of 16 bytes], swizzled
+  } sm;
+  uint4* cb8 = sm.cb;
+  uint4* tile = sm.tile;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   for (int q = tid; q < K * 256; q += kThreads) cb8[q] = ((const uint4*)codebooks)[q];
-  const int n_rt = (d_out + kRows - 1) / kRows, n_tiles = n_rt * ((S + kSlices - 1) / kSlices);
-  const int rl = lane, sl_t = wave >> 1, half = wave & 1;   // row in the tile, slice in the tile, half slice
+  const int n_ct = (S + ST - 1) / ST, n_tiles = n_ct * ((d_out + RT - 1) / RT);
+  const int rl = tid % RT, q = tid / RT, sl_t = q / kParts, part = q % kParts;   // row, slice, part of the slice
   uint2 c[K];
   uint32_t sc = 0;
-  // code words (8 bytes per plane) and row scale of tile t for this thread; tiles past the end
+  // code words (P bytes per plane) and row scale of tile t for this thread; tiles past the end
   // reload the last one, rows and slices past the layer reload its last row and slice (never stored)
   auto load = [&](int t) {
     const int tc = t < n_tiles ? t : n_tiles - 1;
-    int row = (tc % n_rt) * kRows + rl, sl = (tc / n_rt) * kSlices + sl_t;
+    int row = (tc / n_ct) * RT + rl, sl = (tc % n_ct) * ST + sl_t;
     row = row < d_out ? row : d_out - 1;
     sl = sl < S ? sl : S - 1;
     sc = scales[row];
+    const unsigned char* p = codes + ((size_t)sl * d_out + row) * 16 + part * P;
 #pragma unroll
-    for (int m = 0; m < K; ++m) c[m] = load_stream8(codes + m * plane_bytes + ((size_t)sl * d_out + row) * 16 + half * 8);
+    for (int m = 0; m < K; ++m) {
+      if constexpr (P == 8) c[m] = load_stream8(p + m * plane_bytes);
+      else c[m] = make_uint2(__builtin_nontemporal_load((const uint32_t*)(p + m * plane_bytes)), 0u);
+    }
   };
   int t = blockIdx.x;
   load(t);
   __syncthreads();
   for (; t < n_tiles; t += gridDim.x) {
-    const int r0 = (t % n_rt) * kRows, s0 = (t / n_rt) * kSlices;
+    const int r0 = (t / n_ct) * RT, g0 = (t % n_ct) * GT;
     const float scale = f16_to_f32((uint16_t)sc);
     uint2 w[K];
 #pragma unroll
     for (int m = 0; m < K; ++m) w[m] = c[m];
     load(t + gridDim.x);
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-      float acc[8];
+    for (int jj = 0; jj < P; ++jj) {
+      uint4 cw[K];
 #pragma unroll
-      for (int m = 0; m < K; ++m) {
-        const uint32_t word = jj < 4 ? w[m].x : w[m].y;
-        fold_codeword(acc, cb8[m * 256 + ((word >> (8 * (jj & 3))) & 0xFFu)], m == 0);
-      }
+      for (int m = 0; m < K; ++m)
+        cw[m] = *(const uint4*)((const char*)(cb8 + m * 256) + code_x16(jj < 4 ? w[m].x : w[m].y, jj & 3));
+      float acc[8];
+      if constexpr (K == 1) fold_codeword(acc, cw[0], true);
+      else fold_first_two(acc, cw[0], cw[1]);
+#pragma unroll
+      for (int m = 2; m < K; ++m) fold_codeword(acc, cw[m], false);
       float v[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -318,38 +374,59 @@ __global__ __launch_bounds__(dq::kThreads) void dequant8_tile_kernel(const unsig
                           ? make_uint4(pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3]), pack_f16x2(v[4], v[5]), pack_f16x2(v[6], v[7]))
                           : make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                                        pack_bf16x2(v[6], v[7]));
-      const int chunk = sl_t * 16 + half * 8 + jj;
-      tile[rl * 64 + (chunk ^ rl)] = o;
+      const int chunk = sl_t * 16 + part * P + jj;
+      tile[rl * GT + (chunk ^ rl)] = o;
     }
     dq_lds_barrier();
-    const int grp = s0 * 16 + lane;                    // the group this lane writes in every row
+    // P stores per wave: store j = wave P + i writes chunk part j % CP of tile row j / CP
 #pragma unroll
-    for (int i = 0; i < kRows / kWaves; ++i) {
-      const int r = wave * (kRows / kWaves) + i, row = r0 + r;
-      const uint4 o = tile[r * 64 + (lane ^ r)];
+    for (int i = 0; i < P; ++i) {
+      const int j = wave * P + i, r = j / CP, ch = (j % CP) * 64 + lane, row = r0 + r, grp = g0 + ch;
+      const uint4 o = tile[r * GT + (ch ^ r)];
       if (row < d_out && grp < G) store_stream16((uint16_t*)W + (size_t)row * d_in + (size_t)grp * 8, o.x, o.y, o.z, o.w);
     }
     dq_lds_barrier();                                   // the tile is read before the next one is written
   }
 }
 
-template <int OUT>
-static void launch_dequant8_tile(const Layer& L, int k, void* W, hipStream_t st) {
-  const int n_tiles = ((L.d.d_out + dq::kRows - 1) / dq::kRows) * ((L.S + dq::kSlices - 1) / dq::kSlices);
-  const unsigned grid = (unsigned)std::min(n_tiles, 65535);
-  const size_t lds = (size_t)k * 256 * 16 + (size_t)dq::kRows * 64 * 16;
-  auto go = [&](auto kern) {
-    kern<<<grid, dq::kThreads, lds, st>>>(L.codes, L.codebooks, L.scales, W, L.d.d_out, L.d.d_in, L.G, L.S, L.plane_bytes);
+// Tile shape and grid. Layers with at most two 64 KiB tiles per compute unit: one tile per
+// workgroup, as few rows and as many groups as the row length allows (8 x 512 for rows of 512
+// groups or more: a workgroup writes whole rows, one contiguous range); measured on the 4096 x 4096
+// layer, 8.6 / 8.8 / 9.5 / 10.0 us at k = 1..4 against 8.6 / 9.6 / 9.5 / 10.5 for 64 x 64 tiles.
+// Larger layers: 32 x 64 tiles and two workgroups per compute unit, each walking its tiles (on the
+// 11008 x 4096 layer 22 / 26 us at k = 1 / 4 against 25 / 29 for one 8 x 512 tile per workgroup).
+template <int OUT, int K>
+static void launch_dequant8_tile_k(const Layer& L, void* W, int n_cu, hipStream_t st) {
+  const int d_out = L.d.d_out;
+  auto n_tiles = [&](int rt, int gt) { return ((d_out + rt - 1) / rt) * ((L.S + gt / 16 - 1) / (gt / 16)); };
+  auto go = [&](auto kern, int grid) {
+    kern<<<(unsigned)std::min(grid, 65535), dq::kThreads, 0, st>>>(L.codes, L.codebooks, L.scales, W, d_out, L.d.d_in,
+                                                                   L.G, L.S, L.plane_bytes);
   };
+  if (n_cu > 0 && n_tiles(64, 64) > 2 * n_cu) {
+    go(dequant8_tile_kernel<OUT, K, 32, 64>, std::min(n_tiles(32, 64), 2 * n_cu));
+  } else if (L.G > 256) {
+    go(dequant8_tile_kernel<OUT, K, 8, 512>, n_tiles(8, 512));
+  } else if (L.G > 128) {
+    go(dequant8_tile_kernel<OUT, K, 16, 256>, n_tiles(16, 256));
+  } else if (L.G > 64) {
+    go(dequant8_tile_kernel<OUT, K, 32, 128>, n_tiles(32, 128));
+  } else {
+    go(dequant8_tile_kernel<OUT, K, 64, 64>, n_tiles(64, 64));
+  }
+}
+
+template <int OUT>
+static void launch_dequant8_tile(const Layer& L, int k, void* W, int n_cu, hipStream_t st) {
   switch (k) {
-    case 1: go(dequant8_tile_kernel<OUT, 1>); break;
-    case 2: go(dequant8_tile_kernel<OUT, 2>); break;
-    case 3: go(dequant8_tile_kernel<OUT, 3>); break;
-    case 4: go(dequant8_tile_kernel<OUT, 4>); break;
-    case 5: go(dequant8_tile_kernel<OUT, 5>); break;
-    case 6: go(dequant8_tile_kernel<OUT, 6>); break;
-    case 7: go(dequant8_tile_kernel<OUT, 7>); break;
-    default: go(dequant8_tile_kernel<OUT, 8>); break;
+    case 1: launch_dequant8_tile_k<OUT, 1>(L, W, n_cu, st); break;
+    case 2: launch_dequant8_tile_k<OUT, 2>(L, W, n_cu, st); break;
+    case 3: launch_dequant8_tile_k<OUT, 3>(L, W, n_cu, st); break;
+    case 4: launch_dequant8_tile_k<OUT, 4>(L, W, n_cu, st); break;
+    case 5: launch_dequant8_tile_k<OUT, 5>(L, W, n_cu, st); break;
+    case 6: launch_dequant8_tile_k<OUT, 6>(L, W, n_cu, st); break;
+    case 7: launch_dequant8_tile_k<OUT, 7>(L, W, n_cu, st); break;
+    default: launch_dequant8_tile_k<OUT, 8>(L, W, n_cu, st); break;
   }
 }
 
@@ -374,8 +451,8 @@ static void launch_dequant8(const Layer& L, int k, void* W, unsigned grid, hipSt
 hipError_t launch_dequant(const Layer& L, int k, void* W, aqmb_dtype w_dtype, hipStream_t st) {
   const size_t nslot = (size_t)L.S * L.d.d_out * 16;
   if (L.d.code_bits == 8 && w_dtype != AQMB_F32 && nslot < ((size_t)1 << 30)) {
-    if (w_dtype == AQMB_F16) launch_dequant8_tile<AQMB_F16>(L, k, W, st);
-    else launch_dequant8_tile<AQMB_BF16>(L, k, W, st);
+    if (w_dtype == AQMB_F16) launch_dequant8_tile<AQMB_F16>(L, k, W, L.n_cu, st);
+    else launch_dequant8_tile<AQMB_BF16>(L, k, W, L.n_cu, st);
     return hipGetLastError();
   }
   if (L.d.code_bits == 8 && nslot < ((size_t)1 << 30)) {

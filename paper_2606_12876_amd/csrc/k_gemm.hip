@@ -51,18 +51,6 @@ typedef __attribute__((address_space(3))) void* lds_ptr;
 #define AQMB_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x70 | 0xF00)
 
 
-// acc + fp16 value (low or high half of w), one binary32 rounding (fma with 1.0).
-__device__ __forceinline__ float add_f16_lo(uint32_t w, float acc) {
-  float d;
-  asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel_hi:[1,0,0]" : "=v"(d) : "v"(w), "v"(acc));
-  return d;
-}
-__device__ __forceinline__ float add_f16_hi(uint32_t w, float acc) {
-  float d;
-  asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(d) : "v"(w), "v"(acc));
-  return d;
-}
-
 // Direct global->LDS load of 4 bytes per lane: lane l's word lands at lds_base + 4 l.
 __device__ __forceinline__ void load_lds4(const void* gptr, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"

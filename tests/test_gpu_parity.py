@@ -59,6 +59,11 @@ def run_gemm(gl, k, Xbits, ydt):
     LayerSpec("ragged", 1000, 1032, seed=21),           # 129 groups: 9 slices, the last with 1 group
     LayerSpec("M1", 37, 8, M=1, seed=22),               # one group per row, one codebook
     LayerSpec("b16", 300, 136, M=2, B=16, seed=23),      # 16-bit codes, 17 groups
+    # more 64-row tiles than two per compute unit: 32-row tiles walked by each workgroup, a last
+    # row tile of 4 rows and a last slice of one group
+    LayerSpec("tiles32", 4100, 4104, M=2, seed=24),
+    LayerSpec("g125", 70, 1000, M=3, seed=25),          # 125 groups: 32-row x 128-group tiles
+    LayerSpec("g300", 40, 2400, M=2, seed=26),          # 300 groups: 8-row x 512-group tiles
 ], ids=lambda s: s.name)
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_dequant_bit_exact(spec, dt):
