@@ -289,6 +289,16 @@ __host__ __device__ inline size_t row_stride(int S) {   // bytes per staged x ro
 
 constexpr int kCwMaxBlocks = 4;   // 512-group blocks per row held in registers: d_in <= 16384
 
+// Paired codebook layout of the batch-1 direct gathers (when it fits next to x): 64 KiB regions
+// of 256 rows of 256 bytes; row c of region p holds 8 copies of C_2p[c] in its first 128 bytes and
+// 8 copies of C_2p+1[c] in the second, and a plane without a partner (odd k) has a region of 16
+// copies. A 16-byte LDS gather by 16 lanes is free of bank conflicts only when the lanes hit the
+// 16 distinct 16-byte units of a 256-byte bank row; with 8 interleaved copies of one book lanes l
+// and l + 8 share a copy and collide whenever their codewords have the same parity. Here each
+// instruction of a pair's two gathers has lanes 0..7 in one half and lanes 8..15 in the other, each
+// on its own copy: the 16 lanes cover the 16 units whatever the codes, in the LDS of 8 copies.
+constexpr uint32_t kCwRegion = 256 * 256;
+
 // <x group, codeword> of fp16 values added to s (a group's running sum over the planes).
 __device__ __forceinline__ float group_dot_acc(uint4 xw, uint4 cw, float s) {
   s = dot2_f16(xw.x, cw.x, s);
@@ -312,7 +322,7 @@ __device__ __forceinline__ float group_dot_acc(uint4 xw, uint4 cw, float s) {
 struct CwNothing {
   __device__ void operator()() const {}
 };
-template <int K, int NB, int UB, bool XS, typename After = CwNothing>
+template <int K, int NB, int UB, bool XS, bool PL, typename After = CwNothing>
 __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4* cb_rep, const uint16_t* xs,
                                         size_t rstride, int Gp, int cb_shift, uint32_t rep_off,
                                         float (&red)[cw::kWaves][cw::kRows][NB], int b0, int batch, int row,
@@ -322,6 +332,7 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rw = lane & 15, part = tid >> 4;
   const uint32_t cb_stride = 1u << cb_shift;
+  static_assert(!PL || NB == 1, "the paired layout serves one batch row");
   float acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = 0.f;
@@ -338,13 +349,67 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
       float t[8];                                          // per-group sums over the planes
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) t[jj] = 0.f;
+      if constexpr (PL) {
+        // paired layout: rows 0..7 of the block take plane 2p from their own copy in the first
+        // half of the codeword's row and plane 2p + 1 from the second half, rows 8..15 the other
+        // way round in each instruction; a group's sum adds the pair in the order of its first
+        // instruction (fixed per row, so results are reproducible)
+        const bool upper = (lane & 8) != 0;
+        const uint32_t r8 = (uint32_t)(lane & 7) * 16 + (upper ? 128u : 0u);
+#pragma unroll
+        for (int pp = 0; pp < K / 2; ++pp) {
+          uint2 ca = code[u][2 * pp], cb = code[u][2 * pp + 1];
+          asm volatile("" : "+v"(ca), "+v"(cb));
+          const uint2 w0 = upper ? cb : ca, w1 = upper ? ca : cb;
+          const char* reg = (const char*)cb_rep + pp * kCwRegion;
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {                 // four groups at a time: 8 gathers in flight
+            uint4 g0[4], g1[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const uint32_t c0 = ((hh ? w0.y : w0.x) >> (8 * q)) & 0xFFu;
+              const uint32_t c1 = ((hh ? w1.y : w1.x) >> (8 * q)) & 0xFFu;
+              g0[q] = *(const uint4*)(reg + (c0 << 8) + r8);
+              g1[q] = *(const uint4*)(reg + (c1 << 8) + (r8 ^ 128u));
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              t[4 * hh + q] = group_dot_acc(xg[4 * hh + q], g0[q], t[4 * hh + q]);
+              t[4 * hh + q] = group_dot_acc(xg[4 * hh + q], g1[q], t[4 * hh + q]);
+            }
+          }
+        }
+        if constexpr (K & 1) {                             // the plane without a partner: 16 copies
+          uint2 cm = code[u][K - 1];
+          asm volatile("" : "+v"(cm));
+          const char* reg = (const char*)cb_rep + (K / 2) * kCwRegion + (uint32_t)(lane & 15) * 16;
+          uint4 g[8];
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) {
+            const uint32_t c = ((jj < 4 ? cm.x : cm.y) >> (8 * (jj & 3))) & 0xFFu;
+            g[jj] = *(const uint4*)(reg + (c << 8));
+          }
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) t[jj] = group_dot_acc(xg[jj], g[jj], t[jj]);
+        }
+      } else {
+        // the same order of planes per group as the paired layout (rows 8..15 of the block take
+        // each complete pair in the other order), so both layouts give identical results
+        const bool upper = (lane & 8) != 0;
 #pragma unroll
       for (int m = 0; m < K; ++m) {
         // plane m's code word is awaited here, not earlier (the empty asm keeps its unpacking
         // from being hoisted above the gathers of the previous planes)
+        const bool sw = upper && m < 2 * (K / 2);
         uint2 cm = code[u][m];
-        asm volatile("" : "+v"(cm));
-        const uint32_t base = (uint32_t)(m * 256) * cb_stride + rep_off;
+        if (m < 2 * (K / 2)) {                             // a complete pair (known after unrolling)
+          uint2 co = code[u][m ^ 1];
+          asm volatile("" : "+v"(cm), "+v"(co));           // values, so that the pick is a select of registers
+          cm = upper ? co : cm;
+        } else {
+          asm volatile("" : "+v"(cm));
+        }
+        const uint32_t base = (uint32_t)((sw ? m ^ 1 : m) * 256) * cb_stride + rep_off;
         uint4 cw[8];
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
@@ -354,6 +419,7 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
         }
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) t[jj] = group_dot_acc(xg[jj], cw[jj], t[jj]);
+      }
       }
       if constexpr (XS) {                                  // the group scales, read once the sums are done
         const float4 s0 = *(const float4*)(scl + j0), s1 = *(const float4*)(scl + j0 + 4);
@@ -435,6 +501,52 @@ __device__ __forceinline__ void cw_replicate(uint4* cb_rep, uint4 cbv, int nrep,
   }
 }
 
+// The codebook word that replication slot q (a thread, q < K * 256) loads for the paired layout:
+// slots of a pair region alternate between its two planes, so that the 16 lanes of a write
+// cover the 16 units of a row.
+template <int K>
+__device__ __forceinline__ int cw_pair_word(int q) {
+  if (q < (K / 2) * 512) return (2 * (q >> 9) + (q & 1)) * 256 + ((q & 511) >> 1);
+  return q;
+}
+
+// This thread's codebook word (slot q = tid) into the paired layout: 8 copies in its half of
+// codeword c's row of a pair region, or 16 copies in the lone plane's region; write i of slot q
+// goes to unit (i + c) % 8 of its half (% 16 for the lone plane), so no two of a write's 16 lanes
+// share a bank.
+template <int K>
+__device__ __forceinline__ void cw_replicate_paired(uint4* cb_rep, uint4 v) {
+  const int q = threadIdx.x;
+  char* base = (char*)cb_rep;
+  if (q < (K / 2) * 512) {
+    const int c = (q & 511) >> 1, half = q & 1;
+    char* row = base + (q >> 9) * kCwRegion + c * 256 + half * 128;
+    for (int i = 0; i < 8; ++i) *(uint4*)(row + ((i + c) & 7) * 16) = v;
+  } else if (q < K * 256) {
+    const int c = q - (K / 2) * 512;
+    char* row = base + (K / 2) * kCwRegion + c * 256;
+    for (int i = 0; i < 16; ++i) *(uint4*)(row + ((i + c) & 15) * 16) = v;
+  }
+}
+
+template <int K, bool PL>
+__device__ __forceinline__ uint4 cw_first_word(const uint16_t* codebooks) {
+  const int q = (int)threadIdx.x % (K * 256);              // K * 256 <= 1024 codewords
+  return ((const uint4*)codebooks)[PL ? cw_pair_word<K>(q) : q];
+}
+
+template <int K, bool PL>
+__device__ __forceinline__ void cw_replicate_any(uint4* cb_rep, uint4 cbv, int nrep, int cb_shift) {
+  if constexpr (PL) cw_replicate_paired<K>(cb_rep, cbv);
+  else cw_replicate<K>(cb_rep, cbv, nrep, cb_shift);
+}
+
+// uint4 words of LDS the replicated codebooks take.
+template <int K, bool PL>
+__device__ __forceinline__ int cw_rep_words(int nrep) {
+  return PL ? ((K + 1) / 2) * (int)(kCwRegion / 16) : K * 256 * nrep;
+}
+
 // x rows b0 .. b0 + NB - 1 into LDS by direct loads; elements past d_in (and rows past `batch`)
 // read zeros from the zero page.
 template <int NB>
@@ -510,13 +622,13 @@ __device__ __forceinline__ void cw_load_codes(uint2 (&code)[UB][K], const unsign
   }
 }
 
-template <int K, int NB, int XDT, int UB>
+template <int K, int NB, int XDT, int UB, bool PL>
 __global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_cw_kernel(GemvArgs a) {
   extern __shared__ uint4 smem_cw[];
   const int nrep = a.nrep;
-  uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords
-  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);    // [NB][row_stride] x tile
+  uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords, or PL regions
+  uint16_t* xs = (uint16_t*)(cb_rep + cw_rep_words<K, PL>(nrep));   // [NB][row_stride] x tile
   __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group
   const int tid = threadIdx.x, lane = tid & 63;
@@ -531,7 +643,7 @@ void gemv_cw_kernel(GemvArgs a) {
 
   cw_stage_x<NB>(a.x, a.zero_page, 0, a.batch, a.d_in, rstride, xs_base);
   asm volatile("" ::: "memory");
-  const uint4 cbv = ((const uint4*)a.codebooks)[tid % (K * 256)];   // K * 256 <= 1024 codewords
+  const uint4 cbv = cw_first_word<K, PL>(a.codebooks);
   asm volatile("" ::: "memory");
   const uint16_t sbits = a.scales[rowc];                   // the row scale, needed only at the end
   cw_small_loads_first();
@@ -540,21 +652,21 @@ void gemv_cw_kernel(GemvArgs a) {
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in (older than the scale and codes)
   float* scl = (float*)((char*)xs + NB * rstride);         // bf16 x: [NB][rstride / 16] group scales
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
-  cw_replicate<K>(cb_rep, cbv, nrep, a.cb_shift);
+  cw_replicate_any<K, PL>(cb_rep, cbv, nrep, a.cb_shift);
   __syncthreads();
 
   // The first batch tile is peeled out of the loop so that its waits for the code planes are exact.
   const float scale = f16_to_f32(sbits);
-  cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row, row_ok,
-                          scale, a.y, a.d_out, a.y_dtype, scl);
+  cw_tile<K, NB, UB, kXS, PL>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row, row_ok,
+                              scale, a.y, a.d_out, a.y_dtype, scl);
   for (int b0 = NB; b0 < a.batch; b0 += NB) {
     __syncthreads();                                       // the previous tile's reads of xs are done
     cw_stage_x<NB>(a.x, a.zero_page, b0, a.batch, a.d_in, rstride, xs_base);
     wait_vmcnt<0>();
     if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
     __syncthreads();
-    cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, b0, a.batch, row, row_ok,
-                            scale, a.y, a.d_out, a.y_dtype, scl);
+    cw_tile<K, NB, UB, kXS, PL>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, b0, a.batch, row, row_ok,
+                                scale, a.y, a.d_out, a.y_dtype, scl);
   }
 }
 
@@ -564,14 +676,14 @@ void gemv_cw_kernel(GemvArgs a) {
 // next block are requested before the current block is gathered (two register sets in turn), so
 // a block costs its gathers, not a workgroup's start-up, load latency and replica writes. Same
 // arithmetic and reduction order as gemv_cw_kernel.
-template <int K, int NB, int XDT>
+template <int K, int NB, int XDT, bool PL>
 __global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_cw_persist_kernel(GemvArgs a) {
   constexpr int UB = 1;
   extern __shared__ uint4 smem_cw[];
   const int nrep = a.nrep;
-  uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords
-  uint16_t* xs = (uint16_t*)(cb_rep + K * 256 * nrep);    // [NB][row_stride] x tile
+  uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords, or PL regions
+  uint16_t* xs = (uint16_t*)(cb_rep + cw_rep_words<K, PL>(nrep));   // [NB][row_stride] x tile
   __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group
   const int tid = threadIdx.x, lane = tid & 63;
@@ -591,14 +703,14 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   };
   auto run_block = [&](int rb, uint32_t sbits, const uint2 (&code)[UB][K]) {
     const int row = rb * cw::kRows + rw;
-    cw_tile<K, NB, UB, kXS>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
-                            row < a.d_out, f16_to_f32((uint16_t)sbits), a.y, a.d_out, a.y_dtype, scl);
+    cw_tile<K, NB, UB, kXS, PL>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
+                                row < a.d_out, f16_to_f32((uint16_t)sbits), a.y, a.d_out, a.y_dtype, scl);
   };
 
   int rb = blockIdx.x;                                     // the grid never exceeds the block count
   cw_stage_x<NB>(a.x, a.zero_page, 0, a.batch, a.d_in, rstride, xs_base);
   asm volatile("" ::: "memory");
-  const uint4 cbv = ((const uint4*)a.codebooks)[tid % (K * 256)];   // K * 256 <= 1024 codewords
+  const uint4 cbv = cw_first_word<K, PL>(a.codebooks);
   asm volatile("" ::: "memory");
   uint32_t sa, sb;
   uint2 ca[UB][K], cb[UB][K];
@@ -606,7 +718,7 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   load_block(rb, sa, ca);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
-  cw_replicate<K>(cb_rep, cbv, nrep, a.cb_shift);
+  cw_replicate_any<K, PL>(cb_rep, cbv, nrep, a.cb_shift);
   __syncthreads();
   for (;;) {
     int nrb = rb + (int)gridDim.x;
@@ -651,7 +763,7 @@ struct GemvMultiArgs {
   int n_layers, d_in, S, batch, y_dtype, nrep, cb_shift;
 };
 
-template <int K, int NB, int XDT, int UB, bool DB>
+template <int K, int NB, int XDT, int UB, bool DB, bool PL>
 __global__ __launch_bounds__(cw::kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemv_cw_multi_kernel(GemvMultiArgs a) {
   extern __shared__ uint4 smem_cw[];
@@ -661,8 +773,9 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   // row reduction's barrier then separates those writes from the next layer's gathers, and no
   // barrier of its own is needed. A set (or buffer) is written again two layers later, after a
   // barrier that every wave reaches only once it has finished reading it.
-  uint4* rep[2] = {smem_cw, smem_cw + (DB ? K * 256 * nrep : 0)};
-  uint16_t* xs = (uint16_t*)(smem_cw + (DB ? 2 : 1) * K * 256 * nrep);
+  const int rep_words = cw_rep_words<K, PL>(nrep);
+  uint4* rep[2] = {smem_cw, smem_cw + (DB ? rep_words : 0)};
+  uint16_t* xs = (uint16_t*)(smem_cw + (DB ? 2 : 1) * rep_words);
   __shared__ float red[DB ? 2 : 1][cw::kWaves][cw::kRows][NB];
   const int tid = threadIdx.x, lane = tid & 63;
   const int rw = lane & 15;
@@ -679,7 +792,7 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   };
   // the layer's codebook word (first) and row scale; its code words
   auto load_small = [&](int l, uint4& cbv, uint32_t& sbits) {
-    cbv = ((const uint4*)a.L[l].codebooks)[tid % (K * 256)];
+    cbv = cw_first_word<K, PL>(a.L[l].codebooks);
     asm volatile("" ::: "memory");                        // the codebook word goes out first
     const int d_out = a.L[l].d_out;
     sbits = a.L[l].scales[row < d_out ? row : d_out - 1];
@@ -704,11 +817,11 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
       if constexpr (DB) {
         if (next) {
           wait_vmcnt<UB * K + 1>();                        // the next codebook word is in
-          cw_replicate<K>(rep[buf ^ 1], cbn, nrep, a.cb_shift);
+          cw_replicate_any<K, PL>(rep[buf ^ 1], cbn, nrep, a.cb_shift);
         }
       }
     };
-    cw_tile<K, NB, UB, kXS>(code, rep[buf], xs, rstride, Gp, a.cb_shift, rep_off, red[DB ? buf : 0], 0, a.batch,
+    cw_tile<K, NB, UB, kXS, PL>(code, rep[buf], xs, rstride, Gp, a.cb_shift, rep_off, red[DB ? buf : 0], 0, a.batch,
                             row, row < d_out, f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype, scl, after);
   };
   // after layer `cur` (its reduction barrier passed): make `nxt` current
@@ -717,7 +830,7 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
       buf ^= 1;
     } else {
       wait_vmcnt<UB * K + 1>();                            // the next codebook word is in
-      cw_replicate<K>(rep[0], cbn, nrep, a.cb_shift);
+      cw_replicate_any<K, PL>(rep[0], cbn, nrep, a.cb_shift);
       __syncthreads();
     }
   };
@@ -733,7 +846,7 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   load_codes(cur, ca);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
-  cw_replicate<K>(rep[0], cba, nrep, a.cb_shift);
+  cw_replicate_any<K, PL>(rep[0], cba, nrep, a.cb_shift);
   __syncthreads();
   for (;;) {
     int nxt = next_layer(cur);
@@ -771,6 +884,16 @@ static int cw_nrep(int K, int nb, int S, bool bf16, bool allow16 = false) {
 }
 static int cw_shift(int nrep) { return nrep == 16 ? 8 : nrep == 8 ? 7 : 6; }
 
+// LDS bytes with the paired layout (batch 1): (k + 1) / 2 regions plus the x tile; `sets`
+// replica sets (the multi-layer kernel's double buffering).
+static size_t cw_lds_paired(int K, int S, bool bf16, int sets = 1) {
+  const size_t xt = cw::row_stride(S);
+  return (size_t)sets * ((K + 1) / 2) * kCwRegion + xt + (bf16 ? xt / 4 : 0);
+}
+static size_t cw_budget(int nb, int sets = 1) {   // LDS left next to the row sums
+  return 160 * 1024 - (size_t)sets * cw::kWaves * cw::kRows * 4 * nb - 512;
+}
+
 static int cw_nb(int batch) { return batch == 1 ? 1 : batch == 2 ? 2 : 4; }
 static int cw_blocks(int S) { return (S * 16 + 511) / 512; }
 
@@ -786,11 +909,24 @@ static hipError_t launch_cw_nb(GemvArgs a, hipStream_t st) {
   if (a.nrep == 0) return hipErrorInvalidValue;  // x tile does not fit: caller uses another path
   a.cb_shift = cw_shift(a.nrep);
   const dim3 grid(n_rb);
+  const bool persist = cw_blocks(a.S) == 1 && a.batch <= NB && n_rb > a.n_cu && a.n_cu > 0;   // one workgroup per CU
+  if constexpr (NB == 1) {
+    // the paired layout from k = 3, and at k = 2 on rows of one 512-group block (where the
+    // interleaved copies measured faster: 4096 x 11008, k = 2, 16 copies: 7.05 against 7.28 us;
+    // paired elsewhere: 4096 x 4096, k = 3: 5.01 -> 4.70 us, k = 4: 5.70 -> 5.23 us; 11008 x
+    // 4096, k = 4: 11.6 -> 10.9 us)
+    const size_t lds = cw_lds_paired(K, a.S, XDT == AQMB_BF16);
+    if ((K >= 3 || (K == 2 && cw_blocks(a.S) == 1)) && lds <= cw_budget(NB)) {
+      if (persist) gemv_cw_persist_kernel<K, NB, XDT, true><<<dim3(a.n_cu), cw::kThreads, lds, st>>>(a);
+      else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1, true><<<grid, cw::kThreads, lds, st>>>(a);
+      else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks, true><<<grid, cw::kThreads, lds, st>>>(a);
+      return hipGetLastError();
+    }
+  }
   const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
-  if (cw_blocks(a.S) == 1 && a.batch <= NB && n_rb > a.n_cu && a.n_cu > 0)   // one workgroup per CU
-    gemv_cw_persist_kernel<K, NB, XDT><<<dim3(a.n_cu), cw::kThreads, lds, st>>>(a);
-  else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1><<<grid, cw::kThreads, lds, st>>>(a);
-  else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks><<<grid, cw::kThreads, lds, st>>>(a);
+  if (persist) gemv_cw_persist_kernel<K, NB, XDT, false><<<dim3(a.n_cu), cw::kThreads, lds, st>>>(a);
+  else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1, false><<<grid, cw::kThreads, lds, st>>>(a);
+  else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks, false><<<grid, cw::kThreads, lds, st>>>(a);
   return hipGetLastError();
 }
 
@@ -894,16 +1030,36 @@ static hipError_t launch_multi_nb(GemvMultiArgs a, int grid, hipStream_t st) {
   // two replica sets when they fit (k <= 2, one 512-group block, rows of at most 512 groups)
   const size_t lds2 = lds + (size_t)K * 256 * a.nrep * 16;
   const size_t budget = 160 * 1024 - (size_t)2 * cw::kWaves * cw::kRows * 4 * NB - 512;
+  // the paired layout at even k, where it fits (16 layers of 4096 x 4096 per launch, k = 2:
+  // 2.40 -> 2.11 us per layer, k = 4: 3.99 -> 3.75 us); at odd k the lone plane's 16 copies cost
+  // more replica writes per layer than its conflict-free gathers save (k = 1: 1.62 -> 2.28 us;
+  // k = 3: 3.15 -> 3.72 us). Both layouts give identical results.
+  if constexpr (NB == 1 && K % 2 == 0) {
+    const bool bf = XDT == AQMB_BF16;
+    if constexpr (K <= 2) {
+      const size_t p2 = cw_lds_paired(K, a.S, bf, 2);
+      if (cw_blocks(a.S) == 1 && p2 <= cw_budget(NB, 2)) {
+        gemv_cw_multi_kernel<K, NB, XDT, 1, true, true><<<grid, cw::kThreads, p2, st>>>(a);
+        return hipGetLastError();
+      }
+    }
+    const size_t p1 = cw_lds_paired(K, a.S, bf);
+    if (p1 <= cw_budget(NB)) {
+      if (cw_blocks(a.S) == 1) gemv_cw_multi_kernel<K, NB, XDT, 1, false, true><<<grid, cw::kThreads, p1, st>>>(a);
+      else gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false, true><<<grid, cw::kThreads, p1, st>>>(a);
+      return hipGetLastError();
+    }
+  }
   if constexpr (K <= 2) {
     if (cw_blocks(a.S) == 1 && lds2 <= budget) {
-      gemv_cw_multi_kernel<K, NB, XDT, 1, true><<<grid, cw::kThreads, lds2, st>>>(a);
+      gemv_cw_multi_kernel<K, NB, XDT, 1, true, false><<<grid, cw::kThreads, lds2, st>>>(a);
       return hipGetLastError();
     }
   }
   if (cw_blocks(a.S) == 1) {
-    gemv_cw_multi_kernel<K, NB, XDT, 1, false><<<grid, cw::kThreads, lds, st>>>(a);
+    gemv_cw_multi_kernel<K, NB, XDT, 1, false, false><<<grid, cw::kThreads, lds, st>>>(a);
   } else {
-    gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false><<<grid, cw::kThreads, lds, st>>>(a);
+    gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false, false><<<grid, cw::kThreads, lds, st>>>(a);
   }
   return hipGetLastError();
 }
