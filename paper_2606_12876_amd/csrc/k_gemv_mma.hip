@@ -478,21 +478,25 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
 
 // Partial tiles of the 16 waves summed in a fixed order, scaled once and rounded once, for the 16
 // weight rows from row0. Element e of lane l of a tile is batch row 4 (l / 16) + e, weight row
-// l % 16; read as floats, a tile holds 256 outputs, output o = 4 l + e. Thread t < 256 reads the
-// 16 partials of output t (all requested at once) and adds them in a fixed tree, scales and
-// stores. sbits is the scale of weight row row0 + (t / 4) % 16. Ends with the partial tiles read
-// by threads < 256 (the caller separates two calls with a barrier).
+// l % 16; read as floats, a tile holds 256 outputs, output o = 4 l + e. The four waves of group
+// grp (threads 256 grp .. 256 grp + 255; t = tid % 256) each read the 16 partials of output t (all
+// requested at once), add them in a fixed tree, scale and store; a persistent workgroup rotates
+// the group from block to block, so the extra work does not fall on the same waves at every
+// block end. sbits is the scale of weight row row0 + (t / 4) % 16. Ends with the partial tiles
+// read by the group (the caller separates two calls with a barrier).
 __device__ __forceinline__ int mg_out_row(int t) { return (t >> 2) & 15; }
+__device__ __forceinline__ bool mg_in_group(int grp) { return ((int)threadIdx.x >> 8) == grp; }
 __device__ __forceinline__ void mg_reduce_store(const GemvMmaArgs& a, mg::f32x4_t* red, const mg::f32x4_t (&acc)[4],
-                                                int row0, uint16_t sbits) {
+                                                int row0, uint16_t sbits, int grp = 0) {
   using namespace mg;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   red[wave * 64 + lane] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   __syncthreads();
-  const int b = 4 * (tid >> 6) + (tid & 3);                  // batch row of output tid (tid < 256)
-  const int row = row0 + mg_out_row(tid);
-  if (tid < 256 && b < a.batch && row < a.d_out) {
-    const float* rf = (const float*)red + tid;
+  const int t = tid & 255;
+  const int b = 4 * (t >> 6) + (t & 3);                      // batch row of output t
+  const int row = row0 + mg_out_row(t);
+  if (mg_in_group(grp) && b < a.batch && row < a.d_out) {
+    const float* rf = (const float*)red + t;
     float p[kWaves];
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) p[w] = rf[w * 256];
@@ -616,10 +620,11 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   auto block_row0 = [&](int i) {                             // first row of the block of item i
     return ((int)blockIdx.x + ((i < n_items ? i : n_items - 1) / per) * (int)gridDim.x) * kRows;
   };
-  // The scale of the row this thread stores (threads < 256), requested a block ahead.
+  // The scale of the row this thread stores (in the block's reducing group), requested a block ahead.
+  auto group_of = [&](int i) { return ((i < n_items ? i : n_items - 1) / per) & 3; };   // the block's reducing waves
   auto scale_of = [&](int i) -> uint16_t {
-    const int row = block_row0(i) + mg_out_row(tid);
-    return tid < 256 ? a.scales[row < a.d_out ? row : a.d_out - 1] : 0;
+    const int row = block_row0(i) + mg_out_row(tid & 255);
+    return mg_in_group(group_of(i)) ? a.scales[row < a.d_out ? row : a.d_out - 1] : 0;
   };
   uint16_t sbits;
   f32x4_t acc[4];
@@ -627,7 +632,7 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   // waves go on to block b + 1; block b + 2 writes the buffer again only after block b + 1's
   // barrier, which every thread reaches after its reads of block b.
   auto end_block = [&](int i) {                              // item i closed its block
-    mg_reduce_store(a, red + ((i / per) & 1) * (kWaves * 64), acc, block_row0(i), sbits);
+    mg_reduce_store(a, red + ((i / per) & 1) * (kWaves * 64), acc, block_row0(i), sbits, group_of(i));
     sbits = scale_of(i + 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -637,8 +642,10 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
   const uint4 w0 = mg_first_word<K, CB, kSpl>(a);
   sbits = scale_of(0);
   load_item(0, ra);
-  load_item(1, rb);
+  // the codebook replication waits only for the codebook word and the first item's loads; the
+  // second item's loads queue behind the replica writes
   mg_replicate<K, CB, kSpl>(a, cb_rep, w0);
+  load_item(1, rb);
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
