@@ -322,12 +322,29 @@ __device__ __forceinline__ float group_dot_acc(uint4 xw, uint4 cw, float s) {
 struct CwNothing {
   __device__ void operator()() const {}
 };
-template <int K, int NB, int UB, bool XS, bool PL, typename After = CwNothing>
+// x of a thread's 8 groups (and, for bf16 x, their scales) held in registers by kernels that run
+// several row blocks or layers on one x (one batch row, rows of one 512-group block), so that the
+// staged x is read from LDS once per workgroup instead of once per block.
+struct CwXReg {
+  uint4 x[8];
+  float s[8];
+};
+template <bool XS>
+__device__ __forceinline__ void cw_load_xreg(const uint16_t* xs, const float* scl, int Gp, CwXReg& xr) {
+  const int j0 = ((int)threadIdx.x >> 4) * 8;
+  const bool ok = j0 < Gp;                                 // parts past the padded groups: never used
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) xr.x[jj] = ok ? *(const uint4*)((const char*)xs + (size_t)(j0 + jj) * 16) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) xr.s[jj] = XS && ok ? scl[j0 + jj] : 0.f;
+}
+template <int K, int NB, int UB, bool XS, bool PL, bool XR = false, typename After = CwNothing>
 __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4* cb_rep, const uint16_t* xs,
                                         size_t rstride, int Gp, int cb_shift, uint32_t rep_off,
                                         float (&red)[cw::kWaves][cw::kRows][NB], int b0, int batch, int row,
                                         bool row_ok, float scale, void* y, int d_out, int y_dtype,
-                                        const float* scl, const After& after_gathers = After()) {
+                                        const float* scl, const CwXReg& xr, const After& after_gathers = After()) {
+  static_assert(!XR || (NB == 1 && UB == 1), "x in registers: one batch row, one block per row");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rw = lane & 15, part = tid >> 4;
@@ -345,7 +362,7 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
       // plane-major: x for the 8 groups in registers, 8 independent gathers per plane
       uint4 xg[8];
 #pragma unroll
-      for (int jj = 0; jj < 8; ++jj) xg[jj] = *(const uint4*)(xrow + jj * 16);
+      for (int jj = 0; jj < 8; ++jj) xg[jj] = XR ? xr.x[jj] : *(const uint4*)(xrow + jj * 16);
       float t[8];                                          // per-group sums over the planes
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) t[jj] = 0.f;
@@ -422,8 +439,15 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
       }
       }
       if constexpr (XS) {                                  // the group scales, read once the sums are done
-        const float4 s0 = *(const float4*)(scl + j0), s1 = *(const float4*)(scl + j0 + 4);
-        const float xsc[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        float xsc[8];
+        if constexpr (XR) {
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) xsc[jj] = xr.s[jj];
+        } else {
+          const float4 s0 = *(const float4*)(scl + j0), s1 = *(const float4*)(scl + j0 + 4);
+          xsc[0] = s0.x; xsc[1] = s0.y; xsc[2] = s0.z; xsc[3] = s0.w;
+          xsc[4] = s1.x; xsc[5] = s1.y; xsc[6] = s1.z; xsc[7] = s1.w;
+        }
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) acc[0] = __builtin_fmaf(t[jj], xsc[jj], acc[0]);
       } else {
@@ -657,8 +681,9 @@ void gemv_cw_kernel(GemvArgs a) {
 
   // The first batch tile is peeled out of the loop so that its waits for the code planes are exact.
   const float scale = f16_to_f32(sbits);
+  CwXReg xr_unused;
   cw_tile<K, NB, UB, kXS, PL>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row, row_ok,
-                              scale, a.y, a.d_out, a.y_dtype, scl);
+                              scale, a.y, a.d_out, a.y_dtype, scl, xr_unused);
   for (int b0 = NB; b0 < a.batch; b0 += NB) {
     __syncthreads();                                       // the previous tile's reads of xs are done
     cw_stage_x<NB>(a.x, a.zero_page, b0, a.batch, a.d_in, rstride, xs_base);
@@ -666,7 +691,7 @@ void gemv_cw_kernel(GemvArgs a) {
     if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
     __syncthreads();
     cw_tile<K, NB, UB, kXS, PL>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, b0, a.batch, row, row_ok,
-                                scale, a.y, a.d_out, a.y_dtype, scl);
+                                scale, a.y, a.d_out, a.y_dtype, scl, xr_unused);
   }
 }
 
@@ -695,6 +720,7 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   const int n_rb = (a.d_out + cw::kRows - 1) / cw::kRows;
   float* scl = (float*)((char*)xs + NB * rstride);         // bf16 x: [NB][rstride / 16] group scales
 
+  CwXReg xr;                                               // batch 1: x of this thread's groups, for every block
   auto load_block = [&](int rb, uint32_t& sbits, uint2 (&code)[UB][K]) {
     const int row = rb * cw::kRows + rw;
     const int rowc = row < a.d_out ? row : a.d_out - 1;
@@ -703,8 +729,8 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   };
   auto run_block = [&](int rb, uint32_t sbits, const uint2 (&code)[UB][K]) {
     const int row = rb * cw::kRows + rw;
-    cw_tile<K, NB, UB, kXS, PL>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
-                                row < a.d_out, f16_to_f32((uint16_t)sbits), a.y, a.d_out, a.y_dtype, scl);
+    cw_tile<K, NB, UB, kXS, PL, NB == 1>(code, cb_rep, xs, rstride, Gp, a.cb_shift, rep_off, red, 0, a.batch, row,
+                                         row < a.d_out, f16_to_f32((uint16_t)sbits), a.y, a.d_out, a.y_dtype, scl, xr);
   };
 
   int rb = blockIdx.x;                                     // the grid never exceeds the block count
@@ -720,6 +746,7 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
   cw_replicate_any<K, PL>(cb_rep, cbv, nrep, a.cb_shift);
   __syncthreads();
+  if constexpr (NB == 1) cw_load_xreg<kXS>(xs, scl, Gp, xr);
   for (;;) {
     int nrb = rb + (int)gridDim.x;
     load_block(nrb < n_rb ? nrb : rb, sb, cb);            // past the last block: a harmless reload
@@ -809,6 +836,10 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group, once
   float* scl = (float*)((char*)xs + NB * rstride);         // [NB][rstride / 16] group scales
   int buf = 0;                                             // the replica set and row-sum buffer in use
+  // batch 1: x of this thread's groups in registers for every layer (not with bf16 x at k = 2 in
+  // two paired replica sets, where they would not fit)
+  constexpr bool kXR = NB == 1 && UB == 1 && !(XDT == AQMB_BF16 && K == 2 && DB && PL);
+  CwXReg xr;
   // layer l from replica set `buf`; with DB and a next layer, its replicas (word cbn) go to the
   // other set once this wave's gathers are done
   auto run_layer = [&](int l, uint32_t sbits, const uint2 (&code)[UB][K], bool next, const uint4& cbn) {
@@ -821,8 +852,10 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
         }
       }
     };
-    cw_tile<K, NB, UB, kXS, PL>(code, rep[buf], xs, rstride, Gp, a.cb_shift, rep_off, red[DB ? buf : 0], 0, a.batch,
-                            row, row < d_out, f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype, scl, after);
+    cw_tile<K, NB, UB, kXS, PL, kXR>(code, rep[buf], xs, rstride, Gp, a.cb_shift, rep_off,
+                                                    red[DB ? buf : 0], 0, a.batch, row, row < d_out,
+                                                    f16_to_f32((uint16_t)sbits), a.L[l].y, d_out, a.y_dtype, scl, xr,
+                                                    after);
   };
   // after layer `cur` (its reduction barrier passed): make `nxt` current
   auto switch_to = [&](const uint4& cbn) {
@@ -848,6 +881,7 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
   cw_replicate_any<K, PL>(rep[0], cba, nrep, a.cb_shift);
   __syncthreads();
+  if constexpr (kXR) cw_load_xreg<kXS>(xs, scl, Gp, xr);
   for (;;) {
     int nxt = next_layer(cur);
     load_layer(nxt >= 0 ? nxt : cur, cbb, sb, cb);         // without a next layer: a harmless reload
