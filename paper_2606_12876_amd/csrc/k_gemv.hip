@@ -299,6 +299,18 @@ constexpr int kCwMaxBlocks = 4;   // 512-group blocks per row held in registers:
 // on its own copy: the 16 lanes cover the 16 units whatever the codes, in the LDS of 8 copies.
 constexpr uint32_t kCwRegion = 256 * 256;
 
+// LDS address of a codeword in the paired layout, one v_perm_b32: byte 1 is the code (byte j of the
+// code word w: rows of 256 bytes), bytes 0, 2 and 3 come from `base` (the lane's 16-byte unit in the
+// row, plus the LDS address of the region, a multiple of 64 KiB: the codebooks open the kernels'
+// LDS, which holds no static variables, so their address is 0).
+__device__ __forceinline__ uint32_t cw_pair_addr(uint32_t w, uint32_t base, int j) {
+  return __builtin_amdgcn_perm(w, base, 0x03020000u | ((4u + (uint32_t)j) << 8));
+}
+__device__ __forceinline__ uint4 cw_lds_read16(uint32_t addr) {
+  const u32x4_t v = *(const __attribute__((address_space(3))) u32x4_t*)(uintptr_t)addr;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // <x group, codeword> of fp16 values added to s (a group's running sum over the planes).
 __device__ __forceinline__ float group_dot_acc(uint4 xw, uint4 cw, float s) {
   s = dot2_f16(xw.x, cw.x, s);
@@ -378,16 +390,15 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
           uint2 ca = code[u][2 * pp], cb = code[u][2 * pp + 1];
           asm volatile("" : "+v"(ca), "+v"(cb));
           const uint2 w0 = upper ? cb : ca, w1 = upper ? ca : cb;
-          const char* reg = (const char*)cb_rep + pp * kCwRegion;
+          const uint32_t rb = lds_addr(cb_rep) + ((uint32_t)pp << 16);   // region base (low 16 bits zero)
+          const uint32_t b0 = r8 | rb, b1 = (r8 ^ 128u) | rb;
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {                 // four groups at a time: 8 gathers in flight
             uint4 g0[4], g1[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              const uint32_t c0 = ((hh ? w0.y : w0.x) >> (8 * q)) & 0xFFu;
-              const uint32_t c1 = ((hh ? w1.y : w1.x) >> (8 * q)) & 0xFFu;
-              g0[q] = *(const uint4*)(reg + (c0 << 8) + r8);
-              g1[q] = *(const uint4*)(reg + (c1 << 8) + (r8 ^ 128u));
+              g0[q] = cw_lds_read16(cw_pair_addr(hh ? w0.y : w0.x, b0, q));
+              g1[q] = cw_lds_read16(cw_pair_addr(hh ? w1.y : w1.x, b1, q));
             }
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
@@ -399,13 +410,10 @@ __device__ __forceinline__ void cw_tile(const uint2 (&code)[UB][K], const uint4*
         if constexpr (K & 1) {                             // the plane without a partner: 16 copies
           uint2 cm = code[u][K - 1];
           asm volatile("" : "+v"(cm));
-          const char* reg = (const char*)cb_rep + (K / 2) * kCwRegion + (uint32_t)(lane & 15) * 16;
+          const uint32_t bl = (uint32_t)(lane & 15) * 16 | (lds_addr(cb_rep) + ((uint32_t)(K / 2) << 16));
           uint4 g[8];
 #pragma unroll
-          for (int jj = 0; jj < 8; ++jj) {
-            const uint32_t c = ((jj < 4 ? cm.x : cm.y) >> (8 * (jj & 3))) & 0xFFu;
-            g[jj] = *(const uint4*)(reg + (c << 8));
-          }
+          for (int jj = 0; jj < 8; ++jj) g[jj] = cw_lds_read16(cw_pair_addr(jj < 4 ? cm.x : cm.y, bl, jj & 3));
 #pragma unroll
           for (int jj = 0; jj < 8; ++jj) t[jj] = group_dot_acc(xg[jj], g[jj], t[jj]);
         }
@@ -524,6 +532,16 @@ __device__ __forceinline__ void cw_replicate(uint4* cb_rep, uint4 cbv, int nrep,
     for (int i = 0; i < nrep; ++i) cb_rep[q * nrep + ((i + rot) & (nrep - 1))] = cbv;
   }
 }
+
+// The per-wave row sums of the direct-gather kernels sit in dynamic LDS after the x tile and its
+// group scales (the codebooks stay at LDS address 0, where codeword offsets are addresses): `sets`
+// buffers of kWaves x kRows x NB floats.
+template <int NB, int SETS = 1>
+__device__ __forceinline__ float (&cw_red(const float* scl, size_t rstride, bool bf16))[SETS][cw::kWaves][cw::kRows][NB] {
+  char* p = (char*)scl + (bf16 ? (size_t)NB * rstride / 4 : 0);
+  return *reinterpret_cast<float (*)[SETS][cw::kWaves][cw::kRows][NB]>(p);
+}
+__host__ __device__ inline size_t cw_red_bytes(int nb, int sets = 1) { return (size_t)sets * cw::kWaves * cw::kRows * nb * 4; }
 
 // The codebook word that replication slot q (a thread, q < K * 256) loads for the paired layout:
 // slots of a pair region alternate between its two planes, so that the 16 lanes of a write
@@ -653,7 +671,6 @@ void gemv_cw_kernel(GemvArgs a) {
   const int nrep = a.nrep;
   uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords, or PL regions
   uint16_t* xs = (uint16_t*)(cb_rep + cw_rep_words<K, PL>(nrep));   // [NB][row_stride] x tile
-  __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group
   const int tid = threadIdx.x, lane = tid & 63;
   const int rw = lane & 15;
@@ -675,6 +692,7 @@ void gemv_cw_kernel(GemvArgs a) {
   cw_load_codes<K, UB>(code, a.codes, a.plane_bytes, a.d_out, rowc, Gp);
   wait_vmcnt<UB * K + 1>();                                // x and the codebook word are in (older than the scale and codes)
   float* scl = (float*)((char*)xs + NB * rstride);         // bf16 x: [NB][rstride / 16] group scales
+  float (&red)[cw::kWaves][cw::kRows][NB] = cw_red<NB>(scl, rstride, kXS)[0];   // per-wave row sums
   if constexpr (kXS) cw_convert_own_bf16<NB>(xs, scl, rstride);
   cw_replicate_any<K, PL>(cb_rep, cbv, nrep, a.cb_shift);
   __syncthreads();
@@ -709,7 +727,6 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   const int nrep = a.nrep;
   uint4* cb_rep = smem_cw;                               // [K][256][nrep] codewords, or PL regions
   uint16_t* xs = (uint16_t*)(cb_rep + cw_rep_words<K, PL>(nrep));   // [NB][row_stride] x tile
-  __shared__ float red[cw::kWaves][cw::kRows][NB];        // per-wave row sums
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group
   const int tid = threadIdx.x, lane = tid & 63;
   const int rw = lane & 15;
@@ -719,6 +736,7 @@ void gemv_cw_persist_kernel(GemvArgs a) {
   const uint32_t rep_off = (uint32_t)(lane % nrep) * 16;
   const int n_rb = (a.d_out + cw::kRows - 1) / cw::kRows;
   float* scl = (float*)((char*)xs + NB * rstride);         // bf16 x: [NB][rstride / 16] group scales
+  float (&red)[cw::kWaves][cw::kRows][NB] = cw_red<NB>(scl, rstride, kXS)[0];   // per-wave row sums
 
   CwXReg xr;                                               // batch 1: x of this thread's groups, for every block
   auto load_block = [&](int rb, uint32_t& sbits, uint2 (&code)[UB][K]) {
@@ -803,7 +821,6 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   const int rep_words = cw_rep_words<K, PL>(nrep);
   uint4* rep[2] = {smem_cw, smem_cw + (DB ? rep_words : 0)};
   uint16_t* xs = (uint16_t*)(smem_cw + (DB ? 2 : 1) * rep_words);
-  __shared__ float red[DB ? 2 : 1][cw::kWaves][cw::kRows][NB];
   const int tid = threadIdx.x, lane = tid & 63;
   const int rw = lane & 15;
   const int row = blockIdx.x * cw::kRows + rw;
@@ -835,6 +852,7 @@ void gemv_cw_multi_kernel(GemvMultiArgs a) {
   };
   constexpr bool kXS = XDT == AQMB_BF16;                   // bf16 x: converted to fp16 per group, once
   float* scl = (float*)((char*)xs + NB * rstride);         // [NB][rstride / 16] group scales
+  float (&red)[DB ? 2 : 1][cw::kWaves][cw::kRows][NB] = cw_red<NB, DB ? 2 : 1>(scl, rstride, kXS);   // row sums
   int buf = 0;                                             // the replica set and row-sum buffer in use
   // batch 1: x of this thread's groups in registers for every layer (not with bf16 x at k = 2 in
   // two paired replica sets, where they would not fit)
@@ -951,16 +969,16 @@ static hipError_t launch_cw_nb(GemvArgs a, hipStream_t st) {
     // 4096, k = 4: 11.6 -> 10.9 us)
     const size_t lds = cw_lds_paired(K, a.S, XDT == AQMB_BF16);
     if ((K >= 3 || (K == 2 && cw_blocks(a.S) == 1)) && lds <= cw_budget(NB)) {
-      if (persist) gemv_cw_persist_kernel<K, NB, XDT, true><<<dim3(a.n_cu), cw::kThreads, lds, st>>>(a);
-      else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1, true><<<grid, cw::kThreads, lds, st>>>(a);
-      else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks, true><<<grid, cw::kThreads, lds, st>>>(a);
+      if (persist) gemv_cw_persist_kernel<K, NB, XDT, true><<<dim3(a.n_cu), cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
+      else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1, true><<<grid, cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
+      else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks, true><<<grid, cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
       return hipGetLastError();
     }
   }
   const size_t lds = cw_lds(K, NB, a.S, a.nrep, XDT == AQMB_BF16);
-  if (persist) gemv_cw_persist_kernel<K, NB, XDT, false><<<dim3(a.n_cu), cw::kThreads, lds, st>>>(a);
-  else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1, false><<<grid, cw::kThreads, lds, st>>>(a);
-  else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks, false><<<grid, cw::kThreads, lds, st>>>(a);
+  if (persist) gemv_cw_persist_kernel<K, NB, XDT, false><<<dim3(a.n_cu), cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
+  else if (cw_blocks(a.S) == 1) gemv_cw_kernel<K, NB, XDT, 1, false><<<grid, cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
+  else gemv_cw_kernel<K, NB, XDT, kCwMaxBlocks, false><<<grid, cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
   return hipGetLastError();
 }
 
@@ -1073,27 +1091,27 @@ static hipError_t launch_multi_nb(GemvMultiArgs a, int grid, hipStream_t st) {
     if constexpr (K <= 2) {
       const size_t p2 = cw_lds_paired(K, a.S, bf, 2);
       if (cw_blocks(a.S) == 1 && p2 <= cw_budget(NB, 2)) {
-        gemv_cw_multi_kernel<K, NB, XDT, 1, true, true><<<grid, cw::kThreads, p2, st>>>(a);
+        gemv_cw_multi_kernel<K, NB, XDT, 1, true, true><<<grid, cw::kThreads, p2 + cw_red_bytes(NB, 2), st>>>(a);
         return hipGetLastError();
       }
     }
     const size_t p1 = cw_lds_paired(K, a.S, bf);
     if (p1 <= cw_budget(NB)) {
-      if (cw_blocks(a.S) == 1) gemv_cw_multi_kernel<K, NB, XDT, 1, false, true><<<grid, cw::kThreads, p1, st>>>(a);
-      else gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false, true><<<grid, cw::kThreads, p1, st>>>(a);
+      if (cw_blocks(a.S) == 1) gemv_cw_multi_kernel<K, NB, XDT, 1, false, true><<<grid, cw::kThreads, p1 + cw_red_bytes(NB), st>>>(a);
+      else gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false, true><<<grid, cw::kThreads, p1 + cw_red_bytes(NB), st>>>(a);
       return hipGetLastError();
     }
   }
   if constexpr (K <= 2) {
     if (cw_blocks(a.S) == 1 && lds2 <= budget) {
-      gemv_cw_multi_kernel<K, NB, XDT, 1, true, false><<<grid, cw::kThreads, lds2, st>>>(a);
+      gemv_cw_multi_kernel<K, NB, XDT, 1, true, false><<<grid, cw::kThreads, lds2 + cw_red_bytes(NB, 2), st>>>(a);
       return hipGetLastError();
     }
   }
   if (cw_blocks(a.S) == 1) {
-    gemv_cw_multi_kernel<K, NB, XDT, 1, false, false><<<grid, cw::kThreads, lds, st>>>(a);
+    gemv_cw_multi_kernel<K, NB, XDT, 1, false, false><<<grid, cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
   } else {
-    gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false, false><<<grid, cw::kThreads, lds, st>>>(a);
+    gemv_cw_multi_kernel<K, NB, XDT, kCwMaxBlocks, false, false><<<grid, cw::kThreads, lds + cw_red_bytes(NB), st>>>(a);
   }
   return hipGetLastError();
 }
