@@ -384,28 +384,39 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
     }
   }
   if constexpr (mg_paired<K, CB, kSplit>()) {
-    const char* base = (const char*)cb_rep;
+    // Codeword addresses in one v_perm_b32 each: byte 1 is the code (a byte of the run's code
+    // word), bytes 0, 2 and 3 come from a per-lane base (the lane's 16-byte unit in the 256-byte
+    // row, plus the LDS address of the region, a multiple of 64 KiB: the codebooks open the
+    // kernel's LDS, which holds no static variables).
     const bool upper = (lane & 8) != 0;                       // weight rows 8..15 of the tile
     const uint32_t r8 = (uint32_t)(lane & 7) * 16 + (upper ? 128u : 0u);   // slot 0: own half
-    // the code of plane m for step j (this lane's weight row and group)
-    auto code_of = [&](int m, int j) -> uint32_t {
-      if constexpr (mg_codes_t<K, CB>()) {
-        return (cd[m] >> (8 * j)) & 0xFFu;
-      } else {
-        const uint32_t word = j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
-        return (word >> (8 * kc)) & 0xFFu;
-      }
+    const uint32_t lds0 = lds_addr(cb_rep);
+    const uint32_t kcsel = 0x03020000u | ((4u + (uint32_t)kc) << 8);      // byte kc of a slice word
+    // the word holding the code of plane m for step j (this lane's weight row and group), and the
+    // selector of its byte
+    auto word_of = [&](int m, int j) -> uint32_t {
+      if constexpr (mg_codes_t<K, CB>()) return cd[m];
+      else return j == 0 ? R.c[m].x : j == 1 ? R.c[m].y : j == 2 ? R.c[m].z : R.c[m].w;
+    };
+    auto sel_of = [&](int j) -> uint32_t {
+      if constexpr (mg_codes_t<K, CB>()) return 0x03020000u | ((4u + (uint32_t)j) << 8);
+      else return kcsel;
+    };
+    auto read = [&](uint32_t addr) -> uint4 {
+      const u32x4_t v = *(const __attribute__((address_space(3))) u32x4_t*)(uintptr_t)addr;
+      return make_uint4(v.x, v.y, v.z, v.w);
     };
     if constexpr (!kSplit) {
 #pragma unroll
       for (int pp = 0; pp < K / 2; ++pp) {
-        const char* reg = base + pp * kMgRegion;
+        const uint32_t rb = lds0 + ((uint32_t)pp << 16);
+        const uint32_t b0 = r8 | rb, b1 = (r8 ^ 128u) | rb;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const uint32_t ca = code_of(2 * pp, j), cb2 = code_of(2 * pp + 1, j);
-          const uint32_t c0 = upper ? cb2 : ca, c1 = upper ? ca : cb2;    // slot 0: own half's plane
-          const uint4 w0 = *(const uint4*)(reg + (c0 << 8) + r8);
-          const uint4 w1 = *(const uint4*)(reg + (c1 << 8) + (r8 ^ 128u));
+          const uint32_t wa = word_of(2 * pp, j), wb = word_of(2 * pp + 1, j);
+          const uint32_t w0w = upper ? wb : wa, w1w = upper ? wa : wb;     // slot 0: own half's plane
+          const uint4 w0 = read(__builtin_amdgcn_perm(w0w, b0, sel_of(j)));
+          const uint4 w1 = read(__builtin_amdgcn_perm(w1w, b1, sel_of(j)));
           dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
                                                           __builtin_bit_cast(f16x8_t, w0), dst[j], 0, 0, 0);
           dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
@@ -413,10 +424,10 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
         }
       }
       if constexpr (K & 1) {                                 // the plane without a partner: 16 copies
-        const char* reg = base + (K / 2) * kMgRegion + (uint32_t)(lane & 15) * 16;
+        const uint32_t bl = (uint32_t)(lane & 15) * 16 | (lds0 + ((uint32_t)(K / 2) << 16));
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const uint4 w = *(const uint4*)(reg + (code_of(K - 1, j) << 8));
+          const uint4 w = read(__builtin_amdgcn_perm(word_of(K - 1, j), bl, sel_of(j)));
           dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
                                                           __builtin_bit_cast(f16x8_t, w), dst[j], 0, 0, 0);
         }
@@ -424,12 +435,12 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
     } else {
 #pragma unroll
       for (int m = 0; m < K; ++m) {
-        const char* reg = base + m * kMgRegion;
+        const uint32_t bm = r8 | (lds0 + ((uint32_t)m << 16));
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const uint32_t c = code_of(m, j) << 8;
-          const uint4 w0 = *(const uint4*)(reg + c + r8);            // high (rows 0..7) or low part
-          const uint4 w1 = *(const uint4*)(reg + c + (r8 ^ 128u));   // the other part
+          const uint32_t a0 = __builtin_amdgcn_perm(word_of(m, j), bm, sel_of(j));
+          const uint4 w0 = read(a0);                                  // high (rows 0..7) or low part
+          const uint4 w1 = read(a0 ^ 128u);                           // the other part
           const b16x8_t xb = __builtin_bit_cast(b16x8_t, xs[j]);
           acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, w0), acc[j], 0, 0, 0);
           acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, w1), acc[j], 0, 0, 0);
