@@ -130,14 +130,17 @@ def test_eight_codebooks():
 
 def test_full_size_sampled_groups():
     """The benchmarked shape (4096 x 4096 weights, M = 4, k = 4, beam 8, blocks of 4096 seeded
-    calibration inputs): the whole matrix on the GPU, 120 groups spread over it against the oracle."""
+    calibration inputs): the whole matrix on the GPU, against the oracle on 1000 groups spread over
+    it, every group of the first row (each group has its own block of H) and a few fixed ones
+    (about 7 s of oracle time)."""
     L = make_layer(LayerSpec("square", 4096, 4096, M=4, seed=2))
     Wb = make_weights(L)
     Hb = _blocks(L, 4096)
     c_gpu, e_gpu = _gpu(L, Wb, Hb, 4, 8)
     rng = np.random.default_rng(6)
-    groups = [(int(i), int(j)) for i, j in zip(rng.integers(0, 4096, 120), rng.integers(0, 512, 120))]
-    groups += [(0, 0), (4095, 511), (4095, 0), (0, 511), (255, 3), (256, 3)]
+    groups = [(int(i), int(j)) for i, j in zip(rng.integers(0, 4096, 1000), rng.integers(0, 512, 1000))]
+    groups += [(0, j) for j in range(512)] + [(4095, 511), (4095, 0), (255, 3), (256, 3)]
+    groups = sorted(set(groups))
     c_ref, e_ref = _oracle(L, Wb, Hb, 4, 8, groups=groups)
     for (i, j) in groups:
         assert np.array_equal(c_gpu[:, i, j], c_ref[:, i, j]), f"codes differ at ({i}, {j})"
