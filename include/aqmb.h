@@ -227,6 +227,32 @@ aqmb_status aqmb_gemm_select(aqmb_layer_t layer, int k, const void* X, int n_tok
                              aqmb_dtype y_dtype, aqmb_gemm_tiling tiling, aqmb_stream_t stream);
 
 /*
+ * The prefill GEMM of aqmb_gemm (section 5 partial reconstruction, same definition, arguments and
+ * errors) with a caller-owned device workspace. Where aqmb_gemm_workspace_bytes reports a
+ * non-zero size and `workspace_bytes` is at least that size, the call runs in two passes: the
+ * unscaled bf16 weights Wb_k (the same binary32 fold and rounding) are written once into the
+ * workspace, tiled in matrix-core operand order, and a dense kernel multiplies X by them. The
+ * output is bit-identical to aqmb_gemm's for the same arguments. Otherwise (workspace null or too
+ * small, or the size is 0) the call is exactly aqmb_gemm.
+ *   workspace        device memory, 256-byte aligned, owned by the caller; the call writes it
+ *                    (stream-ordered on `stream`), so calls that share a workspace must be ordered
+ *   workspace_bytes  its size in bytes
+ * Errors: those of aqmb_gemm; EINVAL for a workspace that is not 256-byte aligned.
+ */
+aqmb_status aqmb_gemm_ws(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y,
+                         aqmb_dtype y_dtype, void* workspace, size_t workspace_bytes,
+                         aqmb_stream_t stream);
+
+/*
+ * *bytes = the workspace aqmb_gemm_ws needs to run the two-pass GEMM for (k, n_tokens) on this
+ * layer (2 bytes per weight, rows rounded up to 32 and d_in to 64), or 0 where that path does not
+ * apply: it is taken for k >= 2 with 4- or 8-bit codes when the one-pass choice is the 256 x 128
+ * tiling and that tiling fills every compute unit. Errors: EINVAL (bad handle, null bytes, k
+ * outside [1, M], n_tokens < 1).
+ */
+aqmb_status aqmb_gemm_workspace_bytes(aqmb_layer_t layer, int k, int n_tokens, size_t* bytes);
+
+/*
  * Dequantize (the section 5 partial reconstruction W_k written out as a dense matrix):
  * W[i][t] = W_k[i][t] in w_dtype in {F16, BF16, F32}, bit-exact to this evaluation
  * order: each fp16 codebook entry is taken exactly to binary32; the entries of planes

@@ -87,6 +87,8 @@ def _load() -> ctypes.CDLL:
     L.aqmb_gemm_select.argtypes = [vp, i32, vp, i32, vp, i32, i32, vp]
     L.aqmb_gemv_multi.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, i32, ctypes.POINTER(vp), i32, vp]
     L.aqmb_gemm.argtypes = [vp, i32, vp, i32, vp, i32, vp]
+    L.aqmb_gemm_ws.argtypes = [vp, i32, vp, i32, vp, i32, vp, ctypes.c_size_t, vp]
+    L.aqmb_gemm_workspace_bytes.argtypes = [vp, i32, i32, ctypes.POINTER(ctypes.c_size_t)]
     L.aqmb_dequant.argtypes = [vp, i32, vp, i32, vp]
     L.aqmb_prefix_distortion.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
     L.aqmb_prefix_distortion_noalloc.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp]
@@ -101,7 +103,7 @@ def _load() -> ctypes.CDLL:
     L.aqmb_last_error.restype = ctypes.c_char_p
     for f in ("aqmb_create", "aqmb_create_prefix", "aqmb_load_planes", "aqmb_drop_planes", "aqmb_resident_planes",
               "aqmb_destroy", "aqmb_get_desc", "aqmb_gemv", "aqmb_gemv_select", "aqmb_gemv_multi", "aqmb_gemm",
-              "aqmb_gemm_select",
+              "aqmb_gemm_select", "aqmb_gemm_ws", "aqmb_gemm_workspace_bytes",
               "aqmb_dequant", "aqmb_prefix_distortion", "aqmb_prefix_distortion_noalloc", "aqmb_beam_search",
               "aqmb_beam_search_weighted",
               "aqmb_validate"):
@@ -291,6 +293,24 @@ def gemm_select(layer: int, k: int, X, n_tokens: int, Y, y_dtype, tiling, stream
         _need(Y, n_tokens * d.d_out, y_dtype, "Y", "aqmb_gemm_select")
     _check(lib.aqmb_gemm_select(layer, k, _ptr(X), n_tokens, _ptr(Y), int(y_dtype), int(tiling), _stream(stream)),
            "aqmb_gemm_select")
+
+
+def gemm_workspace_bytes(layer: int, k: int, n_tokens: int) -> int:
+    """aqmb_gemm_workspace_bytes: the workspace gemm_ws needs for its two-pass path (0: not taken)."""
+    n = ctypes.c_size_t(0)
+    _check(lib.aqmb_gemm_workspace_bytes(layer, k, n_tokens, ctypes.byref(n)), "aqmb_gemm_workspace_bytes")
+    return n.value
+
+
+def gemm_ws(layer: int, k: int, X, n_tokens: int, Y, y_dtype, workspace, stream=None) -> None:
+    """aqmb_gemm_ws: aqmb_gemm with a caller-owned device workspace (a tensor, or None)."""
+    d = get_desc(layer)
+    if n_tokens >= 1:
+        _need(X, n_tokens * d.d_in, DType.BF16, "X", "aqmb_gemm_ws")
+        _need(Y, n_tokens * d.d_out, y_dtype, "Y", "aqmb_gemm_ws")
+    nb = _nbytes(workspace) if workspace is not None else 0
+    _check(lib.aqmb_gemm_ws(layer, k, _ptr(X), n_tokens, _ptr(Y), int(y_dtype), _ptr(workspace), nb or 0,
+                            _stream(stream)), "aqmb_gemm_ws")
 
 
 def dequant(layer: int, k: int, W, w_dtype, stream=None) -> None:

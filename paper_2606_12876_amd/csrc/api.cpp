@@ -433,6 +433,35 @@ aqmb_status aqmb_gemm_select(aqmb_layer_t layer, int k, const void* X, int n_tok
   return gemm_impl(layer, k, X, n_tokens, Y, y_dtype, tiling, stream, "gemm_select");
 }
 
+aqmb_status aqmb_gemm_workspace_bytes(aqmb_layer_t layer, int k, int n_tokens, size_t* bytes) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "gemm_workspace_bytes: not a live layer");
+  if (!bytes) return fail(AQMB_EINVAL, "gemm_workspace_bytes: null bytes");
+  if (k < 1 || k > L->d.num_codebooks)
+    return fail(AQMB_EINVAL, "gemm_workspace_bytes: k = %d outside [1, %d]", k, L->d.num_codebooks);
+  if (n_tokens < 1) return fail(AQMB_EINVAL, "gemm_workspace_bytes: n_tokens = %d", n_tokens);
+  *bytes = gemm_two_pass_bytes(*L, k, n_tokens);
+  return AQMB_OK;
+}
+
+aqmb_status aqmb_gemm_ws(aqmb_layer_t layer, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
+                         void* workspace, size_t workspace_bytes, aqmb_stream_t stream) {
+  clear_error();
+  Layer* L = (Layer*)layer;
+  if (!is_live(L)) return fail(AQMB_EINVAL, "gemm_ws: not a live layer");
+  if ((uintptr_t)workspace % 256 != 0) return fail(AQMB_EINVAL, "gemm_ws: workspace is not 256-byte aligned");
+  aqmb_status s = validate_call(&L->d, 1, k, n_tokens, AQMB_BF16, y_dtype, X, Y);
+  if (s != AQMB_OK) return s;
+  const size_t need = gemm_two_pass_bytes(*L, k, n_tokens);
+  if (need == 0 || !workspace || workspace_bytes < need)
+    return gemm_impl(layer, k, X, n_tokens, Y, y_dtype, AQMB_GEMM_AUTO, stream, "gemm_ws");
+  if ((s = check_resident(L, k, "gemm_ws")) != AQMB_OK) return s;
+  if ((s = check_device(L)) != AQMB_OK) return s;
+  const hipError_t e = launch_gemm_two_pass(*L, k, X, n_tokens, Y, y_dtype, workspace, (hipStream_t)stream);
+  return e == hipSuccess ? AQMB_OK : hip_fail(e, "gemm_ws");
+}
+
 aqmb_status aqmb_prefix_distortion(aqmb_layer_t layer, const void* W, aqmb_dtype w_dtype, const void* X,
                                    aqmb_dtype x_dtype, int n, double* D, aqmb_stream_t stream) {
   clear_error();

@@ -301,6 +301,218 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   }
 }
 
+// ---------------------------------------------------------------------------------------------
+// Two-pass prefill GEMM (a caller-provided workspace, k >= 2 at large token counts). With the large
+// tiles every column block of weights is dequantized once per token tile (eight times for 2048
+// tokens), and at k >= 2 the producer waves' codeword gathers (one unreplicated LDS copy of the
+// codebooks: the X ring leaves no room for replicas) outlast the matrix cores. Here the weights
+// are reconstructed once, by the same fold and rounding, into the workspace, tiled in the order
+// in which the MFMAs read them; a dense kernel then streams X and those tiles. Same products in
+// the same order as gemm_kernel<., 256, 128>: the results are bit-identical.
+//
+// Workspace layout (bf16): chunk ((c32 * nsteps + s) * 4 + i), 512 values, holds weight rows
+// 32 c32 .. 32 c32 + 31 and inputs 64 s + 16 i .. + 15 as the B fragment of one MFMA K-block:
+// value 8 l + e is row 32 c32 + (l % 32), input 64 s + 16 i + 8 (l / 32) + e (zero past d_out and
+// past d_in), which is also the order of a weight slab in gemm_kernel's LDS.
+namespace gemm2 {
+constexpr int kTileWaves = 4, kRep = 2;            // tiling pass: 4 waves, two codebook copies
+constexpr int kWaves = 8, kThreads = 64 * kWaves;  // dense pass: 8 waves (two per SIMD)
+constexpr int BM = 256, BN = 128, BK = 64, kDepth = 3;
+constexpr int kXStage = BM * BK;                   // bf16 values: 256 rows x 128 bytes
+constexpr int kSlab = (BN / 32) * 4 * gemm::kChunk;
+constexpr int kStage = kXStage + kSlab;
+}  // namespace gemm2
+
+// Pass 1. A wave takes 32 weight rows and two K-steps (lane l: row l % 32, step l / 32), a
+// workgroup 32 rows and 8 steps per item; the lane folds the 8 groups of its step and writes each
+// one 16-byte piece (a wave's writes of one group are two 512-byte runs). Codebooks: two
+// interleaved copies in LDS, lane parity choosing the copy.
+template <int K, int CB>
+__global__ __launch_bounds__(64 * gemm2::kTileWaves) void gemm_wtile_kernel(const unsigned char* __restrict__ codes,
+                                                                          const uint16_t* __restrict__ codebooks,
+                                                                          uint16_t* __restrict__ Wt, int d_out, int G,
+                                                                          int nsteps, size_t plane_bytes, int n_c32) {
+  using namespace gemm2;
+  constexpr int NCW = 1 << CB;
+  extern __shared__ uint4 cb_lds[];                // [K][NCW][kRep]
+  for (int q = threadIdx.x; q < K * NCW; q += 64 * kTileWaves) {
+    const uint4 v = ((const uint4*)codebooks)[q];
+#pragma unroll
+    for (int r = 0; r < kRep; ++r) cb_lds[q * kRep + r] = v;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rep = lane & (kRep - 1);
+  constexpr int kSteps = 2 * kTileWaves;           // steps per item
+  const int n_sc = (nsteps + kSteps - 1) / kSteps;
+  const int items = n_c32 * n_sc;
+  for (int it = blockIdx.x; it < items; it += gridDim.x) {
+    const int c32 = it / n_sc;
+    const int s = (it - c32 * n_sc) * kSteps + wave * 2 + (lane >> 5);
+    if (s >= nsteps) continue;
+    const int row = c32 * 32 + (lane & 31);
+    const bool row_ok = row < d_out;
+    const int rl = row_ok ? row : d_out - 1;
+    uint32_t w[K][2];                              // the step's 8 codes of the row, per plane
+#pragma unroll
+    for (int m = 0; m < K; ++m) {
+      if constexpr (CB == 8) {                     // 8 bytes of a 16-group slice
+        const uint2 v = *(const uint2*)(codes + m * plane_bytes + ((size_t)((8 * s) >> 4) * d_out + rl) * 16 + ((8 * s) & 15));
+        w[m][0] = v.x; w[m][1] = v.y;
+      } else {                                     // 4 bytes (8 nibbles) of a 32-group slice
+        w[m][0] = *(const uint32_t*)(codes + m * plane_bytes + ((size_t)((8 * s) >> 5) * d_out + rl) * 16 + (((8 * s) & 31) >> 1));
+        w[m][1] = 0;
+      }
+    }
+    uint16_t* dst = Wt + ((size_t)c32 * nsteps + s) * 4 * gemm::kChunk + (lane & 31) * 8;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      uint4 c[K];
+#pragma unroll
+      for (int m = 0; m < K; ++m) {
+        const uint32_t code = CB == 8 ? (w[m][g >> 2] >> (8 * (g & 3))) & 0xFFu : (w[m][0] >> (4 * g)) & 15u;
+        c[m] = cb_lds[(m * NCW + code) * kRep + rep];
+      }
+      uint4 v = fold_bf16<K>(c);
+      if (!row_ok || 8 * s + g >= G) v = make_uint4(0, 0, 0, 0);
+      *(uint4*)(dst + (g >> 1) * gemm::kChunk + 32 * (g & 1) * 8) = v;
+    }
+  }
+}
+
+// Pass 2: 256 x 128 output tiles, 8 waves (two per SIMD) of 64 tokens x 64 weight rows (2 x 2 MFMA
+// blocks of 32 x 32), d_in in steps of 64 through a ring of three LDS stages, each holding the
+// step's X rows (the swizzled layout of gemm_kernel) and its weight tile, both filled by direct
+// global->LDS loads two steps ahead; one barrier per step. Column blocks start their K walk at the
+// steps gemm_kernel uses. Workgroups are placed on XCDs (workgroup w runs on XCD w mod 8) in a
+// grid of ga x gb blocks of token tiles x column blocks, so that the workgroups sharing weight
+// tiles and X rows share an L2 (ga = 0: the plain order).
+template <int YDT>
+__global__ __launch_bounds__(gemm2::kThreads) void gemm_dense_kernel(const uint16_t* __restrict__ Wt,
+                                                                    const uint16_t* __restrict__ scales,
+                                                                    const uint16_t* __restrict__ X, void* __restrict__ Y,
+                                                                    int n_tokens, int d_out, int d_in, int nsteps,
+                                                                    int n_tb, int n_cb, int n_c32, int ga, int gb) {
+  using namespace gemm2;
+  constexpr int MA = 2, NBB = 2;                   // 32 x 32 blocks per wave: 2 token x 2 weight row
+  constexpr int kXLoads = BM / (8 * kWaves), kWLoads = BN / (8 * kWaves), kLoads = kXLoads + kWLoads;
+  constexpr int kRowsW = BM / kWaves;              // X rows loaded by each wave
+  extern __shared__ uint4 smem2[];
+  uint16_t* S = (uint16_t*)smem2;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int half = lane >> 5, r32 = lane & 31;
+  int tb = blockIdx.x % n_tb, cb = blockIdx.x / n_tb;
+  if (ga > 0) {
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3, per_cb = n_cb / gb, per_tb = n_tb / ga;
+    cb = per_cb * (xcd % gb) + j % per_cb;
+    tb = per_tb * (xcd / gb) + j / per_cb;
+  }
+  const int n0 = tb * BM, i0 = cb * BN;
+  const int s0 = (int)(((long long)cb * nsteps) / n_cb);
+  auto step_of = [&](int seq) { int st = s0 + seq; return st >= nsteps ? st - nsteps : st; };
+
+  auto load_stage = [&](int seq) {
+    const int st = step_of(seq);
+    const int k0 = st * BK;
+    uint16_t* stage = S + (seq % kDepth) * kStage;
+#pragma unroll
+    for (int t = 0; t < kWLoads; ++t) {            // chunk c: column block c / 4, K-block c % 4
+      const int c = wave * kWLoads + t;
+      int c32 = i0 / 32 + (c >> 2);
+      if (c32 >= n_c32) c32 = n_c32 - 1;           // rows past d_out: any valid tile, never stored
+      load_lds16(Wt + (((size_t)c32 * nsteps + st) * 4 + (c & 3)) * gemm::kChunk + lane * 8,
+                 lds_addr(stage + kXStage + c * gemm::kChunk));
+    }
+    const int pos = lane & 7, rsub = lane >> 3;
+    if (k0 + BK <= d_in) {
+#pragma unroll
+      for (int t = 0; t < kXLoads; ++t) {
+        const int r = wave * kRowsW + t * 8 + rsub;
+        const int kc = pos ^ ((r >> 1) & 7);
+        const int row = n0 + r < n_tokens ? n0 + r : n_tokens - 1;
+        load_lds16(X + (size_t)row * d_in + k0 + kc * 8, lds_addr(stage + (wave * kRowsW + t * 8) * BK));
+      }
+    } else {                                       // the ragged last step: zero past d_in
+#pragma unroll
+      for (int t = 0; t < kXLoads; ++t) {
+        const int r = wave * kRowsW + t * 8 + rsub;
+        const int kc = pos ^ ((r >> 1) & 7);
+        const int row = n0 + r;
+        uint16_t* base = stage + (wave * kRowsW + t * 8) * BK;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (row < n_tokens && k0 + kc * 8 < d_in) v = *(const uint4*)(X + (size_t)row * d_in + k0 + kc * 8);
+        *(uint4*)(base + lane * 8) = v;
+      }
+    }
+  };
+  const int wm = wave >> 1, wn = wave & 1;         // tokens 64 wm .., weight rows 64 wn ..
+  f32x16_t acc[MA][NBB];
+#pragma unroll
+  for (int a = 0; a < MA; ++a)
+#pragma unroll
+    for (int b = 0; b < NBB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
+  struct Frags { bf16x8_t a[MA], b[NBB]; };
+  auto read_frags = [&](const uint16_t* xst, const uint16_t* bsl, int i, Frags& f) {
+#pragma unroll
+    for (int b = 0; b < NBB; ++b) f.b[b] = *(const bf16x8_t*)(bsl + ((wn * NBB + b) * 4 + i) * gemm::kChunk + lane * 8);
+    const int kc = 2 * i + half;
+#pragma unroll
+    for (int a = 0; a < MA; ++a) {
+      const int r = wm * 64 + a * 32 + r32;
+      f.a[a] = *(const bf16x8_t*)(xst + r * BK + ((kc ^ ((r >> 1) & 7)) * 8));
+    }
+  };
+  auto mfmas = [&](const Frags& f) {
+#pragma unroll
+    for (int a = 0; a < MA; ++a)
+#pragma unroll
+      for (int b = 0; b < NBB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
+  };
+  for (int seq = 0; seq < kDepth - 1 && seq < nsteps; ++seq) load_stage(seq);
+  for (int seq = 0; seq < nsteps; ++seq) {
+    {                                              // own loads of step seq done (step seq + 1's may be out)
+      const int after = min(kDepth - 2, nsteps - 1 - seq);
+      if (after >= 1) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
+    }
+    __syncthreads();                               // stage seq published; stage seq - 1 free
+    if (seq + kDepth - 1 < nsteps) load_stage(seq + kDepth - 1);
+    const uint16_t* xst = S + (seq % kDepth) * kStage;
+    const uint16_t* bsl = xst + kXStage;
+    Frags f0, f1;
+    read_frags(xst, bsl, 0, f0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      Frags& cur = (i & 1) ? f1 : f0;
+      Frags& nxt = (i & 1) ? f0 : f1;
+      if (i < 3) read_frags(xst, bsl, i + 1, nxt);
+      mfmas(cur);
+      if (i < 3) {
+        __builtin_amdgcn_sched_group_barrier(0x100, MA + NBB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NBB * MA, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < NBB; ++b) {
+    const int col = i0 + wn * 64 + b * 32 + r32;
+    if (col >= d_out) continue;
+    const float scale = f16_to_f32(scales[col]);
+#pragma unroll
+    for (int a = 0; a < MA; ++a) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = n0 + wm * 64 + a * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+        if (row < n_tokens) OutT<YDT>::store(Y, (size_t)row * d_out + col, acc[a][b][e] * scale);
+      }
+    }
+  }
+}
+
 template <int K, int CB, int BMT, int BNT>
 static void launch_kcm(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
   using namespace gemm;
@@ -365,6 +577,66 @@ hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void*
     case 7: launch_k<7>(L, X, n_tokens, Y, y_dtype, tile, st); break;
     default: launch_k<8>(L, X, n_tokens, Y, y_dtype, tile, st); break;
   }
+  return hipGetLastError();
+}
+
+
+// Workspace bytes of the two-pass GEMM (0: the path does not apply). It applies at k >= 2 with 4-
+// or 8-bit codes where the library's choice is the 256 x 128 tiling with at least one workgroup
+// per compute unit (the same per-output arithmetic as that tiling).
+size_t gemm_two_pass_bytes(const Layer& L, int k, int n_tokens) {
+  if (k < 2 || (L.d.code_bits != 8 && L.d.code_bits != 4)) return 0;
+  if (gemm_tile(L, n_tokens, -1) != 0) return 0;
+  const long long wg = (long long)((n_tokens + gemm2::BM - 1) / gemm2::BM) * ((L.d.d_out + gemm2::BN - 1) / gemm2::BN);
+  if (wg < (L.n_cu > 0 ? L.n_cu : 256)) return 0;
+  const size_t n_c32 = (L.d.d_out + 31) / 32, nsteps = (L.d.d_in + gemm2::BK - 1) / gemm2::BK;
+  return n_c32 * nsteps * 4 * gemm::kChunk * 2;
+}
+
+template <int K, int CB>
+static void launch_wtile(const Layer& L, uint16_t* Wt, int n_c32, int nsteps, hipStream_t st) {
+  using namespace gemm2;
+  const int items = n_c32 * ((nsteps + 2 * kTileWaves - 1) / (2 * kTileWaves));
+  const int grid = items < 2048 ? items : 2048;
+  const size_t lds = (size_t)K * (1 << CB) * kRep * 16;
+  gemm_wtile_kernel<K, CB><<<grid, 64 * kTileWaves, lds, st>>>(L.codes, L.codebooks, Wt, L.d.d_out, L.G, nsteps,
+                                                              L.plane_bytes, n_c32);
+}
+
+template <int K>
+static void launch_wtile_k(const Layer& L, uint16_t* Wt, int n_c32, int nsteps, hipStream_t st) {
+  if (L.d.code_bits == 4) launch_wtile<K, 4>(L, Wt, n_c32, nsteps, st);
+  else launch_wtile<K, 8>(L, Wt, n_c32, nsteps, st);
+}
+
+hipError_t launch_gemm_two_pass(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
+                                void* workspace, hipStream_t st) {
+  using namespace gemm2;
+  const int n_c32 = (L.d.d_out + 31) / 32, nsteps = (L.d.d_in + BK - 1) / BK;
+  uint16_t* Wt = (uint16_t*)workspace;
+  switch (k) {
+    case 2: launch_wtile_k<2>(L, Wt, n_c32, nsteps, st); break;
+    case 3: launch_wtile_k<3>(L, Wt, n_c32, nsteps, st); break;
+    case 4: launch_wtile_k<4>(L, Wt, n_c32, nsteps, st); break;
+    case 5: launch_wtile_k<5>(L, Wt, n_c32, nsteps, st); break;
+    case 6: launch_wtile_k<6>(L, Wt, n_c32, nsteps, st); break;
+    case 7: launch_wtile_k<7>(L, Wt, n_c32, nsteps, st); break;
+    default: launch_wtile_k<8>(L, Wt, n_c32, nsteps, st); break;
+  }
+  const int n_tb = (n_tokens + BM - 1) / BM, n_cb = (L.d.d_out + BN - 1) / BN;
+  // XCD blocks: token tiles in ga groups, column blocks in gb groups, ga * gb = 8
+  int ga = 0, gb = 0;
+  const int cand[4][2] = {{2, 4}, {1, 8}, {4, 2}, {8, 1}};
+  for (const auto& c : cand)
+    if (n_tb % c[0] == 0 && n_cb % c[1] == 0) { ga = c[0]; gb = c[1]; break; }
+  const size_t lds = (size_t)kDepth * kStage * 2;
+  const dim3 grid(n_tb * n_cb);
+  if (y_dtype == AQMB_BF16)
+    gemm_dense_kernel<AQMB_BF16><<<grid, kThreads, lds, st>>>(Wt, L.scales, (const uint16_t*)X, Y, n_tokens, L.d.d_out,
+                                                             L.d.d_in, nsteps, n_tb, n_cb, n_c32, ga, gb);
+  else
+    gemm_dense_kernel<AQMB_F32><<<grid, kThreads, lds, st>>>(Wt, L.scales, (const uint16_t*)X, Y, n_tokens, L.d.d_out,
+                                                            L.d.d_in, nsteps, n_tb, n_cb, n_c32, ga, gb);
   return hipGetLastError();
 }
 

@@ -58,5 +58,10 @@ hipError_t launch_gemm_small(const Layer& L, int k, const void* X, int n_tokens,
 // 1 = 128 x 128, 2 = 128 x 64 (tokens x weight rows).
 hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, int tile,
                        hipStream_t st);
+// Two-pass prefill GEMM (bit-identical to the 256 x 128 tiling): workspace bytes (0 where it does
+// not apply) and the launch (workspace of at least that many bytes, 256-byte aligned).
+size_t gemm_two_pass_bytes(const Layer& L, int k, int n_tokens);
+hipError_t launch_gemm_two_pass(const Layer& L, int k, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype,
+                                void* workspace, hipStream_t st);
 
 }  // namespace aqmb
