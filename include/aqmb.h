@@ -246,7 +246,7 @@ aqmb_status aqmb_gemm_ws(aqmb_layer_t layer, int k, const void* X, int n_tokens,
 /*
  * *bytes = the workspace aqmb_gemm_ws needs to run the two-pass GEMM for (k, n_tokens) on this
  * layer (2 bytes per weight, rows rounded up to 32 and d_in to 64), or 0 where that path does not
- * apply: it is taken for k >= 2 with 4- or 8-bit codes when the one-pass choice is the 256 x 128
+ * apply: it is taken for k >= 3 with 4- or 8-bit codes when the one-pass choice is the 256 x 128
  * tiling and that tiling fills every compute unit. Errors: EINVAL (bad handle, null bytes, k
  * outside [1, M], n_tokens < 1).
  */

@@ -39,7 +39,7 @@ namespace aqmb {
 
 namespace gemm {
 constexpr int BM = 256, BN = 128, BK = 64;
-constexpr int kThreads = 512;                        // waves 0-3 consume, waves 4-7 produce
+constexpr int kThreads = 512;                        // waves 0-3 consume, waves 4-7 produce (four consumer waves)
 template <int K> constexpr int x_depth() { return K <= 4 ? 3 : 2; }   // X stages (LDS budget)
 template <int BMT> constexpr int x_stage() { return BMT * BK; }   // bf16 elements: BMT rows x 128 bytes
 constexpr int kChunk = 512;                          // one weight fragment: 64 lanes x 8 bf16
@@ -87,8 +87,8 @@ __device__ __forceinline__ uint4 dequant_group_bf16(const uint4* __restrict__ cb
 }
 
 // CB = code bits: 8 (256 codewords per codebook) or 4 (16 codewords).
-template <int K, int YDT, int CB, int BMT, int BNT>
-__global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned char* __restrict__ codes,
+template <int K, int YDT, int CB, int BMT, int BNT, int CW = 4>
+__global__ __launch_bounds__(64 * (CW + 4)) void gemm_kernel(const unsigned char* __restrict__ codes,
                                                               const uint16_t* __restrict__ codebooks,
                                                               const uint16_t* __restrict__ scales,
                                                               const uint16_t* __restrict__ X, void* __restrict__ Y,
@@ -98,9 +98,11 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   constexpr int kDepth = x_depth<K>();
   constexpr int NCW = 1 << CB;
   constexpr int kXStage = x_stage<BMT>();
-  constexpr int MA = BMT / 64;                     // 32-row MFMA blocks per consumer wave
+  constexpr int kThreads = 64 * (CW + 4);          // CW consumer waves, then 4 producer waves
+  constexpr int MA = BMT / (CW / 2) / 32;          // 32-row MFMA blocks per consumer wave
   constexpr int NBB = BNT / 64;                    // 32-column MFMA blocks per consumer wave
-  constexpr int kXLoads = BMT / 32;                // direct X loads per consumer wave and step
+  constexpr int kXLoads = BMT / (8 * CW);          // direct X loads per consumer wave and step
+  constexpr int kRowsW = BMT / CW;                 // X rows loaded by each consumer wave
   constexpr int kSlab = slab_elems<BNT>();
   constexpr int QG = BNT / 32;                     // groups per producer thread and step
   extern __shared__ uint4 smem[];
@@ -120,16 +122,16 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
 
   for (int q = tid; q < K * NCW; q += kThreads) cbs[q] = ((const uint4*)codebooks)[q];
 
-  if (wave >= 4) {
+  if (wave >= CW) {
     // ------------------------------------------------------------------ producers
-    const int p = tid - 256;
+    const int p = tid - 64 * CW;
     const int col = p & (BNT - 1), gq = p / BNT;   // weight row; groups QG gq .. QG gq + QG - 1 of a step
     const bool col_ok = i0 + col < d_out;
     // Code words: each producer wave streams exactly the words its own lanes need (one 4-byte
     // word per plane holding this thread's groups of its column in the step) straight into its own
     // LDS ring, kCodeDepth steps ahead, and waits only for its own loads (no other wave reads
     // them). Exactly K loads per step per wave, so "step q's words are in" is a fixed vmcnt.
-    const int pw = wave - 4;
+    const int pw = wave - CW;
     const int col_ld = col_ok ? i0 + col : d_out - 1;
     auto ring_base = [&](int seq) {
       return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)(cring + ((seq % kCodeDepth) * 4 + pw) * K * 64);
@@ -199,7 +201,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
   }
 
   // -------------------------------------------------------------------- consumers
-  const int wm = wave >> 1, wn = wave & 1;          // BMT/2 x 64 block of the tile
+  const int wm = wave >> 1, wn = wave & 1;          // BMT/(CW/2) x 64 block of the tile
   // X stage layout: row r's 16-byte piece kc (8 bf16 of K) sits at r * 128 + ((kc ^ ((r >> 1) & 7)) * 16)
   // bytes. A direct load covers 8 rows x 128 bytes (8 lanes per row, full cache lines); the
   // XOR keeps fragment reads (32 rows, one piece each) on distinct banks.
@@ -210,19 +212,19 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
     if (k0 + BK <= d_in) {
 #pragma unroll
       for (int t = 0; t < kXLoads; ++t) {           // this wave's rows (BMT/4) wave .. + BMT/4 - 1
-        const int r = wave * (BMT / 4) + t * 8 + rsub;
+        const int r = wave * kRowsW + t * 8 + rsub;
         const int kc = pos ^ ((r >> 1) & 7);
         const int row = n0 + r < n_tokens ? n0 + r : n_tokens - 1;
-        uint16_t* base = stage + (wave * (BMT / 4) + t * 8) * BK;   // 1 KiB: 8 rows, written lane-ordered
+        uint16_t* base = stage + (wave * kRowsW + t * 8) * BK;   // 1 KiB: 8 rows, written lane-ordered
         load_lds16(X + (size_t)row * d_in + k0 + kc * 8, (uint32_t)(uintptr_t)(lds_ptr)base);
       }
     } else {                                         // the ragged last step: zero past d_in
 #pragma unroll
       for (int t = 0; t < kXLoads; ++t) {
-        const int r = wave * (BMT / 4) + t * 8 + rsub;
+        const int r = wave * kRowsW + t * 8 + rsub;
         const int kc = pos ^ ((r >> 1) & 7);
         const int row = n0 + r;
-        uint16_t* base = stage + (wave * (BMT / 4) + t * 8) * BK;
+        uint16_t* base = stage + (wave * kRowsW + t * 8) * BK;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (row < n_tokens && k0 + kc * 8 < d_in) v = *(const uint4*)(X + (size_t)row * d_in + k0 + kc * 8);
         *(uint4*)(base + lane * 8) = v;
@@ -244,7 +246,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
     const int kc = 2 * i + half;
 #pragma unroll
     for (int a = 0; a < MA; ++a) {
-      const int r = wm * (BMT / 2) + a * 32 + r32;
+      const int r = wm * (BMT / (CW / 2)) + a * 32 + r32;
       f.a[a] = *(const bf16x8_t*)(xst + r * BK + ((kc ^ ((r >> 1) & 7)) * 8));
     }
   };
@@ -294,7 +296,7 @@ __global__ __launch_bounds__(gemm::kThreads) void gemm_kernel(const unsigned cha
     for (int a = 0; a < MA; ++a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int row = n0 + wm * (BMT / 2) + a * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+        const int row = n0 + wm * (BMT / (CW / 2)) + a * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
         if (row < n_tokens) OutT<YDT>::store(Y, (size_t)row * d_out + col, acc[a][b][e] * scale);
       }
     }
@@ -513,7 +515,7 @@ __global__ __launch_bounds__(gemm2::kThreads) void gemm_dense_kernel(const uint1
   }
 }
 
-template <int K, int CB, int BMT, int BNT>
+template <int K, int CB, int BMT, int BNT, int CW>
 static void launch_kcm(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, hipStream_t st) {
   using namespace gemm;
   constexpr int kDepth = x_depth<K>();
@@ -522,10 +524,10 @@ static void launch_kcm(const Layer& L, const void* X, int n_tokens, void* Y, aqm
                      (size_t)kCodeDepth * 4 * K * 64 * 4;
   const dim3 grid(n_tb * n_cb);
   if (y_dtype == AQMB_BF16)
-    gemm_kernel<K, AQMB_BF16, CB, BMT, BNT><<<grid, kThreads, lds, st>>>(
+    gemm_kernel<K, AQMB_BF16, CB, BMT, BNT, CW><<<grid, 64 * (CW + 4), lds, st>>>(
         L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y, n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
   else
-    gemm_kernel<K, AQMB_F32, CB, BMT, BNT><<<grid, kThreads, lds, st>>>(
+    gemm_kernel<K, AQMB_F32, CB, BMT, BNT, CW><<<grid, 64 * (CW + 4), lds, st>>>(
         L.codes, L.codebooks, L.scales, (const uint16_t*)X, Y, n_tokens, L.d.d_out, L.d.d_in, L.G, L.plane_bytes, n_tb, n_cb);
 }
 
@@ -552,9 +554,15 @@ template <int K, int CB>
 static void launch_kc(const Layer& L, const void* X, int n_tokens, void* Y, aqmb_dtype y_dtype, int tile,
                       hipStream_t st) {
   switch (gemm_tile(L, n_tokens, tile)) {
-    case 0: launch_kcm<K, CB, 256, 128>(L, X, n_tokens, Y, y_dtype, st); break;
-    case 1: launch_kcm<K, CB, 128, 128>(L, X, n_tokens, Y, y_dtype, st); break;
-    default: launch_kcm<K, CB, 128, 64>(L, X, n_tokens, Y, y_dtype, st); break;
+    // 256 x 128 tiles at k <= 2: eight consumer waves (two per SIMD, 64 x 64 each) beside the four
+    // producers (2048 tokens, 4096 x 4096: 73.2 -> 72.0 us at k = 1, 79.9 -> 77.5 us at k = 2); from
+    // k = 3, and on the smaller tiles, four consumer waves are faster
+    case 0:
+      if constexpr (K <= 2) launch_kcm<K, CB, 256, 128, 8>(L, X, n_tokens, Y, y_dtype, st);
+      else launch_kcm<K, CB, 256, 128, 4>(L, X, n_tokens, Y, y_dtype, st);
+      break;
+    case 1: launch_kcm<K, CB, 128, 128, 4>(L, X, n_tokens, Y, y_dtype, st); break;
+    default: launch_kcm<K, CB, 128, 64, 4>(L, X, n_tokens, Y, y_dtype, st); break;
   }
 }
 
@@ -581,11 +589,12 @@ hipError_t launch_gemm(const Layer& L, int k, const void* X, int n_tokens, void*
 }
 
 
-// Workspace bytes of the two-pass GEMM (0: the path does not apply). It applies at k >= 2 with 4-
+// Workspace bytes of the two-pass GEMM (0: the path does not apply). It applies at k >= 3 with 4-
 // or 8-bit codes where the library's choice is the 256 x 128 tiling with at least one workgroup
-// per compute unit (the same per-output arithmetic as that tiling).
+// per compute unit (the same per-output arithmetic as that tiling). At k <= 2 the one-pass kernel
+// with eight consumer waves is as fast (2048 x 4096 x 4096, k = 2: 77.5 us against 80.1).
 size_t gemm_two_pass_bytes(const Layer& L, int k, int n_tokens) {
-  if (k < 2 || (L.d.code_bits != 8 && L.d.code_bits != 4)) return 0;
+  if (k < 3 || (L.d.code_bits != 8 && L.d.code_bits != 4)) return 0;
   if (gemm_tile(L, n_tokens, -1) != 0) return 0;
   const long long wg = (long long)((n_tokens + gemm2::BM - 1) / gemm2::BM) * ((L.d.d_out + gemm2::BN - 1) / gemm2::BN);
   if (wg < (L.n_cu > 0 ? L.n_cu : 256)) return 0;

@@ -4,7 +4,7 @@ dense matrix-core kernel), against the oracle's GEMM reference and bit for bit a
 The two-pass path forms the same bf16 weight tile (binary32 left fold over the first k planes,
 round to nearest even) and adds the same products in the same order as aqmb_gemm's 256 x 128
 tiling, so outputs must be identical; the oracle check (gemm_reference, the definition with the
-explicit bf16 weight rounding) pins both. Shapes: the full prefill workload at every k >= 2, 4-bit
+explicit bf16 weight rounding) pins both. Shapes: the full prefill workload at every k >= 3, 4-bit
 codes, ragged rows / inputs / tokens with and without an XCD placement of the workgroups, both
 output dtypes, and the cases that fall back to aqmb_gemm.
 """
@@ -61,31 +61,31 @@ def _check(spec, n, ks, ydts=("bf16",), oracle_rows=None):
 
 
 def test_prefill_workload_every_k():
-    """2048 tokens x 4096 x 4096, M = 4: k = 2, 3, 4 against the full oracle product."""
+    """2048 tokens x 4096 x 4096, M = 4: k = 3, 4 against the full oracle product."""
     spec = config("prefill")
-    _check(spec, spec.n_tokens, (2, 3, 4), ydts=("bf16", "f32"))
+    _check(spec, spec.n_tokens, (3, 4), ydts=("bf16", "f32"))
 
 
 def test_ragged_everywhere_xcd_blocks():
     """d_out = 4000 (the last 32-row tile half empty), d_in = 4040 (505 groups: a ragged last
     K-step), 2000 tokens (a ragged last token tile); 8 x 32 workgroups in XCD blocks."""
-    _check(LayerSpec("rg", 4000, 4040, M=3, seed=301), 2000, (2, 3), oracle_rows=np.r_[0:40, 1950:2000])
+    _check(LayerSpec("rg", 4000, 4040, M=3, seed=301), 2000, (3,), oracle_rows=np.r_[0:40, 1950:2000])
 
 
 def test_plain_workgroup_order():
     """9 token tiles x 31 column blocks: no XCD blocking divides the grid (plain order)."""
-    _check(LayerSpec("po", 3900, 1024, M=2, seed=302), 2100, (2,), ydts=("f32",),
+    _check(LayerSpec("po", 3900, 1024, M=3, seed=302), 2100, (3,), ydts=("f32",),
            oracle_rows=np.r_[0:32, 2048:2100])
 
 
 def test_four_bit_codes_and_eight_planes():
     """16-codeword books (nibble codes) and k up to 8."""
-    _check(LayerSpec("b4", 4096, 2048, M=4, B=4, seed=303), 2048, (2, 4), oracle_rows=np.r_[0:24, 2024:2048])
+    _check(LayerSpec("b4", 4096, 2048, M=4, B=4, seed=303), 2048, (3, 4), oracle_rows=np.r_[0:24, 2024:2048])
     _check(LayerSpec("m8", 4096, 1024, M=8, seed=304), 2048, (5, 8), oracle_rows=np.r_[0:16, 2040:2048])
 
 
 def test_fallbacks_and_rejections():
-    """k = 1, few tokens or a small / absent workspace: exactly aqmb_gemm. A workspace that is not
+    """k <= 2, few tokens or a small / absent workspace: exactly aqmb_gemm. A workspace that is not
     256-byte aligned is refused and nothing is written."""
     spec = config("prefill")
     L = make_layer(spec)
@@ -94,6 +94,7 @@ def test_fallbacks_and_rejections():
     X = to_dev(Xbits).view(torch.bfloat16)
     with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
         assert A.gemm_workspace_bytes(gl.handle, 1, n) == 0
+        assert A.gemm_workspace_bytes(gl.handle, 2, n) == 0
         assert A.gemm_workspace_bytes(gl.handle, 4, 100) == 0          # 16-row tiling
         assert A.gemm_workspace_bytes(gl.handle, 4, 512) == 0          # smaller tiles
         nb = A.gemm_workspace_bytes(gl.handle, 4, n)
