@@ -72,6 +72,12 @@ def test_ragged_everywhere_xcd_blocks():
     _check(LayerSpec("rg", 4000, 4040, M=3, seed=301), 2000, (3,), oracle_rows=np.r_[0:40, 1950:2000])
 
 
+def test_two_rounds_of_workgroups():
+    """4096 tokens (16 token tiles x 32 column blocks: two workgroups per compute unit in turn)."""
+    spec = config("prefill")
+    _check(spec, 4096, (4,), oracle_rows=np.r_[0:16, 2040:2056, 4080:4096])
+
+
 def test_plain_workgroup_order():
     """9 token tiles x 31 column blocks: no XCD blocking divides the grid (plain order)."""
     _check(LayerSpec("po", 3900, 1024, M=3, seed=302), 2100, (3,), ydts=("f32",),
