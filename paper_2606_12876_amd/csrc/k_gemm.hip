@@ -377,7 +377,8 @@ __global__ __launch_bounds__(64 * gemm2::kTileWaves) void gemm_wtile_kernel(cons
       }
       uint4 v = fold_bf16<K>(c);
       if (!row_ok || 8 * s + g >= G) v = make_uint4(0, 0, 0, 0);
-      *(uint4*)(dst + (g >> 1) * gemm::kChunk + 32 * (g & 1) * 8) = v;
+      const u32x4_t vv = {v.x, v.y, v.z, v.w};        // non-temporal: the tiles are read once, by the dense pass
+      __builtin_nontemporal_store(vv, (u32x4_t*)(dst + (g >> 1) * gemm::kChunk + 32 * (g & 1) * 8));
     }
   }
 }
