@@ -406,47 +406,76 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
       const u32x4_t v = *(const __attribute__((address_space(3))) u32x4_t*)(uintptr_t)addr;
       return make_uint4(v.x, v.y, v.z, v.w);
     };
+    // The run's codeword reads, listed in the order their MFMAs consume them, are issued kAhead
+    // ahead of those MFMAs (scheduling groups: kAhead reads, then one MFMA and one read in turn),
+    // so the LDS latency of a gather is not paid before every product; consecutive MFMAs go to
+    // the four steps' accumulators in turn. Each accumulator still adds its products in the same
+    // order (pair by pair, slot 0 then slot 1).
+    constexpr int kReads = kSplit ? 2 * K * 4 : (K / 2) * 8 + (K & 1) * 4;
+    constexpr int kAhead = kReads < 4 ? kReads : 4;
+    uint4 wv[kReads];
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (!kSplit) {
 #pragma unroll
       for (int pp = 0; pp < K / 2; ++pp) {
         const uint32_t rb = lds0 + ((uint32_t)pp << 16);
         const uint32_t b0 = r8 | rb, b1 = (r8 ^ 128u) | rb;
+        uint32_t w0w[4], w1w[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const uint32_t wa = word_of(2 * pp, j), wb = word_of(2 * pp + 1, j);
-          const uint32_t w0w = upper ? wb : wa, w1w = upper ? wa : wb;     // slot 0: own half's plane
-          const uint4 w0 = read(__builtin_amdgcn_perm(w0w, b0, sel_of(j)));
-          const uint4 w1 = read(__builtin_amdgcn_perm(w1w, b1, sel_of(j)));
-          dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
-                                                          __builtin_bit_cast(f16x8_t, w0), dst[j], 0, 0, 0);
-          dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
-                                                          __builtin_bit_cast(f16x8_t, w1), dst[j], 0, 0, 0);
+          w0w[j] = upper ? wb : wa;                          // slot 0: own half's plane
+          w1w[j] = upper ? wa : wb;
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wv[pp * 8 + j] = read(__builtin_amdgcn_perm(w0w[j], b0, sel_of(j)));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wv[pp * 8 + 4 + j] = read(__builtin_amdgcn_perm(w1w[j], b1, sel_of(j)));
       }
       if constexpr (K & 1) {                                 // the plane without a partner: 16 copies
         const uint32_t bl = (uint32_t)(lane & 15) * 16 | (lds0 + ((uint32_t)(K / 2) << 16));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint4 w = read(__builtin_amdgcn_perm(word_of(K - 1, j), bl, sel_of(j)));
+        for (int j = 0; j < 4; ++j) wv[(K / 2) * 8 + j] = read(__builtin_amdgcn_perm(word_of(K - 1, j), bl, sel_of(j)));
+      }
+#pragma unroll
+      for (int pp = 0; pp < K / 2; ++pp)
+#pragma unroll
+        for (int q = 0; q < 8; ++q)                          // slot q / 4 of step q % 4
+          dst[q & 3] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[q & 3]),
+                                                              __builtin_bit_cast(f16x8_t, wv[pp * 8 + q]), dst[q & 3], 0, 0, 0);
+      if constexpr (K & 1) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
           dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
-                                                          __builtin_bit_cast(f16x8_t, w), dst[j], 0, 0, 0);
-        }
+                                                          __builtin_bit_cast(f16x8_t, wv[(K / 2) * 8 + j]), dst[j], 0, 0, 0);
       }
     } else {
 #pragma unroll
       for (int m = 0; m < K; ++m) {
         const uint32_t bm = r8 | (lds0 + ((uint32_t)m << 16));
+        uint32_t a0[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t a0 = __builtin_amdgcn_perm(word_of(m, j), bm, sel_of(j));
-          const uint4 w0 = read(a0);                                  // high (rows 0..7) or low part
-          const uint4 w1 = read(a0 ^ 128u);                           // the other part
-          const b16x8_t xb = __builtin_bit_cast(b16x8_t, xs[j]);
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, w0), acc[j], 0, 0, 0);
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, __builtin_bit_cast(b16x8_t, w1), acc[j], 0, 0, 0);
-        }
+        for (int j = 0; j < 4; ++j) a0[j] = __builtin_amdgcn_perm(word_of(m, j), bm, sel_of(j));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wv[m * 8 + j] = read(a0[j]);             // high (rows 0..7) or low part
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wv[m * 8 + 4 + j] = read(a0[j] ^ 128u);  // the other part
       }
+#pragma unroll
+      for (int m = 0; m < K; ++m)
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          acc[q & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(b16x8_t, xs[q & 3]),
+                                                               __builtin_bit_cast(b16x8_t, wv[m * 8 + q]), acc[q & 3], 0, 0, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+#pragma unroll
+    for (int t = kAhead; t < kReads; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+    __builtin_amdgcn_sched_barrier(0);
   } else {
 #pragma unroll
   for (int m = 0; m < K; ++m) {
