@@ -4,10 +4,11 @@
 //
 // A workgroup computes a BM x BN tile of Y (256 tokens x 128 output rows; 128 x 128 or 128 x 64
 // when larger tiles would leave compute units idle), walking
-// d_in in steps of BK = 64 (four MFMA K-blocks of 16). Eight waves share the four SIMDs in two
+// d_in in steps of BK = 64 (four MFMA K-blocks of 16). CW + 4 waves share the four SIMDs in two
 // roles, handing data over through LDS with one barrier per step:
-//   - four consumer waves each own a BM/2 x 64 block of the tile (BM/64 x 2 MFMA blocks of
-//     32 x 32, fp32 accumulators in registers). They also stream X: direct global->LDS loads (16 bytes
+//   - CW consumer waves (four, or eight on the 256 x 128 tile at k <= 2) each own a
+//     BM/(CW/2) x 64 block of the tile (MFMA blocks of 32 x 32, fp32 accumulators in registers;
+//     the same products in the same order for either CW). They also stream X: direct global->LDS loads (16 bytes
 //     per lane, eight lanes per 128-byte row segment) fill a ring of X stages several steps
 //     ahead, so X reaches LDS without passing through registers. Within a step the fragments
 //     of K-block i + 1 are read from LDS while the MFMAs of block i run;
@@ -39,7 +40,6 @@ namespace aqmb {
 
 namespace gemm {
 constexpr int BM = 256, BN = 128, BK = 64;
-constexpr int kThreads = 512;                        // waves 0-3 consume, waves 4-7 produce (four consumer waves)
 template <int K> constexpr int x_depth() { return K <= 4 ? 3 : 2; }   // X stages (LDS budget)
 template <int BMT> constexpr int x_stage() { return BMT * BK; }   // bf16 elements: BMT rows x 128 bytes
 constexpr int kChunk = 512;                          // one weight fragment: 64 lanes x 8 bf16
