@@ -246,12 +246,17 @@ __device__ __forceinline__ uint4 mg_row_shift(uint4 v) {
 // codes of plane 4 t + m, the code of step j in byte j (8-bit) or nibble j (4-bit).
 __device__ __forceinline__ void mg_rows_transpose(uint32_t (&d)[4]);
 __device__ __forceinline__ void mg_codes_transpose(uint4 v, uint32_t (&d)[4]) {
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {                              // byte q of each slice word: group 4 j + q
-    const uint32_t lo = __builtin_amdgcn_perm(v.y, v.x, 0x0C0C0000u | ((4u + q) << 8) | q);
-    const uint32_t hi = __builtin_amdgcn_perm(v.w, v.z, (((4u + q) << 24) | (q << 16)) | 0x0C0Cu);
-    d[q] = lo | hi;
-  }
+  // byte q of each slice word (group 4 j + q) into dword q, a 4 x 4 byte transpose in two rounds
+  // of byte selections (v_perm_b32: selector bytes 0..3 pick bytes of the second source, 4..7 of
+  // the first): (x, y) and (z, w) interleaved by byte pairs, then the pairs joined
+  const uint32_t xy01 = __builtin_amdgcn_perm(v.y, v.x, 0x05010400u);   // x0 y0 x1 y1
+  const uint32_t xy23 = __builtin_amdgcn_perm(v.y, v.x, 0x07030602u);   // x2 y2 x3 y3
+  const uint32_t zw01 = __builtin_amdgcn_perm(v.w, v.z, 0x05010400u);   // z0 w0 z1 w1
+  const uint32_t zw23 = __builtin_amdgcn_perm(v.w, v.z, 0x07030602u);   // z2 w2 z3 w3
+  d[0] = __builtin_amdgcn_perm(zw01, xy01, 0x05040100u);                 // x0 y0 z0 w0
+  d[1] = __builtin_amdgcn_perm(zw01, xy01, 0x07060302u);                 // x1 y1 z1 w1
+  d[2] = __builtin_amdgcn_perm(zw23, xy23, 0x05040100u);
+  d[3] = __builtin_amdgcn_perm(zw23, xy23, 0x07060302u);
   mg_rows_transpose(d);
 }
 __device__ __forceinline__ void mg_codes_transpose(uint2 v, uint32_t (&d)[4]) {
@@ -506,12 +511,15 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
   }
   }
   if constexpr (kConv) {
-    // element e of this lane is batch row 4 kc + e, whose shift lane 4 kc + e computed
+    // element e of this lane is batch row 4 kc + e, whose shift lane 4 kc + e computed; its sum is
+    // scaled by that lane's factor 2^sh (a normal or subnormal float: -141 <= sh <= 113) inside
+    // the add, one rounding as after an exact scaling
     const f32x4_t t = (run[0] + run[1]) + (run[2] + run[3]);
+    const int f = __float_as_int(ldexpf(1.0f, sh));
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int she = __builtin_amdgcn_ds_bpermute((4 * kc + e) * 4, sh);
-      acc[0][e] += ldexpf(t[e], she);
+      const float fe = __int_as_float(__builtin_amdgcn_ds_bpermute((4 * kc + e) * 4, f));
+      acc[0][e] = fmaf(t[e], fe, acc[0][e]);
     }
   }
 }
