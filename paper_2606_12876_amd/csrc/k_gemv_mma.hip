@@ -71,8 +71,11 @@ struct MgRun {
 
 // Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of the
 // run in the layout above (zeros past d_in, past the batch, and for dummy runs; skipped when
-// with_x is false and R already holds it), and slice r of the row in every plane.
-template <int K, int CB, int NX>
+// with_x is false and R already holds it), and slice r of the row in every plane. With kSwap
+// (four-plane loads feeding the paired gathers), the lanes of weight rows 8..15 load the planes
+// of each pair in swapped order (plane 4 t + (m ^ 1) in place of 4 t + m), so that every lane
+// finds the plane of its own half (slot 0 of the pair's gathers) in the pair's first dword.
+template <int K, int CB, int NX, bool kSwap = false>
 __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int rowc, bool xok, MgRun<K, CB, NX>& R,
                                             bool with_x = true) {
   constexpr int kRowsX = 4 * NX, kPer = 4 / NX;              // batch rows per load, steps per load
@@ -91,7 +94,8 @@ __device__ __forceinline__ void mg_load_run(const GemvMmaArgs& a, int r, int row
   if constexpr (mg_codes_t<K, CB>()) {
 #pragma unroll
     for (int t = 0; t < mg_code_loads<K, CB>(); ++t) {
-      const int m = 4 * t + kc < K ? 4 * t + kc : K - 1;     // rows past the last plane reload it (unused)
+      const int q = kSwap && (lane & 8) ? kc ^ 1 : kc;
+      const int m = 4 * t + q < K ? 4 * t + q : K - 1;       // rows past the last plane reload it (unused)
       if constexpr (CB == 8) R.c[t] = load_stream16(a.codes + m * a.plane_bytes + ((size_t)rc * a.d_out + rowc) * 16);
       else R.c[t] = load_stream8(a.codes + m * a.plane_bytes + ((size_t)(rc >> 1) * a.d_out + rowc) * 16 + (rc & 1) * 8);
     }
@@ -127,6 +131,9 @@ template <int K, int CB> constexpr bool mg_preload() { return K * (1 << CB) <= m
 // halves: fixed, so results are reproducible). Regions: ceil(k / 2), or k in the split form.
 template <int K, bool kSplit> constexpr int mg_regions() { return kSplit ? K : (K + 1) / 2; }
 template <int K, int CB, bool kSplit> constexpr bool mg_paired() { return CB == 8 && mg_regions<K, kSplit>() <= 2; }
+// Paired gathers of plane pairs (fp16 codewords, k >= 2: always four-plane code loads): the code
+// loads swap each pair's planes in the lanes of rows 8..15 (mg_load_run's kSwap).
+template <int K, int CB, bool kSplit> constexpr bool mg_swap_pairs() { return mg_paired<K, CB, kSplit>() && !kSplit && K >= 2; }
 constexpr uint32_t kMgRegion = 256 * 256;                    // bytes per region
 
 // The codebook word (index m * NCW + c) that replication slot q copies: in the paired layout
@@ -372,11 +379,13 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
 #pragma unroll
   for (int t = 0; t < NX; ++t) xa[t] = R.xa[t];
   const uint4 xs[4] = {mg_x_step<NX, 0>(xa), mg_x_step<NX, 1>(xa), mg_x_step<NX, 2>(xa), mg_x_step<NX, 3>(xa)};
-  // bf16 x: the run's products go to fresh sums, scaled by each batch row's 2^sh at the end
+  // bf16 x: the run's products go to two fresh sums (steps j and j + 2 share one), scaled by each
+  // batch row's 2^sh at the end; otherwise to the four steps' accumulators
   f32x4_t run[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) run[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   f32x4_t (&dst)[4] = kConv ? run : acc;
+  constexpr int kDst = kConv ? 1 : 3;                        // accumulator of step j: j & kDst
   constexpr int kCT = mg_codes_t<K, CB>() ? 4 * mg_code_loads<K, CB>() : 1;
   uint32_t cd[kCT];
   if constexpr (mg_codes_t<K, CB>()) {
@@ -414,7 +423,7 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
     // The run's codeword reads, listed in the order their MFMAs consume them, are issued kAhead
     // ahead of those MFMAs (scheduling groups: kAhead reads, then one MFMA and one read in turn),
     // so the LDS latency of a gather is not paid before every product; consecutive MFMAs go to
-    // the four steps' accumulators in turn. Each accumulator still adds its products in the same
+    // the steps' accumulators in turn. Each accumulator still adds its products in the same
     // order (pair by pair, slot 0 then slot 1).
     constexpr int kReads = kSplit ? 2 * K * 4 : (K / 2) * 8 + (K & 1) * 4;
     constexpr int kAhead = kReads < 4 ? kReads : 4;
@@ -425,17 +434,14 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
       for (int pp = 0; pp < K / 2; ++pp) {
         const uint32_t rb = lds0 + ((uint32_t)pp << 16);
         const uint32_t b0 = r8 | rb, b1 = (r8 ^ 128u) | rb;
-        uint32_t w0w[4], w1w[4];
+        // slot 0: the plane of the lane's own half, in the pair's first code dword (the loads
+        // swapped the pair's planes in rows 8..15), slot 1 the other
+        static_assert(K < 2 || (mg_swap_pairs<K, CB, kSplit>() && mg_codes_t<K, CB>()), "pairs come from swapped four-plane loads");
+        const uint32_t w0 = cd[2 * pp], w1 = cd[2 * pp + 1];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t wa = word_of(2 * pp, j), wb = word_of(2 * pp + 1, j);
-          w0w[j] = upper ? wb : wa;                          // slot 0: own half's plane
-          w1w[j] = upper ? wa : wb;
-        }
+        for (int j = 0; j < 4; ++j) wv[pp * 8 + j] = read(__builtin_amdgcn_perm(w0, b0, sel_of(j)));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) wv[pp * 8 + j] = read(__builtin_amdgcn_perm(w0w[j], b0, sel_of(j)));
-#pragma unroll
-        for (int j = 0; j < 4; ++j) wv[pp * 8 + 4 + j] = read(__builtin_amdgcn_perm(w1w[j], b1, sel_of(j)));
+        for (int j = 0; j < 4; ++j) wv[pp * 8 + 4 + j] = read(__builtin_amdgcn_perm(w1, b1, sel_of(j)));
       }
       if constexpr (K & 1) {                                 // the plane without a partner: 16 copies
         const uint32_t bl = (uint32_t)(lane & 15) * 16 | (lds0 + ((uint32_t)(K / 2) << 16));
@@ -446,13 +452,13 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
       for (int pp = 0; pp < K / 2; ++pp)
 #pragma unroll
         for (int q = 0; q < 8; ++q)                          // slot q / 4 of step q % 4
-          dst[q & 3] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[q & 3]),
-                                                              __builtin_bit_cast(f16x8_t, wv[pp * 8 + q]), dst[q & 3], 0, 0, 0);
+          dst[q & kDst] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[q & 3]),
+                                                                 __builtin_bit_cast(f16x8_t, wv[pp * 8 + q]), dst[q & kDst], 0, 0, 0);
       if constexpr (K & 1) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
-                                                          __builtin_bit_cast(f16x8_t, wv[(K / 2) * 8 + j]), dst[j], 0, 0, 0);
+          dst[j & kDst] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
+                                                                 __builtin_bit_cast(f16x8_t, wv[(K / 2) * 8 + j]), dst[j & kDst], 0, 0, 0);
       }
     } else {
 #pragma unroll
@@ -499,8 +505,8 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
       const uint32_t off = (((uint32_t)(m * NCW) + code) << a.cb_shift) + rep_off;
       const uint4 cw = *(const uint4*)((const char*)cb_rep + off);
       if constexpr (!kSplit) {
-        dst[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
-                                                        __builtin_bit_cast(f16x8_t, cw), dst[j], 0, 0, 0);
+        dst[j & kDst] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xs[j]),
+                                                               __builtin_bit_cast(f16x8_t, cw), dst[j & kDst], 0, 0, 0);
       } else {
         const uint4 cl = *(const uint4*)((const char*)cb_rep + ((uint32_t)(K * NCW) << a.cb_shift) + off);
         const b16x8_t xb = __builtin_bit_cast(b16x8_t, xs[j]);
@@ -514,7 +520,7 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
     // element e of this lane is batch row 4 kc + e, whose shift lane 4 kc + e computed; its sum is
     // scaled by that lane's factor 2^sh (a normal or subnormal float: -141 <= sh <= 113) inside
     // the add, one rounding as after an exact scaling
-    const f32x4_t t = (run[0] + run[1]) + (run[2] + run[3]);
+    const f32x4_t t = run[0] + run[1];
     const int f = __float_as_int(ldexpf(1.0f, sh));
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -585,8 +591,9 @@ __device__ __forceinline__ void mg_one_block(const GemvMmaArgs& a, int blk) {
   const uint4 w0 = mg_first_word<K, CB, kSpl>(a);
   const int srow = row0 + mg_out_row(tid);                   // the row this thread stores, if any
   const uint16_t sbits = tid < 256 ? a.scales[srow < a.d_out ? srow : a.d_out - 1] : 0;
-  mg_load_run<K, CB, NX>(a, r, rowc, true, ra);
-  mg_load_run<K, CB, NX>(a, r + kWaves, rowc, true, rb);
+  constexpr bool kSw = mg_swap_pairs<K, CB, kSpl>();
+  mg_load_run<K, CB, NX, kSw>(a, r, rowc, true, ra);
+  mg_load_run<K, CB, NX, kSw>(a, r + kWaves, rowc, true, rb);
   mg_replicate<K, CB, kSpl>(a, cb_rep, w0);
   __syncthreads();
 
@@ -598,9 +605,9 @@ __device__ __forceinline__ void mg_one_block(const GemvMmaArgs& a, int blk) {
   for (; r < n_runs; r += 2 * kWaves) {
     mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, ra, acc);
     if (r + kWaves >= n_runs) break;
-    if (r + 2 * kWaves < n_runs) mg_load_run<K, CB, NX>(a, r + 2 * kWaves, rowc, true, ra);
+    if (r + 2 * kWaves < n_runs) mg_load_run<K, CB, NX, kSw>(a, r + 2 * kWaves, rowc, true, ra);
     mg_compute<K, XDT, CB, NX>(a, cb_rep, rep_off, rb, acc);
-    if (r + 3 * kWaves < n_runs) mg_load_run<K, CB, NX>(a, r + 3 * kWaves, rowc, true, rb);
+    if (r + 3 * kWaves < n_runs) mg_load_run<K, CB, NX, kSw>(a, r + 3 * kWaves, rowc, true, rb);
   }
   mg_reduce_store(a, red, acc, row0, sbits);
 }
@@ -663,7 +670,8 @@ void gemv_mma_persist_kernel(GemvMmaArgs a) {
     const int ic = i < n_items ? i : n_items - 1;
     const int row = ((int)blockIdx.x + (ic / per) * (int)gridDim.x) * kRows + col;
     const int r = wave + (ic % per) * kWaves;
-    mg_load_run<K, CB, NX>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R, i < 2 || per > 2);
+    mg_load_run<K, CB, NX, mg_swap_pairs<K, CB, kSpl>()>(a, r, row < a.d_out ? row : a.d_out - 1, r < n_runs, R,
+                                                        i < 2 || per > 2);
   };
   auto block_row0 = [&](int i) {                             // first row of the block of item i
     return ((int)blockIdx.x + ((i < n_items ? i : n_items - 1) / per) * (int)gridDim.x) * kRows;
