@@ -208,6 +208,28 @@ def test_gemv_more_row_blocks_than_cus(xdt):
                     check_close(got, ref, ydt, f"5000 rows {xdt} b={b} k={k} y={ydt}", terms=T, n_terms=k * 520)
 
 
+@pytest.mark.parametrize("xdt", ["f16", "bf16"])
+def test_gemv_tall_layer_long_rows(xdt):
+    """4400 rows (275 blocks of 16) of 545 groups (35 runs of 16, the last with one group): the
+    persistent matrix-core kernel with three items per wave and block, so x is loaded with every
+    item rather than held across blocks; batch 1 (fp16 x: matrix cores on rows of more than 512
+    groups; bf16 x: direct gathers), 8 and 16, every k, against the oracle with the fp32
+    summation bound."""
+    spec = LayerSpec("tall_long", 4400, 4360, M=4, seed=44, act_dtype=xdt)
+    L = make_layer(spec)
+    C, s = _f64(L)
+    with GpuLayer(L.codes, L.codebooks, L.scales) as gl:
+        for b in (1, 8, 16):
+            xbits = make_activations(L, b, xdt, heavy_tail=True)
+            x = act_values(xbits, xdt)
+            for k in range(1, 5):
+                ref = oracle.linear(x, L.codes, C, s, k)
+                T = abs_terms(x, L.codes, C, s, k)
+                for ydt in ("f32", xdt):
+                    got = run_gemv(gl, k, xbits, xdt, ydt)
+                    check_close(got, ref, ydt, f"4400 x 4360 {xdt} b={b} k={k} y={ydt}", terms=T, n_terms=k * 4360)
+
+
 def test_gemv_plane_linearity():
     """gemv(k) - gemv(k-1) equals the GEMV of a one-codebook layer holding plane k-1 alone."""
     spec = LayerSpec("lin", 777, 1024, seed=36)
