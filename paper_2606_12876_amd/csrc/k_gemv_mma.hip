@@ -66,7 +66,9 @@ template <int K, int CB, int NX>
 struct MgRun {
   uint4 xa[NX];
   typename std::conditional<CB == 8, uint4, uint2>::type c[mg_code_loads<K, CB>()];
-  int sh;                                                    // bf16 x converted in place: the lane's shift
+  // bf16 x converted in place: the factor 2^sh of the batch row of each of this lane's four
+  // accumulator elements (set with the conversion, kept while the set holds the same x)
+  float f[4];
 };
 
 // Loads of run r of weight row rowc (r clamped to the last run: a reload, never used): x of the
@@ -361,8 +363,8 @@ __device__ __forceinline__ uint4 mg_x_step(const uint4 (&xa)[NX]) {
 // The MFMAs of one run. Step j of a run: group 4 j + kc of the run (8-bit codes: byte 4 j + kc of
 // the plane's slice word; 4-bit codes: nibble 4 j + kc of its 8 bytes).
 // With bf16 x in the converted form, `convert` says whether R holds x as loaded: it is then
-// converted in place (R.xa, R.sh), so a register set that keeps its run's x for several blocks
-// (the persistent kernel) converts it once.
+// converted in place (R.xa, with the row factors R.f), so a register set that keeps its run's x
+// for several blocks (the persistent kernel) converts it, and fetches the factors, once.
 template <int K, int XDT, int CB, int NX, bool P = false>
 __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb_rep, uint32_t rep_off,
                                            MgRun<K, CB, NX>& R, mg::f32x4_t (&acc)[4], bool convert = true) {
@@ -370,10 +372,15 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
   constexpr int NCW = 1 << CB;
   const int lane = threadIdx.x & 63, kc = lane >> 4;
   constexpr bool kSplit = mg_split_p<K, XDT, NX, P>(), kConv = XDT == AQMB_BF16 && !kSplit;
-  int sh = 0;
   if constexpr (kConv) {
-    if (convert) R.sh = mg_bf16_to_f16<NX>(R.xa, a.batch);
-    sh = R.sh;
+    if (convert) {
+      const int sh = mg_bf16_to_f16<NX>(R.xa, a.batch);
+      // element e of this lane's accumulators is batch row 4 kc + e, whose shift lane 4 kc + e
+      // computed: its factor 2^sh (a normal or subnormal float: -141 <= sh <= 113)
+      const int f = __float_as_int(ldexpf(1.0f, sh));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) R.f[e] = __int_as_float(__builtin_amdgcn_ds_bpermute((4 * kc + e) * 4, f));
+    }
   }
   uint4 xa[NX];
 #pragma unroll
@@ -517,16 +524,11 @@ __device__ __forceinline__ void mg_compute(const GemvMmaArgs& a, const uint4* cb
   }
   }
   if constexpr (kConv) {
-    // element e of this lane is batch row 4 kc + e, whose shift lane 4 kc + e computed; its sum is
-    // scaled by that lane's factor 2^sh (a normal or subnormal float: -141 <= sh <= 113) inside
-    // the add, one rounding as after an exact scaling
+    // each batch row's sum scaled by its factor inside the add: one rounding, as after an exact
+    // scaling
     const f32x4_t t = run[0] + run[1];
-    const int f = __float_as_int(ldexpf(1.0f, sh));
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float fe = __int_as_float(__builtin_amdgcn_ds_bpermute((4 * kc + e) * 4, f));
-      acc[0][e] = fmaf(t[e], fe, acc[0][e]);
-    }
+    for (int e = 0; e < 4; ++e) acc[0][e] = fmaf(t[e], R.f[e], acc[0][e]);
   }
 }
 
