@@ -101,7 +101,7 @@ def gemv_kernel_name(spec, k, b, xdt):
         return f"gemv_b16_kernel<KC={min(k, 4)}>"
     wide = G > 512
     rb = (spec.d_out + 15) // 16
-    if b >= 2 or wide:
+    if b >= 2 or (wide and (xdt == "f16" or k >= 3)):
         return ("gemv_mma_persist_kernel" if rb > 256 else "gemv_mma_kernel") + f"<K={k}> (batch {b})"
     return ("gemv_cw_persist_kernel" if rb > 256 else "gemv_cw_kernel") + f"<K={k}> (batch {b})"
 

@@ -170,9 +170,10 @@ aqmb_status aqmb_gemv_select(aqmb_layer_t layer, int k, const void* x, aqmb_dtyp
  * gate/up): for each l < n_layers, ys[l][b][i] = sum_t x[b][t] * W_k^(l)[i][t], exactly what
  * aqmb_gemv(layers[l], k, x, x_dtype, batch, ys[l], y_dtype, stream) computes (same arithmetic,
  * same rounding), in one launch when either
- *   - every layer has 8-bit codes, k <= 4 and aqmb_gemv would use the direct-gather kernel (batch
- *     1 on rows of at most 512 groups: one workgroup per row block walks through the layers,
- *     loading the next layer's codes while it works on the current one), or
+ *   - every layer has 8-bit codes, k <= 4, aqmb_gemv would use the direct-gather kernel (batch 1;
+ *     on rows of more than 512 groups only bf16 x at k < 3) and, for rows of more than 512
+ *     groups, k = 1 (one workgroup per row block walks through the layers, loading the next
+ *     layer's codes while it works on the current one), or
  *   - n_layers >= 2, every layer would take the matrix-core kernel (batch >= 2, and batch 1 on
  *     rows of more than 512 groups: see aqmb_gemv's kernel choice in the library source), all
  *     have the same code width and none has more 16-row blocks than the device has compute units

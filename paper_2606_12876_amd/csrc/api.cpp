@@ -137,9 +137,10 @@ static aqmb_status create_impl(aqmb_layer_t* out, const aqmb_desc* desc, int res
 // GEMV kernel choice (AQMB_GEMV_AUTO), measured faster in each case: 4-bit codes -> the
 // matrix-core kernel at batch >= 2 and, for fp16 x at k >= 2, at batch 1 on rows of more than 512
 // groups; their direct-gather kernel otherwise. 8-bit codes -> the matrix-core kernel at batch >= 2
-// and at batch 1 on rows of more than 512 groups (bf16 x on 4096 x 11008, mean of three runs,
-// direct gathers against the matrix cores: 5.77 / 7.44 / 8.92 / 10.74 against 5.60 / 7.55 / 8.69 /
-// 9.92 us at k = 1..4); otherwise the direct-gather kernel when it fits (k <= 4, rows of at most
+// and at batch 1 on rows of more than 512 groups for fp16 x, and for bf16 x from k = 3 (4096 x
+// 11008, mean of three runs, direct gathers against the matrix cores: 5.77 / 7.44 / 8.92 / 10.74
+// against 5.60 / 7.55 / 8.69 / 9.92 us at k = 1..4; in a bench run 7.4 against 8.2 us at k = 2
+// and even at k = 1); otherwise the direct-gather kernel when it fits (k <= 4, rows of at most
 // 16384 inputs), else the matrix-core kernel. 16-bit codes -> their direct-gather kernel.
 // (At batch 1 on rows of at most 512 groups the matrix cores are 3-5 % faster with fp16 x from
 // k = 2 on a 4096 x 4096 layer, but the direct-gather kernel stays: aqmb_gemv_multi runs such
@@ -149,7 +150,7 @@ static aqmb_gemv_kernel gemv_auto(const Layer& L, int k, int batch, aqmb_dtype x
   const bool wide = L.S * L.J > 512;
   if (L.d.code_bits == 4)
     return batch >= 2 || (x_dtype == AQMB_F16 && wide && k >= 2) ? AQMB_GEMV_MMA : AQMB_GEMV_DIRECT;
-  if (batch >= 2 || wide) return AQMB_GEMV_MMA;
+  if (batch >= 2 || (wide && (x_dtype == AQMB_F16 || k >= 3))) return AQMB_GEMV_MMA;
   return gemv_cw_fits(L, k, batch, x_dtype) ? AQMB_GEMV_DIRECT : AQMB_GEMV_MMA;
 }
 
